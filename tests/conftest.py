@@ -1,0 +1,24 @@
+import os
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+
+def pytest_configure(config):
+    config.addinivalue_line("markers", "gpu: needs an MI355X (gfx950) GPU and the built HIP library")
+    config.addinivalue_line("markers", "slow: full-size workload (minutes)")
+
+
+def golden(name):
+    import yaml
+    with open(os.path.join(ROOT, "tests", "golden", name)) as f:
+        return yaml.safe_load(f)
+
+
+@pytest.fixture
+def load_golden():
+    return golden
