@@ -1,0 +1,175 @@
+/*
+ * oprag.h - C ABI of the MI355X (gfx950) exact-retrieval core of OpRAG.
+ *
+ * The paper's operator model (Section 3.2) states the three calls this library implements:
+ *   E  = Op_embed(D; b_e)          - outside the library: callers pass unit-norm vectors
+ *                                    (the embedding path ends in an L2 normalisation, Section 4.3);
+ *   I' = Op_upsert(I, E; b_u)      - oprag_upsert: bulk insertion of new embeddings;
+ *   R_k = Op_retrieve(q, I)        - oprag_search_dense: exact top-k by inner product;
+ * and the hybrid retrieval of Section 4.4 (dense scores plus inverted-postings BM25 over the
+ * full corpus, fused, then partial top-k): oprag_sparse_attach / oprag_search_sparse /
+ * oprag_rrf_fuse / oprag_search_hybrid.
+ *
+ * Conventions for every function:
+ *  - Return value: OPRAG_OK (0) or a negative oprag_status; the reason is available from
+ *    oprag_last_error() (thread-local string).  Nothing throws across the ABI.
+ *  - Validation is synchronous and complete before anything is enqueued: on error nothing
+ *    is enqueued and the index is unchanged.  Faults inside kernels surface at the caller's
+ *    next synchronisation of the stream.
+ *  - Memory: every large buffer (slab, CSR arrays, queries, outputs, workspace) is device
+ *    memory owned by the caller and must stay valid while the index or call uses it.  The
+ *    library allocates only small per-index device arrays at create / attach time and never
+ *    in upsert or search.  Device pointers must be 16-byte aligned.
+ *  - Streams: `stream` is a hipStream_t (NULL = default stream).  Calls are asynchronous on
+ *    it.  An index keeps host-side state (row count) and a small device control block, so
+ *    calls on one index must be issued from one host thread at a time and ordered on one
+ *    stream (or ordered by the caller with events).
+ *  - Ranked lists are ordered by score descending, then id ascending.  Lists shorter than k
+ *    are padded with id -1 and score -inf.  1 <= k <= OPRAG_MAX_K.
+ */
+#ifndef OPRAG_H_
+#define OPRAG_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define OPRAG_ABI_VERSION 1
+#define OPRAG_MAX_K 128
+#define OPRAG_MAX_DIM 8192
+
+typedef enum oprag_status {
+  OPRAG_OK = 0,
+  OPRAG_E_INVALID = -1,     /* bad argument (null/misaligned pointer, size, dtype, k, ...) */
+  OPRAG_E_CAPACITY = -2,    /* upsert would exceed the slab capacity */
+  OPRAG_E_STATE = -3,       /* call not valid in the index's state (e.g. no sparse index) */
+  OPRAG_E_UNSUPPORTED = -4, /* valid request outside what this build supports */
+  OPRAG_E_DEVICE = -5       /* a HIP call failed */
+} oprag_status;
+
+typedef enum oprag_dtype { OPRAG_F32 = 0, OPRAG_BF16 = 1, OPRAG_F16 = 2 } oprag_dtype;
+
+typedef enum oprag_op { OPRAG_OP_DENSE = 0, OPRAG_OP_SPARSE = 1, OPRAG_OP_HYBRID = 2 } oprag_op;
+
+typedef struct oprag_index oprag_index; /* opaque handle */
+
+typedef struct oprag_index_desc {
+  int32_t dim;      /* vector dimension d: 1..OPRAG_MAX_DIM; multiple of 4 (f32) or 64 (bf16, f16) */
+  int32_t dtype;    /* oprag_dtype of the stored vectors and of queries */
+  int64_t capacity; /* rows the slab holds: 1 .. 2^31 - 2 */
+  int32_t device;   /* HIP device ordinal of the slab */
+  int32_t reserved; /* must be 0 */
+} oprag_index_desc;
+
+int32_t oprag_abi_version(void);
+
+/* Message describing the last failure on this thread ("" if none). */
+const char *oprag_last_error(void);
+
+/*
+ * Create an index over a caller-owned slab: row-major [capacity x dim] in desc->dtype,
+ * slab_bytes >= capacity * dim * sizeof(dtype).  The index starts empty (n_rows = 0);
+ * row ids are insertion positions.  Allocates a small device control block (zeroed).
+ * Errors: E_INVALID (desc, slab, out), E_DEVICE.
+ */
+oprag_status oprag_index_create(const oprag_index_desc *desc, void *slab_dev, size_t slab_bytes, oprag_index **out);
+
+/* Release the handle and the arrays the library allocated; never touches caller buffers.
+ * The caller must make sure no work using the index is still pending.  NULL is OK. */
+oprag_status oprag_index_destroy(oprag_index *idx);
+
+/* Rows currently in the index (host state, advanced when an upsert is enqueued). */
+oprag_status oprag_index_size(const oprag_index *idx, int64_t *n_rows);
+
+/*
+ * Upsert (Section 3.2, "Upsert"; bulk commit, Section 4.1), append-only: copies m rows
+ * [m x dim] of rows_dtype into slab rows [n_rows, n_rows + m) and advances n_rows.
+ * rows_dtype must equal the index dtype, or be OPRAG_F32 for a bf16 / f16 index (converted
+ * with round-to-nearest-even).  All or nothing: if n_rows + m > capacity nothing is
+ * enqueued and E_CAPACITY is returned.  m = 0 is a no-op.  *first_row (may be NULL)
+ * receives the id of the first new row.  Searches enqueued later on the same stream see
+ * the new rows.
+ */
+oprag_status oprag_upsert(oprag_index *idx, const void *rows_dev, int32_t rows_dtype, int64_t m, void *stream,
+                          int64_t *first_row);
+
+/*
+ * Attach the inverted-postings index BM25 scores from (Section 4.4): CSR term -> (chunk, tf)
+ * over chunk ids [0, n_docs) (the same ids as the dense rows; n_docs <= capacity).
+ *   term_indptr_dev [vocab + 1] int64, term_indptr[0] = 0, term_indptr[vocab] = nnz;
+ *   post_chunk_dev  [nnz] int32, strictly ascending within a term, in [0, n_docs);
+ *   post_tf_dev     [nnz] int32 >= 1;  doc_len_dev [n_docs] int32 >= 0 (tokens per chunk).
+ * The arrays stay caller-owned and are read by later searches.  The library checks them on
+ * the device (E_INVALID on any violation), then computes idf(t) = ln(1 + (N - df + 0.5) /
+ * (df + 0.5)) and per-chunk length norms k1 (1 - b + b dl / avgdl) into arrays it owns.
+ * Synchronises `stream`.  Re-attaching replaces the previous sparse index.
+ * k1 >= 0, 0 <= b <= 1.
+ */
+oprag_status oprag_sparse_attach(oprag_index *idx, int32_t vocab, int64_t n_docs, int64_t nnz,
+                                 const int64_t *term_indptr_dev, const int32_t *post_chunk_dev,
+                                 const int32_t *post_tf_dev, const int32_t *doc_len_dev, float k1, float b,
+                                 void *stream);
+
+/*
+ * Workspace bytes a search of nq queries needs (op: oprag_op; k_dense is the dense k for
+ * OPRAG_OP_DENSE and OPRAG_OP_HYBRID, k_sparse the sparse k for OPRAG_OP_SPARSE and
+ * OPRAG_OP_HYBRID).  The value does not depend on the current row count, so a workspace
+ * sized once stays valid as the index grows.
+ */
+oprag_status oprag_workspace_bytes(const oprag_index *idx, int32_t op, int64_t nq, int32_t k_dense, int32_t k_sparse,
+                                   size_t *bytes);
+
+/*
+ * Exact dense top-k, R_k = Op_retrieve(q, I) (Section 3.2, "Retrieval"; scoring by matrix
+ * products over the embedding matrix and partial top-k selection, Section 4.4):
+ * s(q, i) = sum_j Q[q, j] X[i, j] over rows 0 <= i < n_rows, accumulated in fp32.
+ *   q_dev      [nq x dim] in the index dtype;
+ *   scores_dev [nq x k] fp32;  ids_dev [nq x k] int64 (row ids).
+ * nq = 0 is a no-op.  workspace_dev must hold oprag_workspace_bytes(OPRAG_OP_DENSE) bytes.
+ */
+oprag_status oprag_search_dense(oprag_index *idx, const void *q_dev, int64_t nq, int32_t k, float *scores_dev,
+                                int64_t *ids_dev, void *workspace_dev, size_t workspace_bytes, void *stream);
+
+/*
+ * Exact BM25 top-k (Section 4.4) over the attached sparse index.  Query q's terms are
+ * qterms_dev[qterm_indptr_dev[q] .. qterm_indptr_dev[q + 1]) (int32; repeated terms count
+ * once per occurrence; ids outside [0, vocab) match nothing).  Only chunks with a positive
+ * score are ranked.  scores_dev [nq x k] fp32, ids_dev [nq x k] int64.
+ * E_STATE without an attached sparse index.
+ */
+oprag_status oprag_search_sparse(oprag_index *idx, const int32_t *qterm_indptr_dev, const int32_t *qterms_dev,
+                                 int64_t nq, int32_t k, float *scores_dev, int64_t *ids_dev, void *workspace_dev,
+                                 size_t workspace_bytes, void *stream);
+
+/*
+ * Reciprocal rank fusion of two ranked id lists per query (the fusion the hybrid workload
+ * specifies; the paper's own Section 4.4 fusion is a weighted score sum with unstated
+ * weights): fused(d) = sum over lists holding d of 1 / (rrf_k + rank), ranks 1-based over
+ * the list's valid prefix (ids >= 0).  Compared exactly as rationals; ties by ascending id.
+ *   dense_ids_dev [nq x k_dense] int64, sparse_ids_dev [nq x k_sparse] int64;
+ *   fused_dev [nq x k] fp32 (the exact value rounded to fp32), ids_dev [nq x k] int64.
+ * 0 <= rrf_k <= 1000000.  Needs no index and no workspace.
+ */
+oprag_status oprag_rrf_fuse(const int64_t *dense_ids_dev, int32_t k_dense, const int64_t *sparse_ids_dev,
+                            int32_t k_sparse, int64_t nq, int32_t rrf_k, int32_t k, float *fused_dev,
+                            int64_t *ids_dev, void *stream);
+
+/*
+ * Hybrid search (Section 4.4): exact dense top-k_dense and exact BM25 top-k_sparse over the
+ * full corpus, fused by reciprocal rank fusion (rrf_k), cut at k.  Equivalent to
+ * oprag_search_dense + oprag_search_sparse + oprag_rrf_fuse on the same stream.
+ * workspace_dev must hold oprag_workspace_bytes(OPRAG_OP_HYBRID) bytes.
+ */
+oprag_status oprag_search_hybrid(oprag_index *idx, const void *q_dev, const int32_t *qterm_indptr_dev,
+                                 const int32_t *qterms_dev, int64_t nq, int32_t k_dense, int32_t k_sparse,
+                                 int32_t rrf_k, int32_t k, float *fused_dev, int64_t *ids_dev, void *workspace_dev,
+                                 size_t workspace_bytes, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* OPRAG_H_ */

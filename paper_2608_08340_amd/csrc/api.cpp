@@ -1,0 +1,445 @@
+// Host runtime behind the C ABI of include/oprag.h: argument validation (always complete
+// before the first HIP call), the index handle and its device control block, workspace
+// planning and kernel dispatch.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+
+#include "../../include/oprag.h"
+#include "oprag_internal.h"
+
+using oprag::kMaxK;
+using oprag::kMaxQPerLaunch;
+
+struct oprag_index {
+  int32_t dim = 0, dtype = 0, device = 0;
+  int64_t capacity = 0;
+  void* slab = nullptr;
+  size_t slab_bytes = 0;
+  int64_t n_rows = 0;
+  void* cb_mem = nullptr;
+  oprag::ControlBlock cb;
+  bool has_sparse = false;
+  oprag::SparseIndex sp;
+  void* sp_mem = nullptr;
+};
+
+namespace {
+
+thread_local std::string g_err;
+
+oprag_status fail(oprag_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return s;
+}
+
+oprag_status ok() {
+  g_err.clear();
+  return OPRAG_OK;
+}
+
+oprag_status hip_fail(hipError_t e, const char* what) {
+  return fail(OPRAG_E_DEVICE, "%s: %s", what, hipGetErrorString(e));
+}
+
+size_t elem_size(int32_t dt) { return dt == OPRAG_F32 ? 4 : 2; }
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+bool valid_dtype(int32_t dt) { return dt == OPRAG_F32 || dt == OPRAG_BF16 || dt == OPRAG_F16; }
+
+// Makes idx->device current for the scope and restores the caller's device.
+class DeviceScope {
+ public:
+  explicit DeviceScope(int dev) {
+    err_ = hipGetDevice(&prev_);
+    if (err_ == hipSuccess && prev_ != dev) {
+      err_ = hipSetDevice(dev);
+      switched_ = err_ == hipSuccess;
+    }
+  }
+  ~DeviceScope() {
+    if (switched_) (void)hipSetDevice(prev_);
+  }
+  hipError_t error() const { return err_; }
+
+ private:
+  int prev_ = 0;
+  bool switched_ = false;
+  hipError_t err_ = hipSuccess;
+};
+
+oprag_status check_index(const oprag_index* idx) {
+  if (!idx) return fail(OPRAG_E_INVALID, "index handle is NULL");
+  return OPRAG_OK;
+}
+
+oprag_status check_k(int32_t k, const char* name) {
+  if (k < 1 || k > kMaxK) return fail(OPRAG_E_INVALID, "%s = %d outside [1, %d]", name, k, kMaxK);
+  return OPRAG_OK;
+}
+
+oprag_status check_buf(const void* p, const char* name) {
+  if (!p) return fail(OPRAG_E_INVALID, "%s is NULL", name);
+  if (!aligned16(p)) return fail(OPRAG_E_INVALID, "%s is not 16-byte aligned", name);
+  return OPRAG_OK;
+}
+
+size_t align_up(size_t x) { return (x + 255) & ~size_t(255); }
+
+size_t dense_ws(const oprag_index* idx, int64_t nq, int32_t k) {
+  const int nql = (int)std::min<int64_t>(nq, kMaxQPerLaunch);
+  const oprag::DensePlan p = oprag::plan_dense(idx->dtype, idx->dim, idx->capacity, nql, k);
+  return oprag::dense_workspace_bytes(p, nql);
+}
+
+size_t sparse_ws(const oprag_index* idx, int64_t nq, int32_t k) {
+  return oprag::sparse_workspace_bytes(idx->has_sparse ? idx->sp.n_docs : idx->capacity, (int)nq, k);
+}
+
+size_t hybrid_ws(const oprag_index* idx, int64_t nq, int32_t kd, int32_t ks) {
+  const size_t lists = align_up((size_t)nq * kd * 8) + align_up((size_t)nq * kd * 4) +
+                       align_up((size_t)nq * ks * 8) + align_up((size_t)nq * ks * 4);
+  return lists + std::max(align_up(dense_ws(idx, nq, kd)), align_up(sparse_ws(idx, nq, ks)));
+}
+
+oprag_status do_dense(oprag_index* idx, const void* q, int64_t nq, int32_t k, float* scores, int64_t* ids, void* ws,
+                      size_t ws_bytes, hipStream_t s) {
+  const size_t es = elem_size(idx->dtype);
+  for (int64_t q0 = 0; q0 < nq; q0 += kMaxQPerLaunch) {
+    const int nql = (int)std::min<int64_t>(kMaxQPerLaunch, nq - q0);
+    const oprag::DensePlan p = oprag::plan_dense(idx->dtype, idx->dim, idx->n_rows, nql, k);
+    if (p.kernel < 0) return fail(OPRAG_E_UNSUPPORTED, "no dense kernel for dtype %d, k %d", idx->dtype, k);
+    if (oprag::dense_workspace_bytes(p, nql) > ws_bytes)
+      return fail(OPRAG_E_INVALID, "workspace too small: %zu < %zu bytes", ws_bytes,
+                  oprag::dense_workspace_bytes(p, nql));
+    oprag::DenseArgs a;
+    a.X = idx->slab;
+    a.n_rows = idx->n_rows;
+    a.d = idx->dim;
+    a.Q = static_cast<const unsigned char*>(q) + (size_t)q0 * idx->dim * es;
+    a.nq = nql;
+    a.k = k;
+    a.n_qblocks = p.n_qblocks;
+    a.n_chunks = p.n_chunks;
+    a.rows_per_chunk = p.rows_per_chunk;
+    a.thr = idx->cb.thr;
+    a.cnt = idx->cb.cnt;
+    a.done = idx->cb.done;
+    a.cand = static_cast<unsigned long long*>(ws);
+    a.cap = p.cap;
+    a.out_scores = scores + q0 * k;
+    a.out_ids = reinterpret_cast<long long*>(ids) + q0 * k;
+    const hipError_t e = oprag::launch_dense(p, idx->dtype, a, s);
+    if (e != hipSuccess) return hip_fail(e, "dense search launch");
+  }
+  return OPRAG_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t oprag_abi_version(void) { return OPRAG_ABI_VERSION; }
+
+const char* oprag_last_error(void) { return g_err.c_str(); }
+
+oprag_status oprag_index_create(const oprag_index_desc* desc, void* slab_dev, size_t slab_bytes, oprag_index** out) {
+  if (!out) return fail(OPRAG_E_INVALID, "out is NULL");
+  *out = nullptr;
+  if (!desc) return fail(OPRAG_E_INVALID, "desc is NULL");
+  if (!valid_dtype(desc->dtype)) return fail(OPRAG_E_INVALID, "dtype %d is not an oprag_dtype", desc->dtype);
+  if (desc->dim < 1 || desc->dim > OPRAG_MAX_DIM) return fail(OPRAG_E_INVALID, "dim %d outside [1, %d]", desc->dim, OPRAG_MAX_DIM);
+  if (desc->dtype == OPRAG_F32 && desc->dim % 4)
+    return fail(OPRAG_E_UNSUPPORTED, "fp32 dim %d is not a multiple of 4", desc->dim);
+  if (desc->dtype != OPRAG_F32 && desc->dim % 64)
+    return fail(OPRAG_E_UNSUPPORTED, "bf16/fp16 dim %d is not a multiple of 64", desc->dim);
+  if (desc->capacity < 1 || desc->capacity > (int64_t)0x7ffffffe)
+    return fail(OPRAG_E_INVALID, "capacity %lld outside [1, 2^31 - 2]", (long long)desc->capacity);
+  if (desc->device < 0) return fail(OPRAG_E_INVALID, "device %d < 0", desc->device);
+  if (desc->reserved != 0) return fail(OPRAG_E_INVALID, "reserved field must be 0");
+  if (oprag_status st = check_buf(slab_dev, "slab_dev")) return st;
+  const size_t need = (size_t)desc->capacity * (size_t)desc->dim * elem_size(desc->dtype);
+  if (slab_bytes < need) return fail(OPRAG_E_INVALID, "slab_bytes %zu < capacity * dim * elem = %zu", slab_bytes, need);
+
+  DeviceScope ds(desc->device);
+  if (ds.error() != hipSuccess) return hip_fail(ds.error(), "select device");
+  const size_t nthr = kMaxQPerLaunch, ndone = kMaxQPerLaunch / oprag::kMinBN;
+  const size_t cb_bytes = (2 * nthr + ndone) * sizeof(uint32_t);
+  void* mem = nullptr;
+  hipError_t e = hipMalloc(&mem, cb_bytes);
+  if (e != hipSuccess) return hip_fail(e, "control block allocation");
+  e = hipMemset(mem, 0, cb_bytes);
+  if (e == hipSuccess) e = hipDeviceSynchronize();
+  if (e != hipSuccess) {
+    (void)hipFree(mem);
+    return hip_fail(e, "control block clear");
+  }
+  oprag_index* idx = new oprag_index;
+  idx->dim = desc->dim;
+  idx->dtype = desc->dtype;
+  idx->device = desc->device;
+  idx->capacity = desc->capacity;
+  idx->slab = slab_dev;
+  idx->slab_bytes = slab_bytes;
+  idx->cb_mem = mem;
+  idx->cb.thr = static_cast<uint32_t*>(mem);
+  idx->cb.cnt = idx->cb.thr + nthr;
+  idx->cb.done = idx->cb.cnt + nthr;
+  *out = idx;
+  return ok();
+}
+
+oprag_status oprag_index_destroy(oprag_index* idx) {
+  if (!idx) return ok();
+  DeviceScope ds(idx->device);
+  if (idx->cb_mem) (void)hipFree(idx->cb_mem);
+  if (idx->sp_mem) (void)hipFree(idx->sp_mem);
+  delete idx;
+  return ok();
+}
+
+oprag_status oprag_index_size(const oprag_index* idx, int64_t* n_rows) {
+  if (oprag_status st = check_index(idx)) return st;
+  if (!n_rows) return fail(OPRAG_E_INVALID, "n_rows is NULL");
+  *n_rows = idx->n_rows;
+  return ok();
+}
+
+oprag_status oprag_upsert(oprag_index* idx, const void* rows_dev, int32_t rows_dtype, int64_t m, void* stream,
+                          int64_t* first_row) {
+  if (oprag_status st = check_index(idx)) return st;
+  if (m < 0) return fail(OPRAG_E_INVALID, "m = %lld < 0", (long long)m);
+  if (!valid_dtype(rows_dtype)) return fail(OPRAG_E_INVALID, "rows_dtype %d is not an oprag_dtype", rows_dtype);
+  if (rows_dtype != idx->dtype && !(rows_dtype == OPRAG_F32 && idx->dtype != OPRAG_F32))
+    return fail(OPRAG_E_INVALID, "rows_dtype %d cannot be stored in a dtype %d index", rows_dtype, idx->dtype);
+  if (m > idx->capacity - idx->n_rows)
+    return fail(OPRAG_E_CAPACITY, "upsert of %lld rows exceeds capacity (%lld of %lld used)", (long long)m,
+                (long long)idx->n_rows, (long long)idx->capacity);
+  if (m == 0) {
+    if (first_row) *first_row = idx->n_rows;
+    return ok();
+  }
+  if (oprag_status st = check_buf(rows_dev, "rows_dev")) return st;
+  DeviceScope ds(idx->device);
+  if (ds.error() != hipSuccess) return hip_fail(ds.error(), "select device");
+  const hipError_t e = oprag::launch_upsert(idx->slab, idx->dtype, idx->dim, idx->n_rows, rows_dev, rows_dtype, m,
+                                            static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "upsert launch");
+  if (first_row) *first_row = idx->n_rows;
+  idx->n_rows += m;
+  return ok();
+}
+
+oprag_status oprag_sparse_attach(oprag_index* idx, int32_t vocab, int64_t n_docs, int64_t nnz,
+                                 const int64_t* term_indptr_dev, const int32_t* post_chunk_dev,
+                                 const int32_t* post_tf_dev, const int32_t* doc_len_dev, float k1, float b,
+                                 void* stream) {
+  if (oprag_status st = check_index(idx)) return st;
+  if (vocab < 1) return fail(OPRAG_E_INVALID, "vocab %d < 1", vocab);
+  if (n_docs < 1 || n_docs > idx->capacity)
+    return fail(OPRAG_E_INVALID, "n_docs %lld outside [1, capacity]", (long long)n_docs);
+  if (nnz < 0 || nnz > (int64_t)1 << 40) return fail(OPRAG_E_INVALID, "nnz %lld out of range", (long long)nnz);
+  if (!(std::isfinite(k1) && k1 >= 0.f)) return fail(OPRAG_E_INVALID, "k1 must be finite and >= 0");
+  if (!(std::isfinite(b) && b >= 0.f && b <= 1.f)) return fail(OPRAG_E_INVALID, "b must be in [0, 1]");
+  if (oprag_status st = check_buf(term_indptr_dev, "term_indptr_dev")) return st;
+  if (oprag_status st = check_buf(doc_len_dev, "doc_len_dev")) return st;
+  if (nnz > 0) {
+    if (oprag_status st = check_buf(post_chunk_dev, "post_chunk_dev")) return st;
+    if (oprag_status st = check_buf(post_tf_dev, "post_tf_dev")) return st;
+  }
+  DeviceScope ds(idx->device);
+  if (ds.error() != hipSuccess) return hip_fail(ds.error(), "select device");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  // Library-owned arrays: [flag u32 | sum u64 | idfk f32 x vocab | norm f32 x n_docs].
+  const size_t off_sum = 256, off_idf = 512;
+  const size_t off_norm = off_idf + align_up((size_t)vocab * 4);
+  const size_t bytes = off_norm + align_up((size_t)n_docs * 4);
+  void* mem = nullptr;
+  hipError_t e = hipMalloc(&mem, bytes);
+  if (e != hipSuccess) return hip_fail(e, "sparse arrays allocation");
+  unsigned char* base = static_cast<unsigned char*>(mem);
+  unsigned int* d_flag = reinterpret_cast<unsigned int*>(base);
+  e = oprag::sparse_validate(vocab, n_docs, nnz, reinterpret_cast<const long long*>(term_indptr_dev), post_chunk_dev,
+                             post_tf_dev, doc_len_dev, d_flag, s);
+  unsigned int bad = 0;
+  if (e == hipSuccess) e = hipMemcpyAsync(&bad, d_flag, sizeof(bad), hipMemcpyDeviceToHost, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  if (e != hipSuccess) {
+    (void)hipFree(mem);
+    return hip_fail(e, "sparse index validation");
+  }
+  if (bad) {
+    (void)hipFree(mem);
+    return fail(OPRAG_E_INVALID, "sparse index fails %u structural checks (indptr/chunk order/range/tf/doc_len)", bad);
+  }
+  oprag::SparseIndex sp;
+  sp.vocab = vocab;
+  sp.n_docs = n_docs;
+  sp.nnz = nnz;
+  sp.term_indptr = reinterpret_cast<const long long*>(term_indptr_dev);
+  sp.post_chunk = post_chunk_dev;
+  sp.post_tf = post_tf_dev;
+  sp.idfk = reinterpret_cast<float*>(base + off_idf);
+  sp.norm = reinterpret_cast<float*>(base + off_norm);
+  sp.k1 = k1;
+  sp.b = b;
+  e = oprag::sparse_prepare(sp, doc_len_dev, reinterpret_cast<unsigned long long*>(base + off_sum), s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  if (e != hipSuccess) {
+    (void)hipFree(mem);
+    return hip_fail(e, "sparse index preparation");
+  }
+  if (sp.avgdl <= 0.0 && b > 0.f) {
+    (void)hipFree(mem);
+    return fail(OPRAG_E_INVALID, "all chunks are empty (avgdl = 0) while b > 0");
+  }
+  if (idx->sp_mem) (void)hipFree(idx->sp_mem);
+  idx->sp_mem = mem;
+  idx->sp = sp;
+  idx->has_sparse = true;
+  return ok();
+}
+
+oprag_status oprag_workspace_bytes(const oprag_index* idx, int32_t op, int64_t nq, int32_t k_dense, int32_t k_sparse,
+                                   size_t* bytes) {
+  if (oprag_status st = check_index(idx)) return st;
+  if (!bytes) return fail(OPRAG_E_INVALID, "bytes is NULL");
+  if (nq < 0) return fail(OPRAG_E_INVALID, "nq < 0");
+  switch (op) {
+    case OPRAG_OP_DENSE:
+      if (oprag_status st = check_k(k_dense, "k_dense")) return st;
+      *bytes = nq ? dense_ws(idx, nq, k_dense) : 0;
+      return ok();
+    case OPRAG_OP_SPARSE:
+      if (oprag_status st = check_k(k_sparse, "k_sparse")) return st;
+      *bytes = nq ? sparse_ws(idx, nq, k_sparse) : 0;
+      return ok();
+    case OPRAG_OP_HYBRID:
+      if (oprag_status st = check_k(k_dense, "k_dense")) return st;
+      if (oprag_status st = check_k(k_sparse, "k_sparse")) return st;
+      *bytes = nq ? hybrid_ws(idx, nq, k_dense, k_sparse) : 0;
+      return ok();
+    default:
+      return fail(OPRAG_E_INVALID, "op %d is not an oprag_op", op);
+  }
+}
+
+oprag_status oprag_search_dense(oprag_index* idx, const void* q_dev, int64_t nq, int32_t k, float* scores_dev,
+                                int64_t* ids_dev, void* workspace_dev, size_t workspace_bytes, void* stream) {
+  if (oprag_status st = check_index(idx)) return st;
+  if (oprag_status st = check_k(k, "k")) return st;
+  if (nq < 0 || nq > (int64_t)1 << 31) return fail(OPRAG_E_INVALID, "nq %lld out of range", (long long)nq);
+  if (nq == 0) return ok();
+  if (oprag_status st = check_buf(q_dev, "q_dev")) return st;
+  if (oprag_status st = check_buf(scores_dev, "scores_dev")) return st;
+  if (oprag_status st = check_buf(ids_dev, "ids_dev")) return st;
+  const size_t need = dense_ws(idx, nq, k);
+  if (need && (!workspace_dev || !aligned16(workspace_dev)))
+    return fail(OPRAG_E_INVALID, "workspace_dev is NULL or misaligned");
+  if (workspace_bytes < need) return fail(OPRAG_E_INVALID, "workspace too small: %zu < %zu bytes", workspace_bytes, need);
+  DeviceScope ds(idx->device);
+  if (ds.error() != hipSuccess) return hip_fail(ds.error(), "select device");
+  if (oprag_status st = do_dense(idx, q_dev, nq, k, scores_dev, ids_dev, workspace_dev, workspace_bytes,
+                                 static_cast<hipStream_t>(stream)))
+    return st;
+  return ok();
+}
+
+oprag_status oprag_search_sparse(oprag_index* idx, const int32_t* qterm_indptr_dev, const int32_t* qterms_dev,
+                                 int64_t nq, int32_t k, float* scores_dev, int64_t* ids_dev, void* workspace_dev,
+                                 size_t workspace_bytes, void* stream) {
+  if (oprag_status st = check_index(idx)) return st;
+  if (!idx->has_sparse) return fail(OPRAG_E_STATE, "no sparse index attached");
+  if (oprag_status st = check_k(k, "k")) return st;
+  if (nq < 0 || nq > (int64_t)1 << 24) return fail(OPRAG_E_INVALID, "nq %lld out of range", (long long)nq);
+  if (nq == 0) return ok();
+  if (oprag_status st = check_buf(qterm_indptr_dev, "qterm_indptr_dev")) return st;
+  if (!qterms_dev) return fail(OPRAG_E_INVALID, "qterms_dev is NULL");
+  if (oprag_status st = check_buf(scores_dev, "scores_dev")) return st;
+  if (oprag_status st = check_buf(ids_dev, "ids_dev")) return st;
+  const size_t need = sparse_ws(idx, nq, k);
+  if (need && (!workspace_dev || !aligned16(workspace_dev) || workspace_bytes < need))
+    return fail(OPRAG_E_INVALID, "workspace missing or too small (%zu < %zu bytes)", workspace_bytes, need);
+  DeviceScope ds(idx->device);
+  if (ds.error() != hipSuccess) return hip_fail(ds.error(), "select device");
+  const hipError_t e = oprag::launch_sparse(idx->sp, qterm_indptr_dev, qterms_dev, (int)nq, k, scores_dev,
+                                            reinterpret_cast<long long*>(ids_dev), workspace_dev,
+                                            static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "sparse search launch");
+  return ok();
+}
+
+oprag_status oprag_rrf_fuse(const int64_t* dense_ids_dev, int32_t k_dense, const int64_t* sparse_ids_dev,
+                            int32_t k_sparse, int64_t nq, int32_t rrf_k, int32_t k, float* fused_dev,
+                            int64_t* ids_dev, void* stream) {
+  if (oprag_status st = check_k(k_dense, "k_dense")) return st;
+  if (oprag_status st = check_k(k_sparse, "k_sparse")) return st;
+  if (oprag_status st = check_k(k, "k")) return st;
+  if (rrf_k < 0 || rrf_k > 1000000) return fail(OPRAG_E_INVALID, "rrf_k %d outside [0, 1000000]", rrf_k);
+  if (nq < 0 || nq > (int64_t)1 << 31) return fail(OPRAG_E_INVALID, "nq %lld out of range", (long long)nq);
+  if (nq == 0) return ok();
+  if (oprag_status st = check_buf(dense_ids_dev, "dense_ids_dev")) return st;
+  if (oprag_status st = check_buf(sparse_ids_dev, "sparse_ids_dev")) return st;
+  if (oprag_status st = check_buf(fused_dev, "fused_dev")) return st;
+  if (oprag_status st = check_buf(ids_dev, "ids_dev")) return st;
+  const hipError_t e = oprag::launch_rrf(reinterpret_cast<const long long*>(dense_ids_dev), k_dense,
+                                         reinterpret_cast<const long long*>(sparse_ids_dev), k_sparse, nq, rrf_k, k,
+                                         fused_dev, reinterpret_cast<long long*>(ids_dev),
+                                         static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "rrf launch");
+  return ok();
+}
+
+oprag_status oprag_search_hybrid(oprag_index* idx, const void* q_dev, const int32_t* qterm_indptr_dev,
+                                 const int32_t* qterms_dev, int64_t nq, int32_t k_dense, int32_t k_sparse,
+                                 int32_t rrf_k, int32_t k, float* fused_dev, int64_t* ids_dev, void* workspace_dev,
+                                 size_t workspace_bytes, void* stream) {
+  if (oprag_status st = check_index(idx)) return st;
+  if (!idx->has_sparse) return fail(OPRAG_E_STATE, "no sparse index attached");
+  if (oprag_status st = check_k(k_dense, "k_dense")) return st;
+  if (oprag_status st = check_k(k_sparse, "k_sparse")) return st;
+  if (oprag_status st = check_k(k, "k")) return st;
+  if (rrf_k < 0 || rrf_k > 1000000) return fail(OPRAG_E_INVALID, "rrf_k %d outside [0, 1000000]", rrf_k);
+  if (nq < 0 || nq > (int64_t)1 << 24) return fail(OPRAG_E_INVALID, "nq %lld out of range", (long long)nq);
+  if (nq == 0) return ok();
+  if (oprag_status st = check_buf(q_dev, "q_dev")) return st;
+  if (oprag_status st = check_buf(qterm_indptr_dev, "qterm_indptr_dev")) return st;
+  if (!qterms_dev) return fail(OPRAG_E_INVALID, "qterms_dev is NULL");
+  if (oprag_status st = check_buf(fused_dev, "fused_dev")) return st;
+  if (oprag_status st = check_buf(ids_dev, "ids_dev")) return st;
+  const size_t need = hybrid_ws(idx, nq, k_dense, k_sparse);
+  if (!workspace_dev || !aligned16(workspace_dev) || workspace_bytes < need)
+    return fail(OPRAG_E_INVALID, "workspace missing or too small (%zu < %zu bytes)", workspace_bytes, need);
+  DeviceScope ds(idx->device);
+  if (ds.error() != hipSuccess) return hip_fail(ds.error(), "select device");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  unsigned char* w = static_cast<unsigned char*>(workspace_dev);
+  int64_t* d_ids = reinterpret_cast<int64_t*>(w);
+  w += align_up((size_t)nq * k_dense * 8);
+  float* d_sc = reinterpret_cast<float*>(w);
+  w += align_up((size_t)nq * k_dense * 4);
+  int64_t* s_ids = reinterpret_cast<int64_t*>(w);
+  w += align_up((size_t)nq * k_sparse * 8);
+  float* s_sc = reinterpret_cast<float*>(w);
+  w += align_up((size_t)nq * k_sparse * 4);
+  const size_t inner = workspace_bytes - (size_t)(w - static_cast<unsigned char*>(workspace_dev));
+  if (oprag_status st = do_dense(idx, q_dev, nq, k_dense, d_sc, d_ids, w, inner, s)) return st;
+  hipError_t e = oprag::launch_sparse(idx->sp, qterm_indptr_dev, qterms_dev, (int)nq, k_sparse, s_sc,
+                                      reinterpret_cast<long long*>(s_ids), w, s);
+  if (e != hipSuccess) return hip_fail(e, "sparse search launch");
+  e = oprag::launch_rrf(reinterpret_cast<const long long*>(d_ids), k_dense, reinterpret_cast<const long long*>(s_ids),
+                        k_sparse, nq, rrf_k, k, fused_dev, reinterpret_cast<long long*>(ids_dev), s);
+  if (e != hipSuccess) return hip_fail(e, "rrf launch");
+  return ok();
+}
+
+}  // extern "C"

@@ -1,0 +1,352 @@
+// Lexical retrieval: BM25 over an inverted-postings (CSR term -> (chunk, tf)) index that
+// visits only the chunks containing a query term yet gives exact full-corpus BM25 scores
+// (Section 4.4), with partial top-k selection instead of a full sort.
+//
+// Scoring reading (the paper does not fix the variant):
+//   idf(t)  = ln(1 + (N - df + 0.5) / (df + 0.5)),  df = postings of t,  N = chunks;
+//   score   = sum over query-term OCCURRENCES t of idf(t) tf (k1 + 1) / (tf + k1 (1 - b + b dl / avgdl)).
+// Per-term factors idf(t)(k1 + 1) and per-chunk length norms are computed once in fp64 at
+// attach time and stored as fp32; scores accumulate in fp32.
+//
+// One workgroup scores one query over a range of up to 32,768 chunks held as an fp32
+// accumulator in LDS (128 KiB).  Terms are applied one after another with a barrier in
+// between, and a term's postings name distinct chunks, so every chunk's score is summed
+// in query-term order with no atomics: the result is deterministic.  A 4 x 8-bit radix
+// select over the accumulator then finds the k-th best score, and the winners are sorted
+// (score desc, chunk asc) by a wave-wide bitonic network.
+#include <algorithm>
+
+#include "oprag_internal.h"
+#include "select.h"
+
+namespace oprag {
+namespace {
+
+using namespace dev;
+
+constexpr int kNT = 512;  // threads per scoring workgroup
+
+__global__ void validate_kernel(int vocab, long long n_docs, long long nnz, const long long* indptr,
+                                const int* chunk, const int* tf, const int* doc_len, unsigned int* flag) {
+  const long long tid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  const long long stride = (long long)gridDim.x * blockDim.x;
+  if (tid == 0 && (indptr[0] != 0 || indptr[vocab] != nnz)) atomicAdd(flag, 1u);
+  for (long long t = tid; t < vocab; t += stride) {
+    const long long lo = indptr[t], hi = indptr[t + 1];
+    if (lo < 0 || hi < lo || hi > nnz) {
+      atomicAdd(flag, 1u);
+      continue;
+    }
+    int prev = -1;
+    for (long long p = lo; p < hi; ++p) {
+      const int c = chunk[p];
+      if (c < 0 || c >= n_docs || c <= prev || tf[p] < 1) {
+        atomicAdd(flag, 1u);
+        break;
+      }
+      prev = c;
+    }
+  }
+  for (long long dd = tid; dd < n_docs; dd += stride)
+    if (doc_len[dd] < 0) atomicAdd(flag, 1u);
+}
+
+__global__ void doclen_sum_kernel(const int* doc_len, long long n_docs, unsigned long long* sum) {
+  __shared__ unsigned long long part[256];
+  unsigned long long s = 0;
+  for (long long i = threadIdx.x; i < n_docs; i += blockDim.x) s += (unsigned long long)doc_len[i];
+  part[threadIdx.x] = s;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    unsigned long long t = 0;
+    for (int i = 0; i < 256; ++i) t += part[i];
+    *sum = t;
+  }
+}
+
+__global__ void prepare_kernel(int vocab, long long n_docs, const long long* indptr, const int* doc_len, double avgdl,
+                               double k1, double b, float* idfk, float* norm) {
+  const long long tid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  const long long stride = (long long)gridDim.x * blockDim.x;
+  const double N = (double)n_docs;
+  for (long long t = tid; t < vocab; t += stride) {
+    const double df = (double)(indptr[t + 1] - indptr[t]);
+    idfk[t] = (float)(log(1.0 + (N - df + 0.5) / (df + 0.5)) * (k1 + 1.0));
+  }
+  for (long long dd = tid; dd < n_docs; dd += stride)
+    norm[dd] = (float)(k1 * (1.0 - b + b * (double)doc_len[dd] / avgdl));
+}
+
+// First position p in [lo, hi) with chunk[p] >= key (chunks ascending within a term).
+__device__ __forceinline__ long long lower_bound(const int* chunk, long long lo, long long hi, long long key) {
+  while (lo < hi) {
+    const long long mid = (lo + hi) >> 1;
+    if (chunk[mid] < key) lo = mid + 1;
+    else hi = mid;
+  }
+  return lo;
+}
+
+// Block-wide exclusive prefix sum of one int per thread (kNT threads).
+__device__ __forceinline__ int block_excl_scan(int v, int* wave_tot) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  int x = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(x, o, 64);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) wave_tot[w] = x;
+  __syncthreads();
+  int before = 0;
+  for (int i = 0; i < w; ++i) before += wave_tot[i];
+  __syncthreads();
+  return before + x - v;
+}
+
+struct SparseArgs {
+  int vocab;
+  long long n_docs;
+  const long long* indptr;
+  const int* chunk;
+  const int* tf;
+  const float* idfk;
+  const float* norm;
+  const int* qterm_indptr;
+  const int* qterms;
+  int nq;
+  int k;
+  int n_ranges;
+  float* out_scores;            // final output when n_ranges == 1
+  long long* out_ids;
+  unsigned long long* partial;  // [nq x n_ranges x k] when n_ranges > 1
+};
+
+__global__ __launch_bounds__(kNT) void bm25_kernel(SparseArgs a) {
+  __shared__ __attribute__((aligned(16))) float acc[kSparseRange];
+  __shared__ unsigned int hist[256];
+  __shared__ int wave_tot[kNT / 64];
+  __shared__ unsigned long long selbuf[kMaxK];
+  __shared__ unsigned int s_prefix, s_need, s_take_all, s_ngt;
+  __shared__ long long s_lo, s_hi;
+
+  const int tid = threadIdx.x;
+  const int q = blockIdx.x / a.n_ranges;
+  const int range = blockIdx.x % a.n_ranges;
+  const long long d0 = (long long)range * kSparseRange;
+  const int len = (int)std::min<long long>(kSparseRange, a.n_docs - d0);
+
+  for (int i = tid; i < kSparseRange; i += kNT) acc[i] = 0.f;
+  __syncthreads();
+
+  const int tb = a.qterm_indptr[q], te = a.qterm_indptr[q + 1];
+  for (int j = tb; j < te; ++j) {
+    const int t = a.qterms[j];
+    if (t < 0 || t >= a.vocab) continue;  // unknown terms match nothing (uniform branch)
+    if (tid == 0) {
+      long long lo = a.indptr[t], hi = a.indptr[t + 1];
+      if (a.n_ranges > 1) {
+        lo = lower_bound(a.chunk, lo, hi, d0);
+        hi = lower_bound(a.chunk, lo, hi, d0 + len);
+      }
+      s_lo = lo;
+      s_hi = hi;
+    }
+    __syncthreads();
+    const long long lo = s_lo, hi = s_hi;
+    const float w = a.idfk[t];
+    for (long long p = lo + tid; p < hi; p += kNT) {
+      const int c = a.chunk[p];
+      const float f = (float)a.tf[p];
+      acc[c - d0] += (w * f) / (f + a.norm[c]);
+    }
+    __syncthreads();
+  }
+
+  // ---- radix select of the k-th largest positive score (positive fp32 bits order as uints)
+  const uint32_t* keys = reinterpret_cast<const uint32_t*>(acc);
+  if (tid == 0) {
+    s_prefix = 0u;
+    s_need = (unsigned)a.k;
+    s_take_all = 0u;
+  }
+  for (int pass = 0; pass < 4; ++pass) {
+    const int shift = 24 - 8 * pass;
+    const uint32_t hmask = pass == 0 ? 0u : (0xffffffffu << (shift + 8));
+    for (int i = tid; i < 256; i += kNT) hist[i] = 0u;
+    __syncthreads();
+    const uint32_t prefix = s_prefix;
+    if (!s_take_all) {
+      for (int i = tid; i < len; i += kNT) {
+        const uint32_t u = keys[i];
+        if (u != 0u && (u & hmask) == prefix) atomicAdd(&hist[(u >> shift) & 255u], 1u);
+      }
+    }
+    __syncthreads();
+    if (tid == 0 && !s_take_all) {
+      unsigned int cum = 0, need = s_need;
+      int bsel = -1;
+      for (int bin = 255; bin >= 0; --bin) {
+        if (cum + hist[bin] >= need) {
+          bsel = bin;
+          break;
+        }
+        cum += hist[bin];
+      }
+      if (bsel < 0) {
+        s_take_all = 1u;  // fewer than k positive scores (only possible in pass 0)
+      } else {
+        s_prefix = prefix | ((uint32_t)bsel << shift);
+        s_need = need - cum;
+      }
+    }
+    __syncthreads();
+  }
+  const bool take_all = s_take_all != 0u;
+  const uint32_t T = s_prefix;
+  const unsigned int need_eq = take_all ? 0u : s_need;
+
+  // ---- collect: every key > T, then the need_eq smallest chunk ids with key == T
+  if (tid == 0) s_ngt = 0u;
+  __syncthreads();
+  const int per = (len + kNT - 1) / kNT;
+  const int b0 = tid * per, b1 = std::min(len, b0 + per);
+  int n_eq = 0;
+  for (int i = b0; i < b1; ++i) {
+    const uint32_t u = keys[i];
+    if (u == 0u) continue;
+    if (take_all ? true : u > T) {
+      const unsigned int slot = atomicAdd(&s_ngt, 1u);
+      selbuf[slot] = ((u64)u << 32) | (uint32_t)(~(uint32_t)(d0 + i));
+    } else if (u == T) {
+      ++n_eq;
+    }
+  }
+  const int before = block_excl_scan(n_eq, wave_tot);
+  if (!take_all && n_eq && before < (int)need_eq) {
+    const unsigned int ngt = (unsigned int)a.k - need_eq;
+    int r = before;
+    for (int i = b0; i < b1 && r < (int)need_eq; ++i) {
+      if (keys[i] == T) {
+        selbuf[ngt + r] = ((u64)T << 32) | (uint32_t)(~(uint32_t)(d0 + i));
+        ++r;
+      }
+    }
+  }
+  __syncthreads();
+  const int nsel = take_all ? (int)s_ngt : a.k;
+
+  // ---- sort the winners (<= 128) with wave 0 and write them out
+  if (tid < 64) {
+    const int lane = tid;
+    u64 x0 = lane < nsel ? selbuf[lane] : 0ull;
+    u64 x1 = lane + 64 < nsel ? selbuf[lane + 64] : 0ull;
+    x0 = wave_sort64_desc(x0, lane);
+    x1 = wave_sort64_desc(x1, lane);
+    u64 q1 = 0ull;
+    wave_merge128(x0, q1, x1, lane);
+    // The stored key is the raw fp32 bit pattern of a positive score.
+    if (a.n_ranges == 1) {
+      const long long o = (long long)q * a.k;
+      if (lane < a.k) {
+        a.out_ids[o + lane] = x0 ? (long long)comp_row(x0) : -1ll;
+        a.out_scores[o + lane] = x0 ? __uint_as_float((uint32_t)(x0 >> 32)) : -__builtin_inff();
+      }
+      if (lane + 64 < a.k) {
+        a.out_ids[o + lane + 64] = q1 ? (long long)comp_row(q1) : -1ll;
+        a.out_scores[o + lane + 64] = q1 ? __uint_as_float((uint32_t)(q1 >> 32)) : -__builtin_inff();
+      }
+    } else {
+      unsigned long long* dst = a.partial + ((long long)q * a.n_ranges + range) * a.k;
+      if (lane < a.k) dst[lane] = x0;
+      if (lane + 64 < a.k) dst[lane + 64] = q1;
+    }
+  }
+}
+
+// Merge P partial lists of kp composites per query (raw positive-fp32 keys) into the top-k.
+__global__ __launch_bounds__(64) void partial_merge_kernel(const unsigned long long* partial, int P, int kp, int nq,
+                                                           int k, float* out_scores, long long* out_ids) {
+  const int q = blockIdx.x, lane = threadIdx.x;
+  if (q >= nq) return;
+  u64 q0 = 0ull, q1 = 0ull;
+  const long long n = (long long)P * kp;
+  const unsigned long long* src = partial + (long long)q * n;
+  for (long long base = 0; base < n; base += 64) {
+    const u64 c = base + lane < n ? src[base + lane] : 0ull;
+    wave_offer(q0, q1, c, queue_at(q0, q1, k - 1), lane);
+  }
+  const long long o = (long long)q * k;
+  if (lane < k) {
+    out_ids[o + lane] = q0 ? (long long)comp_row(q0) : -1ll;
+    out_scores[o + lane] = q0 ? __uint_as_float((uint32_t)(q0 >> 32)) : -__builtin_inff();
+  }
+  if (lane + 64 < k) {
+    out_ids[o + lane + 64] = q1 ? (long long)comp_row(q1) : -1ll;
+    out_scores[o + lane + 64] = q1 ? __uint_as_float((uint32_t)(q1 >> 32)) : -__builtin_inff();
+  }
+}
+
+}  // namespace
+
+hipError_t sparse_validate(int vocab, long long n_docs, long long nnz, const long long* indptr, const int* chunk,
+                           const int* tf, const int* doc_len, unsigned int* d_flag, hipStream_t s) {
+  hipError_t e = hipMemsetAsync(d_flag, 0, sizeof(unsigned int), s);
+  if (e != hipSuccess) return e;
+  const long long work = std::max<long long>(vocab, n_docs);
+  const int blocks = (int)std::min<long long>(1024, (work + 255) / 256);
+  hipLaunchKernelGGL(validate_kernel, dim3(std::max(1, blocks)), dim3(256), 0, s, vocab, n_docs, nnz, indptr, chunk,
+                     tf, doc_len, d_flag);
+  return hipGetLastError();
+}
+
+hipError_t sparse_prepare(SparseIndex& sp, const int* doc_len, unsigned long long* dsum, hipStream_t s) {
+  hipLaunchKernelGGL(doclen_sum_kernel, dim3(1), dim3(256), 0, s, doc_len, sp.n_docs, dsum);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  unsigned long long total = 0;
+  e = hipMemcpyAsync(&total, dsum, sizeof(total), hipMemcpyDeviceToHost, s);
+  if (e != hipSuccess) return e;
+  e = hipStreamSynchronize(s);
+  if (e != hipSuccess) return e;
+  sp.avgdl = (double)total / (double)sp.n_docs;
+  const long long work = std::max<long long>(sp.vocab, sp.n_docs);
+  const int blocks = (int)std::min<long long>(1024, (work + 255) / 256);
+  hipLaunchKernelGGL(prepare_kernel, dim3(std::max(1, blocks)), dim3(256), 0, s, sp.vocab, sp.n_docs, sp.term_indptr,
+                     doc_len, sp.avgdl, (double)sp.k1, (double)sp.b, sp.idfk, sp.norm);
+  return hipGetLastError();
+}
+
+size_t sparse_workspace_bytes(long long n_docs, int nq, int k) {
+  const long long n_ranges = (n_docs + kSparseRange - 1) / kSparseRange;
+  if (n_ranges <= 1) return 0;
+  return (size_t)nq * (size_t)n_ranges * (size_t)k * sizeof(unsigned long long);
+}
+
+hipError_t launch_sparse(const SparseIndex& sp, const int* qterm_indptr, const int* qterms, int nq, int k,
+                         float* out_scores, long long* out_ids, void* ws, hipStream_t s) {
+  SparseArgs a;
+  a.vocab = sp.vocab;
+  a.n_docs = sp.n_docs;
+  a.indptr = sp.term_indptr;
+  a.chunk = sp.post_chunk;
+  a.tf = sp.post_tf;
+  a.idfk = sp.idfk;
+  a.norm = sp.norm;
+  a.qterm_indptr = qterm_indptr;
+  a.qterms = qterms;
+  a.nq = nq;
+  a.k = k;
+  a.n_ranges = (int)((sp.n_docs + kSparseRange - 1) / kSparseRange);
+  a.out_scores = out_scores;
+  a.out_ids = out_ids;
+  a.partial = static_cast<unsigned long long*>(ws);
+  hipLaunchKernelGGL(bm25_kernel, dim3((unsigned)(nq * a.n_ranges)), dim3(kNT), 0, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || a.n_ranges == 1) return e;
+  hipLaunchKernelGGL(partial_merge_kernel, dim3((unsigned)nq), dim3(64), 0, s, a.partial, a.n_ranges, k, nq, k,
+                     out_scores, out_ids);
+  return hipGetLastError();
+}
+
+}  // namespace oprag

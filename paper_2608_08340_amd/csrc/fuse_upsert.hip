@@ -1,0 +1,168 @@
+// Reciprocal rank fusion of a dense and a sparse top list, and append-only upsert.
+//
+// Fusion: the hybrid path combines dense and lexical evidence over the full corpus
+// (Section 4.4).  The hybrid workload fuses the two top lists with reciprocal rank fusion
+// (Cormack, Clarke and Buettcher, SIGIR 2009): fused(d) = sum over the lists L holding d of
+// 1 / (k_rrf + rank_L(d)), 1-based ranks.  Fused values are compared exactly as fractions
+// num / den in 64-bit integers (den = product of at most two (k_rrf + rank) factors), so
+// exact ties such as 1/63 = 2/126 stay ties and are broken by ascending id.
+//
+// Upsert: Op_upsert (Section 3.2, "Upsert") inserts new embeddings, I' = Op_upsert(I, E; b_u),
+// committed in bulk.  Here: rows are appended at ids n_rows .. n_rows + m - 1 of a
+// preallocated slab, converting fp32 input to the slab's bf16 / fp16 with
+// round-to-nearest-even when the dtypes differ.
+#include <algorithm>
+
+#include "oprag_internal.h"
+#include "select.h"
+
+namespace oprag {
+namespace {
+
+using namespace dev;
+
+constexpr int kMaxCand = 2 * kMaxK;
+
+// One wave per query.
+__global__ __launch_bounds__(64) void rrf_kernel(const long long* dense_ids, int kd, const long long* sparse_ids, int ks,
+                                                 long long nq, int rrf_k, int k, float* out_fused, long long* out_ids) {
+  __shared__ long long cid[kMaxCand];
+  __shared__ long long cnum[kMaxCand];
+  __shared__ long long cden[kMaxCand];
+  __shared__ long long sp_ids[kMaxK];
+  __shared__ int s_nc;
+  const long long q = blockIdx.x;
+  const int lane = threadIdx.x;
+  if (q >= nq) return;
+  const long long* D = dense_ids + q * kd;
+  const long long* S = sparse_ids + q * ks;
+  for (int j = lane; j < ks; j += 64) sp_ids[j] = S[j];
+  if (lane == 0) s_nc = 0;
+  __syncthreads();
+  // Dense entries (rank = position + 1), with the sparse rank of the same id if present.
+  for (int i = lane; i < kd; i += 64) {
+    const long long id = D[i];
+    if (id < 0) continue;
+    const long long a = (long long)rrf_k + i + 1;
+    long long num = 1, den = a;
+    for (int j = 0; j < ks; ++j) {
+      if (sp_ids[j] == id) {
+        const long long b = (long long)rrf_k + j + 1;
+        num = a + b;
+        den = a * b;
+        break;
+      }
+    }
+    const int slot = atomicAdd(&s_nc, 1);
+    cid[slot] = id;
+    cnum[slot] = num;
+    cden[slot] = den;
+  }
+  // Sparse entries absent from the dense list.
+  for (int j = lane; j < ks; j += 64) {
+    const long long id = sp_ids[j];
+    if (id < 0) continue;
+    bool in_dense = false;
+    for (int i = 0; i < kd; ++i)
+      if (D[i] == id) {
+        in_dense = true;
+        break;
+      }
+    if (in_dense) continue;
+    const int slot = atomicAdd(&s_nc, 1);
+    cid[slot] = id;
+    cnum[slot] = 1;
+    cden[slot] = (long long)rrf_k + j + 1;
+  }
+  __syncthreads();
+  const int nc = s_nc;
+  // Rank of every candidate = number of candidates that beat it (exact fraction compare).
+  for (int c = lane; c < nc; c += 64) {
+    const long long n0 = cnum[c], d0 = cden[c], id0 = cid[c];
+    int rank = 0;
+    for (int o = 0; o < nc; ++o) {
+      const long long lhs = cnum[o] * d0, rhs = n0 * cden[o];
+      rank += (lhs > rhs || (lhs == rhs && cid[o] < id0)) ? 1 : 0;
+    }
+    if (rank < k) {
+      out_ids[q * k + rank] = id0;
+      out_fused[q * k + rank] = (float)((double)n0 / (double)d0);
+    }
+  }
+  for (int r = nc + lane; r < k; r += 64) {
+    out_ids[q * k + r] = -1;
+    out_fused[q * k + r] = -__builtin_inff();
+  }
+}
+
+__device__ __forceinline__ unsigned short f32_to_bf16_rne(float x) {
+  const uint32_t u = __float_as_uint(x);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (unsigned short)((u >> 16) | 0x40u);  // NaN stays (quiet) NaN
+  return (unsigned short)((u + 0x7fffu + ((u >> 16) & 1u)) >> 16);
+}
+
+// Same-dtype copy, 16 bytes per thread per step.
+__global__ void copy16_kernel(const uint4* __restrict__ src, uint4* __restrict__ dst, long long n16) {
+  const long long stride = (long long)gridDim.x * blockDim.x;
+  for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += stride) dst[i] = src[i];
+}
+
+// fp32 -> bf16 (DT 1) or fp16 (DT 2), 8 elements per thread per step.
+template <int DT>
+__global__ void convert8_kernel(const float4* __restrict__ src, uint4* __restrict__ dst, long long n8) {
+  const long long stride = (long long)gridDim.x * blockDim.x;
+  for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < n8; i += stride) {
+    const float4 a = src[2 * i], b = src[2 * i + 1];
+    const float v[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+    unsigned short h[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      if constexpr (DT == kDtypeBF16) {
+        h[j] = f32_to_bf16_rne(v[j]);
+      } else {
+        _Float16 f = (_Float16)v[j];  // v_cvt_f16_f32: round to nearest even
+        h[j] = __builtin_bit_cast(unsigned short, f);
+      }
+    }
+    uint4 o;
+    o.x = h[0] | ((uint32_t)h[1] << 16);
+    o.y = h[2] | ((uint32_t)h[3] << 16);
+    o.z = h[4] | ((uint32_t)h[5] << 16);
+    o.w = h[6] | ((uint32_t)h[7] << 16);
+    dst[i] = o;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_rrf(const long long* dense_ids, int k_dense, const long long* sparse_ids, int k_sparse, long long nq,
+                      int rrf_k, int k, float* out_fused, long long* out_ids, hipStream_t s) {
+  hipLaunchKernelGGL(rrf_kernel, dim3((unsigned)nq), dim3(64), 0, s, dense_ids, k_dense, sparse_ids, k_sparse, nq, rrf_k,
+                     k, out_fused, out_ids);
+  return hipGetLastError();
+}
+
+hipError_t launch_upsert(void* slab, int slab_dtype, int d, long long first_row, const void* rows, int rows_dtype,
+                         long long m, hipStream_t s) {
+  const size_t es = slab_dtype == kDtypeF32 ? 4 : 2;
+  unsigned char* dst = static_cast<unsigned char*>(slab) + (size_t)first_row * d * es;
+  const long long n = m * (long long)d;
+  if (rows_dtype == slab_dtype) {
+    const long long n16 = n * (long long)es / 16;
+    const int blocks = (int)std::min<long long>(4096, (n16 + 255) / 256);
+    hipLaunchKernelGGL(copy16_kernel, dim3(std::max(1, blocks)), dim3(256), 0, s, static_cast<const uint4*>(rows),
+                       reinterpret_cast<uint4*>(dst), n16);
+  } else {
+    const long long n8 = n / 8;
+    const int blocks = (int)std::min<long long>(4096, (n8 + 255) / 256);
+    if (slab_dtype == kDtypeBF16)
+      hipLaunchKernelGGL(convert8_kernel<kDtypeBF16>, dim3(std::max(1, blocks)), dim3(256), 0, s,
+                         static_cast<const float4*>(rows), reinterpret_cast<uint4*>(dst), n8);
+    else
+      hipLaunchKernelGGL(convert8_kernel<kDtypeF16>, dim3(std::max(1, blocks)), dim3(256), 0, s,
+                         static_cast<const float4*>(rows), reinterpret_cast<uint4*>(dst), n8);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace oprag

@@ -1,0 +1,91 @@
+// Internal declarations shared by the host runtime (api.cpp) and the HIP kernels.
+// Not part of the C ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+namespace oprag {
+
+constexpr int kMaxK = 128;                 // largest k any list may ask for
+constexpr int kMaxQPerLaunch = 32768;      // queries per dense launch = control-block capacity
+constexpr int kMinBN = 16;                 // smallest query block of any dense kernel
+constexpr int kDtypeF32 = 0, kDtypeBF16 = 1, kDtypeF16 = 2;
+
+// Per-index device control block for the dense search.  Every dense launch leaves it
+// zeroed: the last workgroup of each query block resets what it used.
+struct ControlBlock {
+  uint32_t* thr = nullptr;   // [kMaxQPerLaunch] running k-th-best score key per query
+  uint32_t* cnt = nullptr;   // [kMaxQPerLaunch] candidates appended per query
+  uint32_t* done = nullptr;  // [kMaxQPerLaunch / kMinBN] finished workgroups per query block
+};
+
+struct DenseArgs {
+  const void* X;                // slab rows [n_rows x d]
+  long long n_rows;
+  int d;
+  const void* Q;                // queries of this launch [nq x d]
+  int nq;
+  int k;
+  int n_qblocks;
+  int n_chunks;
+  long long rows_per_chunk;     // multiple of the kernel's tile rows
+  uint32_t* thr;
+  uint32_t* cnt;
+  uint32_t* done;
+  unsigned long long* cand;     // [nq x cap] candidate composite keys
+  long long cap;
+  float* out_scores;            // [nq x k]
+  long long* out_ids;           // [nq x k]
+};
+
+struct DensePlan {
+  int kernel = 0;               // index into the dense kernel table
+  int bn = 0;                   // queries per workgroup
+  int tile_rows = 0;            // rows per tile
+  int n_qblocks = 0;
+  int n_chunks = 0;
+  long long rows_per_chunk = 0;
+  long long cap = 0;            // candidate slots per query
+  long long grid = 0;
+  size_t lds_bytes = 0;
+};
+
+DensePlan plan_dense(int dtype, int d, long long n_rows, int nq, int k);
+size_t dense_workspace_bytes(const DensePlan& p, int nq);
+hipError_t launch_dense(const DensePlan& p, int dtype, const DenseArgs& a, hipStream_t s);
+
+// ---------------------------------------------------------------- sparse (BM25)
+struct SparseIndex {
+  int vocab = 0;
+  long long n_docs = 0;
+  long long nnz = 0;
+  const long long* term_indptr = nullptr;   // caller-owned
+  const int* post_chunk = nullptr;          // caller-owned
+  const int* post_tf = nullptr;             // caller-owned
+  float* idfk = nullptr;                    // library-owned [vocab]: idf(t) * (k1 + 1)
+  float* norm = nullptr;                    // library-owned [n_docs]: k1 * (1 - b + b * dl / avgdl)
+  double avgdl = 0.0;
+  float k1 = 0.f, b = 0.f;
+};
+
+constexpr int kSparseRange = 32768;        // chunks scored per workgroup (LDS accumulator)
+
+// Validates the CSR on the device; returns the number of violations found (synchronous).
+hipError_t sparse_validate(int vocab, long long n_docs, long long nnz, const long long* indptr,
+                           const int* chunk, const int* tf, const int* doc_len, unsigned int* d_flag,
+                           hipStream_t s);
+hipError_t sparse_prepare(SparseIndex& sp, const int* doc_len, unsigned long long* d_sum, hipStream_t s);
+size_t sparse_workspace_bytes(long long n_docs, int nq, int k);
+hipError_t launch_sparse(const SparseIndex& sp, const int* qterm_indptr, const int* qterms, int nq, int k,
+                         float* out_scores, long long* out_ids, void* ws, hipStream_t s);
+
+// ---------------------------------------------------------------- fusion and upsert
+hipError_t launch_rrf(const long long* dense_ids, int k_dense, const long long* sparse_ids, int k_sparse,
+                      long long nq, int rrf_k, int k, float* out_fused, long long* out_ids, hipStream_t s);
+hipError_t launch_upsert(void* slab, int slab_dtype, int d, long long first_row, const void* rows,
+                         int rows_dtype, long long m, hipStream_t s);
+
+}  // namespace oprag

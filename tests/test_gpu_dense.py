@@ -1,0 +1,144 @@
+"""Dense exact top-k on the GPU against the fp64 oracle (parity), through the C ABI."""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import accept
+from oracle import dense as od
+from oracle.storage import decode
+from tests.gpu_helpers import check_dense, device, log, make_index, oracle_scores
+
+pytestmark = pytest.mark.gpu
+
+
+def _run(rows, queries, k, dtype, capacity=None):
+    dev = device()
+    idx = make_index(rows, dtype, capacity)
+    sc, ids = idx.search_dense(queries.to(dev), k)
+    torch.cuda.synchronize()
+    return idx, sc.cpu(), ids.cpu()
+
+
+def test_tiny_f32_1k_x_384():
+    """1,024 x 384 fp32 rows, 16 perturbed queries, exact cosine top-5 (rtol 1e-5)."""
+    device()
+    w = synth.tiny_dense()
+    log("tiny f32", tuple(w.rows.shape), w.k)
+    _, sc, ids = _run(w.rows, w.queries, w.k, "f32")
+    S, X, Q = oracle_scores(w.rows, w.queries, "f32")
+    check_dense(S, X, Q, ids, sc, w.k, "f32")
+    # the noisy copy of a chunk finds its source first at this size
+    assert (ids[:, 0].numpy() == w.src).all()
+
+
+@pytest.fixture(scope="module")
+def c2():
+    device()
+    return synth.dense_32k()
+
+
+@pytest.mark.parametrize("nq", [1, 16, 256, 1024])
+def test_32k_x_1024_bf16_top5(c2, nq):
+    """32,768 x 1,024 bf16 mixture rows; query batches 1, 16, 256, 1,024; exact top-5."""
+    log("32k bf16 nq", nq)
+    q = c2.queries[:nq].contiguous()
+    _, sc, ids = _run(c2.rows, q, 5, "bf16")
+    S, X, Q = oracle_scores(c2.rows, q, "bf16")
+    reps = check_dense(S, X, Q, ids, sc, 5, "bf16")
+    assert all(r.recall == 1.0 for r in reps)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f16", "f32"])
+@pytest.mark.parametrize("k", [1, 5, 16, 100])
+def test_exact_integer_scores_and_ties(dtype, k):
+    """Small-integer vectors give exact dot products with many exact ties: ids must match the
+    oracle exactly, ties by ascending id."""
+    device()
+    g = np.random.default_rng(1000 + k)
+    n, d, nq = 3001, 128, 37
+    X = g.integers(-2, 3, size=(n, d)).astype(np.float32)
+    Q = g.integers(-2, 3, size=(nq, d)).astype(np.float32)
+    rows, qs = synth.to_storage(X, dtype), synth.to_storage(Q, dtype)
+    _, sc, ids = _run(rows, qs, k, dtype)
+    S = Q.astype(np.float64) @ X.astype(np.float64).T
+    ref_ids, ref_sc = od.topk_from_scores(S, k)
+    assert np.array_equal(ids.numpy(), ref_ids)
+    assert np.array_equal(sc.numpy().astype(np.float64), ref_sc)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
+@pytest.mark.parametrize("n,nq,k", [(3000, 1, 7), (3000, 17, 8), (3000, 65, 9), (2500, 130, 16), (3000, 40, 17),
+                                    (4100, 33, 64), (5000, 70, 100), (3000, 9, 128), (64, 5, 100), (1, 3, 4)])
+def test_ragged_sizes_and_k(dtype, n, nq, k):
+    """Row counts that are not tile multiples, query counts that are not block multiples, k across
+    both selection strategies, k larger than the index (padding)."""
+    device()
+    w = synth.mixture_dense(200 + n % 97, n, 64, 16, nq, k, dtype)
+    _, sc, ids = _run(w.rows, w.queries, k, dtype)
+    S, X, Q = oracle_scores(w.rows, w.queries, dtype)
+    check_dense(S, X, Q, ids, sc, k, dtype, label=f"n={n} nq={nq} k={k}")
+
+
+def test_empty_index_pads():
+    dev = device()
+    from paper_2608_08340_amd import Index
+    idx = Index(64, 100, torch.bfloat16)
+    q = synth.to_storage(np.ones((3, 64), np.float32), "bf16").to(dev)
+    sc, ids = idx.search_dense(q, 5)
+    torch.cuda.synchronize()
+    assert (ids.cpu() == -1).all() and torch.isneginf(sc.cpu()).all()
+
+
+def test_repeatable_batch_invariant_prefix_consistent(c2):
+    dev = device()
+    idx = make_index(c2.rows, "bf16")
+    q = c2.queries[:300].to(dev)
+    s1, i1 = idx.search_dense(q, 10)
+    s2, i2 = idx.search_dense(q, 10)
+    s3, i3 = idx.search_dense(q[100:140].contiguous(), 10)
+    s5, i5 = idx.search_dense(q, 5)
+    torch.cuda.synchronize()
+    assert torch.equal(i1, i2) and torch.equal(s1.view(torch.int32), s2.view(torch.int32))
+    assert torch.equal(i3, i1[100:140]) and torch.equal(s3, s1[100:140])
+    assert torch.equal(i5, i1[:, :5]) and torch.equal(s5, s1[:, :5])
+
+
+def test_more_queries_than_one_launch():
+    """More queries than one launch's control block holds: the host splits the batch."""
+    device()
+    w = synth.mixture_dense(300, 512, 64, 8, 33000, 3, "bf16")
+    _, sc, ids = _run(w.rows, w.queries, 3, "bf16")
+    S, X, Q = oracle_scores(w.rows, w.queries, "bf16")
+    sel = np.r_[0:50, 32700:33000]
+    check_dense(S[sel], X, Q[sel], ids[sel], sc[sel], 3, "bf16", strict=False)
+
+
+@pytest.mark.timeout(600)
+def test_1m_x_768_bf16_top10_sampled():
+    """1,048,576 x 768 bf16 rows (4,096-cluster mixture), 1,024 queries, exact top-10.
+    Every query: returned scores against fp64 and list order; 64 sampled queries: full oracle."""
+    dev = device()
+    log("generating 1M x 768")
+    w = synth.mixture_dense(4, 1 << 20, 768, 4096, 1024, 10, "bf16")
+    idx = make_index(w.rows, "bf16")
+    sc, ids = idx.search_dense(w.queries.to(dev), 10)
+    torch.cuda.synchronize()
+    sc, ids = sc.cpu().numpy(), ids.cpu().numpy()
+    log("checking")
+    Xb = synth.storage_bits(w.rows)
+    Q = decode(synth.storage_bits(w.queries), "bf16")
+    # every query: score parity of what was returned (fp64 recomputation) and order
+    Xr = decode(Xb[ids.reshape(-1)], "bf16").reshape(1024, 10, 768)
+    s_ret = np.einsum("qkd,qd->qk", Xr, Q)
+    err = accept.strict_err(np.einsum("qkd,qd->qk", np.abs(Xr), np.abs(Q)), 768)
+    for q in range(1024):
+        rep = accept.certificate(s_ret[q], ids[q], sc[q], err[q])
+        assert rep.ok, (q, rep.problems)
+    # sampled queries: full fp64 scores and the complete acceptance rules
+    samp = np.random.default_rng(4).choice(1024, 64, replace=False)
+    S = np.zeros((64, 1 << 20))
+    for lo in range(0, 1 << 20, 1 << 17):
+        S[:, lo:lo + (1 << 17)] = od.scores(decode(Xb[lo:lo + (1 << 17)], "bf16"), Q[samp])
+    reps = accept.check_batch(S, ids[samp], sc[samp], 10, rtol=2e-3)
+    assert all(r.ok for r in reps), [r.problems for r in reps if not r.ok][:2]
