@@ -7,8 +7,10 @@ document).  The paper leaves the BM25 variant open; the reading used here:
 * tf(t, d)  = occurrences of term t in chunk d;  dl(d) = token count of d;
 * N = number of chunks;  avgdl = sum(dl) / N;  df(t) = #{d : tf(t, d) > 0};
 * idf(t)    = ln(1 + (N - df + 0.5) / (df + 0.5))          (always positive);
-* score(q, d) = sum over the term OCCURRENCES t of q, in query order, of
-      idf(t) * tf * (k1 + 1) / (tf + k1 * (1 - b + b * dl / avgdl)).
+* score(q, d) = sum over the term OCCURRENCES t of q that occur in d, in query order, of
+      idf(t) * tf * (k1 + 1) / (tf + k1 * (1 - b + b * dl / avgdl));
+  a term absent from d adds exactly 0 (this matters when k1 = 0, where the formula would
+  read 0 / 0 for tf = 0).
 
 Nothing here reads a postings list: term frequencies are counted from the token sequences.
 """
@@ -65,7 +67,8 @@ def scores_batch(doc_indptr, tokens, qterm_indptr, qterms, k1: float, b: float) 
         for t in qterms[qterm_indptr[q]:qterm_indptr[q + 1]]:
             j = row[int(t)]
             f = tf[j]
-            out[q] += w_idf[j] * f * (k1 + 1.0) / (f + norm)
+            has = f > 0                     # a term absent from a chunk adds nothing to its score
+            out[q, has] += w_idf[j] * f[has] * (k1 + 1.0) / (f[has] + norm[has])
     return out
 
 

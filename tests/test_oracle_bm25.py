@@ -99,6 +99,18 @@ def test_invariants():
     assert (bm25.idf(100, np.arange(1, 101)) > 0).all()
 
 
+def test_k1_zero_absent_term_adds_nothing():
+    # k1 = 0 makes the length norm 0; a chunk without the term must score 0, not 0/0
+    ind, toks = _corpus([[0, 1], [1, 1], [2]])
+    qi, qt = _queries([[0], [0, 1]])
+    S = bm25.scores_batch(ind, toks, qi, qt, 0.0, 0.75)
+    assert np.isfinite(S).all()
+    idf0 = bm25.idf(3, np.array([1]))[0]
+    idf1 = bm25.idf(3, np.array([2]))[0]
+    np.testing.assert_allclose(S[0], [idf0, 0.0, 0.0], rtol=1e-15)
+    np.testing.assert_allclose(S[1], [idf0 + idf1, idf1, 0.0], rtol=1e-15)
+
+
 def test_sparse_topk_excludes_zero_and_orders_ties_by_id():
     S = np.array([[0.0, 2.0, 1.0, 2.0, 0.0, 0.5]])
     ids, sc = bm25.sparse_topk_from_scores(S, 6)
