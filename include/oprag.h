@@ -18,12 +18,13 @@
  *    next synchronisation of the stream.
  *  - Memory: every large buffer (slab, CSR arrays, queries, outputs, workspace) is device
  *    memory owned by the caller and must stay valid while the index or call uses it.  The
- *    library allocates only small per-index device arrays at create / attach time and never
- *    in upsert or search.  Device pointers must be 16-byte aligned.
+ *    library allocates only the small BM25 statistics arrays at attach time and never in
+ *    create, upsert or search.  Device pointers must be 16-byte aligned.
  *  - Streams: `stream` is a hipStream_t (NULL = default stream).  Calls are asynchronous on
- *    it.  An index keeps host-side state (row count) and a small device control block, so
- *    calls on one index must be issued from one host thread at a time and ordered on one
- *    stream (or ordered by the caller with events).
+ *    it.  An index keeps host-side state (row count), so calls on one index must be issued
+ *    from one host thread at a time; an upsert is seen by searches ordered after it on the
+ *    device (same stream, or ordered by the caller with events).  A workspace holds
+ *    intermediate results of one call: concurrent calls need separate workspaces.
  *  - Ranked lists are ordered by score descending, then id ascending.  Lists shorter than k
  *    are padded with id -1 and score -inf.  1 <= k <= OPRAG_MAX_K.
  */
@@ -57,7 +58,7 @@ typedef enum oprag_op { OPRAG_OP_DENSE = 0, OPRAG_OP_SPARSE = 1, OPRAG_OP_HYBRID
 typedef struct oprag_index oprag_index; /* opaque handle */
 
 typedef struct oprag_index_desc {
-  int32_t dim;      /* vector dimension d: 1..OPRAG_MAX_DIM; multiple of 4 (f32) or 64 (bf16, f16) */
+  int32_t dim;      /* vector dimension d: 1..OPRAG_MAX_DIM; multiple of 4 (f32) or 128 (bf16, f16) */
   int32_t dtype;    /* oprag_dtype of the stored vectors and of queries */
   int64_t capacity; /* rows the slab holds: 1 .. 2^31 - 2 */
   int32_t device;   /* HIP device ordinal of the slab */
@@ -72,8 +73,8 @@ const char *oprag_last_error(void);
 /*
  * Create an index over a caller-owned slab: row-major [capacity x dim] in desc->dtype,
  * slab_bytes >= capacity * dim * sizeof(dtype).  The index starts empty (n_rows = 0);
- * row ids are insertion positions.  Allocates a small device control block (zeroed).
- * Errors: E_INVALID (desc, slab, out), E_DEVICE.
+ * row ids are insertion positions.  Allocates nothing on the device.
+ * Errors: E_INVALID (desc, slab, out, device ordinal), E_DEVICE.
  */
 oprag_status oprag_index_create(const oprag_index_desc *desc, void *slab_dev, size_t slab_bytes, oprag_index **out);
 
@@ -148,7 +149,8 @@ oprag_status oprag_search_sparse(oprag_index *idx, const int32_t *qterm_indptr_d
  * Reciprocal rank fusion of two ranked id lists per query (the fusion the hybrid workload
  * specifies; the paper's own Section 4.4 fusion is a weighted score sum with unstated
  * weights): fused(d) = sum over lists holding d of 1 / (rrf_k + rank), ranks 1-based over
- * the list's valid prefix (ids >= 0).  Compared exactly as rationals; ties by ascending id.
+ * the list's valid prefix (ids >= 0; ids within one list are distinct, as search outputs are).
+ * Compared exactly as rationals; ties by ascending id.
  *   dense_ids_dev [nq x k_dense] int64, sparse_ids_dev [nq x k_sparse] int64;
  *   fused_dev [nq x k] fp32 (the exact value rounded to fp32), ids_dev [nq x k] int64.
  * 0 <= rrf_k <= 1000000.  Needs no index and no workspace.

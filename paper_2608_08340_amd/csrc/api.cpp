@@ -1,6 +1,5 @@
 // Host runtime behind the C ABI of include/oprag.h: argument validation (always complete
-// before the first HIP call), the index handle and its device control block, workspace
-// planning and kernel dispatch.
+// before the first HIP call), the index handle, workspace planning and kernel dispatch.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -22,8 +21,6 @@ struct oprag_index {
   void* slab = nullptr;
   size_t slab_bytes = 0;
   int64_t n_rows = 0;
-  void* cb_mem = nullptr;
-  oprag::ControlBlock cb;
   bool has_sparse = false;
   oprag::SparseIndex sp;
   void* sp_mem = nullptr;
@@ -131,11 +128,7 @@ oprag_status do_dense(oprag_index* idx, const void* q, int64_t nq, int32_t k, fl
     a.n_qblocks = p.n_qblocks;
     a.n_chunks = p.n_chunks;
     a.rows_per_chunk = p.rows_per_chunk;
-    a.thr = idx->cb.thr;
-    a.cnt = idx->cb.cnt;
-    a.done = idx->cb.done;
-    a.cand = static_cast<unsigned long long*>(ws);
-    a.cap = p.cap;
+    a.partial = static_cast<unsigned long long*>(ws);
     a.out_scores = scores + q0 * k;
     a.out_ids = reinterpret_cast<long long*>(ids) + q0 * k;
     const hipError_t e = oprag::launch_dense(p, idx->dtype, a, s);
@@ -160,8 +153,8 @@ oprag_status oprag_index_create(const oprag_index_desc* desc, void* slab_dev, si
   if (desc->dim < 1 || desc->dim > OPRAG_MAX_DIM) return fail(OPRAG_E_INVALID, "dim %d outside [1, %d]", desc->dim, OPRAG_MAX_DIM);
   if (desc->dtype == OPRAG_F32 && desc->dim % 4)
     return fail(OPRAG_E_UNSUPPORTED, "fp32 dim %d is not a multiple of 4", desc->dim);
-  if (desc->dtype != OPRAG_F32 && desc->dim % 64)
-    return fail(OPRAG_E_UNSUPPORTED, "bf16/fp16 dim %d is not a multiple of 64", desc->dim);
+  if (desc->dtype != OPRAG_F32 && desc->dim % 128)
+    return fail(OPRAG_E_UNSUPPORTED, "bf16/fp16 dim %d is not a multiple of 128", desc->dim);
   if (desc->capacity < 1 || desc->capacity > (int64_t)0x7ffffffe)
     return fail(OPRAG_E_INVALID, "capacity %lld outside [1, 2^31 - 2]", (long long)desc->capacity);
   if (desc->device < 0) return fail(OPRAG_E_INVALID, "device %d < 0", desc->device);
@@ -170,19 +163,10 @@ oprag_status oprag_index_create(const oprag_index_desc* desc, void* slab_dev, si
   const size_t need = (size_t)desc->capacity * (size_t)desc->dim * elem_size(desc->dtype);
   if (slab_bytes < need) return fail(OPRAG_E_INVALID, "slab_bytes %zu < capacity * dim * elem = %zu", slab_bytes, need);
 
-  DeviceScope ds(desc->device);
-  if (ds.error() != hipSuccess) return hip_fail(ds.error(), "select device");
-  const size_t nthr = kMaxQPerLaunch, ndone = kMaxQPerLaunch / oprag::kMinBN;
-  const size_t cb_bytes = (2 * nthr + ndone) * sizeof(uint32_t);
-  void* mem = nullptr;
-  hipError_t e = hipMalloc(&mem, cb_bytes);
-  if (e != hipSuccess) return hip_fail(e, "control block allocation");
-  e = hipMemset(mem, 0, cb_bytes);
-  if (e == hipSuccess) e = hipDeviceSynchronize();
-  if (e != hipSuccess) {
-    (void)hipFree(mem);
-    return hip_fail(e, "control block clear");
-  }
+  int n_dev = 0;
+  const hipError_t e = hipGetDeviceCount(&n_dev);
+  if (e != hipSuccess) return hip_fail(e, "device count");
+  if (desc->device >= n_dev) return fail(OPRAG_E_INVALID, "device %d does not exist (%d devices)", desc->device, n_dev);
   oprag_index* idx = new oprag_index;
   idx->dim = desc->dim;
   idx->dtype = desc->dtype;
@@ -190,19 +174,16 @@ oprag_status oprag_index_create(const oprag_index_desc* desc, void* slab_dev, si
   idx->capacity = desc->capacity;
   idx->slab = slab_dev;
   idx->slab_bytes = slab_bytes;
-  idx->cb_mem = mem;
-  idx->cb.thr = static_cast<uint32_t*>(mem);
-  idx->cb.cnt = idx->cb.thr + nthr;
-  idx->cb.done = idx->cb.cnt + nthr;
   *out = idx;
   return ok();
 }
 
 oprag_status oprag_index_destroy(oprag_index* idx) {
   if (!idx) return ok();
-  DeviceScope ds(idx->device);
-  if (idx->cb_mem) (void)hipFree(idx->cb_mem);
-  if (idx->sp_mem) (void)hipFree(idx->sp_mem);
+  if (idx->sp_mem) {
+    DeviceScope ds(idx->device);
+    (void)hipFree(idx->sp_mem);
+  }
   delete idx;
   return ok();
 }

@@ -10,17 +10,8 @@
 namespace oprag {
 
 constexpr int kMaxK = 128;                 // largest k any list may ask for
-constexpr int kMaxQPerLaunch = 32768;      // queries per dense launch = control-block capacity
-constexpr int kMinBN = 16;                 // smallest query block of any dense kernel
+constexpr int kMaxQPerLaunch = 1 << 20;    // queries per dense launch (the host splits larger batches)
 constexpr int kDtypeF32 = 0, kDtypeBF16 = 1, kDtypeF16 = 2;
-
-// Per-index device control block for the dense search.  Every dense launch leaves it
-// zeroed: the last workgroup of each query block resets what it used.
-struct ControlBlock {
-  uint32_t* thr = nullptr;   // [kMaxQPerLaunch] running k-th-best score key per query
-  uint32_t* cnt = nullptr;   // [kMaxQPerLaunch] candidates appended per query
-  uint32_t* done = nullptr;  // [kMaxQPerLaunch / kMinBN] finished workgroups per query block
-};
 
 struct DenseArgs {
   const void* X;                // slab rows [n_rows x d]
@@ -32,11 +23,7 @@ struct DenseArgs {
   int n_qblocks;
   int n_chunks;
   long long rows_per_chunk;     // multiple of the kernel's tile rows
-  uint32_t* thr;
-  uint32_t* cnt;
-  uint32_t* done;
-  unsigned long long* cand;     // [nq x cap] candidate composite keys
-  long long cap;
+  unsigned long long* partial;  // [nq x n_chunks x k] per-chunk lists (when n_chunks > 1)
   float* out_scores;            // [nq x k]
   long long* out_ids;           // [nq x k]
 };
@@ -48,7 +35,7 @@ struct DensePlan {
   int n_qblocks = 0;
   int n_chunks = 0;
   long long rows_per_chunk = 0;
-  long long cap = 0;            // candidate slots per query
+  long long cap = 0;            // partial-list slots per query (bounds n_chunks * k)
   long long grid = 0;
   size_t lds_bytes = 0;
 };

@@ -65,6 +65,8 @@ def test_create_unsupported_dims(lib):
     h = ctypes.c_void_p()
     assert lib.oprag_index_create(ctypes.byref(_desc(dim=100, dtype=1)), ctypes.c_void_p(4096), 1 << 30,
                                   ctypes.byref(h)) == E_UNSUPPORTED
+    assert lib.oprag_index_create(ctypes.byref(_desc(dim=64, dtype=2)), ctypes.c_void_p(4096), 1 << 30,
+                                  ctypes.byref(h)) == E_UNSUPPORTED
     assert lib.oprag_index_create(ctypes.byref(_desc(dim=6, dtype=0)), ctypes.c_void_p(4096), 1 << 30,
                                   ctypes.byref(h)) == E_UNSUPPORTED
     assert lib.oprag_index_create(None, ctypes.c_void_p(4096), 1 << 30, ctypes.byref(h)) == E_INVALID

@@ -74,7 +74,7 @@ def test_ragged_sizes_and_k(dtype, n, nq, k):
     """Row counts that are not tile multiples, query counts that are not block multiples, k across
     both selection strategies, k larger than the index (padding)."""
     device()
-    w = synth.mixture_dense(200 + n % 97, n, 64, 16, nq, k, dtype)
+    w = synth.mixture_dense(200 + n % 97, n, 128, 16, nq, k, dtype)
     _, sc, ids = _run(w.rows, w.queries, k, dtype)
     S, X, Q = oracle_scores(w.rows, w.queries, dtype)
     check_dense(S, X, Q, ids, sc, k, dtype, label=f"n={n} nq={nq} k={k}")
@@ -83,8 +83,8 @@ def test_ragged_sizes_and_k(dtype, n, nq, k):
 def test_empty_index_pads():
     dev = device()
     from paper_2608_08340_amd import Index
-    idx = Index(64, 100, torch.bfloat16)
-    q = synth.to_storage(np.ones((3, 64), np.float32), "bf16").to(dev)
+    idx = Index(128, 100, torch.bfloat16)
+    q = synth.to_storage(np.ones((3, 128), np.float32), "bf16").to(dev)
     sc, ids = idx.search_dense(q, 5)
     torch.cuda.synchronize()
     assert (ids.cpu() == -1).all() and torch.isneginf(sc.cpu()).all()
@@ -104,10 +104,10 @@ def test_repeatable_batch_invariant_prefix_consistent(c2):
     assert torch.equal(i5, i1[:, :5]) and torch.equal(s5, s1[:, :5])
 
 
-def test_more_queries_than_one_launch():
-    """More queries than one launch's control block holds: the host splits the batch."""
+def test_large_query_batch():
+    """A large query batch (33,000 queries over 512 rows)."""
     device()
-    w = synth.mixture_dense(300, 512, 64, 8, 33000, 3, "bf16")
+    w = synth.mixture_dense(300, 512, 128, 8, 33000, 3, "bf16")
     _, sc, ids = _run(w.rows, w.queries, 3, "bf16")
     S, X, Q = oracle_scores(w.rows, w.queries, "bf16")
     sel = np.r_[0:50, 32700:33000]

@@ -1,0 +1,174 @@
+"""BM25 over CSR postings, RRF fusion and the hybrid path on the GPU against the oracle."""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import accept, bm25, rrf
+from oracle import dense as od
+from tests.gpu_helpers import check_dense, device, log, make_index, oracle_scores
+
+pytestmark = pytest.mark.gpu
+
+
+def _t(a, dev):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+
+
+def _attach(idx, csr, dev, k1=1.2, b=0.75):
+    idx.attach_sparse(_t(csr.term_indptr, dev), _t(csr.post_chunk, dev), _t(csr.post_tf, dev),
+                      _t(csr.doc_len, dev), k1, b)
+
+
+def _check_sparse(B, ids, sc, k, label=""):
+    ids = ids.cpu().numpy()
+    sc = sc.cpu().numpy()
+    bad = []
+    for q in range(B.shape[0]):
+        rep = accept.check_ranked(B[q], ids[q], sc[q], k, rtol=1e-5, ranked=B[q] > 0)
+        if not rep.ok:
+            bad.append((q, rep.problems))
+    assert not bad, f"{label}: {len(bad)} queries fail, first {bad[:2]}"
+
+
+def _small_corpus(seed, n_docs, vocab, mean_len, nq):
+    ind, toks = synth.sparse_corpus(synth.rng(seed, 3), n_docs, vocab, 1.1, mean_len)
+    csr = synth.csr_from_tokens(ind, toks, vocab)
+    g = np.random.default_rng(seed)
+    qs = [list(g.integers(0, vocab, size=g.integers(1, 9))) for _ in range(nq)]
+    qs[0] = []                                 # no terms
+    qs[1] = [-1, vocab, vocab + 5]             # only unknown terms
+    qs[2] = [3, 3, 3, 0]                       # repeats
+    qs[3] = [0, -7, 1]                         # known and unknown
+    qi = np.zeros(nq + 1, dtype=np.int32)
+    qi[1:] = np.cumsum([len(q) for q in qs])
+    qt = np.array([t for q in qs for t in q], dtype=np.int32)
+    return ind, toks, csr, qi, qt
+
+
+@pytest.mark.parametrize("k", [1, 10, 100, 128])
+def test_bm25_small_corpus(k):
+    dev = device()
+    ind, toks, csr, qi, qt = _small_corpus(500 + k, 3000, 400, 40.0, 60)
+    idx = make_index(torch.zeros((3000, 128), dtype=torch.bfloat16), "bf16")
+    _attach(idx, csr, dev)
+    sc, ids = idx.search_sparse(_t(qi, dev), _t(qt, dev), k)
+    torch.cuda.synchronize()
+    qt_oracle = np.where((qt >= 0) & (qt < 400), qt, 10 ** 6).astype(np.int64)  # unknown terms match nothing
+    B = bm25.scores_batch(ind, toks, qi, qt_oracle, 1.2, 0.75)
+    _check_sparse(B, ids, sc, k, f"k={k}")
+    assert (ids.cpu()[0] == -1).all() and (ids.cpu()[1] == -1).all()
+
+
+@pytest.mark.parametrize("k1,b", [(1.2, 0.75), (0.0, 0.75), (1.2, 0.0), (2.0, 1.0)])
+def test_bm25_parameters(k1, b):
+    dev = device()
+    ind, toks, csr, qi, qt = _small_corpus(600, 2000, 300, 30.0, 40)
+    idx = make_index(torch.zeros((2000, 128), dtype=torch.bfloat16), "bf16")
+    _attach(idx, csr, dev, k1, b)
+    sc, ids = idx.search_sparse(_t(qi, dev), _t(qt, dev), 50)
+    torch.cuda.synchronize()
+    qt_oracle = np.where((qt >= 0) & (qt < 300), qt, 10 ** 6).astype(np.int64)
+    B = bm25.scores_batch(ind, toks, qi, qt_oracle, k1, b)
+    _check_sparse(B, ids, sc, 50, f"k1={k1} b={b}")
+
+
+def test_bm25_several_chunk_ranges():
+    """More chunks than one workgroup's LDS accumulator: per-range lists are merged."""
+    dev = device()
+    ind, toks, csr, qi, qt = _small_corpus(700, 70001, 2000, 20.0, 30)
+    idx = make_index(torch.zeros((70001, 128), dtype=torch.bfloat16), "bf16")
+    _attach(idx, csr, dev)
+    sc, ids = idx.search_sparse(_t(qi, dev), _t(qt, dev), 64)
+    torch.cuda.synchronize()
+    qt_oracle = np.where((qt >= 0) & (qt < 2000), qt, 10 ** 6).astype(np.int64)
+    B = bm25.scores_batch(ind, toks, qi, qt_oracle, 1.2, 0.75)
+    _check_sparse(B, ids, sc, 64, "multi-range")
+
+
+def test_attach_rejects_malformed_csr():
+    dev = device()
+    from paper_2608_08340_amd import OpragError
+    ind, toks, csr, qi, qt = _small_corpus(800, 500, 50, 10.0, 5)
+    idx = make_index(torch.zeros((500, 128), dtype=torch.bfloat16), "bf16")
+    bad = csr.post_chunk.copy()
+    lo, hi = csr.term_indptr[0], csr.term_indptr[1]
+    bad[lo], bad[lo + 1] = bad[lo + 1], bad[lo]            # not ascending within term 0
+    with pytest.raises(OpragError):
+        idx.attach_sparse(_t(csr.term_indptr, dev), _t(bad, dev), _t(csr.post_tf, dev), _t(csr.doc_len, dev))
+    badtf = csr.post_tf.copy()
+    badtf[5] = 0
+    with pytest.raises(OpragError):
+        idx.attach_sparse(_t(csr.term_indptr, dev), _t(csr.post_chunk, dev), _t(badtf, dev), _t(csr.doc_len, dev))
+    with pytest.raises(OpragError):   # search before any successful attach
+        idx.search_sparse(_t(qi, dev), _t(qt, dev), 5)
+
+
+def test_rrf_kernel_matches_exact_fractions():
+    dev = device()
+    from paper_2608_08340_amd import rrf_fuse
+    g = np.random.default_rng(9)
+    nq, kd, ks = 200, 100, 100
+    D = np.full((nq, kd), -1, np.int64)
+    S = np.full((nq, ks), -1, np.int64)
+    for q in range(nq):
+        pool = g.permutation(300)
+        nd, ns = int(g.integers(0, kd + 1)), int(g.integers(0, ks + 1))
+        D[q, :nd] = pool[:nd]
+        S[q, :ns] = g.permutation(pool[: max(ns, 1) + int(g.integers(0, 100))])[:ns]
+    D[0], S[0] = -1, -1
+    D[0, :3], S[0, :2] = [7, 3, 9], [3, 5]          # the hand example, lists otherwise empty
+    for k in (5, 100, 128):
+        fused, ids = rrf_fuse(_t(D, dev), _t(S, dev), 60, k)
+        torch.cuda.synchronize()
+        ref_ids, ref_f32, _ = rrf.fuse(D, S, 60, k)
+        assert np.array_equal(ids.cpu().numpy(), ref_ids)
+        assert np.array_equal(fused.cpu().numpy().view(np.uint32), ref_f32.view(np.uint32))
+    fused, ids = rrf_fuse(_t(D, dev), _t(S, dev), 0, 10)
+    torch.cuda.synchronize()
+    ref_ids, ref_f32, _ = rrf.fuse(D, S, 0, 10)
+    assert np.array_equal(ids.cpu().numpy(), ref_ids)
+
+
+@pytest.fixture(scope="module")
+def c3():
+    device()
+    return synth.hybrid_32k()
+
+
+@pytest.mark.timeout(300)
+@pytest.mark.parametrize("correlated", [False, True])
+def test_hybrid_32k_bm25_rrf_top5(c3, correlated):
+    """32,768 x 1,024 bf16 index + Zipf(1.1) CSR corpus (30,000 terms, Poisson(256) lengths),
+    256 queries of 8 terms: dense top-100 and BM25 top-100 each pass the acceptance rules, and
+    the fused top-5 equals exact RRF(60) of the GPU's own two lists."""
+    dev = device()
+    h = c3 if not correlated else synth.hybrid_32k(correlated=True, dense=synth.dense_32k())
+    w = h.dense
+    log("hybrid", "correlated" if correlated else "independent", tuple(w.rows.shape), h.csr.nnz)
+    idx = make_index(w.rows, "bf16")
+    _attach(idx, h.csr, dev, h.k1, h.b)
+    q = w.queries.to(dev)
+    qi, qt = _t(h.qterm_indptr, dev), _t(h.qterms, dev)
+    fused, fids = idx.search_hybrid(q, qi, qt, 100, 100, 60, 5)
+    dsc, dids = idx.search_dense(q, 100)
+    ssc, sids = idx.search_sparse(qi, qt, 100)
+    torch.cuda.synchronize()
+    # stage 1: dense top-100
+    S, X, Q = oracle_scores(w.rows, w.queries, "bf16")
+    check_dense(S, X, Q, dids, dsc, 100, "bf16", label="dense top-100")
+    # stage 2: BM25 top-100 from the raw token sequences
+    B = bm25.scores_batch(h.doc_indptr, h.tokens, h.qterm_indptr, h.qterms, h.k1, h.b)
+    _check_sparse(B, sids, ssc, 100, "bm25 top-100")
+    # stage 3: exact RRF of the GPU's own lists, and equality with the composition
+    ref_ids, ref_f32, _ = rrf.fuse(dids.cpu().numpy(), sids.cpu().numpy(), 60, 5)
+    assert np.array_equal(fids.cpu().numpy(), ref_ids)
+    assert np.array_equal(fused.cpu().numpy().view(np.uint32), ref_f32.view(np.uint32))
+    # where the GPU lists equal the oracle lists, the fused output equals the oracle's
+    od_ids, _ = od.topk_from_scores(S, 100)
+    ob_ids, _ = bm25.sparse_topk_from_scores(B, 100)
+    same = (dids.cpu().numpy() == od_ids).all(1) & (sids.cpu().numpy() == ob_ids).all(1)
+    o_ids, _, _ = rrf.fuse(od_ids, ob_ids, 60, 5)
+    assert same.mean() > 0.2
+    assert np.array_equal(fids.cpu().numpy()[same], o_ids[same])
+    log("queries whose stage lists equal the oracle's exactly:", int(same.sum()), "of", len(same))
