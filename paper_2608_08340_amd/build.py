@@ -22,6 +22,9 @@ FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function",
     # Keep packed-fp32 instructions out of the generated code.
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # MFMA accumulators in VGPRs: the AGPR form leaves some accumulations untied, and the
+    # register copies that follow stall the matrix pipe.
+    "-mllvm", "-amdgpu-mfma-vgpr-form",
 ]
 
 

@@ -68,6 +68,17 @@ __device__ __forceinline__ void dma16(const void* g, void* lds_base) {
   __builtin_amdgcn_global_load_lds(g, OPRAG_LDS(lds_base), 16, 0, 0);
 }
 
+// Raw buffer resource over [base, base + bytes): 16-byte loads at offsets past the end
+// return zeros instead of touching memory (gfx9 descriptor word 3: 32-bit data format).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base, long long bytes) {
+  const int n = (int)(unsigned)(bytes < 0 ? 0 : (bytes > 0xffffffffll ? 0xffffffffll : bytes));
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, n, 0x00020000);
+}
+
+__device__ __forceinline__ u32x4 buffer_load16(__amdgpu_buffer_rsrc_t r, int voffset) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, voffset, 0, 0);
+}
+
 template <int N>
 __device__ __forceinline__ void wait_vm() {
   static_assert(N >= 0 && N < 64, "vmcnt range");
@@ -143,6 +154,18 @@ struct SelSmall {
   RegTopK<KS> run;  // running list of the query (owner thread, sub == 0)
 
   __device__ __forceinline__ void init() { run.clear(); }
+
+  // scratch regions shared with the register epilogue of the MFMA kernel
+  static __device__ __forceinline__ u64* cand_of(unsigned char* sc) { return reinterpret_cast<u64*>(sc); }
+  static __device__ __forceinline__ float* tau_of(unsigned char* sc) {
+    return reinterpret_cast<float*>(sc + BN * CAP * 8 + kVals + TPQ * BN * 4);
+  }
+  static __device__ __forceinline__ int* cnt_of(unsigned char* sc) {
+    return reinterpret_cast<int*>(sc + BN * CAP * 8 + kVals + TPQ * BN * 4 + BN * 8);
+  }
+  static __device__ __forceinline__ int* flag_of(unsigned char* sc) {
+    return reinterpret_cast<int*>(sc + BN * CAP * 8 + kVals + TPQ * BN * 4 + BN * 12);
+  }
 
   __device__ __forceinline__ float run_value(int i) const {  // value of entry i (runtime i)
     u64 c = 0ull;
@@ -380,14 +403,292 @@ struct SelOf<BN, KS, 1> {
 };
 
 // ------------------------------------------------------------------------------------
+// Selection straight from the MFMA accumulators (k <= 16).  acc[mi][ni][r] is the score of
+// row tile0 + 16*MW*wave + 16*mi + 4*(lane/16) + r against query 16*ni + lane%16 of the
+// block.  Each lane's MW*4 values of a query form one group; the M best values of every
+// group are actual, distinct scores, so the k-th largest of them together with the running
+// list is a lower bound tau of the k-th best score so far.  Only scores >= tau (a handful per
+// query) go to LDS as candidates and the owner thread inserts them into its running list.
+// Returns false, with the running lists untouched, when some query has more than CAP
+// candidates (many equal scores); the caller then takes the exact LDS path.
+// ------------------------------------------------------------------------------------
+template <int BN, int MW, int KS, typename Sel>
+__device__ __forceinline__ bool reg_epilogue(const f32x4 (&acc)[MW][BN / 16], Sel& sel, float* gv,
+                                             unsigned char* scratch, long long tile0, long long row_end, int q_lim,
+                                             int k) {
+  constexpr int NW = BN / 16;
+  constexpr int M = KS <= 5 ? 1 : (KS <= 8 ? 2 : 4);  // values kept per group
+  constexpr int NG = kWaves * 4 * M;                  // group values per query
+  constexpr int CAP = Sel::CAP;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  // candidates as (score bits, row offset in the tile), in the candidate area of the selector
+  uint2* cand = reinterpret_cast<uint2*>(Sel::cand_of(scratch));
+  float* thr = Sel::tau_of(scratch);
+  int* cnt = Sel::cnt_of(scratch);
+  int* flag = Sel::flag_of(scratch);
+  constexpr int TR = kWaves * MW * 16;
+  const int row0 = w * MW * 16 + (lane >> 4) * 4;  // tile offset of this lane's value (0, r = 0)
+  // element (mi, r) of this lane is a valid row iff 16*mi + r < lim
+  const int lim = (int)min((long long)TR, row_end - tile0) - row0;
+  const int g = w * 4 + (lane >> 4);
+
+#pragma unroll
+  for (int ni = 0; ni < NW; ++ni) {
+    ValTop<M> t;
+    t.clear();
+#pragma unroll
+    for (int mi = 0; mi < MW; ++mi)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) t.insert(mi * 16 + r < lim ? acc[mi][ni][r] : kNegInf);
+#pragma unroll
+    for (int j = 0; j < M; ++j) gv[(g * M + j) * BN + ni * 16 + (lane & 15)] = t.v[j];
+  }
+  lds_barrier();
+  if (tid < BN) {
+    float tau = __builtin_inff();  // queries past the batch take no candidates
+    if (tid < q_lim) {
+      ValTop<KS> L;
+      L.clear();
+      for (int j = 0; j < NG; ++j) L.insert(gv[j * BN + tid]);
+#pragma unroll
+      for (int i = 0; i < KS; ++i)
+        if (i < k && sel.run.v[i]) L.insert(comp_score(sel.run.v[i]));
+      tau = L.at(k);
+    }
+    thr[tid] = tau;
+    cnt[tid] = 0;
+  }
+  if (tid == 0) *flag = 0;
+  lds_barrier();
+  // Count first, reserve once per (lane, query), then write: one LDS atomic per query
+  // fragment instead of one per candidate.
+  float th[NW];
+  int c[NW], base[NW];
+#pragma unroll
+  for (int ni = 0; ni < NW; ++ni) {
+    th[ni] = thr[ni * 16 + (lane & 15)];
+    int cc = 0;
+#pragma unroll
+    for (int mi = 0; mi < MW; ++mi)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) cc += (mi * 16 + r < lim && acc[mi][ni][r] >= th[ni]) ? 1 : 0;
+    c[ni] = cc;
+  }
+#pragma unroll
+  for (int ni = 0; ni < NW; ++ni) base[ni] = c[ni] ? atomicAdd(&cnt[ni * 16 + (lane & 15)], c[ni]) : 0;
+#pragma unroll
+  for (int ni = 0; ni < NW; ++ni) {
+    if (c[ni] == 0) continue;
+    if (base[ni] + c[ni] > CAP) {
+      *flag = 1;
+      continue;
+    }
+    uint2* dst = cand + (ni * 16 + (lane & 15)) * CAP;
+    int j = base[ni];
+#pragma unroll
+    for (int mi = 0; mi < MW; ++mi)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float x = acc[mi][ni][r];
+        if (mi * 16 + r < lim && x >= th[ni]) {
+          dst[j] = make_uint2(__float_as_uint(x), (unsigned)(row0 + mi * 16 + r));
+          ++j;
+        }
+      }
+  }
+  lds_barrier();
+  if (*flag) return false;
+  if (tid < q_lim) {
+    const int n = cnt[tid];
+    for (int j = 0; j < n; ++j) {
+      const uint2 e = cand[tid * CAP + j];
+      sel.run.insert(composite(__uint_as_float(e.x), (uint32_t)(tile0 + e.y)));
+    }
+  }
+  return true;
+}
+
+// ------------------------------------------------------------------------------------
+// k <= 5: the same lower bound tau from the group maxima, but the groups themselves are
+// handed over: a lane whose maximum for a query reaches tau (at most k such groups per
+// query, barring ties) copies its MW*4 scores of that query to one of SLOTS blocks in LDS,
+// and the owner thread takes every score >= tau from its query's blocks.  Returns false,
+// with the running lists untouched, when a query has more than SLOTS such groups.
+// ------------------------------------------------------------------------------------
+template <int MW, int BN>
+struct BlockArea {
+  static constexpr int SLOTS = 7;
+  static constexpr int VALS = MW * 4;              // scores per block
+  static constexpr int QSTR = SLOTS * VALS + 4;    // floats per query; the pad spreads banks
+  static constexpr int kBytes = BN * QSTR * 4 + BN * 4;
+};
+
+template <int BN, int MW, typename Sel>
+__device__ __forceinline__ bool blk_epilogue(const f32x4 (&acc)[MW][BN / 16], Sel& sel, unsigned char* area,
+                                             unsigned char* scratch, long long tile0, long long row_end, int q_lim,
+                                             int k) {
+  constexpr int NW = BN / 16;
+  constexpr int KS = 5;
+  constexpr int NG = kWaves * 4;          // groups (lanes) per query
+  constexpr int TPQ = kThreads / BN;      // threads per query in the gathering step
+  using B = BlockArea<MW, BN>;
+  constexpr int SLOTS = B::SLOTS, VALS = B::VALS, QSTR = B::QSTR;
+  constexpr int CAP = Sel::CAP;
+  float* blk = reinterpret_cast<float*>(area);                      // [BN][QSTR]: SLOTS x VALS
+  int* gmask = reinterpret_cast<int*>(area + BN * QSTR * 4);        // [BN] active groups
+  float* gmax = reinterpret_cast<float*>(Sel::cand_of(scratch));    // [NG][BN], then
+  uint2* cand = reinterpret_cast<uint2*>(Sel::cand_of(scratch));    // [BN][CAP] (score, row offset)
+  float* thr = Sel::tau_of(scratch);
+  int* cnt = Sel::cnt_of(scratch);
+  int* flag = Sel::flag_of(scratch);
+  constexpr int TR = kWaves * MW * 16;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int g = w * 4 + (lane >> 4);
+  const int lim = (int)min((long long)TR, row_end - tile0) - (w * MW * 16 + (lane >> 4) * 4);
+
+  // 1. group maxima
+  float lmax[NW];
+#pragma unroll
+  for (int ni = 0; ni < NW; ++ni) {
+    float m = kNegInf;
+#pragma unroll
+    for (int mi = 0; mi < MW; ++mi)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) m = __builtin_fmaxf(m, mi * 16 + r < lim ? acc[mi][ni][r] : kNegInf);
+    lmax[ni] = m;
+    gmax[g * BN + ni * 16 + (lane & 15)] = m;
+  }
+  if (tid == 0) *flag = 0;
+  lds_barrier();
+  // 2. owners: tau, and the groups whose maximum reaches it (slot = rank among them)
+  if (tid < BN) {
+    float tau = __builtin_inff();  // queries past the batch take no candidates
+    int mask = 0;
+    if (tid < q_lim) {
+      float gm[NG];
+#pragma unroll
+      for (int j = 0; j < NG; ++j) gm[j] = gmax[j * BN + tid];
+      ValTop<KS> L;
+      L.clear();
+#pragma unroll
+      for (int j = 0; j < NG; ++j) L.insert(gm[j]);
+#pragma unroll
+      for (int i = 0; i < KS; ++i)
+        if (i < k && sel.run.v[i]) L.insert(comp_score(sel.run.v[i]));
+      tau = L.at(k);
+#pragma unroll
+      for (int j = 0; j < NG; ++j) mask |= (gm[j] >= tau && gm[j] > kNegInf) ? 1 << j : 0;
+      if (__builtin_popcount(mask) > SLOTS) *flag = 1;
+    }
+    thr[tid] = tau;
+    gmask[tid] = mask;
+    cnt[tid] = 0;
+  }
+  lds_barrier();
+  if (*flag) return false;
+  // 3. active groups copy their scores of the query to the block of their rank
+#pragma unroll
+  for (int ni = 0; ni < NW; ++ni) {
+    const int n = ni * 16 + (lane & 15);
+    const int mask = gmask[n];
+    if ((mask >> g) & 1) {
+      const int slot = __builtin_popcount(mask & ((1 << g) - 1));
+      float* dst = blk + n * QSTR + slot * VALS;
+#pragma unroll
+      for (int mi = 0; mi < MW; ++mi) {
+        f32x4 v = acc[mi][ni];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) v[r] = mi * 16 + r < lim ? v[r] : kNegInf;
+        *reinterpret_cast<f32x4*>(dst + mi * 4) = v;
+      }
+    }
+  }
+  lds_barrier();
+  // 4. TPQ threads per query gather the scores >= tau of its blocks into a short list
+  int over = 0;
+  {
+    const int q = tid % BN, sub = tid / BN;
+    if (q < q_lim) {
+      const float tau = thr[q];
+      int mask = gmask[q];
+      // this thread's blocks are the ranks sub, sub + TPQ, ...: count, reserve, write
+      int c = 0;
+      int rank = 0;
+      for (int mm = mask; mm; mm &= mm - 1, ++rank) {
+        if (rank % TPQ != sub) continue;
+        const float* src = blk + q * QSTR + rank * VALS;
+#pragma unroll
+        for (int mi = 0; mi < MW; ++mi) {
+          const f32x4 v = *reinterpret_cast<const f32x4*>(src + mi * 4);
+#pragma unroll
+          for (int r = 0; r < 4; ++r) c += (v[r] >= tau && v[r] > kNegInf) ? 1 : 0;
+        }
+      }
+      if (c) {
+        int j = atomicAdd(&cnt[q], c);
+        if (j + c > CAP) {
+          over = 1;
+        } else {
+          rank = 0;
+          for (int mm = mask; mm; mm &= mm - 1, ++rank) {
+            if (rank % TPQ != sub) continue;
+            const int gg = __builtin_ctz(mm);
+            const int r0 = (gg >> 2) * MW * 16 + (gg & 3) * 4;
+            const float* src = blk + q * QSTR + rank * VALS;
+#pragma unroll
+            for (int mi = 0; mi < MW; ++mi) {
+              const f32x4 v = *reinterpret_cast<const f32x4*>(src + mi * 4);
+#pragma unroll
+              for (int r = 0; r < 4; ++r)
+                if (v[r] >= tau && v[r] > kNegInf)
+                  cand[q * CAP + j++] = make_uint2(__float_as_uint(v[r]), (unsigned)(r0 + mi * 16 + r));
+            }
+          }
+        }
+      }
+    }
+  }
+  if (over) *flag = 1;
+  lds_barrier();
+  // 5. owners insert the list (or, after an overflow, every score >= tau of the blocks)
+  if (tid < q_lim) {
+    if (!*flag) {
+      const int m = cnt[tid];
+      for (int j = 0; j < m; ++j) {
+        const uint2 e = cand[tid * CAP + j];
+        sel.run.insert(composite(__uint_as_float(e.x), (uint32_t)(tile0 + e.y)));
+      }
+    } else {
+      const float tau = thr[tid];
+      int rank = 0;
+      for (int mm = gmask[tid]; mm; mm &= mm - 1, ++rank) {
+        const int gg = __builtin_ctz(mm);
+        const long long r0 = tile0 + (gg >> 2) * MW * 16 + (gg & 3) * 4;
+        const float* src = blk + tid * QSTR + rank * VALS;
+        for (int p = 0; p < VALS; ++p)
+          if (src[p] >= tau && src[p] > kNegInf)
+            sel.run.insert(composite(src[p], (uint32_t)(r0 + (p >> 2) * 16 + (p & 3))));
+      }
+    }
+  }
+  return true;
+}
+
+// ------------------------------------------------------------------------------------
 // bf16 / fp16 MFMA kernel.  Four waves split a tile of TR = 4*MW*16 rows (each wave owns
-// MW distinct 16-row subtiles) and share a block of BN = NW*16 queries.  Stages are 32
-// dimensions.  Row fragments go global -> VGPRs directly in MFMA A-operand layout (each
-// wave reads only its own rows, no LDS); query pieces go global -> VGPRs -> an LDS slot
-// (double-buffered) from which every wave reads its B operands.  Both sit in a register
-// ring of RS stages issued PX = RS - 1 stages ahead; the stage loop runs across the tiles
-// of the chunk, so the next tile's loads are in flight while a tile's selection runs.
-// The epilogue takes G passes of MW/G subtiles per wave through the LDS score tile.
+// MW distinct 16-row subtiles) and share a block of BN = NW*16 queries.  A k-step is one
+// MFMA depth (32 dimensions); four k-steps form a super-step of 128 dimensions.
+//  - Row fragments go global -> VGPRs directly in MFMA A-operand layout (each wave reads
+//    only its own rows); a register ring of RS k-steps keeps RS - 1 of them in flight.
+//    Every k-step issues the same loads (past the end they repeat the last k-step), so
+//    the compiler's load counters stay exact and no wait drains the ring.
+//  - The query block of a super-step (BN x 128 dimensions) is loaded one super-step
+//    ahead into VGPRs, written to one of two LDS slots at the end of the previous
+//    super-step, and read by every wave as B operands, one k-step ahead of its MFMAs.
+//    One barrier per super-step.
+//  - After the last k-step of a tile the scores sit in the accumulators; the register
+//    epilogue (or, when it declines, G passes through an LDS score tile) updates the
+//    running top-k of each query.
 // ------------------------------------------------------------------------------------
 template <int DT, int NW, int MW, int RS, int G, int KS, int SEL>
 __global__ __launch_bounds__(kThreads) void dense_mfma_kernel(DenseArgs a) {
@@ -396,20 +697,27 @@ __global__ __launch_bounds__(kThreads) void dense_mfma_kernel(DenseArgs a) {
   using T = typename M::T;
   constexpr int BN = NW * 16;
   constexpr int TR = kWaves * MW * 16;
-  constexpr int KC = 32;
+  constexpr int KC = 32;                        // dimensions per k-step
+  constexpr int SK = 128;                       // dimensions per super-step
   constexpr int PX = RS - 1;
-  constexpr int QSLOT = BN * KC * 2;            // bytes; a query row is 4 pieces of 16 bytes
-  constexpr int QPC = BN * KC * 2 / 16;         // 16-byte query pieces per stage
-  constexpr int QPT = (QPC + kThreads - 1) / kThreads;
-  constexpr int MWP = MW / G;                   // subtile rows per wave per pass
-  constexpr int RP = kWaves * MWP * 16;         // rows per pass
+  static_assert(RS == 4 || RS == 8 || RS == 16, "ring of whole super-steps");
+  constexpr int BODY = RS;                      // k-steps per loop iteration; divides d / 32
+  constexpr int QSLOT = BN * SK * 2;            // bytes: query row n at n * 256
+  constexpr int QPT = BN * SK * 2 / 16 / kThreads;  // 16-byte query pieces per thread
+  static_assert(QPT * kThreads * 16 == QSLOT, "query pieces");
+  constexpr int MWP = MW / G;                   // subtile rows per wave per fallback pass
+  constexpr int RP = kWaves * MWP * 16;         // rows per fallback pass
   constexpr int SR = RP + 4;                    // S row stride (floats)
   using Sel = typename SelOf<BN, KS, SEL>::type;
   constexpr int QBYTES = 2 * QSLOT;
-  constexpr int SBYTES = BN * SR * 4;
+  constexpr bool kBlk = SEL == 0 && KS == 5;
+  constexpr int SB0 = BN * SR * 4;
+  constexpr int SBYTES = kBlk && BlockArea<MW, BN>::kBytes > SB0 ? BlockArea<MW, BN>::kBytes : SB0;
   constexpr int SMEM = QBYTES + SBYTES + Sel::kBytes;
   static_assert(MW % G == 0 && ((MWP * 16) & (MWP * 16 - 1)) == 0, "pass shape");
   static_assert(SEL == 1 || RP % (4 * (kThreads / BN)) == 0, "slice shape");
+  static_assert(SEL == 1 || kWaves * 4 * (KS <= 5 ? 1 : (KS <= 8 ? 2 : 4)) * BN * 4 <= SBYTES,
+                "group values of the register epilogue fit in the score tile");
   __shared__ __attribute__((aligned(16))) unsigned char smem[SMEM];
   unsigned char* qslots = smem;
   float* S = reinterpret_cast<float*>(smem + QBYTES);
@@ -424,121 +732,174 @@ __global__ __launch_bounds__(kThreads) void dense_mfma_kernel(DenseArgs a) {
   const long long row_begin = chunk * a.rows_per_chunk;
   const long long row_end = min(row_begin + a.rows_per_chunk, a.n_rows);
   const int d = a.d;
-  const int nk = d / KC;                                            // stages per tile
+  const int nk = d / KC;                                            // k-steps per tile
   const int n_tiles = (int)((row_end - row_begin + TR - 1) / TR);   // 0 for an empty chunk
   const int n_st = n_tiles * nk;
   const T* X = static_cast<const T*>(a.X);
-  const T* Q = static_cast<const T*>(a.Q);
-  const int kl = (lane >> 4) * 8;  // this lane's 8 dimensions inside a 32-dim stage
-
-  // query pieces of this thread: piece p -> query row r = p / 4, 16-byte column cc = p % 4,
-  // stored at column (cc + r / 2) % 4 of the row: any 8 consecutive lanes then touch 128
-  // distinct bytes modulo 128, both for the row-wise writes and for the fragment reads
-  // (8 rows, one column).  When a stage has fewer
-  // pieces than threads, several threads copy the same piece (identical bytes, same place),
-  // so every load and store is unconditional.
-  const T* qsrc[QPT];
-  int qdst[QPT];
-#pragma unroll
-  for (int j = 0; j < QPT; ++j) {
-    const int p = (tid + kThreads * j) % QPC;
-    const int r = p / (KC / 8), cc = p % (KC / 8);
-    qsrc[j] = Q + (long long)min(q0 + r, a.nq - 1) * d + cc * 8;
-    qdst[j] = r * 64 + ((cc + (r >> 1)) & 3) * 16;
-  }
-  const int xrow0 = w * MW * 16 + (lane & 15);  // row of subtile 0 inside a tile
-  int fbo[NW];  // byte offset of this lane's B-fragment piece in a query slot
-#pragma unroll
-  for (int ni = 0; ni < NW; ++ni) {
-    const int n = ni * 16 + (lane & 15);
-    fbo[ni] = n * 64 + (((lane >> 4) + (n >> 1)) & 3) * 16;
-  }
-
-  // Register ring of RS = 4 stages; every index below is a literal so the ring stays in VGPRs.
-  static_assert(RS == 4, "the stage loop below is written out for a ring of 4");
-  V xr[RS][MW];
-  u32x4 qr[RS][QPT];
-#define OPRAG_ISSUE(GS, SLOT)                                                            \
-  {                                                                                      \
-    const int t_ = (GS) / nk, c_ = (GS) - t_ * nk;                                       \
-    const long long tile0_ = row_begin + (long long)t_ * TR;                             \
-    _Pragma("unroll") for (int mi = 0; mi < MW; ++mi) {                                  \
-      const long long row_ = min(tile0_ + xrow0 + mi * 16, a.n_rows - 1);               \
-      xr[SLOT][mi] = *reinterpret_cast<const V*>(X + row_ * d + c_ * KC + kl);           \
-    }                                                                                    \
-    _Pragma("unroll") for (int j = 0; j < QPT; ++j) qr[SLOT][j] =                        \
-        *reinterpret_cast<const u32x4*>(qsrc[j] + c_ * KC);                              \
-  }
-#define OPRAG_STEP(U)                                                                    \
-  if (gs0 + (U) < n_st) {                                                                \
-    const int gs = gs0 + (U);                                                            \
-    if (gs + PX < n_st) OPRAG_ISSUE(gs + PX, ((U) + PX) % RS);                           \
-    unsigned char* qs = qslots + (gs & 1) * QSLOT;                                       \
-    _Pragma("unroll") for (int j = 0; j < QPT; ++j)                                      \
-        *reinterpret_cast<u32x4*>(qs + qdst[j]) = qr[U][j];                              \
-    lds_barrier();                                                                       \
-    V fb[NW];                                                                            \
-    _Pragma("unroll") for (int ni = 0; ni < NW; ++ni) fb[ni] =                           \
-        *reinterpret_cast<const V*>(qs + fbo[ni]);                                       \
-    _Pragma("unroll") for (int ni = 0; ni < NW; ++ni)                                    \
-        _Pragma("unroll") for (int mi = 0; mi < MW; ++mi)                                \
-            acc[mi][ni] = M::run(xr[U][mi], fb[ni], acc[mi][ni]);                        \
-  }
+  const T* Qb = static_cast<const T*>(a.Q) + (long long)q0 * d;
+  const int kl = (lane >> 4) * 8;  // this lane's 8 dimensions inside a k-step
 
   Sel sel;
   sel.init();
-  f32x4 acc[MW][NW];
+  if (n_st > 0) {
+    // Query piece p = tid + 256 j: row r = p / 16, 16-byte column c = p % 16 of the
+    // super-step, stored at column c ^ (r % 16) of the row.  Any 16 consecutive lanes then
+    // touch 256 distinct bytes modulo 256 (all 64 banks), for the row-wise writes and for
+    // the fragment reads (16 rows, one column) alike.
+    // Loads go through buffer resources: query rows past the batch and tile rows past the
+    // index read as zeros (their scores are never selected), with no clamping per lane.
+    int qoff[QPT], qdst[QPT];
 #pragma unroll
-  for (int mi = 0; mi < MW; ++mi)
+    for (int j = 0; j < QPT; ++j) {
+      const int p = tid + kThreads * j;
+      const int r = p / 16, c = p % 16;
+      qoff[j] = (r * d + c * 8) * 2;
+      qdst[j] = r * 256 + ((c ^ (r & 15)) * 16);
+    }
+    int xoff[MW];  // byte offset of this lane's 16 bytes of subtile mi inside a k-step of a tile
 #pragma unroll
-    for (int ni = 0; ni < NW; ++ni) acc[mi][ni] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int mi = 0; mi < MW; ++mi) xoff[mi] = ((w * MW * 16 + (lane & 15) + mi * 16) * d + kl) * 2;
+    const long long x_end = a.n_rows * (long long)d;  // elements of the index
+    const long long q_end = (long long)(a.nq - q0) * d;
+    const int fbase = (lane & 15) * 256;  // this lane's query row in fragment ni is 16 ni + lane % 16
+    const int fsw = lane & 15;           // n % 16 is lane % 16 for every fragment row
+    const int fcol = lane >> 4;          // column of k-step 0; k-step j adds 4 j
 
-  if (0 < n_st) OPRAG_ISSUE(0, 0);
-  if (1 < n_st) OPRAG_ISSUE(1, 1);
-  if (2 < n_st) OPRAG_ISSUE(2, 2);
+    V xr[RS][MW];
+    u32x4 qr[QPT];
+    V fb[NW];
+    f32x4 acc[MW][NW];
+#pragma unroll
+    for (int mi = 0; mi < MW; ++mi)
+#pragma unroll
+      for (int ni = 0; ni < NW; ++ni) acc[mi][ni] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  for (int gs0 = 0; gs0 < n_st; gs0 += RS) {
-    // d % 128 == 0 makes nk a multiple of RS, so every group of RS stages lies in one tile
-    OPRAG_STEP(0)
-    OPRAG_STEP(1)
-    OPRAG_STEP(2)
-    OPRAG_STEP(3)
-    if ((gs0 + RS) % nk == 0) {
-      // ---- epilogue of the tile: G passes through the query-major LDS score tile
-      const long long tile0 = row_begin + (long long)(gs0 / nk) * TR;
+    // One buffer resource per operand: rows from the chunk's first row to the end of the
+    // index (the planner keeps a chunk under 2^30 bytes, so 32-bit offsets reach past its
+    // end), and the block's queries.  Scalar cursors: x_ahead = byte offset of the next
+    // k-step to load (k-step c_ahead of its tile), uq = the next query super-step (the
+    // queries repeat for every tile).  Past the chunk the loads read other rows, or zeros
+    // past the index, and are never selected from.
+    const long long e_chunk = row_begin * d;
+    const __amdgpu_buffer_rsrc_t r_x = buffer_rsrc(X + e_chunk, (x_end - e_chunk) * 2);
+    const __amdgpu_buffer_rsrc_t r_q = buffer_rsrc(Qb, q_end * 2);
+    int x_ahead = 0, c_ahead = 0, uq = 0;
+    const int nq4 = nk / 4;
+    const int tile_skip = (TR - 1) * d * 2;  // from past a tile's last k-step to the next tile
+#define OPRAG_ROWS(SLOT)                                                                 \
+  {                                                                                      \
+    _Pragma("unroll") for (int mi = 0; mi < MW; ++mi) xr[SLOT][mi] =                     \
+        __builtin_bit_cast(V, buffer_load16(r_x, xoff[mi] + x_ahead));                   \
+    const bool wrap_ = ++c_ahead == nk;                                                  \
+    c_ahead = wrap_ ? 0 : c_ahead;                                                       \
+    x_ahead += KC * 2 + (wrap_ ? tile_skip : 0);                                         \
+  }
+#define OPRAG_QUERIES()                                                                  \
+  {                                                                                      \
+    _Pragma("unroll") for (int j = 0; j < QPT; ++j) qr[j] =                              \
+        buffer_load16(r_q, qoff[j] + uq * (SK * 2));                                     \
+    uq = uq + 1 == nq4 ? 0 : uq + 1;                                                     \
+  }
+#define OPRAG_BFRAG(QS, J)                                                               \
+  _Pragma("unroll") for (int ni = 0; ni < NW; ++ni) fb[ni] =                             \
+      *reinterpret_cast<const V*>((QS) + fbase + ni * 4096 + (((4 * (J) + fcol) ^ fsw) * 16));
+// One k-step: B operand ni of the next k-step (same slot) is read as soon as the MFMAs of
+// this k-step are done with fb[ni], so a single set of B registers stays one k-step ahead.
+#define OPRAG_KSTEP(U, J, QS)                                                            \
+  {                                                                                      \
+    OPRAG_ROWS(((U) + PX) % RS)                                                          \
+    _Pragma("unroll") for (int ni = 0; ni < NW; ++ni) {                                  \
+      _Pragma("unroll") for (int mi = 0; mi < MW; ++mi)                                  \
+          acc[mi][ni] = M::run(xr[(U) % RS][mi], fb[ni], acc[mi][ni]);                   \
+      if ((J) < 3)                                                                       \
+        fb[ni] = *reinterpret_cast<const V*>((QS) + fbase + ni * 4096 +                  \
+                                             (((4 * (J) + 4 + fcol) ^ fsw) * 16));       \
+    }                                                                                    \
+  }
+#define OPRAG_SUPER(H)                                                                   \
+  {                                                                                      \
+    const int sup = s0 / 4 + (H);                                                        \
+    unsigned char* qs = qslots + (sup & 1) * QSLOT;                                      \
+    unsigned char* qn = qslots + ((sup + 1) & 1) * QSLOT;                                \
+    OPRAG_KSTEP(4 * (H) + 0, 0, qs)                                                      \
+    OPRAG_KSTEP(4 * (H) + 1, 1, qs)                                                      \
+    OPRAG_KSTEP(4 * (H) + 2, 2, qs)                                                      \
+    OPRAG_KSTEP(4 * (H) + 3, 3, qs)                                                      \
+    _Pragma("unroll") for (int j = 0; j < QPT; ++j)                                      \
+        *reinterpret_cast<u32x4*>(qn + qdst[j]) = qr[j];                                 \
+    OPRAG_QUERIES()                                                                      \
+    lds_barrier();                                                                       \
+    OPRAG_BFRAG(qn, 0)                                                                   \
+  }
+
+    // prologue: rows of k-steps 0 .. PX-1, queries of super-steps 0 (to slot 0) and 1
 #pragma unroll
-      for (int g = 0; g < G; ++g) {
+    for (int u = 0; u < PX; ++u) OPRAG_ROWS(u)
+    OPRAG_QUERIES()
 #pragma unroll
-        for (int mi = g * MWP; mi < (g + 1) * MWP; ++mi)
-#pragma unroll
-          for (int ni = 0; ni < NW; ++ni) {
-            const int q = ni * 16 + (lane & 15);
-            const int rl = w * MWP * 16 + (mi - g * MWP) * 16 + (lane >> 4) * 4;
-            *reinterpret_cast<f32x4*>(S + q * SR + rl) = acc[mi][ni];
-          }
-        PassRows pr;
-        pr.tile0 = tile0;
-        pr.blk = MWP * 16;
-        pr.blk_stride = MW * 16;
-        pr.off = g * MWP * 16;
-        int nv = 0;
-#pragma unroll
-        for (int bb = 0; bb < kWaves; ++bb) {
-          const long long start = tile0 + (long long)bb * MW * 16 + g * MWP * 16;
-          nv += (int)max(0ll, min((long long)(MWP * 16), row_end - start));
-        }
-        pr.nvalid = nv;
-        lds_barrier();
-        sel.pass(S, SR, RP, pr, q_lim, a.k, scratch);
-      }
+    for (int j = 0; j < QPT; ++j) *reinterpret_cast<u32x4*>(qslots + qdst[j]) = qr[j];
+    OPRAG_QUERIES()
+    lds_barrier();
+    OPRAG_BFRAG(qslots, 0)
+
+    // Tiles one after another; BODY divides the k-steps of a tile, so ring slots are
+    // literal, and the ring runs across tile boundaries (the next tile's first rows are in
+    // flight during a tile's selection).
+    for (int t = 0; t < n_tiles; ++t) {
 #pragma unroll
       for (int mi = 0; mi < MW; ++mi)
 #pragma unroll
         for (int ni = 0; ni < NW; ++ni) acc[mi][ni] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int s0 = t * nk; s0 < (t + 1) * nk; s0 += BODY) {
+        OPRAG_SUPER(0)
+        if constexpr (BODY >= 8) OPRAG_SUPER(1)
+        if constexpr (BODY == 16) {
+          OPRAG_SUPER(2)
+          OPRAG_SUPER(3)
+        }
+      }
+      // ---- selection for the tile: registers first, else G passes through LDS
+      const long long tile0 = row_begin + (long long)t * TR;
+      bool done = false;
+      if constexpr (kBlk)
+        done = blk_epilogue<BN, MW>(acc, sel, reinterpret_cast<unsigned char*>(S), scratch, tile0, row_end, q_lim,
+                                    a.k);
+      else if constexpr (SEL == 0)
+        done = reg_epilogue<BN, MW, KS>(acc, sel, S, scratch, tile0, row_end, q_lim, a.k);
+      if (!done) {
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+#pragma unroll
+          for (int mi = g * MWP; mi < (g + 1) * MWP; ++mi)
+#pragma unroll
+            for (int ni = 0; ni < NW; ++ni) {
+              const int q = ni * 16 + (lane & 15);
+              const int rl = w * MWP * 16 + (mi - g * MWP) * 16 + (lane >> 4) * 4;
+              *reinterpret_cast<f32x4*>(S + q * SR + rl) = acc[mi][ni];
+            }
+          PassRows pr;
+          pr.tile0 = tile0;
+          pr.blk = MWP * 16;
+          pr.blk_stride = MW * 16;
+          pr.off = g * MWP * 16;
+          int nv = 0;
+#pragma unroll
+          for (int bb = 0; bb < kWaves; ++bb) {
+            const long long start = tile0 + (long long)bb * MW * 16 + g * MWP * 16;
+            nv += (int)max(0ll, min((long long)(MWP * 16), row_end - start));
+          }
+          pr.nvalid = nv;
+          lds_barrier();
+          sel.pass(S, SR, RP, pr, q_lim, a.k, scratch);
+        }
+      }
     }
+#undef OPRAG_SUPER
+#undef OPRAG_KSTEP
+#undef OPRAG_BFRAG
+#undef OPRAG_QUERIES
+#undef OPRAG_ROWS
   }
-#undef OPRAG_STEP
-#undef OPRAG_ISSUE
   sel.write(a, q0, chunk);
 }
 
@@ -628,6 +989,7 @@ __global__ __launch_bounds__(kThreads) void merge_small_kernel(const unsigned lo
                                                                int n_chunks, int nq, int k, float* out_scores,
                                                                long long* out_ids) {
   constexpr int CAP = 2 * KS;
+  constexpr int PR = 16;  // candidates per thread kept in registers (more: read twice)
   __shared__ u64 cand[CAP];
   __shared__ float wl[kWaves][KS];
   __shared__ int wsum[kWaves];
@@ -640,15 +1002,24 @@ __global__ __launch_bounds__(kThreads) void merge_small_kernel(const unsigned lo
   const long long b0 = (long long)t * per;
   const long long b1 = b0 + per < n ? b0 + per : n;
   const unsigned long long* src = partial + (long long)q * n;
+  const bool in_regs = per <= PR;
 
+  u64 rc[PR];
   ValTop<KS> L;
   L.clear();
-  for (long long j = b0; j < b1; j += 4) {
-    u64 c[4];
+  if (in_regs) {
 #pragma unroll
-    for (int u = 0; u < 4; ++u) c[u] = j + u < b1 ? src[j + u] : 0ull;
+    for (int u = 0; u < PR; ++u) rc[u] = b0 + u < b1 ? src[b0 + u] : 0ull;
 #pragma unroll
-    for (int u = 0; u < 4; ++u) L.insert(c[u] ? comp_score(c[u]) : kNegInf);
+    for (int u = 0; u < PR; ++u) L.insert(rc[u] ? comp_score(rc[u]) : kNegInf);
+  } else {
+    for (long long j = b0; j < b1; j += 4) {
+      u64 c4[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) c4[u] = j + u < b1 ? src[j + u] : 0ull;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) L.insert(c4[u] ? comp_score(c4[u]) : kNegInf);
+    }
   }
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) {
@@ -678,12 +1049,22 @@ __global__ __launch_bounds__(kThreads) void merge_small_kernel(const unsigned lo
   const float tau = s_tau;
   const int need = s_need;
   int neq = 0;
-  for (long long j = b0; j < b1; ++j) {
-    const u64 c = src[j];
-    if (!c) continue;
-    const float v = comp_score(c);
-    if (v > tau) cand[atomicAdd(&s_cnt, 1)] = c;
-    neq += v == tau ? 1 : 0;
+  if (in_regs) {
+#pragma unroll
+    for (int u = 0; u < PR; ++u) {
+      if (!rc[u]) continue;
+      const float v = comp_score(rc[u]);
+      if (v > tau) cand[atomicAdd(&s_cnt, 1)] = rc[u];
+      neq += v == tau ? 1 : 0;
+    }
+  } else {
+    for (long long j = b0; j < b1; ++j) {
+      const u64 c = src[j];
+      if (!c) continue;
+      const float v = comp_score(c);
+      if (v > tau) cand[atomicAdd(&s_cnt, 1)] = c;
+      neq += v == tau ? 1 : 0;
+    }
   }
   // exclusive prefix of the tie counts in thread order
   int x = neq;
@@ -696,14 +1077,24 @@ __global__ __launch_bounds__(kThreads) void merge_small_kernel(const unsigned lo
   __syncthreads();
   int pre = x - neq;
   for (int ww = 0; ww < w; ++ww) pre += wsum[ww];
-  if (neq > 0 && pre < need)
-    for (long long j = b0; j < b1 && pre < need; ++j) {
-      const u64 c = src[j];
-      if (c && comp_score(c) == tau) {
-        cand[atomicAdd(&s_cnt, 1)] = c;
-        ++pre;
+  if (neq > 0 && pre < need) {
+    if (in_regs) {
+#pragma unroll
+      for (int u = 0; u < PR; ++u)
+        if (rc[u] && pre < need && comp_score(rc[u]) == tau) {
+          cand[atomicAdd(&s_cnt, 1)] = rc[u];
+          ++pre;
+        }
+    } else {
+      for (long long j = b0; j < b1 && pre < need; ++j) {
+        const u64 c = src[j];
+        if (c && comp_score(c) == tau) {
+          cand[atomicAdd(&s_cnt, 1)] = c;
+          ++pre;
+        }
       }
     }
+  }
   __syncthreads();
   if (t == 0) {
     RegTopK<KS> list;
@@ -754,28 +1145,32 @@ __global__ __launch_bounds__(kThreads) void merge_large_kernel(const unsigned lo
 struct KernelInfo {
   void (*fn)(DenseArgs);
   int dtype, bn, tile_rows, ks, sel, wgs_per_cu, min_nq, max_nq;
+  int ring;  // MFMA kernels: k-steps per loop iteration, which must divide d / 32 (0: none)
 };
 
 #define MFK(DT, NW, MW, RS, G, KS, SEL, OCC, LO, HI) \
-  {dense_mfma_kernel<DT, NW, MW, RS, G, KS, SEL>, DT, NW * 16, kWaves * MW * 16, KS, SEL, OCC, LO, HI}
+  {dense_mfma_kernel<DT, NW, MW, RS, G, KS, SEL>, DT, NW * 16, kWaves * MW * 16, KS, SEL, OCC, LO, HI, RS}
+// Deep rings first; the 4-deep variants serve dimensions that are not multiples of the ring.
+#define MF_KS(DT, NW, MW, RS, G, OCC, LO, HI)                                                   \
+  MFK(DT, NW, MW, RS, G, 5, 0, OCC, LO, HI), MFK(DT, NW, MW, RS, G, 8, 0, OCC, LO, HI),          \
+      MFK(DT, NW, MW, RS, G, 16, 0, OCC, LO, HI)
 #define MF_SET(DT)                                                                              \
-  MFK(DT, 1, 1, 4, 1, 5, 0, 4, 1, 16), MFK(DT, 1, 1, 4, 1, 8, 0, 4, 1, 16),                    \
-      MFK(DT, 1, 1, 4, 1, 16, 0, 4, 1, 16), MFK(DT, 4, 2, 4, 1, 5, 0, 2, 17, 64),              \
-      MFK(DT, 4, 2, 4, 1, 8, 0, 2, 17, 64), MFK(DT, 4, 2, 4, 1, 16, 0, 2, 17, 64),             \
-      MFK(DT, 8, 4, 4, 4, 5, 0, 1, 65, 1 << 30), MFK(DT, 8, 4, 4, 4, 8, 0, 1, 65, 1 << 30),    \
-      MFK(DT, 8, 4, 4, 4, 16, 0, 1, 65, 1 << 30), MFK(DT, 2, 4, 4, 1, 8, 1, 2, 1, 1 << 30)
+  MF_KS(DT, 1, 1, 16, 1, 4, 1, 16), MF_KS(DT, 1, 1, 4, 1, 4, 1, 16), MF_KS(DT, 4, 2, 8, 1, 2, 17, 64), \
+      MF_KS(DT, 4, 2, 4, 1, 2, 17, 64), MFK(DT, 8, 4, 4, 2, 5, 0, 1, 65, 1 << 30),                \
+      MFK(DT, 8, 4, 4, 4, 8, 0, 1, 65, 1 << 30), MFK(DT, 8, 4, 4, 4, 16, 0, 1, 65, 1 << 30),         \
+      MFK(DT, 2, 4, 8, 1, 8, 1, 2, 1, 1 << 30), MFK(DT, 2, 4, 4, 1, 8, 1, 2, 1, 1 << 30)
 
 const KernelInfo kKernels[] = {
-    {dense_f32_kernel<5, 0>, kDtypeF32, 32, 64, 5, 0, 2, 1, 1 << 30},
-    {dense_f32_kernel<8, 0>, kDtypeF32, 32, 64, 8, 0, 2, 1, 1 << 30},
-    {dense_f32_kernel<16, 0>, kDtypeF32, 32, 64, 16, 0, 2, 1, 1 << 30},
-    {dense_f32_kernel<8, 1>, kDtypeF32, 32, 64, 128, 1, 2, 1, 1 << 30},
+    {dense_f32_kernel<5, 0>, kDtypeF32, 32, 64, 5, 0, 2, 1, 1 << 30, 0},
+    {dense_f32_kernel<8, 0>, kDtypeF32, 32, 64, 8, 0, 2, 1, 1 << 30, 0},
+    {dense_f32_kernel<16, 0>, kDtypeF32, 32, 64, 16, 0, 2, 1, 1 << 30, 0},
+    {dense_f32_kernel<8, 1>, kDtypeF32, 32, 64, 128, 1, 2, 1, 1 << 30, 0},
     MF_SET(kDtypeBF16),
     MF_SET(kDtypeF16),
 };
 constexpr int kNumKernels = sizeof(kKernels) / sizeof(kKernels[0]);
 
-int pick_kernel(int dtype, int nq, int k) {
+int pick_kernel(int dtype, int d, int nq, int k) {
   const int sel = k <= 16 ? 0 : 1;
   const int ks = k <= 5 ? 5 : (k <= 8 ? 8 : 16);
   for (int i = 0; i < kNumKernels; ++i) {
@@ -783,6 +1178,7 @@ int pick_kernel(int dtype, int nq, int k) {
     if (ki.dtype != dtype || ki.sel != sel) continue;
     if (sel == 0 && ki.ks != ks) continue;
     if (nq < ki.min_nq || nq > ki.max_nq) continue;
+    if (ki.ring && (d / 32) % ki.ring != 0) continue;
     return i;
   }
   return -1;
@@ -793,9 +1189,8 @@ int pick_kernel(int dtype, int nq, int k) {
 constexpr int kNumCUs = 256;
 
 DensePlan plan_dense(int dtype, int d, long long n_rows, int nq, int k) {
-  (void)d;
   DensePlan p;
-  p.kernel = pick_kernel(dtype, nq, k);
+  p.kernel = pick_kernel(dtype, d, nq, k);
   if (p.kernel < 0) return p;
   const KernelInfo& ki = kKernels[p.kernel];
   p.bn = ki.bn;
@@ -805,10 +1200,18 @@ DensePlan plan_dense(int dtype, int d, long long n_rows, int nq, int k) {
   // Enough workgroups to fill the chip twice over, never more chunks than tiles; the large-k
   // selector wants several tiles per chunk so its queues amortise.
   const long long target = (long long)kNumCUs * ki.wgs_per_cu * 2;
-  const long long bound = std::max(1ll, (target + p.n_qblocks - 1) / p.n_qblocks);
+  long long bound = std::max(1ll, (target + p.n_qblocks - 1) / p.n_qblocks);
+  // MFMA kernels address a chunk with 32-bit byte offsets: keep chunks under 2^30 bytes.
+  // The minimum grows with the row count, so a workspace planned for the capacity suffices.
+  long long min_chunks = 1;
+  if (ki.ring) {
+    const long long max_tiles = std::max(1ll, (1ll << 30) / ((long long)p.tile_rows * d * 2));
+    min_chunks = std::max(1ll, (n_tiles + max_tiles - 1) / max_tiles);
+    bound = std::max(bound, min_chunks);
+  }
   long long chunks = bound;
   if (ki.sel == 1) chunks = std::min(chunks, std::max(1ll, n_tiles / 4));
-  chunks = std::max(1ll, std::min(chunks, n_tiles));
+  chunks = std::max(min_chunks, std::max(1ll, std::min(chunks, n_tiles)));
   const long long tiles_per_chunk = n_tiles ? (n_tiles + chunks - 1) / chunks : 1;
   p.rows_per_chunk = tiles_per_chunk * p.tile_rows;
   p.n_chunks = (int)std::max(1ll, n_tiles ? (n_tiles + tiles_per_chunk - 1) / tiles_per_chunk : 1);
