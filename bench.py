@@ -2,22 +2,31 @@
 
 Workload: exact top-5 by inner product for batches of 256 queries over 32,768 x 1,024 bf16
 unit rows (256-component Gaussian mixture, sigma 0.3; queries are noisy copies of rows),
-fp32 accumulation.  A step is one oprag_search_dense call over one batch.
+fp32 accumulation.  A step is one oprag_search_dense call over one batch: the scoring
+kernel (per-chunk top-k lists) plus the merge of the lists.
 
 Protocol: the index is replicated into 16 slabs (1 GiB in all, more than the 256 MB
 Infinity Cache) and steps rotate over them, so every step streams its slab from HBM.
-Steps are captured into a HIP graph (16 searches, one per slab) and replayed, so the
-Python launch cost does not hide the kernel.  The same searches launched one by one from
-Python are reported as ``eager_queries_per_s``; a single slab reused every step as
-``warm_queries_per_s``.
+Steps are captured into HIP graphs (16 searches, one per slab) and replayed.  The same
+searches launched one by one from Python give ``eager_queries_per_s`` and per-call
+percentiles; a single slab reused every step gives ``warm_queries_per_s``.
 
-Also reported: the roofline fraction of the search kernel (algorithmic HBM bytes per
-launch over its average duration) and the CPU oracle's own throughput on a sample of the
-same workload (fp64 scores with a multithreaded BLAS, full stable sort per query).
+Roofline: the scoring kernel carries a pair of HIP events in its own dispatch on the stream
+it runs on (oprag_time_next_dense_kernel), stamped when the kernel starts and ends; its
+average duration over a pass of 512 timed eager calls of the same workload gives
+achieved = algorithmic bytes per launch (rows + queries + output lists) / that duration.  ``traffic`` is the HBM traffic per launch measured with
+rocprofv3 counters (see --pmc-pass / --pmc-summarize), used only while the kernel source is
+unchanged since the counters were taken.
+
+Also reported: the CPU oracle's own throughput on a bounded sample of the same workload
+(fp64 scores with a multithreaded BLAS, full stable sort per query).
 """
 from __future__ import annotations
 
 import argparse
+import csv
+import glob
+import hashlib
 import json
 import os
 import platform
@@ -25,7 +34,6 @@ import sys
 import time
 
 import numpy as np
-import torch
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
@@ -35,6 +43,9 @@ COPIES = 16
 HBM_PEAK_GBS = 8000.0
 BF16_PEAK_TFLOPS = 2500.0
 METRIC = "queries/s exact top-k (32K×1024 bf16, batch 256) + % of HBM/MFMA roofline"
+KERNEL_SRC = os.path.join(ROOT, "paper_2608_08340_amd", "csrc", "dense.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "dense_scoring_32k_x_1024_bf16_b256_traffic.json")
+COPY_ROWS = 65536  # reference copy for counter scaling: 65,536 x 1,024 bf16 = 128 MiB each way
 
 
 def log(*a):
@@ -51,7 +62,16 @@ def cpu_model() -> str:
     return platform.processor() or "unknown"
 
 
-def cpu_baseline(rows: torch.Tensor, queries: torch.Tensor, budget_s: float) -> dict:
+def kernel_source_sha() -> str:
+    return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
+
+
+def algorithmic_bytes(n_rows: int, dim: int, batch: int, k: int, elem: int = 2) -> int:
+    """Index rows + queries + the k (score, id) results per query."""
+    return n_rows * dim * elem + batch * dim * elem + batch * k * 12
+
+
+def cpu_baseline(rows, queries, budget_s: float) -> dict:
     """The oracle as it stands: fp64 GEMM + full stable sort per query, timed on host cores."""
     from threadpoolctl import threadpool_info
 
@@ -71,10 +91,102 @@ def cpu_baseline(rows: torch.Tensor, queries: torch.Tensor, budget_s: float) -> 
             break
     blas = [i for i in threadpool_info() if i.get("user_api") == "blas"]
     threads = max([i.get("num_threads", 1) for i in blas] or [1])
-    return {"value": done / el, "unit": "queries/s", "cores": int(threads), "kind": "oracle",
+    return {"value": round(done / el, 2), "unit": "queries/s", "cores": int(threads), "kind": "oracle",
             "sample": f"{done} queries in batches of {BATCH} over the same 32,768 x 1,024 bf16 rows, top-{K}: "
                       f"fp64 numpy GEMM ({threads} BLAS threads) + per-query full stable sort (1 thread); "
                       f"{el:.1f} s; host {cpu_model()}, {len(os.sched_getaffinity(0))} cores visible"}
+
+
+def traffic_record():
+    """HBM bytes per scoring launch from the committed counter summary, if still current."""
+    try:
+        rec = json.load(open(TRAFFIC_FILE))
+    except (OSError, ValueError):
+        return None, "no counter summary"
+    if rec.get("kernel_source_sha") != kernel_source_sha():
+        return None, "kernel changed since the counters were taken"
+    return rec.get("traffic_bytes_per_launch"), rec.get("command", "")
+
+
+def pmc_summarize(out_dir: str) -> int:
+    """Turn two rocprofv3 --pmc runs of --pmc-pass (FETCH_SIZE, WRITE_SIZE) into the traffic record."""
+    vals = {}
+    for counter in ("FETCH_SIZE", "WRITE_SIZE"):
+        files = glob.glob(os.path.join(out_dir, counter.lower(), "**", "*counter_collection.csv"), recursive=True)
+        if not files:
+            print(f"no counter file for {counter} under {out_dir}", file=sys.stderr)
+            return 1
+        if len(files) != 1:
+            print(f"{counter}: expected one counter file, found {len(files)}", file=sys.stderr)
+            return 1
+        copies, score = [], []
+        for r in csv.DictReader(open(files[0])):
+            if r["Counter_Name"] != counter:
+                continue
+            name = r["Kernel_Name"]
+            if "copy16_kernel" in name:
+                copies.append((int(r["Dispatch_Id"]), float(r["Counter_Value"])))
+            elif "dense_mfma_kernel" in name:
+                score.append(float(r["Counter_Value"]))
+        if not copies or not score:
+            print(f"{counter}: missing dispatches (copy {len(copies)}, scoring {len(score)})", file=sys.stderr)
+            return 1
+        # the reference copy is the pass's first copy (the index uploads that follow are copies too)
+        vals[counter] = {"copy": min(copies)[1], "score": float(np.median(score)),
+                         "n": {"copy": 1, "score": len(score)}}
+    copy_kib = COPY_ROWS * DIM * 2 / 1024.0
+    f_fetch = copy_kib / vals["FETCH_SIZE"]["copy"]
+    f_write = copy_kib / vals["WRITE_SIZE"]["copy"]
+    fetch = vals["FETCH_SIZE"]["score"] * f_fetch * 1024.0
+    write = vals["WRITE_SIZE"]["score"] * f_write * 1024.0
+    rec = {
+        "kernel": "dense_mfma_kernel (scoring, 32,768 x 1,024 bf16, batch 256, k 5)",
+        "kernel_source_sha": kernel_source_sha(),
+        "fetch_kib_raw": vals["FETCH_SIZE"]["score"], "write_kib_raw": vals["WRITE_SIZE"]["score"],
+        "copy_fetch_kib_raw": vals["FETCH_SIZE"]["copy"], "copy_write_kib_raw": vals["WRITE_SIZE"]["copy"],
+        "copy_bytes_each_way": COPY_ROWS * DIM * 2,
+        "fetch_scale": f_fetch, "write_scale": f_write,
+        "traffic_bytes_per_launch": round(fetch + write),
+        "algorithmic_bytes_per_launch": algorithmic_bytes(N_ROWS, DIM, BATCH, K),
+        "dispatches": {c: vals[c]["n"] for c in vals},
+        "command": "cd /tmp && export TMPDIR=/tmp && for c in FETCH_SIZE WRITE_SIZE; do timeout -s KILL 120 "
+                   "rocprofv3 --pmc $c --output-format csv -d $GRAFT_REPO_ROOT/gpurun_out/pmc/$(echo $c | tr A-Z a-z) "
+                   "-- python3 $GRAFT_REPO_ROOT/bench.py --pmc-pass; done && python3 $GRAFT_REPO_ROOT/bench.py "
+                   "--pmc-summarize $GRAFT_REPO_ROOT/gpurun_out/pmc",
+    }
+    os.makedirs(os.path.dirname(TRAFFIC_FILE), exist_ok=True)
+    json.dump(rec, open(TRAFFIC_FILE, "w"), indent=1)
+    print(json.dumps(rec))
+    return 0
+
+
+STATS_FILE = os.path.join(ROOT, "profiles", "dense_scoring_32k_x_1024_bf16_b256_kernel_stats.txt")
+
+
+def trace_summarize(out_dir: str) -> int:
+    """Write the kernel-trace statistics of a rocprofv3 --kernel-trace --stats run of bench.py."""
+    files = glob.glob(os.path.join(out_dir, "**", "*kernel_stats.csv"), recursive=True)
+    if not files:
+        print(f"no kernel_stats.csv under {out_dir}", file=sys.stderr)
+        return 1
+    rows = list(csv.DictReader(open(files[0])))
+    lines = [
+        "rocprofv3 kernel statistics of the default bench.py run (32,768 x 1,024 bf16, batch 256, k 5)",
+        "command: cd /tmp && export TMPDIR=/tmp && timeout -k 10 300 rocprofv3 --kernel-trace --stats "
+        "--output-format csv -d $GRAFT_REPO_ROOT/gpurun_out/kt_bench -o bench -- python3 $GRAFT_REPO_ROOT/bench.py "
+        "&& python3 $GRAFT_REPO_ROOT/bench.py --trace-summarize $GRAFT_REPO_ROOT/gpurun_out/kt_bench",
+        f"kernel source sha256[:16] of dense.hip: {kernel_source_sha()}",
+        "",
+        f"{'calls':>7} {'avg_us':>9} {'min_us':>9} {'max_us':>9} {'share%':>7}  kernel",
+    ]
+    for r in rows[:12]:
+        name = r["Name"].replace("(anonymous namespace)::", "")
+        lines.append(f"{int(r['Calls']):7d} {float(r['AverageNs']) / 1e3:9.2f} {float(r['MinNs']) / 1e3:9.2f} "
+                     f"{float(r['MaxNs']) / 1e3:9.2f} {float(r['Percentage']):7.2f}  {name[:150]}")
+    os.makedirs(os.path.dirname(STATS_FILE), exist_ok=True)
+    open(STATS_FILE, "w").write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+    return 0
 
 
 def main() -> int:
@@ -85,25 +197,53 @@ def main() -> int:
     ap.add_argument("--copies", type=int, default=COPIES)
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     ap.add_argument("--no-cpu", action="store_true")
-    ap.add_argument("--mode", choices=["graph", "eager"], default="graph")
+    ap.add_argument("--pmc-pass", action="store_true",
+                    help="a short run for counter collection: one reference copy, then 8 cold searches")
+    ap.add_argument("--pmc-summarize", metavar="DIR", help="write the traffic record from two --pmc runs")
+    ap.add_argument("--trace-summarize", metavar="DIR", help="write the kernel statistics of a traced run")
     args = ap.parse_args()
+    if args.pmc_summarize:
+        return pmc_summarize(args.pmc_summarize)
+    if args.trace_summarize:
+        return trace_summarize(args.trace_summarize)
     if args.gpus != 1:
-        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported by this build "
-              f"(the sharded multi-GPU path is a design, not code)", file=sys.stderr)
+        print(f"bench.py runs on one GPU only: --gpus {args.gpus} is not supported (the multi-GPU sharding "
+              f"of the index is a design, not code, in this library)", file=sys.stderr)
         return 2
+
+    import torch
+
+    import synth
+    import paper_2608_08340_amd as P
+    from paper_2608_08340_amd import Index
+
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         return 2
-
-    import synth
-    from paper_2608_08340_amd import Index
-
     dev = torch.device("cuda", 0)
     log("generating 32,768 x 1,024 bf16 rows")
     w = synth.dense_32k()
     rows_dev = w.rows.to(dev)
     q = w.queries[:BATCH].contiguous().to(dev)
     copies = max(1, args.copies)
+
+    if args.pmc_pass:
+        ref = Index(DIM, COPY_ROWS, torch.bfloat16)
+        src = torch.zeros((COPY_ROWS, DIM), dtype=torch.bfloat16, device=dev)
+        ref.upsert(src)  # one same-dtype copy of known size: the scale reference
+        torch.cuda.synchronize()
+        idxs = []
+        for c in range(8):
+            ix = Index(DIM, N_ROWS, torch.bfloat16)
+            ix.upsert(rows_dev)
+            idxs.append(ix)
+        torch.cuda.synchronize()
+        for ix in idxs:
+            ix.search_dense(q, K)
+        torch.cuda.synchronize()
+        print("pmc pass done", flush=True)
+        return 0
+
     idxs = []
     for c in range(copies):
         ix = Index(DIM, N_ROWS, torch.bfloat16)
@@ -116,14 +256,12 @@ def main() -> int:
         idxs[c].workspace(0, BATCH, K)
         idxs[c].search_dense(q, K, out=outs[c])
     torch.cuda.synchronize()
-    # every copy returns the same lists
-    for c in range(1, copies):
+    for c in range(1, copies):  # every copy returns the same lists
         assert torch.equal(outs[c][1], outs[0][1])
 
     steps = max(1, args.steps)
     warm = max(0, args.warmup)
     stream = torch.cuda.current_stream(dev)
-
     def capture(n):
         """A HIP graph of n consecutive steps over slabs 0 .. n-1."""
         gr = torch.cuda.CUDAGraph()
@@ -141,12 +279,12 @@ def main() -> int:
         for _ in range(n // copies):
             g_full.replay()
         if n % copies:
-            (g_rem if n % copies == rem else capture(n % copies)).replay()
+            g_rem.replay()
 
     log(f"warmup {warm} steps")
     run(warm)
     torch.cuda.synchronize()
-    ref = outs[0][1].clone()
+    ref_ids = outs[0][1].clone()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     log(f"timing {steps} steps (graph replay over {copies} slabs)")
     torch.cuda.synchronize()
@@ -156,19 +294,29 @@ def main() -> int:
     e1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    graph_ms = e0.elapsed_time(e1) / steps
+    ms = e0.elapsed_time(e1) / steps
     for c in range(min(copies, steps)):
-        assert torch.equal(outs[c][1], ref), "graph replay changed the result"
+        assert torch.equal(outs[c][1], ref_ids), "graph replay changed the result"
 
-    # ---- eager steps (Python launches each search)
-    eager_steps = min(steps, 512)
+    # ---- eager calls: per-call percentiles, and the scoring kernel's own duration from the
+    # events its dispatch carries
+    n_eager = min(steps, 512)
+    cev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n_eager)]
+    kev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n_eager)]
+    for a, b in kev:  # create the events (torch makes them on first record) before the library records them
+        a.record(stream)
+        b.record(stream)
     torch.cuda.synchronize()
-    e0.record(stream)
-    for i in range(eager_steps):
+    for i in range(n_eager):
+        cev[i][0].record(stream)
+        P.time_next_dense_kernel(*kev[i])
         idxs[i % copies].search_dense(q, K, out=outs[i % copies])
-    e1.record(stream)
+        cev[i][1].record(stream)
     torch.cuda.synchronize()
-    eager_ms = e0.elapsed_time(e1) / eager_steps
+    call_ms = np.array([a.elapsed_time(b) for a, b in cev])
+    kern_ms = np.array([a.elapsed_time(b) for a, b in kev])
+    kernel_ms = float(kern_ms.mean())
+    kernel_src = f"HIP events carried by the kernel's dispatch, mean of {n_eager} eager calls"
 
     # ---- warm: one slab, graph of 16 searches on it
     gw = torch.cuda.CUDAGraph()
@@ -178,18 +326,19 @@ def main() -> int:
     torch.cuda.synchronize()
     gw.replay()
     torch.cuda.synchronize()
+    reps = max(1, 256 // copies)
     e0.record(stream)
-    for _ in range(max(1, 256 // copies)):
+    for _ in range(reps):
         gw.replay()
     e1.record(stream)
     torch.cuda.synchronize()
-    warm_ms = e0.elapsed_time(e1) / (max(1, 256 // copies) * copies)
+    warm_ms = e0.elapsed_time(e1) / (reps * copies)
 
-    ms = graph_ms
     value = BATCH / (ms / 1e3)
-    bytes_per_launch = N_ROWS * DIM * 2 + BATCH * DIM * 2 + BATCH * K * 12
-    flops_per_launch = 2.0 * BATCH * N_ROWS * DIM
-    achieved = bytes_per_launch / (ms / 1e3) / 1e9
+    abytes = algorithmic_bytes(N_ROWS, DIM, BATCH, K)
+    flops = 2.0 * BATCH * N_ROWS * DIM
+    achieved = abytes / (kernel_ms / 1e3) / 1e9
+    traffic, traffic_note = traffic_record()
     result = {
         "metric": METRIC, "value": round(value, 1), "unit": "queries/s", "n_gpus": 1,
         "steps": steps, "warmup": warm, "ms_per_step": round(ms, 5), "higher_is_better": True,
@@ -198,12 +347,16 @@ def main() -> int:
                                "batch 256, fp32 accumulation; 16 slab copies rotated (HBM-cold), HIP-graph replay",
                    "n_rows": N_ROWS, "dim": DIM, "batch": BATCH, "k": K, "slab_copies": copies},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
-                     "kernel": "dense_mfma_kernel<bf16, BN=128, MW=4, KS=8, SEL=0>",
-                     "bytes_per_launch": bytes_per_launch,
-                     "mfma_tflops": round(flops_per_launch / (ms / 1e3) / 1e12, 1),
-                     "mfma_frac": round(flops_per_launch / (ms / 1e3) / 1e12 / BF16_PEAK_TFLOPS, 4)},
-        "eager_queries_per_s": round(BATCH / (eager_ms / 1e3), 1),
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic},
+        "kernel": {"name": "dense_mfma_kernel (scoring; BN=128 queries x 256 rows per workgroup)",
+                   "avg_us": round(kernel_ms * 1e3, 2), "timing": kernel_src,
+                   "p10_p50_p90_us": [round(float(np.percentile(kern_ms, p)) * 1e3, 2) for p in (10, 50, 90)],
+                   "algorithmic_bytes_per_launch": abytes, "flops_per_launch": flops,
+                   "mfma_tflops": round(flops / (kernel_ms / 1e3) / 1e12, 1),
+                   "mfma_frac": round(flops / (kernel_ms / 1e3) / 1e12 / BF16_PEAK_TFLOPS, 4),
+                   "traffic_note": traffic_note},
+        "call_us_p10_p50_p90": [round(float(np.percentile(call_ms, p)) * 1e3, 2) for p in (10, 50, 90)],
+        "eager_queries_per_s": round(BATCH / (float(np.median(call_ms)) / 1e3), 1),
         "warm_queries_per_s": round(BATCH / (warm_ms / 1e3), 1),
         "wall_s_timed": round(wall, 3),
     }

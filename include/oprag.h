@@ -170,6 +170,17 @@ oprag_status oprag_search_hybrid(oprag_index *idx, const void *q_dev, const int3
                                  int32_t rrf_k, int32_t k, float *fused_dev, int64_t *ids_dev, void *workspace_dev,
                                  size_t workspace_bytes, void *stream);
 
+/*
+ * Kernel timing (diagnostics: measuring the scoring kernel against its roofline).  Arms a
+ * pair of caller-created HIP events (hipEvent_t passed as void *) that the next dense
+ * search issued from the calling thread records on its stream immediately before and after
+ * its scoring kernel, the kernel that streams the index (the merge of per-chunk lists that
+ * may follow stays outside the pair; with more than 2^20 queries only the first launch is
+ * bracketed).  One-shot: the pair is disarmed once recorded.  NULL, NULL disarms.  The
+ * library creates, keeps and destroys no event.
+ */
+oprag_status oprag_time_next_dense_kernel(void *start_event, void *stop_event);
+
 #ifdef __cplusplus
 }
 #endif

@@ -54,6 +54,7 @@ _SIGS = {
     "oprag_search_sparse": ([_P, _P, _P, _I64, _I32, _P, _P, _P, _SZ, _P], _I32),
     "oprag_rrf_fuse": ([_P, _I32, _P, _I32, _I64, _I32, _I32, _P, _P, _P], _I32),
     "oprag_search_hybrid": ([_P, _P, _P, _P, _I64, _I32, _I32, _I32, _I32, _P, _P, _P, _SZ, _P], _I32),
+    "oprag_time_next_dense_kernel": ([_P, _P], _I32),
 }
 _lib = None
 _lock = threading.Lock()
@@ -231,3 +232,13 @@ def rrf_fuse(dense_ids: torch.Tensor, sparse_ids: torch.Tensor, rrf_k: int = 60,
     _check(library().oprag_rrf_fuse(_ptr(dense_ids), dense_ids.shape[1], _ptr(sparse_ids), sparse_ids.shape[1], nq,
                                     rrf_k, k, _ptr(fused), _ptr(ids), _stream(dev)))
     return fused, ids
+
+
+def time_next_dense_kernel(start: torch.cuda.Event | None, stop: torch.cuda.Event | None) -> None:
+    """Arm two timing events that the next dense search from this thread records on its stream
+    right before and after its scoring kernel (oprag_time_next_dense_kernel). None, None disarms."""
+    if (start is None) != (stop is None):
+        raise OpragError(-1, "pass both events or neither")
+    a = ctypes.c_void_p(start.cuda_event) if start is not None else None
+    b = ctypes.c_void_p(stop.cuda_event) if stop is not None else None
+    _check(library().oprag_time_next_dense_kernel(a, b))

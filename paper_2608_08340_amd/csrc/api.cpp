@@ -29,6 +29,8 @@ struct oprag_index {
 namespace {
 
 thread_local std::string g_err;
+thread_local bool t_time_armed = false;  // oprag_time_next_dense_kernel
+thread_local void* t_time_ev[2] = {nullptr, nullptr};
 
 oprag_status fail(oprag_status s, const char* fmt, ...) {
   char buf[512];
@@ -131,7 +133,13 @@ oprag_status do_dense(oprag_index* idx, const void* q, int64_t nq, int32_t k, fl
     a.partial = static_cast<unsigned long long*>(ws);
     a.out_scores = scores + q0 * k;
     a.out_ids = reinterpret_cast<long long*>(ids) + q0 * k;
-    const hipError_t e = oprag::launch_dense(p, idx->dtype, a, s);
+    hipEvent_t ev0 = nullptr, ev1 = nullptr;
+    if (q0 == 0 && t_time_armed) {
+      ev0 = static_cast<hipEvent_t>(t_time_ev[0]);
+      ev1 = static_cast<hipEvent_t>(t_time_ev[1]);
+      t_time_armed = false;
+    }
+    const hipError_t e = oprag::launch_dense(p, idx->dtype, a, s, ev0, ev1);
     if (e != hipSuccess) return hip_fail(e, "dense search launch");
   }
   return OPRAG_OK;
@@ -142,6 +150,14 @@ oprag_status do_dense(oprag_index* idx, const void* q, int64_t nq, int32_t k, fl
 extern "C" {
 
 int32_t oprag_abi_version(void) { return OPRAG_ABI_VERSION; }
+
+oprag_status oprag_time_next_dense_kernel(void* start_event, void* stop_event) {
+  if (!start_event != !stop_event) return fail(OPRAG_E_INVALID, "pass both events or neither");
+  t_time_ev[0] = start_event;
+  t_time_ev[1] = stop_event;
+  t_time_armed = start_event != nullptr;
+  return OPRAG_OK;
+}
 
 const char* oprag_last_error(void) { return g_err.c_str(); }
 

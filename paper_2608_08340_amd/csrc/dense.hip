@@ -29,6 +29,8 @@
 // batches of 64 candidates above its k-th entry with a bitonic network.
 #include <algorithm>
 
+#include <hip/hip_ext.h>
+
 #include "oprag_internal.h"
 #include "select.h"
 
@@ -1224,13 +1226,18 @@ size_t dense_workspace_bytes(const DensePlan& p, int nq) {
   return (size_t)nq * (size_t)p.cap * sizeof(unsigned long long);
 }
 
-hipError_t launch_dense(const DensePlan& p, int dtype, const DenseArgs& a, hipStream_t s) {
+hipError_t launch_dense(const DensePlan& p, int dtype, const DenseArgs& a, hipStream_t s, hipEvent_t ev0,
+                        hipEvent_t ev1) {
   (void)dtype;
   const KernelInfo& ki = kKernels[p.kernel];
   DenseArgs arg = a;
   void* params[] = {&arg};
-  hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(ki.fn), dim3((unsigned)p.grid), dim3(kThreads), params,
-                                 0, s);
+  // With timing events the launch carries them in its dispatch packet: they are stamped when
+  // the kernel itself starts and ends.
+  hipError_t e = ev0 ? hipExtLaunchKernel(reinterpret_cast<const void*>(ki.fn), dim3((unsigned)p.grid), dim3(kThreads),
+                                          params, 0, s, ev0, ev1, 0)
+                     : hipLaunchKernel(reinterpret_cast<const void*>(ki.fn), dim3((unsigned)p.grid), dim3(kThreads),
+                                       params, 0, s);
   if (e != hipSuccess || p.n_chunks == 1) return e;
   if (ki.sel == 0) {
     const unsigned blocks = (unsigned)a.nq;

@@ -42,7 +42,9 @@ struct DensePlan {
 
 DensePlan plan_dense(int dtype, int d, long long n_rows, int nq, int k);
 size_t dense_workspace_bytes(const DensePlan& p, int nq);
-hipError_t launch_dense(const DensePlan& p, int dtype, const DenseArgs& a, hipStream_t s);
+// ev0 / ev1 (optional) are recorded on s right before and after the scoring kernel.
+hipError_t launch_dense(const DensePlan& p, int dtype, const DenseArgs& a, hipStream_t s, hipEvent_t ev0 = nullptr,
+                        hipEvent_t ev1 = nullptr);
 
 // ---------------------------------------------------------------- sparse (BM25)
 struct SparseIndex {

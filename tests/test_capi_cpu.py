@@ -109,6 +109,14 @@ def test_rrf_rejects(lib, kd, ks, nq, rk, k, ptr, why):
     assert lib.oprag_rrf_fuse(p, kd, p, ks, nq, rk, k, p, p, None) == E_INVALID, why
 
 
+def test_time_hook_arms_and_disarms(lib):
+    assert lib.oprag_time_next_dense_kernel(None, None) == 0
+    assert lib.oprag_time_next_dense_kernel(ctypes.c_void_p(4096), None) == E_INVALID
+    assert lib.oprag_time_next_dense_kernel(None, ctypes.c_void_p(4096)) == E_INVALID
+    assert lib.oprag_time_next_dense_kernel(ctypes.c_void_p(4096), ctypes.c_void_p(8192)) == 0
+    assert lib.oprag_time_next_dense_kernel(None, None) == 0  # disarm: nothing is recorded
+
+
 def test_rrf_empty_batch_is_noop(lib):
     assert lib.oprag_rrf_fuse(None, 5, None, 5, 0, 60, 5, None, None, None) == 0
 
