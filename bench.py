@@ -189,6 +189,154 @@ def trace_summarize(out_dir: str) -> int:
     return 0
 
 
+def _timed(fn, reps: int, stream) -> float:
+    """Mean milliseconds per call of fn() over reps calls on the stream (one warm-up call)."""
+    import torch
+    fn()
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record(stream)
+    for _ in range(reps):
+        fn()
+    b.record(stream)
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) / reps
+
+
+def _kernel_ms(fn, reps: int, stream) -> float:
+    """Mean duration of the scoring kernel of the dense search fn() performs (dispatch events)."""
+    import torch
+    import paper_2608_08340_amd as P
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+    for a, b in evs:
+        a.record(stream)
+        b.record(stream)
+    torch.cuda.synchronize()
+    for a, b in evs:
+        P.time_next_dense_kernel(a, b)
+        fn()
+    torch.cuda.synchronize()
+    return float(np.mean([a.elapsed_time(b) for a, b in evs]))
+
+
+def suite() -> int:
+    """Every workload once: per-call time, throughput and roofline fractions (one JSON line each)."""
+    import torch
+
+    import synth
+    from paper_2608_08340_amd import Index, rrf_fuse
+
+    dev = torch.device("cuda", 0)
+    stream = torch.cuda.current_stream(dev)
+    out = []
+
+    def report(name, ms, batch, abytes, flops, kern_ms=None, **extra):
+        r = {"workload": name, "us_per_call": round(ms * 1e3, 2), "queries_per_s": round(batch / (ms / 1e3), 1),
+             "hbm_frac_call": round(abytes / (ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4),
+             "mfma_frac_call": round(flops / (ms / 1e3) / 1e12 / BF16_PEAK_TFLOPS, 4)}
+        if kern_ms is not None:
+            r.update({"scoring_kernel_us": round(kern_ms * 1e3, 2),
+                      "hbm_frac_kernel": round(abytes / (kern_ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4),
+                      "mfma_frac_kernel": round(flops / (kern_ms / 1e3) / 1e12 / BF16_PEAK_TFLOPS, 4)})
+        r.update(extra)
+        out.append(r)
+        print(json.dumps(r), flush=True)
+
+    # tiny: 1,024 x 384 fp32, 16 queries, top-5 (launch-bound)
+    w = synth.tiny_dense()
+    ix = Index(384, 1024, torch.float32)
+    ix.upsert(w.rows.to(dev))
+    qt = w.queries.to(dev)
+    ms = _timed(lambda: ix.search_dense(qt, 5), 200, stream)
+    report("tiny 1,024 x 384 fp32, 16 queries, top-5", ms, 16, algorithmic_bytes(1024, 384, 16, 5, 4),
+           2.0 * 16 * 1024 * 384, _kernel_ms(lambda: ix.search_dense(qt, 5), 100, stream))
+    ix.close()
+
+    # 32K x 1,024 bf16, batches 1 / 16 / 256 / 1,024, top-5, HBM-cold (16 slab copies rotated)
+    w = synth.dense_32k()
+    rows = w.rows.to(dev)
+    idxs = []
+    for _ in range(COPIES):
+        ix = Index(DIM, N_ROWS, torch.bfloat16)
+        ix.upsert(rows)
+        idxs.append(ix)
+    for b in (1, 16, 256, 1024):
+        q = w.queries[:b].contiguous().to(dev)
+        outs = [(torch.empty((b, K), device=dev), torch.empty((b, K), dtype=torch.int64, device=dev))
+                for _ in range(COPIES)]
+        it = [0]
+
+        def step():
+            c = it[0] % COPIES
+            it[0] += 1
+            idxs[c].search_dense(q, K, out=outs[c])
+        ms = _timed(step, 256, stream)
+        report(f"32,768 x 1,024 bf16, batch {b}, top-5, cold", ms, b, algorithmic_bytes(N_ROWS, DIM, b, K),
+               2.0 * b * N_ROWS * DIM, _kernel_ms(step, 128, stream))
+
+    # hybrid: the same index + 32,768-chunk Zipf corpus; dense 100 + BM25 100 -> RRF(60) -> 5
+    hw = synth.hybrid_32k(dense=w)
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    csr = [t(hw.csr.term_indptr), t(hw.csr.post_chunk), t(hw.csr.post_tf), t(hw.csr.doc_len)]
+    for ix in idxs:
+        ix.attach_sparse(*csr)
+    qd = hw.dense.queries.to(dev)
+    qi, qterms = t(hw.qterm_indptr), t(hw.qterms)
+    nq = qd.shape[0]
+    it = [0]
+
+    def nxt():
+        it[0] += 1
+        return idxs[it[0] % COPIES]
+    postings = int(sum(int(hw.csr.term_indptr[u + 1] - hw.csr.term_indptr[u]) for u in set(hw.qterms.tolist())))
+    sparse_bytes = postings * 8 + 4 * N_ROWS + 4 * hw.csr.term_indptr.size
+    ms_d = _timed(lambda: nxt().search_dense(qd, 100), 64, stream)
+    report("hybrid: dense top-100, batch 256, cold", ms_d, nq, algorithmic_bytes(N_ROWS, DIM, nq, 100),
+           2.0 * nq * N_ROWS * DIM, _kernel_ms(lambda: nxt().search_dense(qd, 100), 64, stream))
+    ms_s = _timed(lambda: nxt().search_sparse(qi, qterms, 100), 64, stream)
+    report("hybrid: BM25 top-100 over CSR postings, batch 256", ms_s, nq, sparse_bytes, 0.0,
+           distinct_postings=postings)
+    dl = nxt().search_dense(qd, 100)[1]
+    sl = nxt().search_sparse(qi, qterms, 100)[1]
+    ms_r = _timed(lambda: rrf_fuse(dl, sl, 60, 5), 256, stream)
+    report("hybrid: RRF(60) of 100 + 100 -> 5, batch 256", ms_r, nq, nq * 200 * 8 + nq * 5 * 12, 0.0)
+    ms_h = _timed(lambda: nxt().search_hybrid(qd, qi, qterms, 100, 100, 60, 5), 64, stream)
+    report("hybrid: full oprag_search_hybrid, batch 256, cold", ms_h, nq,
+           algorithmic_bytes(N_ROWS, DIM, nq, 5) + sparse_bytes, 2.0 * nq * N_ROWS * DIM)
+    for ix in idxs:
+        ix.close()
+    del idxs, rows
+
+    # 1,048,576 x 768 bf16, batch 1,024, top-10 (larger than the Infinity Cache)
+    w4 = synth.mixture_dense(4, 1 << 20, 768, 4096, 1024, 10, "bf16")
+    ix = Index(768, 1 << 20, torch.bfloat16)
+    ix.upsert(w4.rows.to(dev))
+    q4 = w4.queries.to(dev)
+    ms = _timed(lambda: ix.search_dense(q4, 10), 10, stream)
+    report("1,048,576 x 768 bf16, batch 1,024, top-10", ms, 1024, algorithmic_bytes(1 << 20, 768, 1024, 10),
+           2.0 * 1024 * (1 << 20) * 768, _kernel_ms(lambda: ix.search_dense(q4, 10), 10, stream))
+    ix.close()
+    del w4
+
+    # streaming: 8,388,608 x 384 fp16 (+65,536 fp32 rows per upsert), batch 4,096, top-100
+    n0, m, d = 8388608, 65536, 384
+    cen = synth.mixture_centres(synth.rng(5, 0), 8192, d)
+    base = synth.to_storage(synth.mixture_rows_chunked(5, 1, cen, n0, 0.3), "f16")
+    ix = Index(d, n0 + 16 * m, torch.float16)
+    ix.upsert(base.to(dev))
+    del base
+    new = torch.from_numpy(synth.mixture_rows_chunked(5, 10, cen, m, 0.3)).to(dev)
+    ms_u = _timed(lambda: ix.upsert(new), 1, stream)  # two appends (warm-up + one timed)
+    report("streaming: upsert of 65,536 fp32 rows -> fp16 slab", ms_u, m, m * d * (4 + 2), 0.0)
+    cur = ix.slab[torch.from_numpy(np.random.default_rng(0).integers(0, ix.n_rows, 4096)).to(dev)].clone()
+    ms = _timed(lambda: ix.search_dense(cur, 100), 3, stream)
+    n5 = ix.n_rows
+    report(f"streaming: {n5:,} x 384 fp16, batch 4,096, top-100", ms, 4096, algorithmic_bytes(n5, d, 4096, 100),
+           2.0 * 4096 * n5 * d, _kernel_ms(lambda: ix.search_dense(cur, 100), 3, stream))
+    ix.close()
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -201,11 +349,17 @@ def main() -> int:
                     help="a short run for counter collection: one reference copy, then 8 cold searches")
     ap.add_argument("--pmc-summarize", metavar="DIR", help="write the traffic record from two --pmc runs")
     ap.add_argument("--trace-summarize", metavar="DIR", help="write the kernel statistics of a traced run")
+    ap.add_argument("--suite", action="store_true", help="time every workload (one JSON line each)")
     args = ap.parse_args()
     if args.pmc_summarize:
         return pmc_summarize(args.pmc_summarize)
     if args.trace_summarize:
         return trace_summarize(args.trace_summarize)
+    if args.suite:
+        if args.gpus != 1:
+            print("the suite runs on one GPU only", file=sys.stderr)
+            return 2
+        return suite()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: --gpus {args.gpus} is not supported (the multi-GPU sharding "
               f"of the index is a design, not code, in this library)", file=sys.stderr)

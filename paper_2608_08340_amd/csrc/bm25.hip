@@ -26,6 +26,8 @@ using namespace dev;
 
 constexpr int kNT = 512;  // threads per scoring workgroup
 
+// Structural checks of the CSR, one thread per term, then one thread per posting (a posting
+// finds its term by binary search over the offsets, so long lists are checked in parallel).
 __global__ void validate_kernel(int vocab, long long n_docs, long long nnz, const long long* indptr,
                                 const int* chunk, const int* tf, const int* doc_len, unsigned int* flag) {
   const long long tid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
@@ -33,19 +35,20 @@ __global__ void validate_kernel(int vocab, long long n_docs, long long nnz, cons
   if (tid == 0 && (indptr[0] != 0 || indptr[vocab] != nnz)) atomicAdd(flag, 1u);
   for (long long t = tid; t < vocab; t += stride) {
     const long long lo = indptr[t], hi = indptr[t + 1];
-    if (lo < 0 || hi < lo || hi > nnz) {
-      atomicAdd(flag, 1u);
-      continue;
+    if (lo < 0 || hi < lo || hi > nnz) atomicAdd(flag, 1u);
+  }
+  for (long long p = tid; p < nnz; p += stride) {
+    // term of posting p: the last t with indptr[t] <= p
+    int lo = 0, hi = vocab;  // invariant: indptr[lo] <= p < indptr[hi] when the offsets are valid
+    while (hi - lo > 1) {
+      const int mid = lo + (hi - lo) / 2;
+      if (indptr[mid] <= p)
+        lo = mid;
+      else
+        hi = mid;
     }
-    int prev = -1;
-    for (long long p = lo; p < hi; ++p) {
-      const int c = chunk[p];
-      if (c < 0 || c >= n_docs || c <= prev || tf[p] < 1) {
-        atomicAdd(flag, 1u);
-        break;
-      }
-      prev = c;
-    }
+    const int c = chunk[p];
+    if (c < 0 || c >= n_docs || tf[p] < 1 || (p > indptr[lo] && chunk[p - 1] >= c)) atomicAdd(flag, 1u);
   }
   for (long long dd = tid; dd < n_docs; dd += stride)
     if (doc_len[dd] < 0) atomicAdd(flag, 1u);
@@ -293,7 +296,7 @@ hipError_t sparse_validate(int vocab, long long n_docs, long long nnz, const lon
                            const int* tf, const int* doc_len, unsigned int* d_flag, hipStream_t s) {
   hipError_t e = hipMemsetAsync(d_flag, 0, sizeof(unsigned int), s);
   if (e != hipSuccess) return e;
-  const long long work = std::max<long long>(vocab, n_docs);
+  const long long work = std::max<long long>(std::max<long long>(vocab, n_docs), nnz);
   const int blocks = (int)std::min<long long>(1024, (work + 255) / 256);
   hipLaunchKernelGGL(validate_kernel, dim3(std::max(1, blocks)), dim3(256), 0, s, vocab, n_docs, nnz, indptr, chunk,
                      tf, doc_len, d_flag);

@@ -937,22 +937,37 @@ __global__ __launch_bounds__(kThreads) void dense_f32_kernel(DenseArgs a) {
   Sel sel;
   sel.init();
 
+  // Each thread stages two 16-byte row pieces and one query piece per stage; the next
+  // stage's pieces are loaded while the current one is multiplied.
+  const int pc = tid % (KC / 4);                // 16-byte column of the stage
+  const int pr0 = tid / (KC / 4);               // row of piece 0 (rows pr0 and pr0 + 32)
+  const int qrow = min(q0 + pr0, a.nq - 1);
+  float4 xa, xb, qa;
+  auto fetch = [&](long long tile, int kc) __attribute__((always_inline)) {
+    const bool in = kc + pc * 4 < d;
+    const long long r0 = min(tile + pr0, a.n_rows - 1), r1 = min(tile + pr0 + 32, a.n_rows - 1);
+    xa = in ? *reinterpret_cast<const float4*>(X + r0 * d + kc + pc * 4) : make_float4(0.f, 0.f, 0.f, 0.f);
+    xb = in ? *reinterpret_cast<const float4*>(X + r1 * d + kc + pc * 4) : make_float4(0.f, 0.f, 0.f, 0.f);
+    qa = in ? *reinterpret_cast<const float4*>(Q + (long long)qrow * d + kc + pc * 4)
+            : make_float4(0.f, 0.f, 0.f, 0.f);
+  };
+  if (row_begin < row_end) fetch(row_begin, 0);
   for (long long tile0 = row_begin; tile0 < row_end; tile0 += TR) {
     float acc[8];
 #pragma unroll
     for (int r = 0; r < 8; ++r) acc[r] = 0.f;
     for (int kc = 0; kc < d; kc += KC) {
       __syncthreads();
-      for (int i = tid; i < TR * KC; i += kThreads) {
-        const int r = i / KC, c = i % KC;
-        const long long row = min(tile0 + r, a.n_rows - 1);
-        Xs[r * (KC + 1) + c] = (kc + c < d) ? X[row * d + kc + c] : 0.f;
-      }
-      for (int i = tid; i < BN * KC; i += kThreads) {
-        const int r = i / KC, c = i % KC;
-        const int qr = min(q0 + r, a.nq - 1);
-        Qs[r * (KC + 1) + c] = (kc + c < d) ? Q[(long long)qr * d + kc + c] : 0.f;
-      }
+      float* xd0 = Xs + pr0 * (KC + 1) + pc * 4;
+      float* xd1 = Xs + (pr0 + 32) * (KC + 1) + pc * 4;
+      float* qd = Qs + pr0 * (KC + 1) + pc * 4;
+      xd0[0] = xa.x, xd0[1] = xa.y, xd0[2] = xa.z, xd0[3] = xa.w;
+      xd1[0] = xb.x, xd1[1] = xb.y, xd1[2] = xb.z, xd1[3] = xb.w;
+      qd[0] = qa.x, qd[1] = qa.y, qd[2] = qa.z, qd[3] = qa.w;
+      if (kc + KC < d)
+        fetch(tile0, kc + KC);
+      else if (tile0 + TR < row_end)
+        fetch(tile0 + TR, 0);
       __syncthreads();
 #pragma unroll 4
       for (int c = 0; c < KC; ++c) {

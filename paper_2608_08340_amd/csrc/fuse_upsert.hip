@@ -23,64 +23,69 @@ using namespace dev;
 
 constexpr int kMaxCand = 2 * kMaxK;
 
-// One wave per query.
-__global__ __launch_bounds__(64) void rrf_kernel(const long long* dense_ids, int kd, const long long* sparse_ids, int ks,
-                                                 long long nq, int rrf_k, int k, float* out_fused, long long* out_ids) {
+// One workgroup of 256 threads per query: thread t < kd owns dense entry t, thread kd + j owns
+// sparse entry j (kd, ks <= 128).  Both lists are staged in LDS; every candidate's rank is the
+// number of candidates that beat it in the exact rational order (fused desc, id asc), and a
+// thread stops counting once its candidate is out of the first k.
+constexpr int kRrfThreads = 256;
+__global__ __launch_bounds__(kRrfThreads) void rrf_kernel(const long long* dense_ids, int kd,
+                                                          const long long* sparse_ids, int ks, long long nq, int rrf_k,
+                                                          int k, float* out_fused, long long* out_ids) {
+  __shared__ long long dn_ids[kMaxK];
+  __shared__ long long sp_ids[kMaxK];
   __shared__ long long cid[kMaxCand];
   __shared__ long long cnum[kMaxCand];
   __shared__ long long cden[kMaxCand];
-  __shared__ long long sp_ids[kMaxK];
   __shared__ int s_nc;
   const long long q = blockIdx.x;
-  const int lane = threadIdx.x;
-  if (q >= nq) return;
+  const int t = threadIdx.x;
   const long long* D = dense_ids + q * kd;
   const long long* S = sparse_ids + q * ks;
-  for (int j = lane; j < ks; j += 64) sp_ids[j] = S[j];
-  if (lane == 0) s_nc = 0;
+  if (t < kd) dn_ids[t] = D[t];
+  if (t < ks) sp_ids[t] = S[t];
+  if (t == 0) s_nc = 0;
   __syncthreads();
-  // Dense entries (rank = position + 1), with the sparse rank of the same id if present.
-  for (int i = lane; i < kd; i += 64) {
-    const long long id = D[i];
-    if (id < 0) continue;
-    const long long a = (long long)rrf_k + i + 1;
-    long long num = 1, den = a;
-    for (int j = 0; j < ks; ++j) {
-      if (sp_ids[j] == id) {
-        const long long b = (long long)rrf_k + j + 1;
-        num = a + b;
-        den = a * b;
-        break;
+  long long id = -1, num = 0, den = 1;
+  if (t < kd) {  // dense entry: rank t + 1, plus its sparse rank when present
+    id = dn_ids[t];
+    if (id >= 0) {
+      const long long a = (long long)rrf_k + t + 1;
+      num = 1;
+      den = a;
+      for (int j = 0; j < ks; ++j) {
+        if (sp_ids[j] == id) {
+          const long long b = (long long)rrf_k + j + 1;
+          num = a + b;
+          den = a * b;
+          break;
+        }
       }
     }
+  } else if (t - kd < ks) {  // sparse entry absent from the dense list
+    const int j = t - kd;
+    id = sp_ids[j];
+    if (id >= 0) {
+      for (int i = 0; i < kd; ++i)
+        if (dn_ids[i] == id) {
+          id = -1;
+          break;
+        }
+      num = 1;
+      den = (long long)rrf_k + j + 1;
+    }
+  }
+  if (id >= 0) {
     const int slot = atomicAdd(&s_nc, 1);
     cid[slot] = id;
     cnum[slot] = num;
     cden[slot] = den;
   }
-  // Sparse entries absent from the dense list.
-  for (int j = lane; j < ks; j += 64) {
-    const long long id = sp_ids[j];
-    if (id < 0) continue;
-    bool in_dense = false;
-    for (int i = 0; i < kd; ++i)
-      if (D[i] == id) {
-        in_dense = true;
-        break;
-      }
-    if (in_dense) continue;
-    const int slot = atomicAdd(&s_nc, 1);
-    cid[slot] = id;
-    cnum[slot] = 1;
-    cden[slot] = (long long)rrf_k + j + 1;
-  }
   __syncthreads();
   const int nc = s_nc;
-  // Rank of every candidate = number of candidates that beat it (exact fraction compare).
-  for (int c = lane; c < nc; c += 64) {
-    const long long n0 = cnum[c], d0 = cden[c], id0 = cid[c];
+  if (t < nc) {
+    const long long n0 = cnum[t], d0 = cden[t], id0 = cid[t];
     int rank = 0;
-    for (int o = 0; o < nc; ++o) {
+    for (int o = 0; o < nc && rank < k; ++o) {
       const long long lhs = cnum[o] * d0, rhs = n0 * cden[o];
       rank += (lhs > rhs || (lhs == rhs && cid[o] < id0)) ? 1 : 0;
     }
@@ -89,7 +94,7 @@ __global__ __launch_bounds__(64) void rrf_kernel(const long long* dense_ids, int
       out_fused[q * k + rank] = (float)((double)n0 / (double)d0);
     }
   }
-  for (int r = nc + lane; r < k; r += 64) {
+  for (int r = nc + t; r < k; r += kRrfThreads) {
     out_ids[q * k + r] = -1;
     out_fused[q * k + r] = -__builtin_inff();
   }
@@ -137,8 +142,8 @@ __global__ void convert8_kernel(const float4* __restrict__ src, uint4* __restric
 
 hipError_t launch_rrf(const long long* dense_ids, int k_dense, const long long* sparse_ids, int k_sparse, long long nq,
                       int rrf_k, int k, float* out_fused, long long* out_ids, hipStream_t s) {
-  hipLaunchKernelGGL(rrf_kernel, dim3((unsigned)nq), dim3(64), 0, s, dense_ids, k_dense, sparse_ids, k_sparse, nq, rrf_k,
-                     k, out_fused, out_ids);
+  hipLaunchKernelGGL(rrf_kernel, dim3((unsigned)nq), dim3(kRrfThreads), 0, s, dense_ids, k_dense, sparse_ids, k_sparse,
+                     nq, rrf_k, k, out_fused, out_ids);
   return hipGetLastError();
 }
 

@@ -1,5 +1,7 @@
 """Append-only upsert on the GPU: stored bytes, capacity handling, visibility to later searches
 on the same stream, and streaming rounds of upsert + exact top-100 search."""
+import os
+
 import numpy as np
 import pytest
 import torch
@@ -86,6 +88,19 @@ def test_new_rows_visible_to_search_on_the_same_stream():
     assert (ids[:, 0].cpu().numpy() == np.arange(5000, 6000, 50)).all()
 
 
+def _full_scores(bits, n, Q, step=1 << 18):
+    """fp64 oracle scores of every stored fp16 row [0, n) against Q, one block per task."""
+    import concurrent.futures as cf
+    S = np.empty((Q.shape[0], n))
+
+    def block(lo):
+        S[:, lo:min(n, lo + step)] = od.scores(decode(bits[lo:min(n, lo + step)], "f16"), Q)
+
+    with cf.ThreadPoolExecutor(min(16, os.cpu_count() or 1)) as ex:
+        list(ex.map(block, range(0, n, step)))
+    return S
+
+
 def _streaming(n0, rounds, m, d, clusters, nq, k, sample, workload=5):
     """Start from n0 fp16 rows, then per round append m rows (the same generator) and search
     nq fresh queries drawn from the current rows, exact top-k."""
@@ -128,12 +143,9 @@ def _streaming(n0, rounds, m, d, clusters, nq, k, sample, workload=5):
         for qq in range(nq):
             rep = accept.certificate(s_ret[qq], ids[qq], sc[qq], err[qq])
             assert rep.ok, (r, qq, rep.problems)
-        # sampled queries: full oracle
+        # sampled queries: full oracle (row blocks scored on a thread pool)
         samp = np.random.default_rng(100 + r).choice(nq, sample, replace=False)
-        S = np.zeros((sample, n))
-        step = 1 << 20
-        for lo in range(0, n, step):
-            S[:, lo:lo + step] = od.scores(decode(bits[lo:min(n, lo + step)], "f16"), Q[samp])
+        S = _full_scores(bits, n, Q[samp])
         reps = accept.check_batch(S, ids[samp], sc[samp], k, rtol=2e-3)
         assert all(rp.ok for rp in reps), (r, [rp.problems for rp in reps if not rp.ok][:2])
         log(f"round {r}: n_rows {n} ok")
