@@ -405,6 +405,115 @@ struct SelOf<BN, KS, 1> {
 };
 
 // ------------------------------------------------------------------------------------
+// Filtered mode (k > 16).  Every row whose score reaches the query's threshold becomes a
+// candidate key in the query's global buffer; an exact selection over the buffer follows in
+// select_topk_kernel.  Candidates of a query are staged in LDS (SCAP keys) and written out
+// with one device-scope reservation per flush; a tile with more candidates than the stage
+// reserves global space for itself.  LDS: stage [BN][SCAP] | staged [BN] | tile count [BN] |
+// tile base [BN] (long long).
+// ------------------------------------------------------------------------------------
+template <int BN>
+struct SelFilter {
+  static constexpr int SCAP = 16;
+  static constexpr int kBytes = BN * SCAP * 8 + BN * 8 + BN * 8;
+  __device__ __forceinline__ void init() {}
+  __device__ __forceinline__ void pass(const float*, int, int, const PassRows&, int, int, unsigned char*) {}
+  __device__ __forceinline__ void write(const DenseArgs&, int, long long) const {}
+};
+template <int BN, int KS>
+struct SelOf<BN, KS, 2> {
+  typedef SelFilter<BN> type;
+};
+
+// Owner thread of query slot n: append its staged keys to the global buffer.
+template <int BN>
+__device__ __forceinline__ void filt_flush(int n, int q, unsigned char* area, const DenseArgs& a) {
+  constexpr int SCAP = SelFilter<BN>::SCAP;
+  u64* stage = reinterpret_cast<u64*>(area);
+  int* staged = reinterpret_cast<int*>(area + BN * SCAP * 8);
+  const int c = staged[n];
+  if (c == 0) return;
+  const long long g = atomicAdd(a.ccnt + q, c);
+  u64* dst = a.cbuf + (long long)q * a.cap;
+  for (int j = 0; j < c; ++j)
+    if (g + j < a.cap) dst[g + j] = stage[n * SCAP + j];
+  staged[n] = 0;
+}
+
+// acc[mi][ni][r] = score of row tile0 + 16*MW*wave + 16*mi + 4*(lane/16) + r against query
+// slot 16*ni + lane%16; th[ni] its threshold (+inf for slots past the batch).
+template <int BN, int MW>
+__device__ __forceinline__ void filt_tile(const f32x4 (&acc)[MW][BN / 16], const float (&th)[BN / 16],
+                                          unsigned char* area, long long tile0, long long row_end, int q0,
+                                          const DenseArgs& a) {
+  constexpr int NW = BN / 16;
+  constexpr int SCAP = SelFilter<BN>::SCAP;
+  constexpr int TR = kWaves * MW * 16;
+  u64* stage = reinterpret_cast<u64*>(area);
+  int* staged = reinterpret_cast<int*>(area + BN * SCAP * 8);
+  int* tcnt = staged + BN;
+  long long* tbase = reinterpret_cast<long long*>(area + BN * SCAP * 8 + BN * 8);
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int row0 = w * MW * 16 + (lane >> 4) * 4;
+  const int lim = (int)min((long long)TR, row_end - tile0) - row0;
+  // 1. count this lane's candidates per query and reserve their place in the tile's list
+  int c[NW], off[NW];
+#pragma unroll
+  for (int ni = 0; ni < NW; ++ni) {
+    int cc = 0;
+#pragma unroll
+    for (int mi = 0; mi < MW; ++mi)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) cc += (mi * 16 + r < lim && acc[mi][ni][r] >= th[ni]) ? 1 : 0;
+    c[ni] = cc;
+  }
+#pragma unroll
+  for (int ni = 0; ni < NW; ++ni) off[ni] = c[ni] ? atomicAdd(&tcnt[ni * 16 + (lane & 15)], c[ni]) : 0;
+  lds_barrier();
+  // 2. owners: make room in the stage, or send a large tile list straight to global memory
+  if (tid < BN) {
+    const int tc = tcnt[tid];
+    tbase[tid] = -1;
+    if (tc > 0) {
+      if (staged[tid] + tc > SCAP) filt_flush<BN>(tid, q0 + tid, area, a);
+      if (tc > SCAP) tbase[tid] = atomicAdd(a.ccnt + q0 + tid, tc);
+    }
+  }
+  lds_barrier();
+  // 3. write
+#pragma unroll
+  for (int ni = 0; ni < NW; ++ni) {
+    if (c[ni] == 0) continue;
+    const int n = ni * 16 + (lane & 15);
+    const long long gb = tbase[n];
+    int j = off[ni];
+    u64* dst_g = a.cbuf + (long long)(q0 + n) * a.cap;
+    u64* dst_s = stage + n * SCAP + staged[n];
+#pragma unroll
+    for (int mi = 0; mi < MW; ++mi)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float x = acc[mi][ni][r];
+        if (mi * 16 + r < lim && x >= th[ni]) {
+          const u64 key = composite(x, (uint32_t)(tile0 + row0 + mi * 16 + r));
+          if (gb >= 0) {
+            if (gb + j < a.cap) dst_g[gb + j] = key;
+          } else {
+            dst_s[j] = key;
+          }
+          ++j;
+        }
+      }
+  }
+  lds_barrier();
+  // 4. owners: the tile's list now belongs to the stage (unless it went out directly)
+  if (tid < BN) {
+    if (tbase[tid] < 0) staged[tid] += tcnt[tid];
+    tcnt[tid] = 0;
+  }
+}
+
+// ------------------------------------------------------------------------------------
 // Selection straight from the MFMA accumulators (k <= 16).  acc[mi][ni][r] is the score of
 // row tile0 + 16*MW*wave + 16*mi + 4*(lane/16) + r against query 16*ni + lane%16 of the
 // block.  Each lane's MW*4 values of a query form one group; the M best values of every
@@ -713,12 +822,12 @@ __global__ __launch_bounds__(kThreads) void dense_mfma_kernel(DenseArgs a) {
   using Sel = typename SelOf<BN, KS, SEL>::type;
   constexpr int QBYTES = 2 * QSLOT;
   constexpr bool kBlk = SEL == 0 && KS == 5;
-  constexpr int SB0 = BN * SR * 4;
+  constexpr int SB0 = SEL == 2 ? 0 : BN * SR * 4;
   constexpr int SBYTES = kBlk && BlockArea<MW, BN>::kBytes > SB0 ? BlockArea<MW, BN>::kBytes : SB0;
   constexpr int SMEM = QBYTES + SBYTES + Sel::kBytes;
   static_assert(MW % G == 0 && ((MWP * 16) & (MWP * 16 - 1)) == 0, "pass shape");
-  static_assert(SEL == 1 || RP % (4 * (kThreads / BN)) == 0, "slice shape");
-  static_assert(SEL == 1 || kWaves * 4 * (KS <= 5 ? 1 : (KS <= 8 ? 2 : 4)) * BN * 4 <= SBYTES,
+  static_assert(SEL != 0 || RP % (4 * (kThreads / BN)) == 0, "slice shape");
+  static_assert(SEL != 0 || kWaves * 4 * (KS <= 5 ? 1 : (KS <= 8 ? 2 : 4)) * BN * 4 <= SBYTES,
                 "group values of the register epilogue fit in the score tile");
   __shared__ __attribute__((aligned(16))) unsigned char smem[SMEM];
   unsigned char* qslots = smem;
@@ -743,6 +852,20 @@ __global__ __launch_bounds__(kThreads) void dense_mfma_kernel(DenseArgs a) {
 
   Sel sel;
   sel.init();
+  if constexpr (SEL == 2) {
+    if (tid < BN) {
+      int* staged = reinterpret_cast<int*>(scratch + BN * SelFilter<BN>::SCAP * 8);
+      staged[tid] = 0;
+      staged[BN + tid] = 0;
+    }
+    // no barrier needed here: the first tile's epilogue follows several barriers
+  }
+  float th[NW];  // filtered mode: thresholds of this lane's query slots
+#pragma unroll
+  for (int ni = 0; ni < NW; ++ni) {
+    const int q = q0 + ni * 16 + (lane & 15);
+    th[ni] = q >= a.nq ? __builtin_inff() : (a.th ? a.th[(long long)q * a.th_stride] : kNegInf);
+  }
   if (n_st > 0) {
     // Query piece p = tid + 256 j: row r = p / 16, 16-byte column c = p % 16 of the
     // super-step, stored at column c ^ (r % 16) of the row.  Any 16 consecutive lanes then
@@ -863,7 +986,10 @@ __global__ __launch_bounds__(kThreads) void dense_mfma_kernel(DenseArgs a) {
       // ---- selection for the tile: registers first, else G passes through LDS
       const long long tile0 = row_begin + (long long)t * TR;
       bool done = false;
-      if constexpr (kBlk)
+      if constexpr (SEL == 2) {
+        filt_tile<BN, MW>(acc, th, scratch, tile0, row_end, q0, a);
+        done = true;
+      } else if constexpr (kBlk)
         done = blk_epilogue<BN, MW>(acc, sel, reinterpret_cast<unsigned char*>(S), scratch, tile0, row_end, q_lim,
                                     a.k);
       else if constexpr (SEL == 0)
@@ -902,7 +1028,11 @@ __global__ __launch_bounds__(kThreads) void dense_mfma_kernel(DenseArgs a) {
 #undef OPRAG_QUERIES
 #undef OPRAG_ROWS
   }
-  sel.write(a, q0, chunk);
+  if constexpr (SEL == 2) {
+    if (tid < q_lim) filt_flush<BN>(tid, q0 + tid, scratch, a);
+  } else {
+    sel.write(a, q0, chunk);
+  }
 }
 
 // ------------------------------------------------------------------------------------
@@ -991,6 +1121,98 @@ __global__ __launch_bounds__(kThreads) void dense_f32_kernel(DenseArgs a) {
     __syncthreads();
   }
   sel.write(a, q0, chunk);
+}
+
+// ------------------------------------------------------------------------------------
+// Filtered mode, selection: exact top-k (sorted) of a query's candidate keys.  One workgroup
+// per query finds the k-th largest 64-bit key by most-significant-digit radix selection
+// (8-bit digits; it stops as soon as a whole bucket is needed), gathers the keys at or above
+// it, and ranks them.  Keys are distinct (row ids are), so exactly min(k, n) keys qualify.
+// ------------------------------------------------------------------------------------
+__global__ __launch_bounds__(kThreads) void select_topk_kernel(const unsigned long long* __restrict__ cbuf,
+                                                               const int* __restrict__ ccnt, long long cap, int k,
+                                                               float* out_scores, long long* out_ids, int* overflow) {
+  __shared__ unsigned int hist[256];
+  __shared__ int wtot[kWaves];
+  __shared__ u64 sel[kMaxK];
+  __shared__ u64 s_prefix, s_mask;
+  __shared__ int s_need, s_done, s_ns;
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int q = blockIdx.x;
+  const int cnt = ccnt[q];
+  if (t == 0 && cnt > cap) atomicAdd(overflow, 1);
+  const int n = (int)min((long long)cnt, cap);
+  const u64* src = cbuf + (long long)q * cap;
+  if (t == 0) {
+    s_prefix = 0ull;
+    s_mask = 0ull;
+    s_need = min(k, n);
+    s_done = s_need == 0;
+    s_ns = 0;
+  }
+  __syncthreads();
+  for (int shift = 56; shift >= 0; shift -= 8) {
+    if (s_done) break;  // block-uniform
+    const u64 prefix = s_prefix, mask = s_mask;
+    const int need = s_need;
+    hist[t] = 0u;
+    __syncthreads();
+    for (int i = t; i < n; i += kThreads) {
+      const u64 key = src[i];
+      if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
+    }
+    __syncthreads();
+    // thread t holds digit 255 - t; an inclusive scan over t counts the keys whose digit
+    // is >= 255 - t within the prefix bucket
+    const int hd = (int)hist[255 - t];
+    int x = hd;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int y = __shfl_up(x, o, 64);
+      if (lane >= o) x += y;
+    }
+    if (lane == 63) wtot[w] = x;
+    __syncthreads();
+    int before = 0;
+    for (int i = 0; i < w; ++i) before += wtot[i];
+    const int incl = before + x;        // keys with digit >= 255 - t
+    const int above = incl - hd;        // keys with digit > 255 - t
+    if (above < need && incl >= need) {  // exactly one thread: the digit of the k-th key
+      const int dgt = 255 - t;
+      s_prefix = prefix | ((u64)dgt << shift);
+      s_mask = mask | (255ull << shift);
+      s_need = need - above;
+      s_done = (hd == need - above) ? 1 : 0;  // the whole bucket is needed: stop here
+    }
+    __syncthreads();
+  }
+  const u64 prefix = s_prefix, mask = s_mask;
+  for (int i = t; i < n; i += kThreads) {
+    const u64 key = src[i];
+    if ((key & mask) >= prefix) {
+      const int slot = atomicAdd(&s_ns, 1);
+      if (slot < kMaxK) sel[slot] = key;
+    }
+  }
+  __syncthreads();
+  const int ns = min(s_ns, k);  // == min(k, n)
+  if (t < ns) {
+    const u64 key = sel[t];
+    int rank = 0;
+    for (int j = 0; j < ns; ++j) rank += sel[j] > key ? 1 : 0;
+    out_ids[(long long)q * k + rank] = (long long)comp_row(key);
+    out_scores[(long long)q * k + rank] = comp_score(key);
+  }
+  for (int r = ns + t; r < k; r += kThreads) {
+    out_ids[(long long)q * k + r] = -1ll;
+    out_scores[(long long)q * k + r] = kNegInf;
+  }
+}
+
+// Clears the filtered-mode counters (a kernel, not a memset: safe inside captured graphs).
+__global__ void clear_ints_kernel(int* p, long long n) {
+  for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (long long)gridDim.x * blockDim.x)
+    p[i] = 0;
 }
 
 // ------------------------------------------------------------------------------------
@@ -1175,7 +1397,10 @@ struct KernelInfo {
   MF_KS(DT, 1, 1, 16, 1, 4, 1, 16), MF_KS(DT, 1, 1, 4, 1, 4, 1, 16), MF_KS(DT, 4, 2, 8, 1, 2, 17, 64), \
       MF_KS(DT, 4, 2, 4, 1, 2, 17, 64), MFK(DT, 8, 4, 4, 2, 5, 0, 1, 65, 1 << 30),                \
       MFK(DT, 8, 4, 4, 4, 8, 0, 1, 65, 1 << 30), MFK(DT, 8, 4, 4, 4, 16, 0, 1, 65, 1 << 30),         \
-      MFK(DT, 2, 4, 8, 1, 8, 1, 2, 1, 1 << 30), MFK(DT, 2, 4, 4, 1, 8, 1, 2, 1, 1 << 30)
+      MFK(DT, 2, 4, 8, 1, 8, 1, 2, 1, 1 << 30), MFK(DT, 2, 4, 4, 1, 8, 1, 2, 1, 1 << 30),            \
+      MFK(DT, 1, 1, 16, 1, 5, 2, 4, 1, 16), MFK(DT, 1, 1, 4, 1, 5, 2, 4, 1, 16),                     \
+      MFK(DT, 4, 2, 8, 1, 5, 2, 2, 17, 64), MFK(DT, 4, 2, 4, 1, 5, 2, 2, 17, 64),                    \
+      MFK(DT, 8, 4, 4, 1, 5, 2, 1, 65, 1 << 30)
 
 const KernelInfo kKernels[] = {
     {dense_f32_kernel<5, 0>, kDtypeF32, 32, 64, 5, 0, 2, 1, 1 << 30, 0},
@@ -1187,8 +1412,7 @@ const KernelInfo kKernels[] = {
 };
 constexpr int kNumKernels = sizeof(kKernels) / sizeof(kKernels[0]);
 
-int pick_kernel(int dtype, int d, int nq, int k) {
-  const int sel = k <= 16 ? 0 : 1;
+int pick_kernel(int dtype, int d, int nq, int k, int sel) {
   const int ks = k <= 5 ? 5 : (k <= 8 ? 8 : 16);
   for (int i = 0; i < kNumKernels; ++i) {
     const KernelInfo& ki = kKernels[i];
@@ -1201,58 +1425,159 @@ int pick_kernel(int dtype, int d, int nq, int k) {
   return -1;
 }
 
+constexpr int kNumCUs = 256;
+constexpr long long kFilterFirst = 4096;  // rows of the first filtered level
+constexpr long long kFilterGrow = 64;     // row growth from one level to the next
+
+// Workgroups per query block that fill the chip twice over (at least enough to keep every
+// chunk of a ring kernel under 2^30 bytes of rows, the reach of its 32-bit offsets).
+long long chunk_bound(const KernelInfo& ki, int d, long long n_rows, int n_qblocks, long long* min_chunks) {
+  const long long target = (long long)kNumCUs * ki.wgs_per_cu * 2;
+  long long bound = std::max(1ll, (target + n_qblocks - 1) / n_qblocks);
+  long long mc = 1;
+  if (ki.ring) {
+    const long long n_tiles = (n_rows + ki.tile_rows - 1) / ki.tile_rows;
+    const long long max_tiles = std::max(1ll, (1ll << 30) / ((long long)ki.tile_rows * d * 2));
+    mc = std::max(1ll, (n_tiles + max_tiles - 1) / max_tiles);
+    bound = std::max(bound, mc);
+  }
+  if (min_chunks) *min_chunks = mc;
+  return bound;
+}
+
+// Splits n_rows into chunks (whole tiles) for one launch.
+void split_rows(DensePlan& p, long long n_rows, long long chunks, long long min_chunks) {
+  const long long n_tiles = (n_rows + p.tile_rows - 1) / p.tile_rows;
+  chunks = std::max(min_chunks, std::max(1ll, std::min(chunks, n_tiles)));
+  const long long tiles_per_chunk = n_tiles ? (n_tiles + chunks - 1) / chunks : 1;
+  p.rows_per_chunk = tiles_per_chunk * p.tile_rows;
+  p.n_chunks = (int)std::max(1ll, n_tiles ? (n_tiles + tiles_per_chunk - 1) / tiles_per_chunk : 1);
+  p.grid = (long long)p.n_chunks * p.n_qblocks;
+}
+
+size_t align_up256(size_t x) { return (x + 255) & ~(size_t)255; }
+
 }  // namespace
 
-constexpr int kNumCUs = 256;
-
-DensePlan plan_dense(int dtype, int d, long long n_rows, int nq, int k) {
+DensePlan plan_dense_lists(int dtype, int d, long long n_rows, int nq, int k) {
   DensePlan p;
-  p.kernel = pick_kernel(dtype, d, nq, k);
+  p.kernel = pick_kernel(dtype, d, nq, k, k <= 16 ? 0 : 1);
   if (p.kernel < 0) return p;
   const KernelInfo& ki = kKernels[p.kernel];
   p.bn = ki.bn;
   p.tile_rows = ki.tile_rows;
   p.n_qblocks = (nq + p.bn - 1) / p.bn;
-  const long long n_tiles = (n_rows + p.tile_rows - 1) / p.tile_rows;
-  // Enough workgroups to fill the chip twice over, never more chunks than tiles; the large-k
-  // selector wants several tiles per chunk so its queues amortise.
-  const long long target = (long long)kNumCUs * ki.wgs_per_cu * 2;
-  long long bound = std::max(1ll, (target + p.n_qblocks - 1) / p.n_qblocks);
-  // MFMA kernels address a chunk with 32-bit byte offsets: keep chunks under 2^30 bytes.
-  // The minimum grows with the row count, so a workspace planned for the capacity suffices.
   long long min_chunks = 1;
-  if (ki.ring) {
-    const long long max_tiles = std::max(1ll, (1ll << 30) / ((long long)p.tile_rows * d * 2));
-    min_chunks = std::max(1ll, (n_tiles + max_tiles - 1) / max_tiles);
-    bound = std::max(bound, min_chunks);
-  }
+  const long long bound = chunk_bound(ki, d, n_rows, p.n_qblocks, &min_chunks);
+  const long long n_tiles = (n_rows + p.tile_rows - 1) / p.tile_rows;
   long long chunks = bound;
+  // the queue-based large-k selector wants several tiles per chunk so its queues amortise
   if (ki.sel == 1) chunks = std::min(chunks, std::max(1ll, n_tiles / 4));
-  chunks = std::max(min_chunks, std::max(1ll, std::min(chunks, n_tiles)));
-  const long long tiles_per_chunk = n_tiles ? (n_tiles + chunks - 1) / chunks : 1;
-  p.rows_per_chunk = tiles_per_chunk * p.tile_rows;
-  p.n_chunks = (int)std::max(1ll, n_tiles ? (n_tiles + tiles_per_chunk - 1) / tiles_per_chunk : 1);
+  split_rows(p, n_rows, chunks, min_chunks);
   p.cap = bound * k;  // partial slots per query for any row count (n_chunks <= bound)
-  p.grid = (long long)p.n_chunks * p.n_qblocks;
+  return p;
+}
+
+DensePlan plan_dense(int dtype, int d, long long n_rows, int nq, int k) {
+  if (dtype == kDtypeF32 || k <= 16) return plan_dense_lists(dtype, d, n_rows, nq, k);
+  DensePlan p;
+  p.kernel = pick_kernel(dtype, d, nq, k, 2);
+  if (p.kernel < 0) return plan_dense_lists(dtype, d, n_rows, nq, k);
+  const KernelInfo& ki = kKernels[p.kernel];
+  p.filtered = true;
+  p.bn = ki.bn;
+  p.tile_rows = ki.tile_rows;
+  p.n_qblocks = (nq + p.bn - 1) / p.bn;
+  // Levels: the first kFilterFirst rows with every score a candidate, then prefixes growing
+  // kFilterGrow-fold, each filtered by the previous level's k-th score, then all rows.  A
+  // level then expects about k * kFilterGrow candidates per query; fcap allows four times that.
+  long long r = std::min(n_rows, kFilterFirst);
+  p.n_levels = 0;
+  p.level_rows[p.n_levels++] = r;
+  while (r < n_rows && p.n_levels < 8) {
+    r = (r * kFilterGrow >= n_rows || p.n_levels == 7) ? n_rows : r * kFilterGrow;
+    p.level_rows[p.n_levels++] = r;
+  }
+  p.fcap = std::max(1ll, std::min(n_rows, std::max(kFilterFirst, 4 * kFilterGrow * (long long)k)));
+  p.chunk_bound = chunk_bound(ki, d, n_rows, p.n_qblocks, nullptr);
+  split_rows(p, n_rows, p.chunk_bound, 1);
+  // the per-chunk-list plan is the exact fallback; the workspace covers it as well
+  p.cap = plan_dense_lists(dtype, d, n_rows, nq, k).cap;
   return p;
 }
 
 size_t dense_workspace_bytes(const DensePlan& p, int nq) {
-  return (size_t)nq * (size_t)p.cap * sizeof(unsigned long long);
+  const size_t lists = (size_t)nq * (size_t)p.cap * sizeof(unsigned long long);
+  if (!p.filtered) return lists;
+  const size_t filt = align_up256((size_t)nq * (size_t)p.fcap * 8) + align_up256((size_t)nq * 4) + 256;
+  return std::max(lists, filt);
 }
+
+int* dense_overflow_counter(const DensePlan& p, void* ws, int nq) {
+  return reinterpret_cast<int*>(static_cast<unsigned char*>(ws) + align_up256((size_t)nq * (size_t)p.fcap * 8) +
+                                align_up256((size_t)nq * 4));
+}
+
+namespace {
+
+hipError_t launch_kernel(const KernelInfo& ki, long long grid, DenseArgs& arg, hipStream_t s, hipEvent_t ev0,
+                         hipEvent_t ev1) {
+  void* params[] = {&arg};
+  // With timing events the launch carries them in its dispatch packet: they are stamped when
+  // the kernel itself starts and ends.
+  return ev0 ? hipExtLaunchKernel(reinterpret_cast<const void*>(ki.fn), dim3((unsigned)grid), dim3(kThreads), params,
+                                  0, s, ev0, ev1, 0)
+             : hipLaunchKernel(reinterpret_cast<const void*>(ki.fn), dim3((unsigned)grid), dim3(kThreads), params, 0,
+                               s);
+}
+
+// One filtered level: clear the counts, collect candidates, select.
+hipError_t filter_level(const DensePlan& p, const DenseArgs& a, int level, hipStream_t s, hipEvent_t ev0,
+                        hipEvent_t ev1) {
+  const KernelInfo& ki = kKernels[p.kernel];
+  unsigned long long* cbuf = a.partial;  // the workspace
+  int* ccnt = reinterpret_cast<int*>(reinterpret_cast<unsigned char*>(cbuf) +
+                                     align_up256((size_t)a.nq * (size_t)p.fcap * 8));
+  int* ovf = ccnt + align_up256((size_t)a.nq * 4) / 4;  // [0]: last level, [1]: earlier levels
+  const bool last = level == p.n_levels - 1;
+  hipLaunchKernelGGL(clear_ints_kernel, dim3((unsigned)std::min<long long>(1024, (a.nq + 255) / 256)), dim3(256), 0,
+                     s, ccnt, (long long)a.nq);
+  DensePlan lp = p;
+  split_rows(lp, p.level_rows[level], p.chunk_bound, 1);
+  DenseArgs arg = a;
+  arg.n_rows = p.level_rows[level];
+  arg.n_chunks = lp.n_chunks;
+  arg.rows_per_chunk = lp.rows_per_chunk;
+  arg.th = level == 0 ? nullptr : a.out_scores + (a.k - 1);
+  arg.th_stride = a.k;
+  arg.cbuf = cbuf;
+  arg.ccnt = ccnt;
+  arg.cap = p.fcap;
+  hipError_t e = launch_kernel(ki, lp.grid, arg, s, ev0, ev1);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(select_topk_kernel, dim3((unsigned)a.nq), dim3(kThreads), 0, s, cbuf, ccnt, p.fcap, a.k,
+                     a.out_scores, a.out_ids, ovf + (last ? 0 : 1));
+  return hipGetLastError();
+}
+
+}  // namespace
 
 hipError_t launch_dense(const DensePlan& p, int dtype, const DenseArgs& a, hipStream_t s, hipEvent_t ev0,
                         hipEvent_t ev1) {
   (void)dtype;
   const KernelInfo& ki = kKernels[p.kernel];
+  if (p.filtered) {
+    int* ovf = dense_overflow_counter(p, a.partial, a.nq);
+    hipLaunchKernelGGL(clear_ints_kernel, dim3(1), dim3(64), 0, s, ovf, 2ll);
+    for (int l = 0; l < p.n_levels; ++l) {
+      const bool last = l == p.n_levels - 1;
+      hipError_t e = filter_level(p, a, l, s, last ? ev0 : nullptr, last ? ev1 : nullptr);
+      if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+  }
   DenseArgs arg = a;
-  void* params[] = {&arg};
-  // With timing events the launch carries them in its dispatch packet: they are stamped when
-  // the kernel itself starts and ends.
-  hipError_t e = ev0 ? hipExtLaunchKernel(reinterpret_cast<const void*>(ki.fn), dim3((unsigned)p.grid), dim3(kThreads),
-                                          params, 0, s, ev0, ev1, 0)
-                     : hipLaunchKernel(reinterpret_cast<const void*>(ki.fn), dim3((unsigned)p.grid), dim3(kThreads),
-                                       params, 0, s);
+  hipError_t e = launch_kernel(ki, p.grid, arg, s, ev0, ev1);
   if (e != hipSuccess || p.n_chunks == 1) return e;
   if (ki.sel == 0) {
     const unsigned blocks = (unsigned)a.nq;
@@ -1269,6 +1594,36 @@ hipError_t launch_dense(const DensePlan& p, int dtype, const DenseArgs& a, hipSt
     hipLaunchKernelGGL(merge_large_kernel, dim3((unsigned)((a.nq + kWaves - 1) / kWaves)), dim3(kThreads), 0, s,
                        a.partial, p.n_chunks, a.nq, a.k, a.out_scores, a.out_ids);
   }
+  return hipGetLastError();
+}
+
+hipError_t relaunch_dense_last_level(const DensePlan& p, int dtype, const DenseArgs& a, hipStream_t s) {
+  (void)dtype;
+  if (!p.filtered) return hipSuccess;
+  int* ovf = dense_overflow_counter(p, a.partial, a.nq);
+  hipLaunchKernelGGL(clear_ints_kernel, dim3(1), dim3(64), 0, s, ovf, 2ll);
+  // The current lists are the top-k of a subset of the rows at or above the last threshold:
+  // their k-th scores are valid thresholds again, and no lower than the last ones.
+  DenseArgs arg = a;
+  const KernelInfo& ki = kKernels[p.kernel];
+  unsigned long long* cbuf = a.partial;
+  int* ccnt = reinterpret_cast<int*>(reinterpret_cast<unsigned char*>(cbuf) +
+                                     align_up256((size_t)a.nq * (size_t)p.fcap * 8));
+  hipLaunchKernelGGL(clear_ints_kernel, dim3((unsigned)std::min<long long>(1024, (a.nq + 255) / 256)), dim3(256), 0,
+                     s, ccnt, (long long)a.nq);
+  DensePlan lp = p;
+  split_rows(lp, a.n_rows, p.chunk_bound, 1);
+  arg.n_chunks = lp.n_chunks;
+  arg.rows_per_chunk = lp.rows_per_chunk;
+  arg.th = a.out_scores + (a.k - 1);
+  arg.th_stride = a.k;
+  arg.cbuf = cbuf;
+  arg.ccnt = ccnt;
+  arg.cap = p.fcap;
+  hipError_t e = launch_kernel(ki, lp.grid, arg, s, nullptr, nullptr);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(select_topk_kernel, dim3((unsigned)a.nq), dim3(kThreads), 0, s, cbuf, ccnt, p.fcap, a.k,
+                     a.out_scores, a.out_ids, ovf);
   return hipGetLastError();
 }
 

@@ -26,6 +26,13 @@ struct DenseArgs {
   unsigned long long* partial;  // [nq x n_chunks x k] per-chunk lists (when n_chunks > 1)
   float* out_scores;            // [nq x k]
   long long* out_ids;           // [nq x k]
+  // Filtered mode (k > 16): every row scoring >= th[q * th_stride] (all rows when th is null)
+  // becomes a candidate key in cbuf[q][0 .. cap); ccnt[q] counts them (and may exceed cap).
+  const float* th = nullptr;
+  int th_stride = 0;
+  unsigned long long* cbuf = nullptr;
+  int* ccnt = nullptr;
+  long long cap = 0;
 };
 
 struct DensePlan {
@@ -38,13 +45,29 @@ struct DensePlan {
   long long cap = 0;            // partial-list slots per query (bounds n_chunks * k)
   long long grid = 0;
   size_t lds_bytes = 0;
+  // Filtered mode: candidate passes over growing row prefixes, each one's k-th score the next
+  // one's threshold; the last level is all rows.
+  bool filtered = false;
+  int n_levels = 0;
+  long long level_rows[8] = {};
+  long long fcap = 0;           // candidate slots per query
+  long long chunk_bound = 0;    // workgroups per query block the filter passes aim for
 };
 
 DensePlan plan_dense(int dtype, int d, long long n_rows, int nq, int k);
+// The per-chunk-list plan for any k (the exact fallback of the filtered mode).
+DensePlan plan_dense_lists(int dtype, int d, long long n_rows, int nq, int k);
 size_t dense_workspace_bytes(const DensePlan& p, int nq);
-// ev0 / ev1 (optional) are recorded on s right before and after the scoring kernel.
+// ev0 / ev1 (optional) are recorded on s right before and after the scoring kernel (the first
+// one, in filtered mode).
 hipError_t launch_dense(const DensePlan& p, int dtype, const DenseArgs& a, hipStream_t s, hipEvent_t ev0 = nullptr,
                         hipEvent_t ev1 = nullptr);
+// Filtered mode: device address of the overflow counter inside the workspace (> 0 after a
+// launch when some query found more candidates than fcap).
+int* dense_overflow_counter(const DensePlan& p, void* ws, int nq);
+// Filtered mode: repeats the last level with the current k-th scores as thresholds.
+hipError_t relaunch_dense_last_level(const DensePlan& p, int dtype, const DenseArgs& a, hipStream_t s);
+
 
 // ---------------------------------------------------------------- sparse (BM25)
 struct SparseIndex {
