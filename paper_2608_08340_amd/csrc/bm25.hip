@@ -8,8 +8,8 @@
 // Per-term factors idf(t)(k1 + 1) and per-chunk length norms are computed once in fp64 at
 // attach time and stored as fp32; scores accumulate in fp32.
 //
-// One workgroup scores one query over a range of up to 32,768 chunks held as an fp32
-// accumulator in LDS (128 KiB).  Terms are applied one after another with a barrier in
+// One workgroup scores one query over a range of up to 8,192 chunks held as an fp32
+// accumulator in LDS (32 KiB); a term's postings in the range are found by a 32-ary search.  Terms are applied one after another with a barrier in
 // between, and a term's postings name distinct chunks, so every chunk's score is summed
 // in query-term order with no atomics: the result is deterministic.  A 4 x 8-bit radix
 // select over the accumulator then finds the k-th best score, and the winners are sorted
@@ -24,7 +24,8 @@ namespace {
 
 using namespace dev;
 
-constexpr int kNT = 512;  // threads per scoring workgroup
+constexpr int kNT = 256;         // threads per scoring workgroup (one per radix bin)
+constexpr int kTermBatch = kNT / 32;  // query terms whose posting bounds are found together
 
 // Structural checks of the CSR, one thread per term, then one thread per posting (a posting
 // finds its term by binary search over the offsets, so long lists are checked in parallel).
@@ -125,46 +126,111 @@ struct SparseArgs {
   unsigned long long* partial;  // [nq x n_ranges x k] when n_ranges > 1
 };
 
+// Bounds [lo, hi) of the postings of one term whose chunks fall in [c0, c1), found by the 32
+// threads of a group with a 32-ary search (three rounds for lists up to 32K postings).
+// Every thread of the group returns the same bounds.
+__device__ __forceinline__ void range_bounds32(const int* chunk, long long lo, long long hi, long long c0,
+                                               long long c1, int sub, long long* out_lo, long long* out_hi) {
+  long long a0 = lo, a1 = hi, b0 = lo, b1 = hi;  // first index >= c0 lies in [a0, a1]; >= c1 in [b0, b1]
+  while (a1 - a0 > 0 || b1 - b0 > 0) {
+    // probe 32 evenly spaced positions of each interval (step ceil(len / 32), so they reach
+    // its end); the probes below the key form a prefix of the group
+    const long long sa = (a1 - a0 + 31) / 32, sb = (b1 - b0 + 31) / 32;
+    const long long pa = a0 + (long long)sub * sa, pb = b0 + (long long)sub * sb;
+    const bool la = pa < a1 && chunk[pa] < c0;
+    const bool lb = pb < b1 && chunk[pb] < c1;
+    const unsigned long long ma = __ballot(la), mb = __ballot(lb);
+    const int base = threadIdx.x & 32;  // this group's half of the wave
+    const int ca = __popcll((ma >> base) & 0xffffffffull), cb = __popcll((mb >> base) & 0xffffffffull);
+    if (a1 - a0 > 0) {
+      if (ca == 0) a1 = a0;  // chunk[a0] >= c0
+      else {
+        const long long n0 = a0 + (long long)(ca - 1) * sa + 1;
+        a1 = std::min(a1, a0 + (long long)ca * sa);
+        a0 = n0;
+      }
+    }
+    if (b1 - b0 > 0) {
+      if (cb == 0) b1 = b0;
+      else {
+        const long long n0 = b0 + (long long)(cb - 1) * sb + 1;
+        b1 = std::min(b1, b0 + (long long)cb * sb);
+        b0 = n0;
+      }
+    }
+  }
+  *out_lo = a0;
+  *out_hi = b0;
+}
+
 __global__ __launch_bounds__(kNT) void bm25_kernel(SparseArgs a) {
   __shared__ __attribute__((aligned(16))) float acc[kSparseRange];
   __shared__ unsigned int hist[256];
   __shared__ int wave_tot[kNT / 64];
   __shared__ unsigned long long selbuf[kMaxK];
   __shared__ unsigned int s_prefix, s_need, s_take_all, s_ngt;
-  __shared__ long long s_lo, s_hi;
+  __shared__ long long s_lo[kTermBatch], s_hi[kTermBatch];
 
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int q = blockIdx.x / a.n_ranges;
   const int range = blockIdx.x % a.n_ranges;
   const long long d0 = (long long)range * kSparseRange;
   const int len = (int)std::min<long long>(kSparseRange, a.n_docs - d0);
 
   for (int i = tid; i < kSparseRange; i += kNT) acc[i] = 0.f;
-  __syncthreads();
 
   const int tb = a.qterm_indptr[q], te = a.qterm_indptr[q + 1];
-  for (int j = tb; j < te; ++j) {
-    const int t = a.qterms[j];
-    if (t < 0 || t >= a.vocab) continue;  // unknown terms match nothing (uniform branch)
-    if (tid == 0) {
-      long long lo = a.indptr[t], hi = a.indptr[t + 1];
-      if (a.n_ranges > 1) {
-        lo = lower_bound(a.chunk, lo, hi, d0);
-        hi = lower_bound(a.chunk, lo, hi, d0 + len);
+  for (int j0 = tb; j0 < te; j0 += kTermBatch) {
+    // 1. posting bounds of up to kTermBatch terms at once, 32 threads per term
+    {
+      const int g = tid >> 5, sub = tid & 31;
+      const int j = j0 + g;
+      if (g < kTermBatch) {
+        long long lo = 0, hi = 0;
+        if (j < te) {
+          const int t = a.qterms[j];
+          if (t >= 0 && t < a.vocab) {  // unknown terms match nothing
+            lo = a.indptr[t];
+            hi = a.indptr[t + 1];
+            if (a.n_ranges > 1) range_bounds32(a.chunk, lo, hi, d0, d0 + len, sub, &lo, &hi);
+          }
+        }
+        if (sub == 0) {
+          s_lo[g] = lo;
+          s_hi[g] = hi;
+        }
       }
-      s_lo = lo;
-      s_hi = hi;
     }
     __syncthreads();
-    const long long lo = s_lo, hi = s_hi;
-    const float w = a.idfk[t];
-    for (long long p = lo + tid; p < hi; p += kNT) {
-      const int c = a.chunk[p];
-      const float f = (float)a.tf[p];
-      acc[c - d0] += (w * f) / (f + a.norm[c]);
+    // 2. one term after another (a term's postings name distinct chunks: no atomics)
+    for (int g = 0; g < kTermBatch && j0 + g < te; ++g) {
+      const long long lo = s_lo[g], hi = s_hi[g];
+      if (lo < hi) {
+        const float wt = a.idfk[a.qterms[j0 + g]];
+        long long p = lo + tid;
+        for (; p + 3 * kNT < hi; p += 4 * kNT) {
+          int c[4];
+          float f[4], nm[4];
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            c[u] = a.chunk[p + u * kNT];
+            f[u] = (float)a.tf[p + u * kNT];
+          }
+#pragma unroll
+          for (int u = 0; u < 4; ++u) nm[u] = a.norm[c[u]];
+#pragma unroll
+          for (int u = 0; u < 4; ++u) acc[c[u] - d0] += (wt * f[u]) / (f[u] + nm[u]);
+        }
+        for (; p < hi; p += kNT) {
+          const int c = a.chunk[p];
+          const float f = (float)a.tf[p];
+          acc[c - d0] += (wt * f) / (f + a.norm[c]);
+        }
+      }
+      __syncthreads();
     }
-    __syncthreads();
   }
+  __syncthreads();
 
   // ---- radix select of the k-th largest positive score (positive fp32 bits order as uints)
   const uint32_t* keys = reinterpret_cast<const uint32_t*>(acc);
@@ -173,35 +239,37 @@ __global__ __launch_bounds__(kNT) void bm25_kernel(SparseArgs a) {
     s_need = (unsigned)a.k;
     s_take_all = 0u;
   }
+  __syncthreads();
   for (int pass = 0; pass < 4; ++pass) {
+    if (s_take_all) break;  // block-uniform
     const int shift = 24 - 8 * pass;
     const uint32_t hmask = pass == 0 ? 0u : (0xffffffffu << (shift + 8));
-    for (int i = tid; i < 256; i += kNT) hist[i] = 0u;
-    __syncthreads();
     const uint32_t prefix = s_prefix;
-    if (!s_take_all) {
-      for (int i = tid; i < len; i += kNT) {
-        const uint32_t u = keys[i];
-        if (u != 0u && (u & hmask) == prefix) atomicAdd(&hist[(u >> shift) & 255u], 1u);
-      }
+    const unsigned int need = s_need;
+    hist[tid] = 0u;  // kNT == 256 bins
+    __syncthreads();
+    for (int i = tid; i < len; i += kNT) {
+      const uint32_t u = keys[i];
+      if (u != 0u && (u & hmask) == prefix) atomicAdd(&hist[(u >> shift) & 255u], 1u);
     }
     __syncthreads();
-    if (tid == 0 && !s_take_all) {
-      unsigned int cum = 0, need = s_need;
-      int bsel = -1;
-      for (int bin = 255; bin >= 0; --bin) {
-        if (cum + hist[bin] >= need) {
-          bsel = bin;
-          break;
-        }
-        cum += hist[bin];
-      }
-      if (bsel < 0) {
-        s_take_all = 1u;  // fewer than k positive scores (only possible in pass 0)
-      } else {
-        s_prefix = prefix | ((uint32_t)bsel << shift);
-        s_need = need - cum;
-      }
+    // thread t holds bin 255 - t; inclusive scan = keys in bins >= 255 - t
+    const int hd = (int)hist[255 - tid];
+    int x = hd;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int y = __shfl_up(x, o, 64);
+      if (lane >= o) x += y;
+    }
+    if (lane == 63) wave_tot[w] = x;
+    __syncthreads();
+    int before = 0;
+    for (int i = 0; i < w; ++i) before += wave_tot[i];
+    const int incl = before + x, above = incl - hd;
+    if (tid == kNT - 1 && incl < (int)need) s_take_all = 1u;  // fewer than k positive scores (pass 0)
+    if (above < (int)need && incl >= (int)need) {
+      s_prefix = prefix | ((uint32_t)(255 - tid) << shift);
+      s_need = need - (unsigned)above;
     }
     __syncthreads();
   }
@@ -241,7 +309,6 @@ __global__ __launch_bounds__(kNT) void bm25_kernel(SparseArgs a) {
 
   // ---- sort the winners (<= 128) with wave 0 and write them out
   if (tid < 64) {
-    const int lane = tid;
     u64 x0 = lane < nsel ? selbuf[lane] : 0ull;
     u64 x1 = lane + 64 < nsel ? selbuf[lane + 64] : 0ull;
     x0 = wave_sort64_desc(x0, lane);

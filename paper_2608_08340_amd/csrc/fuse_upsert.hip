@@ -36,6 +36,7 @@ __global__ __launch_bounds__(kRrfThreads) void rrf_kernel(const long long* dense
   __shared__ long long cid[kMaxCand];
   __shared__ long long cnum[kMaxCand];
   __shared__ long long cden[kMaxCand];
+  __shared__ double cval[kMaxCand];
   __shared__ int s_nc;
   const long long q = blockIdx.x;
   const int t = threadIdx.x;
@@ -52,24 +53,29 @@ __global__ __launch_bounds__(kRrfThreads) void rrf_kernel(const long long* dense
       const long long a = (long long)rrf_k + t + 1;
       num = 1;
       den = a;
-      for (int j = 0; j < ks; ++j) {
-        if (sp_ids[j] == id) {
-          const long long b = (long long)rrf_k + j + 1;
-          num = a + b;
-          den = a * b;
-          break;
-        }
+      int hit = -1;
+      for (int j = 0; j < ks; j += 8) {  // eight independent LDS reads per step
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          if (j + u < ks && hit < 0 && sp_ids[j + u] == id) hit = j + u;
+        if (hit >= 0) break;
+      }
+      if (hit >= 0) {
+        const long long b = (long long)rrf_k + hit + 1;
+        num = a + b;
+        den = a * b;
       }
     }
   } else if (t - kd < ks) {  // sparse entry absent from the dense list
     const int j = t - kd;
     id = sp_ids[j];
     if (id >= 0) {
-      for (int i = 0; i < kd; ++i)
-        if (dn_ids[i] == id) {
-          id = -1;
-          break;
-        }
+      bool dup = false;
+      for (int i = 0; i < kd && !dup; i += 8) {
+#pragma unroll
+        for (int u = 0; u < 8; ++u) dup |= i + u < kd && dn_ids[i + u] == id;
+      }
+      if (dup) id = -1;
       num = 1;
       den = (long long)rrf_k + j + 1;
     }
@@ -79,15 +85,30 @@ __global__ __launch_bounds__(kRrfThreads) void rrf_kernel(const long long* dense
     cid[slot] = id;
     cnum[slot] = num;
     cden[slot] = den;
+    cval[slot] = (double)num / (double)den;
   }
   __syncthreads();
   const int nc = s_nc;
   if (t < nc) {
+    // Rank = candidates that beat this one.  The correctly rounded quotients order any two
+    // fused values that differ by more than a few ulps; closer pairs (exact ties such as
+    // 1/63 = 2/126 among them) are compared exactly as int64 cross products.
     const long long n0 = cnum[t], d0 = cden[t], id0 = cid[t];
+    const double v0 = cval[t], hi = v0 * (1.0 + 1e-14), lo = v0 * (1.0 - 1e-14);
     int rank = 0;
-    for (int o = 0; o < nc && rank < k; ++o) {
-      const long long lhs = cnum[o] * d0, rhs = n0 * cden[o];
-      rank += (lhs > rhs || (lhs == rhs && cid[o] < id0)) ? 1 : 0;
+    for (int o = 0; o < nc && rank < k; o += 8) {  // eight candidates per step
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        if (o + u < nc) {
+          const double v = cval[o + u];
+          bool beats = v > hi;
+          if (!beats && v >= lo) {
+            const long long lhs = cnum[o + u] * d0, rhs = n0 * cden[o + u];
+            beats = lhs > rhs || (lhs == rhs && cid[o + u] < id0);
+          }
+          rank += beats ? 1 : 0;
+        }
+      }
     }
     if (rank < k) {
       out_ids[q * k + rank] = id0;

@@ -83,7 +83,7 @@ struct SparseIndex {
   float k1 = 0.f, b = 0.f;
 };
 
-constexpr int kSparseRange = 32768;        // chunks scored per workgroup (LDS accumulator)
+constexpr int kSparseRange = 8192;         // chunks scored per workgroup (LDS accumulator)
 
 // Validates the CSR on the device; returns the number of violations found (synchronous).
 hipError_t sparse_validate(int vocab, long long n_docs, long long nnz, const long long* indptr,
