@@ -620,6 +620,119 @@ __device__ __forceinline__ bool reg_epilogue(const f32x4 (&acc)[MW][BN / 16], Se
 }
 
 // ------------------------------------------------------------------------------------
+// Selection against the running threshold (5 < k <= 16, every tile after a chunk's first).
+// thr[n] holds the k-th best score of query slot n's running list (-inf while the list is
+// short, +inf past the batch); only a score reaching it can still enter the list.  A lane
+// first compares the maximum of its MW*4 scores of each query with the threshold, so a tile
+// with nothing new costs a few dozen instructions per lane and one barrier.  Hits are
+// appended to the query's candidate list (count, reserve once per lane and query, write);
+// the owner threads insert them and raise thr.  Returns false, with the lists untouched, when
+// some query has more than CAP hits in the tile; the caller then takes the group path.
+// ------------------------------------------------------------------------------------
+// Hits of this lane against the thresholds: count, reserve once per query, write.  FULL: the
+// tile lies inside the chunk, so no row needs the row-limit test.
+template <bool FULL, int BN, int MW, int CAP>
+__device__ __forceinline__ void thr_collect(const f32x4 (&acc)[MW][BN / 16], const float* thr, int* cnt, int* flag,
+                                            uint2* cand, int row0, int lim) {
+  constexpr int NW = BN / 16;
+  const int lane = threadIdx.x & 63;
+  auto ok = [&](int mi, int r) { return FULL || mi * 16 + r < lim; };
+  int c[NW];
+#pragma unroll
+  for (int ni = 0; ni < NW; ++ni) {
+    const float th = thr[ni * 16 + (lane & 15)];
+    float m = kNegInf;
+#pragma unroll
+    for (int mi = 0; mi < MW; ++mi)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) m = __builtin_fmaxf(m, ok(mi, r) ? acc[mi][ni][r] : kNegInf);
+    int cc = 0;
+    if (m >= th) {
+#pragma unroll
+      for (int mi = 0; mi < MW; ++mi)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) cc += (ok(mi, r) && acc[mi][ni][r] >= th) ? 1 : 0;
+    }
+    c[ni] = cc;
+  }
+  int base[NW];
+#pragma unroll
+  for (int ni = 0; ni < NW; ++ni) base[ni] = c[ni] ? atomicAdd(&cnt[ni * 16 + (lane & 15)], c[ni]) : 0;
+#pragma unroll
+  for (int ni = 0; ni < NW; ++ni) {
+    if (c[ni] == 0) continue;
+    if (base[ni] + c[ni] > CAP) {
+      *flag = 1;
+      continue;
+    }
+    const int n = ni * 16 + (lane & 15);
+    const float th = thr[n];
+    uint2* dst = cand + n * CAP;
+    int j = base[ni];
+#pragma unroll
+    for (int mi = 0; mi < MW; ++mi)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float x = acc[mi][ni][r];
+        if (ok(mi, r) && x >= th) {
+          dst[j] = make_uint2(__float_as_uint(x), (unsigned)(row0 + mi * 16 + r));
+          ++j;
+        }
+      }
+  }
+}
+
+template <int BN, int MW, typename Sel>
+__device__ __forceinline__ bool thr_epilogue(const f32x4 (&acc)[MW][BN / 16], Sel& sel, unsigned char* scratch,
+                                             long long tile0, long long row_end, int q_lim, int k) {
+  constexpr int CAP = Sel::CAP;
+  constexpr int TR = kWaves * MW * 16;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  uint2* cand = reinterpret_cast<uint2*>(Sel::cand_of(scratch));
+  float* thr = Sel::tau_of(scratch);
+  int* cnt = Sel::cnt_of(scratch);
+  int* flag = Sel::flag_of(scratch) + 1;  // a word of its own: the group path uses the first
+  const int row0 = w * MW * 16 + (lane >> 4) * 4;
+  if (tile0 + TR <= row_end)  // workgroup-uniform
+    thr_collect<true, BN, MW, CAP>(acc, thr, cnt, flag, cand, row0, 0);
+  else
+    thr_collect<false, BN, MW, CAP>(acc, thr, cnt, flag, cand, row0, (int)(row_end - tile0) - row0);
+  lds_barrier();
+  if (*flag) {  // uniform; the group path resets cnt, and thr_reset thr and flag after it
+    lds_barrier();
+    return false;
+  }
+  if (tid < q_lim) {
+    const int n = cnt[tid];
+    if (n > 0) {
+      for (int j = 0; j < n; ++j) {
+        const uint2 e = cand[tid * CAP + j];
+        sel.run.insert(composite(__uint_as_float(e.x), (uint32_t)(tile0 + e.y)));
+      }
+      cnt[tid] = 0;
+      thr[tid] = sel.run_value(k - 1);
+    }
+  }
+  // thr and cnt are next read in the following tile's selection, after the barriers of its
+  // super-steps
+  return true;
+}
+
+// After a tile that took the group path (or the LDS passes): owners restore the running
+// threshold and an empty candidate list.  After the last barrier of that path a thread reads
+// only its own query's thr and cnt, and the fast path's overflow word was last read before
+// the barrier that preceded the group path.
+template <typename Sel>
+__device__ __forceinline__ void thr_reset(const Sel& sel, unsigned char* scratch, int q_lim, int k, int bn) {
+  const int tid = threadIdx.x;
+  if (tid < bn) {
+    Sel::tau_of(scratch)[tid] = tid < q_lim ? sel.run_value(k - 1) : __builtin_inff();
+    Sel::cnt_of(scratch)[tid] = 0;
+  }
+  if (tid == 0) Sel::flag_of(scratch)[1] = 0;
+}
+
+// ------------------------------------------------------------------------------------
 // k <= 5: the same lower bound tau from the group maxima, but the groups themselves are
 // handed over: a lane whose maximum for a query reaches tau (at most k such groups per
 // query, barring ties) copies its MW*4 scores of that query to one of SLOTS blocks in LDS,
@@ -985,15 +1098,26 @@ __global__ __launch_bounds__(kThreads) void dense_mfma_kernel(DenseArgs a) {
       }
       // ---- selection for the tile: registers first, else G passes through LDS
       const long long tile0 = row_begin + (long long)t * TR;
+      bool refresh = false;  // the group path ran: thresholds and lists of the fast path to restore
       bool done = false;
       if constexpr (SEL == 2) {
         filt_tile<BN, MW>(acc, th, scratch, tile0, row_end, q0, a);
         done = true;
-      } else if constexpr (kBlk)
-        done = blk_epilogue<BN, MW>(acc, sel, reinterpret_cast<unsigned char*>(S), scratch, tile0, row_end, q_lim,
-                                    a.k);
-      else if constexpr (SEL == 0)
-        done = reg_epilogue<BN, MW, KS>(acc, sel, S, scratch, tile0, row_end, q_lim, a.k);
+      } else if constexpr (SEL == 0) {
+        // k > 5: a chunk's first tile fills the lists through the group path, which leaves
+        // the running thresholds in place for the tiles after it.  (The k <= 5 kernels keep
+        // the block path for every tile: they already run close to the register limit.)
+        if constexpr (!kBlk)
+          if (t > 0) done = thr_epilogue<BN, MW>(acc, sel, scratch, tile0, row_end, q_lim, a.k);
+        if (!done) {
+          if constexpr (kBlk)
+            done = blk_epilogue<BN, MW>(acc, sel, reinterpret_cast<unsigned char*>(S), scratch, tile0, row_end,
+                                        q_lim, a.k);
+          else
+            done = reg_epilogue<BN, MW, KS>(acc, sel, S, scratch, tile0, row_end, q_lim, a.k);
+          refresh = true;
+        }
+      }
       if (!done) {
 #pragma unroll
         for (int g = 0; g < G; ++g) {
@@ -1021,6 +1145,8 @@ __global__ __launch_bounds__(kThreads) void dense_mfma_kernel(DenseArgs a) {
           sel.pass(S, SR, RP, pr, q_lim, a.k, scratch);
         }
       }
+      if constexpr (SEL == 0 && !kBlk)
+        if (refresh) thr_reset(sel, scratch, q_lim, a.k, BN);
     }
 #undef OPRAG_SUPER
 #undef OPRAG_KSTEP

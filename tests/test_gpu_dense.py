@@ -80,6 +80,32 @@ def test_ragged_sizes_and_k(dtype, n, nq, k):
     check_dense(S, X, Q, ids, sc, k, dtype, label=f"n={n} nq={nq} k={k}")
 
 
+@pytest.mark.parametrize("kind", ["ints", "four_rows"])
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
+@pytest.mark.parametrize("nq,k", [(1, 7), (16, 5), (40, 16), (130, 5), (130, 10)])
+def test_multi_tile_chunks_exact_ties(kind, dtype, nq, k):
+    """393,293 x 128 integer rows: enough rows that every query block walks several tiles per
+    row chunk, so the selection runs against running thresholds.  "ints": entries in
+    {-2..2}, exact scores with ties near the k-th value.  "four_rows": every row is one of four
+    vectors, so each tile holds dozens of rows tied at the best score and the tie handling
+    takes its overflow paths.  Ids and scores must equal the oracle's exactly."""
+    device()
+    g = np.random.default_rng(7000 + 31 * nq + k + (0 if kind == "ints" else 1))
+    n, d = 393_216 + 77, 128
+    if kind == "ints":
+        X = g.integers(-2, 3, size=(n, d)).astype(np.float32)
+    else:
+        X = g.integers(-2, 3, size=(4, d)).astype(np.float32)[g.integers(0, 4, size=n)]
+    Q = g.integers(-2, 3, size=(nq, d)).astype(np.float32)
+    log("multi-tile", kind, dtype, nq, k)
+    _, sc, ids = _run(synth.to_storage(X, dtype), synth.to_storage(Q, dtype), k, dtype)
+    samp = np.unique(np.r_[0:min(nq, 12), nq - 1])
+    S = Q[samp].astype(np.float64) @ X.astype(np.float64).T
+    ref_ids, ref_sc = od.topk_from_scores(S, k)
+    assert np.array_equal(ids.numpy()[samp], ref_ids)
+    assert np.array_equal(sc.numpy()[samp].astype(np.float64), ref_sc)
+
+
 def test_empty_index_pads():
     dev = device()
     from paper_2608_08340_amd import Index
