@@ -146,9 +146,9 @@ struct PassRows {
 
 // k <= KS <= 16.  Scratch in LDS: candidates [BN][CAP] u64 | values [TPQ][BN][KS] f32 |
 // per-thread counts [TPQ][BN] | tau [BN] | need [BN] | count [BN] | flag.
-template <int BN, int KS>
+template <int BN, int KS, int NT>
 struct SelSmall {
-  static constexpr int TPQ = kThreads / BN;  // threads per query: t = q + BN * sub
+  static constexpr int TPQ = NT / BN;  // threads per query: t = q + BN * sub
   static constexpr int CAP = 2 * KS > 16 ? 2 * KS : 16;  // candidate slots per query and pass
   static constexpr int NL = KS <= 8 ? 4 : 2;             // independent value lists per thread
   static constexpr int kVals = TPQ > 1 ? TPQ * BN * KS * 4 : 0;
@@ -395,12 +395,13 @@ struct SelLarge {
   }
 };
 
-template <int BN, int KS, int SEL>
+template <int BN, int KS, int SEL, int NT>
 struct SelOf {
-  typedef SelSmall<BN, KS> type;
+  typedef SelSmall<BN, KS, NT> type;
 };
-template <int BN, int KS>
-struct SelOf<BN, KS, 1> {
+template <int BN, int KS, int NT>
+struct SelOf<BN, KS, 1, NT> {
+  static_assert(NT == kThreads, "the queue selector assumes four waves");
   typedef SelLarge<BN> type;
 };
 
@@ -420,8 +421,8 @@ struct SelFilter {
   __device__ __forceinline__ void pass(const float*, int, int, const PassRows&, int, int, unsigned char*) {}
   __device__ __forceinline__ void write(const DenseArgs&, int, long long) const {}
 };
-template <int BN, int KS>
-struct SelOf<BN, KS, 2> {
+template <int BN, int KS, int NT>
+struct SelOf<BN, KS, 2, NT> {
   typedef SelFilter<BN> type;
 };
 
@@ -442,13 +443,13 @@ __device__ __forceinline__ void filt_flush(int n, int q, unsigned char* area, co
 
 // acc[mi][ni][r] = score of row tile0 + 16*MW*wave + 16*mi + 4*(lane/16) + r against query
 // slot 16*ni + lane%16; th[ni] its threshold (+inf for slots past the batch).
-template <int BN, int MW>
+template <int BN, int MW, int WV>
 __device__ __forceinline__ void filt_tile(const f32x4 (&acc)[MW][BN / 16], const float (&th)[BN / 16],
                                           unsigned char* area, long long tile0, long long row_end, int q0,
                                           const DenseArgs& a) {
   constexpr int NW = BN / 16;
   constexpr int SCAP = SelFilter<BN>::SCAP;
-  constexpr int TR = kWaves * MW * 16;
+  constexpr int TR = WV * MW * 16;
   u64* stage = reinterpret_cast<u64*>(area);
   int* staged = reinterpret_cast<int*>(area + BN * SCAP * 8);
   int* tcnt = staged + BN;
@@ -523,13 +524,13 @@ __device__ __forceinline__ void filt_tile(const f32x4 (&acc)[MW][BN / 16], const
 // Returns false, with the running lists untouched, when some query has more than CAP
 // candidates (many equal scores); the caller then takes the exact LDS path.
 // ------------------------------------------------------------------------------------
-template <int BN, int MW, int KS, typename Sel>
+template <int BN, int MW, int KS, int WV, typename Sel>
 __device__ __forceinline__ bool reg_epilogue(const f32x4 (&acc)[MW][BN / 16], Sel& sel, float* gv,
                                              unsigned char* scratch, long long tile0, long long row_end, int q_lim,
                                              int k) {
   constexpr int NW = BN / 16;
   constexpr int M = KS <= 5 ? 1 : (KS <= 8 ? 2 : 4);  // values kept per group
-  constexpr int NG = kWaves * 4 * M;                  // group values per query
+  constexpr int NG = WV * 4 * M;                      // group values per query
   constexpr int CAP = Sel::CAP;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   // candidates as (score bits, row offset in the tile), in the candidate area of the selector
@@ -537,7 +538,7 @@ __device__ __forceinline__ bool reg_epilogue(const f32x4 (&acc)[MW][BN / 16], Se
   float* thr = Sel::tau_of(scratch);
   int* cnt = Sel::cnt_of(scratch);
   int* flag = Sel::flag_of(scratch);
-  constexpr int TR = kWaves * MW * 16;
+  constexpr int TR = WV * MW * 16;
   const int row0 = w * MW * 16 + (lane >> 4) * 4;  // tile offset of this lane's value (0, r = 0)
   // element (mi, r) of this lane is a valid row iff 16*mi + r < lim
   const int lim = (int)min((long long)TR, row_end - tile0) - row0;
@@ -682,11 +683,11 @@ __device__ __forceinline__ void thr_collect(const f32x4 (&acc)[MW][BN / 16], con
   }
 }
 
-template <int BN, int MW, typename Sel>
+template <int BN, int MW, int WV, typename Sel>
 __device__ __forceinline__ bool thr_epilogue(const f32x4 (&acc)[MW][BN / 16], Sel& sel, unsigned char* scratch,
                                              long long tile0, long long row_end, int q_lim, int k) {
   constexpr int CAP = Sel::CAP;
-  constexpr int TR = kWaves * MW * 16;
+  constexpr int TR = WV * MW * 16;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   uint2* cand = reinterpret_cast<uint2*>(Sel::cand_of(scratch));
   float* thr = Sel::tau_of(scratch);
@@ -747,25 +748,25 @@ struct BlockArea {
   static constexpr int kBytes = BN * QSTR * 4 + BN * 4;
 };
 
-template <int BN, int MW, typename Sel>
+template <int BN, int MW, int WV, typename Sel>
 __device__ __forceinline__ bool blk_epilogue(const f32x4 (&acc)[MW][BN / 16], Sel& sel, unsigned char* area,
                                              unsigned char* scratch, long long tile0, long long row_end, int q_lim,
                                              int k) {
   constexpr int NW = BN / 16;
   constexpr int KS = 5;
-  constexpr int NG = kWaves * 4;          // groups (lanes) per query
-  constexpr int TPQ = kThreads / BN;      // threads per query in the gathering step
+  constexpr int NG = WV * 4;              // groups (lanes) per query
+  constexpr int TPQ = WV * 64 / BN;       // threads per query in the gathering step
   using B = BlockArea<MW, BN>;
   constexpr int SLOTS = B::SLOTS, VALS = B::VALS, QSTR = B::QSTR;
   constexpr int CAP = Sel::CAP;
   float* blk = reinterpret_cast<float*>(area);                      // [BN][QSTR]: SLOTS x VALS
-  int* gmask = reinterpret_cast<int*>(area + BN * QSTR * 4);        // [BN] active groups
+  unsigned* gmask = reinterpret_cast<unsigned*>(area + BN * QSTR * 4);  // [BN] active groups
   float* gmax = reinterpret_cast<float*>(Sel::cand_of(scratch));    // [NG][BN], then
   uint2* cand = reinterpret_cast<uint2*>(Sel::cand_of(scratch));    // [BN][CAP] (score, row offset)
   float* thr = Sel::tau_of(scratch);
   int* cnt = Sel::cnt_of(scratch);
   int* flag = Sel::flag_of(scratch);
-  constexpr int TR = kWaves * MW * 16;
+  constexpr int TR = WV * MW * 16;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int g = w * 4 + (lane >> 4);
   const int lim = (int)min((long long)TR, row_end - tile0) - (w * MW * 16 + (lane >> 4) * 4);
@@ -787,7 +788,7 @@ __device__ __forceinline__ bool blk_epilogue(const f32x4 (&acc)[MW][BN / 16], Se
   // 2. owners: tau, and the groups whose maximum reaches it (slot = rank among them)
   if (tid < BN) {
     float tau = __builtin_inff();  // queries past the batch take no candidates
-    int mask = 0;
+    unsigned mask = 0;
     if (tid < q_lim) {
       float gm[NG];
 #pragma unroll
@@ -801,7 +802,7 @@ __device__ __forceinline__ bool blk_epilogue(const f32x4 (&acc)[MW][BN / 16], Se
         if (i < k && sel.run.v[i]) L.insert(comp_score(sel.run.v[i]));
       tau = L.at(k);
 #pragma unroll
-      for (int j = 0; j < NG; ++j) mask |= (gm[j] >= tau && gm[j] > kNegInf) ? 1 << j : 0;
+      for (int j = 0; j < NG; ++j) mask |= (gm[j] >= tau && gm[j] > kNegInf) ? 1u << j : 0u;
       if (__builtin_popcount(mask) > SLOTS) *flag = 1;
     }
     thr[tid] = tau;
@@ -814,9 +815,9 @@ __device__ __forceinline__ bool blk_epilogue(const f32x4 (&acc)[MW][BN / 16], Se
 #pragma unroll
   for (int ni = 0; ni < NW; ++ni) {
     const int n = ni * 16 + (lane & 15);
-    const int mask = gmask[n];
-    if ((mask >> g) & 1) {
-      const int slot = __builtin_popcount(mask & ((1 << g) - 1));
+    const unsigned mask = gmask[n];
+    if ((mask >> g) & 1u) {
+      const int slot = __builtin_popcount(mask & ((1u << g) - 1u));
       float* dst = blk + n * QSTR + slot * VALS;
 #pragma unroll
       for (int mi = 0; mi < MW; ++mi) {
@@ -834,11 +835,11 @@ __device__ __forceinline__ bool blk_epilogue(const f32x4 (&acc)[MW][BN / 16], Se
     const int q = tid % BN, sub = tid / BN;
     if (q < q_lim) {
       const float tau = thr[q];
-      int mask = gmask[q];
+      const unsigned mask = gmask[q];
       // this thread's blocks are the ranks sub, sub + TPQ, ...: count, reserve, write
       int c = 0;
       int rank = 0;
-      for (int mm = mask; mm; mm &= mm - 1, ++rank) {
+      for (unsigned mm = mask; mm; mm &= mm - 1, ++rank) {
         if (rank % TPQ != sub) continue;
         const float* src = blk + q * QSTR + rank * VALS;
 #pragma unroll
@@ -854,7 +855,7 @@ __device__ __forceinline__ bool blk_epilogue(const f32x4 (&acc)[MW][BN / 16], Se
           over = 1;
         } else {
           rank = 0;
-          for (int mm = mask; mm; mm &= mm - 1, ++rank) {
+          for (unsigned mm = mask; mm; mm &= mm - 1, ++rank) {
             if (rank % TPQ != sub) continue;
             const int gg = __builtin_ctz(mm);
             const int r0 = (gg >> 2) * MW * 16 + (gg & 3) * 4;
@@ -885,7 +886,7 @@ __device__ __forceinline__ bool blk_epilogue(const f32x4 (&acc)[MW][BN / 16], Se
     } else {
       const float tau = thr[tid];
       int rank = 0;
-      for (int mm = gmask[tid]; mm; mm &= mm - 1, ++rank) {
+      for (unsigned mm = gmask[tid]; mm; mm &= mm - 1, ++rank) {
         const int gg = __builtin_ctz(mm);
         const long long r0 = tile0 + (gg >> 2) * MW * 16 + (gg & 3) * 4;
         const float* src = blk + tid * QSTR + rank * VALS;
@@ -914,33 +915,34 @@ __device__ __forceinline__ bool blk_epilogue(const f32x4 (&acc)[MW][BN / 16], Se
 //    epilogue (or, when it declines, G passes through an LDS score tile) updates the
 //    running top-k of each query.
 // ------------------------------------------------------------------------------------
-template <int DT, int NW, int MW, int RS, int G, int KS, int SEL>
-__global__ __launch_bounds__(kThreads) void dense_mfma_kernel(DenseArgs a) {
+template <int DT, int NW, int MW, int RS, int G, int KS, int SEL, int WV>
+__global__ __launch_bounds__(WV * 64) void dense_mfma_kernel(DenseArgs a) {
   using M = Mfma<DT>;
   using V = typename M::V;
   using T = typename M::T;
   constexpr int BN = NW * 16;
-  constexpr int TR = kWaves * MW * 16;
+  constexpr int NT = WV * 64;                  // threads
+  constexpr int TR = WV * MW * 16;
   constexpr int KC = 32;                        // dimensions per k-step
   constexpr int SK = 128;                       // dimensions per super-step
   constexpr int PX = RS - 1;
   static_assert(RS == 4 || RS == 8 || RS == 16, "ring of whole super-steps");
   constexpr int BODY = RS;                      // k-steps per loop iteration; divides d / 32
   constexpr int QSLOT = BN * SK * 2;            // bytes: query row n at n * 256
-  constexpr int QPT = BN * SK * 2 / 16 / kThreads;  // 16-byte query pieces per thread
-  static_assert(QPT * kThreads * 16 == QSLOT, "query pieces");
+  constexpr int QPT = BN * SK * 2 / 16 / NT;   // 16-byte query pieces per thread
+  static_assert(QPT * NT * 16 == QSLOT, "query pieces");
   constexpr int MWP = MW / G;                   // subtile rows per wave per fallback pass
-  constexpr int RP = kWaves * MWP * 16;         // rows per fallback pass
+  constexpr int RP = WV * MWP * 16;             // rows per fallback pass
   constexpr int SR = RP + 4;                    // S row stride (floats)
-  using Sel = typename SelOf<BN, KS, SEL>::type;
+  using Sel = typename SelOf<BN, KS, SEL, NT>::type;
   constexpr int QBYTES = 2 * QSLOT;
   constexpr bool kBlk = SEL == 0 && KS == 5;
   constexpr int SB0 = SEL == 2 ? 0 : BN * SR * 4;
   constexpr int SBYTES = kBlk && BlockArea<MW, BN>::kBytes > SB0 ? BlockArea<MW, BN>::kBytes : SB0;
   constexpr int SMEM = QBYTES + SBYTES + Sel::kBytes;
   static_assert(MW % G == 0 && ((MWP * 16) & (MWP * 16 - 1)) == 0, "pass shape");
-  static_assert(SEL != 0 || RP % (4 * (kThreads / BN)) == 0, "slice shape");
-  static_assert(SEL != 0 || kWaves * 4 * (KS <= 5 ? 1 : (KS <= 8 ? 2 : 4)) * BN * 4 <= SBYTES,
+  static_assert(SEL != 0 || RP % (4 * (NT / BN)) == 0, "slice shape");
+  static_assert(SEL != 0 || WV * 4 * (KS <= 5 ? 1 : (KS <= 8 ? 2 : 4)) * BN * 4 <= SBYTES,
                 "group values of the register epilogue fit in the score tile");
   __shared__ __attribute__((aligned(16))) unsigned char smem[SMEM];
   unsigned char* qslots = smem;
@@ -980,7 +982,7 @@ __global__ __launch_bounds__(kThreads) void dense_mfma_kernel(DenseArgs a) {
     th[ni] = q >= a.nq ? __builtin_inff() : (a.th ? a.th[(long long)q * a.th_stride] : kNegInf);
   }
   if (n_st > 0) {
-    // Query piece p = tid + 256 j: row r = p / 16, 16-byte column c = p % 16 of the
+    // Query piece p = tid + NT j: row r = p / 16, 16-byte column c = p % 16 of the
     // super-step, stored at column c ^ (r % 16) of the row.  Any 16 consecutive lanes then
     // touch 256 distinct bytes modulo 256 (all 64 banks), for the row-wise writes and for
     // the fragment reads (16 rows, one column) alike.
@@ -989,7 +991,7 @@ __global__ __launch_bounds__(kThreads) void dense_mfma_kernel(DenseArgs a) {
     int qoff[QPT], qdst[QPT];
 #pragma unroll
     for (int j = 0; j < QPT; ++j) {
-      const int p = tid + kThreads * j;
+      const int p = tid + NT * j;
       const int r = p / 16, c = p % 16;
       qoff[j] = (r * d + c * 8) * 2;
       qdst[j] = r * 256 + ((c ^ (r & 15)) * 16);
@@ -1070,10 +1072,12 @@ __global__ __launch_bounds__(kThreads) void dense_mfma_kernel(DenseArgs a) {
     OPRAG_BFRAG(qn, 0)                                                                   \
   }
 
-    // prologue: rows of k-steps 0 .. PX-1, queries of super-steps 0 (to slot 0) and 1
+    // prologue: queries of super-step 0 first (their wait then leaves the row loads in
+    // flight), rows of k-steps 0 .. PX-1, queries of super-step 0 to slot 0, queries of
+    // super-step 1
+    OPRAG_QUERIES()
 #pragma unroll
     for (int u = 0; u < PX; ++u) OPRAG_ROWS(u)
-    OPRAG_QUERIES()
 #pragma unroll
     for (int j = 0; j < QPT; ++j) *reinterpret_cast<u32x4*>(qslots + qdst[j]) = qr[j];
     OPRAG_QUERIES()
@@ -1101,20 +1105,20 @@ __global__ __launch_bounds__(kThreads) void dense_mfma_kernel(DenseArgs a) {
       bool refresh = false;  // the group path ran: thresholds and lists of the fast path to restore
       bool done = false;
       if constexpr (SEL == 2) {
-        filt_tile<BN, MW>(acc, th, scratch, tile0, row_end, q0, a);
+        filt_tile<BN, MW, WV>(acc, th, scratch, tile0, row_end, q0, a);
         done = true;
       } else if constexpr (SEL == 0) {
         // k > 5: a chunk's first tile fills the lists through the group path, which leaves
         // the running thresholds in place for the tiles after it.  (The k <= 5 kernels keep
         // the block path for every tile: they already run close to the register limit.)
         if constexpr (!kBlk)
-          if (t > 0) done = thr_epilogue<BN, MW>(acc, sel, scratch, tile0, row_end, q_lim, a.k);
+          if (t > 0) done = thr_epilogue<BN, MW, WV>(acc, sel, scratch, tile0, row_end, q_lim, a.k);
         if (!done) {
           if constexpr (kBlk)
-            done = blk_epilogue<BN, MW>(acc, sel, reinterpret_cast<unsigned char*>(S), scratch, tile0, row_end,
+            done = blk_epilogue<BN, MW, WV>(acc, sel, reinterpret_cast<unsigned char*>(S), scratch, tile0, row_end,
                                         q_lim, a.k);
           else
-            done = reg_epilogue<BN, MW, KS>(acc, sel, S, scratch, tile0, row_end, q_lim, a.k);
+            done = reg_epilogue<BN, MW, KS, WV>(acc, sel, S, scratch, tile0, row_end, q_lim, a.k);
           refresh = true;
         }
       }
@@ -1136,7 +1140,7 @@ __global__ __launch_bounds__(kThreads) void dense_mfma_kernel(DenseArgs a) {
           pr.off = g * MWP * 16;
           int nv = 0;
 #pragma unroll
-          for (int bb = 0; bb < kWaves; ++bb) {
+          for (int bb = 0; bb < WV; ++bb) {
             const long long start = tile0 + (long long)bb * MW * 16 + g * MWP * 16;
             nv += (int)max(0ll, min((long long)(MWP * 16), row_end - start));
           }
@@ -1167,7 +1171,7 @@ __global__ __launch_bounds__(kThreads) void dense_mfma_kernel(DenseArgs a) {
 template <int KS, int SEL>
 __global__ __launch_bounds__(kThreads) void dense_f32_kernel(DenseArgs a) {
   constexpr int BN = 32, TR = 64, KC = 32, SR = TR + 4;
-  using Sel = typename SelOf<BN, KS, SEL>::type;
+  using Sel = typename SelOf<BN, KS, SEL, kThreads>::type;
   constexpr int XB = TR * (KC + 1) * 4, QB = BN * (KC + 1) * 4;
   constexpr int SB = BN * SR * 4;
   constexpr int A1 = XB + QB;
@@ -1510,11 +1514,13 @@ __global__ __launch_bounds__(kThreads) void merge_large_kernel(const unsigned lo
 struct KernelInfo {
   void (*fn)(DenseArgs);
   int dtype, bn, tile_rows, ks, sel, wgs_per_cu, min_nq, max_nq;
-  int ring;  // MFMA kernels: k-steps per loop iteration, which must divide d / 32 (0: none)
+  int ring;     // MFMA kernels: k-steps per loop iteration, which must divide d / 32 (0: none)
+  int threads;  // workgroup size
 };
 
-#define MFK(DT, NW, MW, RS, G, KS, SEL, OCC, LO, HI) \
-  {dense_mfma_kernel<DT, NW, MW, RS, G, KS, SEL>, DT, NW * 16, kWaves * MW * 16, KS, SEL, OCC, LO, HI, RS}
+#define MFKW(DT, NW, MW, RS, G, KS, SEL, OCC, LO, HI, WV) \
+  {dense_mfma_kernel<DT, NW, MW, RS, G, KS, SEL, WV>, DT, NW * 16, WV * MW * 16, KS, SEL, OCC, LO, HI, RS, WV * 64}
+#define MFK(DT, NW, MW, RS, G, KS, SEL, OCC, LO, HI) MFKW(DT, NW, MW, RS, G, KS, SEL, OCC, LO, HI, kWaves)
 // Deep rings first; the 4-deep variants serve dimensions that are not multiples of the ring.
 #define MF_KS(DT, NW, MW, RS, G, OCC, LO, HI)                                                   \
   MFK(DT, NW, MW, RS, G, 5, 0, OCC, LO, HI), MFK(DT, NW, MW, RS, G, 8, 0, OCC, LO, HI),          \
@@ -1529,10 +1535,10 @@ struct KernelInfo {
       MFK(DT, 8, 4, 4, 1, 5, 2, 1, 65, 1 << 30)
 
 const KernelInfo kKernels[] = {
-    {dense_f32_kernel<5, 0>, kDtypeF32, 32, 64, 5, 0, 2, 1, 1 << 30, 0},
-    {dense_f32_kernel<8, 0>, kDtypeF32, 32, 64, 8, 0, 2, 1, 1 << 30, 0},
-    {dense_f32_kernel<16, 0>, kDtypeF32, 32, 64, 16, 0, 2, 1, 1 << 30, 0},
-    {dense_f32_kernel<8, 1>, kDtypeF32, 32, 64, 128, 1, 2, 1, 1 << 30, 0},
+    {dense_f32_kernel<5, 0>, kDtypeF32, 32, 64, 5, 0, 2, 1, 1 << 30, 0, kThreads},
+    {dense_f32_kernel<8, 0>, kDtypeF32, 32, 64, 8, 0, 2, 1, 1 << 30, 0, kThreads},
+    {dense_f32_kernel<16, 0>, kDtypeF32, 32, 64, 16, 0, 2, 1, 1 << 30, 0, kThreads},
+    {dense_f32_kernel<8, 1>, kDtypeF32, 32, 64, 128, 1, 2, 1, 1 << 30, 0, kThreads},
     MF_SET(kDtypeBF16),
     MF_SET(kDtypeF16),
 };
@@ -1651,9 +1657,9 @@ hipError_t launch_kernel(const KernelInfo& ki, long long grid, DenseArgs& arg, h
   void* params[] = {&arg};
   // With timing events the launch carries them in its dispatch packet: they are stamped when
   // the kernel itself starts and ends.
-  return ev0 ? hipExtLaunchKernel(reinterpret_cast<const void*>(ki.fn), dim3((unsigned)grid), dim3(kThreads), params,
+  return ev0 ? hipExtLaunchKernel(reinterpret_cast<const void*>(ki.fn), dim3((unsigned)grid), dim3(ki.threads), params,
                                   0, s, ev0, ev1, 0)
-             : hipLaunchKernel(reinterpret_cast<const void*>(ki.fn), dim3((unsigned)grid), dim3(kThreads), params, 0,
+             : hipLaunchKernel(reinterpret_cast<const void*>(ki.fn), dim3((unsigned)grid), dim3(ki.threads), params, 0,
                                s);
 }
 
