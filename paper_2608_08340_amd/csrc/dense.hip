@@ -1346,135 +1346,103 @@ __global__ void clear_ints_kernel(int* p, long long n) {
 }
 
 // ------------------------------------------------------------------------------------
-// Merge of the per-chunk lists: partial[q][chunk][k] composites (0 = empty slot).
+// Merge of the per-chunk lists (k <= 16), one wave per query.  The query's n = n_chunks * k
+// composites (unique, larger is better, 0 = empty slot) are read in lane-strided order.  The
+// k-th largest of the 64 lane maxima is a lower bound tau of the k-th best composite (the k
+// lanes from the top each hold a composite at least that large), so the composites >= tau
+// are the only candidates; they are compacted into LDS and every candidate's rank is the
+// number of candidates larger than it.  With more than 64 candidates the wave instead extracts the k
+// best one by one (k rounds of a lane-local and a wave-wide maximum).
 // ------------------------------------------------------------------------------------
-// k <= KS <= 16: one workgroup per query.  Thread t owns a contiguous block of the query's
-// candidates (chunk lists in row order, each sorted), so thread order is id order among
-// equal scores.  Pass 1: top-KS values per thread (med3), combined across the wave with
-// shuffles and across waves through LDS into the exact k-th value tau.  Pass 2: candidates
-// above tau and the first (smallest-id) ones equal to tau go to LDS; thread 0 sorts them.
-template <int KS>
-__global__ __launch_bounds__(kThreads) void merge_small_kernel(const unsigned long long* __restrict__ partial,
-                                                               int n_chunks, int nq, int k, float* out_scores,
-                                                               long long* out_ids) {
-  constexpr int CAP = 2 * KS;
-  constexpr int PR = 16;  // candidates per thread kept in registers (more: read twice)
-  __shared__ u64 cand[CAP];
-  __shared__ float wl[kWaves][KS];
-  __shared__ int wsum[kWaves];
-  __shared__ float s_tau;
-  __shared__ int s_need, s_cnt;
-  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
-  const int q = blockIdx.x;
-  const long long n = (long long)n_chunks * k;
-  const int per = (int)((n + kThreads - 1) / kThreads);
-  const long long b0 = (long long)t * per;
-  const long long b1 = b0 + per < n ? b0 + per : n;
-  const unsigned long long* src = partial + (long long)q * n;
-  const bool in_regs = per <= PR;
+__device__ __forceinline__ u64 wave_max64(u64 x) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) x = umax64(x, shfl_xor64(x, o));
+  return x;
+}
 
-  u64 rc[PR];
-  ValTop<KS> L;
-  L.clear();
-  if (in_regs) {
+__global__ __launch_bounds__(kThreads) void merge_lists_kernel(const u64* __restrict__ partial, int n_chunks, int nq,
+                                                               int k, float* out_scores, long long* out_ids) {
+  constexpr int PB = 16;  // composites per lane per batch, loaded before any is used
+  __shared__ u64 cand[kWaves][64];
+  __shared__ u64 s_tau[kWaves];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const long long q = (long long)blockIdx.x * kWaves + w;
+  if (q >= nq) return;  // whole waves; nothing below synchronises the workgroup
+  const long long n = (long long)n_chunks * k;
+  const u64* src = partial + q * n;
+  float* osc = out_scores + q * k;
+  long long* oid = out_ids + q * k;
+  u64 kb[PB];
+  auto load_batch = [&](long long base) {
 #pragma unroll
-    for (int u = 0; u < PR; ++u) rc[u] = b0 + u < b1 ? src[b0 + u] : 0ull;
-#pragma unroll
-    for (int u = 0; u < PR; ++u) L.insert(rc[u] ? comp_score(rc[u]) : kNegInf);
-  } else {
-    for (long long j = b0; j < b1; j += 4) {
-      u64 c4[4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) c4[u] = j + u < b1 ? src[j + u] : 0ull;
-#pragma unroll
-      for (int u = 0; u < 4; ++u) L.insert(c4[u] ? comp_score(c4[u]) : kNegInf);
+    for (int u = 0; u < PB; ++u) {
+      const long long j = base + u * 64 + lane;
+      kb[u] = j < n ? src[j] : 0ull;
     }
+  };
+
+  u64 m = 0;
+  for (long long base = 0; base < n; base += 64 * PB) {
+    load_batch(base);
+#pragma unroll
+    for (int u = 0; u < PB; ++u) m = umax64(m, kb[u]);
   }
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) {
-    float o[KS];
-#pragma unroll
-    for (int i = 0; i < KS; ++i) o[i] = __shfl_xor(L.v[i], off, 64);
-#pragma unroll
-    for (int i = 0; i < KS; ++i) L.insert(o[i]);
+  // tau = the lane maximum of rank k - 1 (ranks from LDS broadcast reads; the maxima are
+  // unique apart from empty lanes), or 0 when fewer than k lanes hold a composite
+  cand[w][lane] = m;
+  if (lane == 0) s_tau[w] = 0ull;
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  {
+    int rank = 0;
+#pragma unroll 8
+    for (int u = 0; u < 64; ++u) rank += cand[w][u] > m ? 1 : 0;
+    if (rank == k - 1) s_tau[w] = m;
   }
-  if (lane == 0)
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  const u64 tau = s_tau[w];
+  const u64 below = (1ull << lane) - 1ull;
+  int c = 0;  // candidates so far (wave-uniform)
+  for (long long base = 0; base < n; base += 64 * PB) {
+    if (n > 64 * PB) load_batch(base);  // a single batch is still in registers
 #pragma unroll
-    for (int i = 0; i < KS; ++i) wl[w][i] = L.v[i];
-  if (t == 0) s_cnt = 0;
-  __syncthreads();
-  if (t == 0) {
-    for (int ww = 1; ww < kWaves; ++ww)
-#pragma unroll
-      for (int i = 0; i < KS; ++i) L.insert(wl[ww][i]);
-    const float tau = L.at(k);
-    int ngt = 0;
-#pragma unroll
-    for (int i = 0; i < KS; ++i) ngt += (i < k && L.v[i] > tau) ? 1 : 0;
-    s_tau = tau;
-    s_need = tau == kNegInf ? 0 : k - ngt;
-  }
-  __syncthreads();
-  const float tau = s_tau;
-  const int need = s_need;
-  int neq = 0;
-  if (in_regs) {
-#pragma unroll
-    for (int u = 0; u < PR; ++u) {
-      if (!rc[u]) continue;
-      const float v = comp_score(rc[u]);
-      if (v > tau) cand[atomicAdd(&s_cnt, 1)] = rc[u];
-      neq += v == tau ? 1 : 0;
-    }
-  } else {
-    for (long long j = b0; j < b1; ++j) {
-      const u64 c = src[j];
-      if (!c) continue;
-      const float v = comp_score(c);
-      if (v > tau) cand[atomicAdd(&s_cnt, 1)] = c;
-      neq += v == tau ? 1 : 0;
-    }
-  }
-  // exclusive prefix of the tie counts in thread order
-  int x = neq;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const int y = __shfl_up(x, o, 64);
-    if (lane >= o) x += y;
-  }
-  if (lane == 63) wsum[w] = x;
-  __syncthreads();
-  int pre = x - neq;
-  for (int ww = 0; ww < w; ++ww) pre += wsum[ww];
-  if (neq > 0 && pre < need) {
-    if (in_regs) {
-#pragma unroll
-      for (int u = 0; u < PR; ++u)
-        if (rc[u] && pre < need && comp_score(rc[u]) == tau) {
-          cand[atomicAdd(&s_cnt, 1)] = rc[u];
-          ++pre;
-        }
-    } else {
-      for (long long j = b0; j < b1 && pre < need; ++j) {
-        const u64 c = src[j];
-        if (c && comp_score(c) == tau) {
-          cand[atomicAdd(&s_cnt, 1)] = c;
-          ++pre;
-        }
+    for (int u = 0; u < PB; ++u) {
+      const bool take = kb[u] != 0ull && kb[u] >= tau;
+      const u64 bal = __ballot(take);
+      if (take) {
+        const int pos = c + __popcll(bal & below);
+        if (pos < 64) cand[w][pos] = kb[u];
       }
+      c += __popcll(bal);
     }
   }
-  __syncthreads();
-  if (t == 0) {
-    RegTopK<KS> list;
-    list.clear();
-    for (int j = 0; j < s_cnt; ++j) list.insert(cand[j]);
+  if (c <= 64) {
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // this wave's LDS writes are complete
+    const u64 me = lane < c ? cand[w][lane] : 0ull;
+    int rank = 0;
+    for (int u = 0; u < c; ++u) rank += cand[w][u] > me ? 1 : 0;
+    if (lane < c && rank < k) {
+      oid[rank] = (long long)comp_row(me);
+      osc[rank] = comp_score(me);
+    }
+    for (int r = c + lane; r < k; r += 64) {
+      oid[r] = -1;
+      osc[r] = kNegInf;
+    }
+  } else {
+    // at least 64 >= k composites reach tau, so every round finds one
+    u64 last = ~0ull;
+    for (int r = 0; r < k; ++r) {
+      u64 mx = 0;
+      for (long long base = 0; base < n; base += 64 * PB) {
+        if (n > 64 * PB) load_batch(base);
 #pragma unroll
-    for (int i = 0; i < KS; ++i) {
-      if (i < k) {
-        const u64 c = list.v[i];
-        out_ids[(long long)q * k + i] = c ? (long long)comp_row(c) : -1ll;
-        out_scores[(long long)q * k + i] = c ? comp_score(c) : kNegInf;
+        for (int u = 0; u < PB; ++u)
+          if (kb[u] >= tau && kb[u] < last) mx = umax64(mx, kb[u]);
+      }
+      last = wave_max64(mx);
+      if (lane == 0) {
+        oid[r] = (long long)comp_row(last);
+        osc[r] = comp_score(last);
       }
     }
   }
@@ -1712,16 +1680,8 @@ hipError_t launch_dense(const DensePlan& p, int dtype, const DenseArgs& a, hipSt
   hipError_t e = launch_kernel(ki, p.grid, arg, s, ev0, ev1);
   if (e != hipSuccess || p.n_chunks == 1) return e;
   if (ki.sel == 0) {
-    const unsigned blocks = (unsigned)a.nq;
-    if (ki.ks == 5)
-      hipLaunchKernelGGL(merge_small_kernel<5>, dim3(blocks), dim3(kThreads), 0, s, a.partial, p.n_chunks, a.nq, a.k,
-                         a.out_scores, a.out_ids);
-    else if (ki.ks == 8)
-      hipLaunchKernelGGL(merge_small_kernel<8>, dim3(blocks), dim3(kThreads), 0, s, a.partial, p.n_chunks, a.nq, a.k,
-                         a.out_scores, a.out_ids);
-    else
-      hipLaunchKernelGGL(merge_small_kernel<16>, dim3(blocks), dim3(kThreads), 0, s, a.partial, p.n_chunks, a.nq,
-                         a.k, a.out_scores, a.out_ids);
+    hipLaunchKernelGGL(merge_lists_kernel, dim3((unsigned)((a.nq + kWaves - 1) / kWaves)), dim3(kThreads), 0, s,
+                       a.partial, p.n_chunks, a.nq, a.k, a.out_scores, a.out_ids);
   } else {
     hipLaunchKernelGGL(merge_large_kernel, dim3((unsigned)((a.nq + kWaves - 1) / kWaves)), dim3(kThreads), 0, s,
                        a.partial, p.n_chunks, a.nq, a.k, a.out_scores, a.out_ids);
