@@ -106,6 +106,29 @@ def test_multi_tile_chunks_exact_ties(kind, dtype, nq, k):
     assert np.array_equal(sc.numpy()[samp].astype(np.float64), ref_sc)
 
 
+@pytest.mark.parametrize("nq,k", [(1, 16), (16, 16), (3, 5), (40, 8)])
+def test_merge_with_candidates_concentrated(nq, k):
+    """32,768 rows where every fourth run of 64 rows scores high and the rest low: the best
+    entries of many per-chunk lists compete, so the list merge sees far more composites above
+    its threshold than one wave can rank at once and extracts the k best one at a time.
+    Integer values: ids and scores must equal the oracle's exactly."""
+    device()
+    n, d = 32_768, 128
+    r = np.arange(n)
+    X = np.zeros((n, d), np.float32)
+    X[:, 0] = np.where((r // 64) % 4 == 0, 100 + r % 37, r % 50)
+    X[:, 1:] = np.random.default_rng(5).integers(-1, 2, size=(n, d - 1))
+    Q = np.zeros((nq, d), np.float32)
+    Q[:, 0] = 1.0
+    Q[:, 1] = np.arange(nq) % 3 - 1  # small query-dependent perturbation
+    log("concentrated", nq, k)
+    _, sc, ids = _run(synth.to_storage(X, "bf16"), synth.to_storage(Q, "bf16"), k, "bf16")
+    S = Q.astype(np.float64) @ X.astype(np.float64).T
+    ref_ids, ref_sc = od.topk_from_scores(S, k)
+    assert np.array_equal(ids.numpy(), ref_ids)
+    assert np.array_equal(sc.numpy().astype(np.float64), ref_sc)
+
+
 def test_empty_index_pads():
     dev = device()
     from paper_2608_08340_amd import Index
