@@ -409,14 +409,12 @@ struct SelOf<BN, KS, 1, NT> {
 // Filtered mode (k > 16).  Every row whose score reaches the query's threshold becomes a
 // candidate key in the query's global buffer; an exact selection over the buffer follows in
 // select_topk_kernel.  Candidates of a query are staged in LDS (SCAP keys) and written out
-// with one device-scope reservation per flush; a tile with more candidates than the stage
-// reserves global space for itself.  LDS: stage [BN][SCAP] | staged [BN] | tile count [BN] |
-// tile base [BN] (long long).
+// with one device-scope reservation per flush.  LDS: stage [BN][SCAP] | staged count [BN].
 // ------------------------------------------------------------------------------------
 template <int BN>
 struct SelFilter {
-  static constexpr int SCAP = 16;
-  static constexpr int kBytes = BN * SCAP * 8 + BN * 8 + BN * 8;
+  static constexpr int SCAP = 32;
+  static constexpr int kBytes = BN * SCAP * 8 + BN * 4;
   __device__ __forceinline__ void init() {}
   __device__ __forceinline__ void pass(const float*, int, int, const PassRows&, int, int, unsigned char*) {}
   __device__ __forceinline__ void write(const DenseArgs&, int, long long) const {}
@@ -426,13 +424,14 @@ struct SelOf<BN, KS, 2, NT> {
   typedef SelFilter<BN> type;
 };
 
-// Owner thread of query slot n: append its staged keys to the global buffer.
+// Owner thread of query slot n: append its staged keys (the stage's first SCAP slots; a count
+// beyond SCAP means the rest already went out directly) to the global buffer.
 template <int BN>
 __device__ __forceinline__ void filt_flush(int n, int q, unsigned char* area, const DenseArgs& a) {
   constexpr int SCAP = SelFilter<BN>::SCAP;
   u64* stage = reinterpret_cast<u64*>(area);
   int* staged = reinterpret_cast<int*>(area + BN * SCAP * 8);
-  const int c = staged[n];
+  const int c = min(staged[n], SCAP);
   if (c == 0) return;
   const long long g = atomicAdd(a.ccnt + q, c);
   u64* dst = a.cbuf + (long long)q * a.cap;
@@ -441,77 +440,76 @@ __device__ __forceinline__ void filt_flush(int n, int q, unsigned char* area, co
   staged[n] = 0;
 }
 
-// acc[mi][ni][r] = score of row tile0 + 16*MW*wave + 16*mi + 4*(lane/16) + r against query
-// slot 16*ni + lane%16; th[ni] its threshold (+inf for slots past the batch).
-template <int BN, int MW, int WV>
-__device__ __forceinline__ void filt_tile(const f32x4 (&acc)[MW][BN / 16], const float (&th)[BN / 16],
-                                          unsigned char* area, long long tile0, long long row_end, int q0,
-                                          const DenseArgs& a) {
+// Hits of one tile: a lane compares the maximum of its MW*4 scores of a query with the
+// threshold and, on a hit, counts them, reserves that many stage slots with one LDS atomic
+// and writes them; hits past the stage's end go straight to the global buffer under one
+// device-scope reservation.  FULL: the tile lies inside the chunk (no row-limit test).
+template <bool FULL, int BN, int MW>
+__device__ __forceinline__ void filt_collect(const f32x4 (&acc)[MW][BN / 16], const float (&th)[BN / 16],
+                                             u64* stage, int* staged, long long tile0, int row0, int lim, int q0,
+                                             const DenseArgs& a) {
   constexpr int NW = BN / 16;
   constexpr int SCAP = SelFilter<BN>::SCAP;
-  constexpr int TR = WV * MW * 16;
-  u64* stage = reinterpret_cast<u64*>(area);
-  int* staged = reinterpret_cast<int*>(area + BN * SCAP * 8);
-  int* tcnt = staged + BN;
-  long long* tbase = reinterpret_cast<long long*>(area + BN * SCAP * 8 + BN * 8);
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int row0 = w * MW * 16 + (lane >> 4) * 4;
-  const int lim = (int)min((long long)TR, row_end - tile0) - row0;
-  // 1. count this lane's candidates per query and reserve their place in the tile's list
-  int c[NW], off[NW];
+  const int lane = threadIdx.x & 63;
+  auto ok = [&](int mi, int r) { return FULL || mi * 16 + r < lim; };
 #pragma unroll
   for (int ni = 0; ni < NW; ++ni) {
-    int cc = 0;
+    float m = kNegInf;
 #pragma unroll
     for (int mi = 0; mi < MW; ++mi)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) cc += (mi * 16 + r < lim && acc[mi][ni][r] >= th[ni]) ? 1 : 0;
-    c[ni] = cc;
-  }
+      for (int r = 0; r < 4; ++r) m = __builtin_fmaxf(m, ok(mi, r) ? acc[mi][ni][r] : kNegInf);
+    if (!(m >= th[ni])) continue;
+    int c = 0;
 #pragma unroll
-  for (int ni = 0; ni < NW; ++ni) off[ni] = c[ni] ? atomicAdd(&tcnt[ni * 16 + (lane & 15)], c[ni]) : 0;
-  lds_barrier();
-  // 2. owners: make room in the stage, or send a large tile list straight to global memory
-  if (tid < BN) {
-    const int tc = tcnt[tid];
-    tbase[tid] = -1;
-    if (tc > 0) {
-      if (staged[tid] + tc > SCAP) filt_flush<BN>(tid, q0 + tid, area, a);
-      if (tc > SCAP) tbase[tid] = atomicAdd(a.ccnt + q0 + tid, tc);
-    }
-  }
-  lds_barrier();
-  // 3. write
+    for (int mi = 0; mi < MW; ++mi)
 #pragma unroll
-  for (int ni = 0; ni < NW; ++ni) {
-    if (c[ni] == 0) continue;
+      for (int r = 0; r < 4; ++r) c += (ok(mi, r) && acc[mi][ni][r] >= th[ni]) ? 1 : 0;
     const int n = ni * 16 + (lane & 15);
-    const long long gb = tbase[n];
-    int j = off[ni];
+    const int pos = atomicAdd(&staged[n], c);
+    const int in_stage = max(0, min(c, SCAP - pos));
+    const long long g = in_stage < c ? atomicAdd(a.ccnt + q0 + n, c - in_stage) : 0ll;
     u64* dst_g = a.cbuf + (long long)(q0 + n) * a.cap;
-    u64* dst_s = stage + n * SCAP + staged[n];
+    int h = 0;
 #pragma unroll
     for (int mi = 0; mi < MW; ++mi)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const float x = acc[mi][ni][r];
-        if (mi * 16 + r < lim && x >= th[ni]) {
+        if (ok(mi, r) && x >= th[ni]) {
           const u64 key = composite(x, (uint32_t)(tile0 + row0 + mi * 16 + r));
-          if (gb >= 0) {
-            if (gb + j < a.cap) dst_g[gb + j] = key;
+          if (h < in_stage) {
+            stage[n * SCAP + pos + h] = key;
           } else {
-            dst_s[j] = key;
+            const long long j = g + (h - in_stage);
+            if (j < a.cap) dst_g[j] = key;
           }
-          ++j;
+          ++h;
         }
       }
   }
+}
+
+// acc[mi][ni][r] = score of row tile0 + 16*MW*wave + 16*mi + 4*(lane/16) + r against query
+// slot 16*ni + lane%16; th[ni] its threshold (+inf for slots past the batch).  One barrier;
+// then the owner of a stage at least half full flushes it.  The stage is next written in the
+// following tile's selection, after the barriers of its super-steps.
+template <int BN, int MW, int WV>
+__device__ __forceinline__ void filt_tile(const f32x4 (&acc)[MW][BN / 16], const float (&th)[BN / 16],
+                                          unsigned char* area, long long tile0, long long row_end, int q0,
+                                          const DenseArgs& a) {
+  constexpr int SCAP = SelFilter<BN>::SCAP;
+  constexpr int TR = WV * MW * 16;
+  u64* stage = reinterpret_cast<u64*>(area);
+  int* staged = reinterpret_cast<int*>(area + BN * SCAP * 8);
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int row0 = w * MW * 16 + (lane >> 4) * 4;
+  if (tile0 + TR <= row_end)  // workgroup-uniform
+    filt_collect<true, BN, MW>(acc, th, stage, staged, tile0, row0, 0, q0, a);
+  else
+    filt_collect<false, BN, MW>(acc, th, stage, staged, tile0, row0, (int)(row_end - tile0) - row0, q0, a);
   lds_barrier();
-  // 4. owners: the tile's list now belongs to the stage (unless it went out directly)
-  if (tid < BN) {
-    if (tbase[tid] < 0) staged[tid] += tcnt[tid];
-    tcnt[tid] = 0;
-  }
+  if (tid < BN && staged[tid] >= SCAP / 2) filt_flush<BN>(tid, q0 + tid, area, a);
 }
 
 // ------------------------------------------------------------------------------------
@@ -968,11 +966,7 @@ __global__ __launch_bounds__(WV * 64) void dense_mfma_kernel(DenseArgs a) {
   Sel sel;
   sel.init();
   if constexpr (SEL == 2) {
-    if (tid < BN) {
-      int* staged = reinterpret_cast<int*>(scratch + BN * SelFilter<BN>::SCAP * 8);
-      staged[tid] = 0;
-      staged[BN + tid] = 0;
-    }
+    if (tid < BN) reinterpret_cast<int*>(scratch + BN * SelFilter<BN>::SCAP * 8)[tid] = 0;
     // no barrier needed here: the first tile's epilogue follows several barriers
   }
   float th[NW];  // filtered mode: thresholds of this lane's query slots
