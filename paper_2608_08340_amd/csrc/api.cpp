@@ -141,32 +141,6 @@ oprag_status do_dense(oprag_index* idx, const void* q, int64_t nq, int32_t k, fl
     }
     hipError_t e = oprag::launch_dense(p, idx->dtype, a, s, ev0, ev1);
     if (e != hipSuccess) return hip_fail(e, "dense search launch");
-    if (p.filtered) {
-      // Exactness check of the filtered mode: did any query find more candidates than the
-      // buffer holds?  Then repeat the last level with the tighter thresholds now known, and
-      // as a last resort take the per-chunk-list path.
-      const int* d_ovf = oprag::dense_overflow_counter(p, ws, nql);
-      for (int attempt = 0;; ++attempt) {
-        int ovf = 0;
-        if ((e = hipMemcpyAsync(&ovf, d_ovf, sizeof(int), hipMemcpyDeviceToHost, s)) != hipSuccess ||
-            (e = hipStreamSynchronize(s)) != hipSuccess)
-          return hip_fail(e, "dense search overflow check");
-        if (ovf == 0) break;
-        if (attempt < 2) {
-          e = oprag::relaunch_dense_last_level(p, idx->dtype, a, s);
-        } else {
-          const oprag::DensePlan lp = oprag::plan_dense_lists(idx->dtype, idx->dim, idx->n_rows, nql, k);
-          oprag::DenseArgs la = a;
-          la.n_qblocks = lp.n_qblocks;
-          la.n_chunks = lp.n_chunks;
-          la.rows_per_chunk = lp.rows_per_chunk;
-          e = oprag::launch_dense(lp, idx->dtype, la, s);
-          if (e != hipSuccess) return hip_fail(e, "dense search launch");
-          break;
-        }
-        if (e != hipSuccess) return hip_fail(e, "dense search launch");
-      }
-    }
   }
   return OPRAG_OK;
 }

@@ -490,6 +490,30 @@ __device__ __forceinline__ void filt_collect(const f32x4 (&acc)[MW][BN / 16], co
   }
 }
 
+// First level (no threshold): every row of [0, n_rows) is a candidate, so each score goes to
+// the slot of its row in the query's buffer; no counting, no atomics, no barrier.  The
+// buffer holds at least n_rows keys at this level.
+template <int BN, int MW, int WV>
+__device__ __forceinline__ void filt_all_tile(const f32x4 (&acc)[MW][BN / 16], long long tile0, long long row_end,
+                                              int q0, int q_lim, const DenseArgs& a) {
+  constexpr int NW = BN / 16;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const long long r0 = tile0 + w * MW * 16 + (lane >> 4) * 4;
+#pragma unroll
+  for (int ni = 0; ni < NW; ++ni) {
+    const int n = ni * 16 + (lane & 15);
+    if (n >= q_lim) continue;
+    u64* dst = a.cbuf + (long long)(q0 + n) * a.cap;
+#pragma unroll
+    for (int mi = 0; mi < MW; ++mi)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const long long row = r0 + mi * 16 + r;
+        if (row < row_end) dst[row] = composite(acc[mi][ni][r], (uint32_t)row);
+      }
+  }
+}
+
 // acc[mi][ni][r] = score of row tile0 + 16*MW*wave + 16*mi + 4*(lane/16) + r against query
 // slot 16*ni + lane%16; th[ni] its threshold (+inf for slots past the batch).  One barrier;
 // then the owner of a stage at least half full flushes it.  The stage is next written in the
@@ -915,6 +939,7 @@ __device__ __forceinline__ bool blk_epilogue(const f32x4 (&acc)[MW][BN / 16], Se
 // ------------------------------------------------------------------------------------
 template <int DT, int NW, int MW, int RS, int G, int KS, int SEL, int WV>
 __global__ __launch_bounds__(WV * 64) void dense_mfma_kernel(DenseArgs a) {
+  if (a.gate != nullptr && *a.gate == 0) return;  // a repair launch with nothing to repair
   using M = Mfma<DT>;
   using V = typename M::V;
   using T = typename M::T;
@@ -1099,7 +1124,10 @@ __global__ __launch_bounds__(WV * 64) void dense_mfma_kernel(DenseArgs a) {
       bool refresh = false;  // the group path ran: thresholds and lists of the fast path to restore
       bool done = false;
       if constexpr (SEL == 2) {
-        filt_tile<BN, MW, WV>(acc, th, scratch, tile0, row_end, q0, a);
+        if (a.th == nullptr)  // launch-uniform
+          filt_all_tile<BN, MW, WV>(acc, tile0, row_end, q0, q_lim, a);
+        else
+          filt_tile<BN, MW, WV>(acc, th, scratch, tile0, row_end, q0, a);
         done = true;
       } else if constexpr (SEL == 0) {
         // k > 5: a chunk's first tile fills the lists through the group path, which leaves
@@ -1153,7 +1181,11 @@ __global__ __launch_bounds__(WV * 64) void dense_mfma_kernel(DenseArgs a) {
 #undef OPRAG_ROWS
   }
   if constexpr (SEL == 2) {
-    if (tid < q_lim) filt_flush<BN>(tid, q0 + tid, scratch, a);
+    if (a.th == nullptr) {
+      if (chunk == 0 && tid < q_lim) a.ccnt[q0 + tid] = (int)a.n_rows;  // every row is a candidate
+    } else if (tid < q_lim) {
+      filt_flush<BN>(tid, q0 + tid, scratch, a);
+    }
   } else {
     sel.write(a, q0, chunk);
   }
@@ -1254,13 +1286,15 @@ __global__ __launch_bounds__(kThreads) void dense_f32_kernel(DenseArgs a) {
 // it, and ranks them.  Keys are distinct (row ids are), so exactly min(k, n) keys qualify.
 // ------------------------------------------------------------------------------------
 __global__ __launch_bounds__(kThreads) void select_topk_kernel(const unsigned long long* __restrict__ cbuf,
-                                                               const int* __restrict__ ccnt, long long cap, int k,
-                                                               float* out_scores, long long* out_ids, int* overflow) {
+                                                               int* __restrict__ ccnt, long long cap, int k,
+                                                               float* out_scores, long long* out_ids, int* overflow,
+                                                               const int* gate) {
   __shared__ unsigned int hist[256];
   __shared__ int wtot[kWaves];
   __shared__ u64 sel[kMaxK];
   __shared__ u64 s_prefix, s_mask;
   __shared__ int s_need, s_done, s_ns;
+  if (gate != nullptr && *gate == 0) return;
   const int t = threadIdx.x, lane = t & 63, w = t >> 6;
   const int q = blockIdx.x;
   const int cnt = ccnt[q];
@@ -1275,6 +1309,7 @@ __global__ __launch_bounds__(kThreads) void select_topk_kernel(const unsigned lo
     s_ns = 0;
   }
   __syncthreads();
+  if (t == 0) ccnt[q] = 0;  // every thread has read it: the next pass starts from zero
   for (int shift = 56; shift >= 0; shift -= 8) {
     if (s_done) break;  // block-uniform
     const u64 prefix = s_prefix, mask = s_mask;
@@ -1334,7 +1369,8 @@ __global__ __launch_bounds__(kThreads) void select_topk_kernel(const unsigned lo
 }
 
 // Clears the filtered-mode counters (a kernel, not a memset: safe inside captured graphs).
-__global__ void clear_ints_kernel(int* p, long long n) {
+__global__ void clear_ints_kernel(int* p, long long n, const int* gate) {
+  if (gate != nullptr && *gate == 0) return;
   for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (long long)gridDim.x * blockDim.x)
     p[i] = 0;
 }
@@ -1445,7 +1481,8 @@ __global__ __launch_bounds__(kThreads) void merge_lists_kernel(const u64* __rest
 // k <= 128: one wave per query keeps a 128-entry queue and merges 64 candidates at a time.
 __global__ __launch_bounds__(kThreads) void merge_large_kernel(const unsigned long long* __restrict__ partial,
                                                                int n_chunks, int nq, int k, float* out_scores,
-                                                               long long* out_ids) {
+                                                               long long* out_ids, const int* gate) {
+  if (gate != nullptr && *gate == 0) return;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int q = blockIdx.x * kWaves + w;
   if (q >= nq) return;
@@ -1600,16 +1637,23 @@ DensePlan plan_dense(int dtype, int d, long long n_rows, int nq, int k) {
   return p;
 }
 
-size_t dense_workspace_bytes(const DensePlan& p, int nq) {
+// Filtered-mode workspace: candidate buffers [nq][fcap] | counts [nq] | (shared with the
+// per-chunk lists of the fallback plan) | four overflow flags past both.
+namespace {
+size_t filtered_body_bytes(const DensePlan& p, int nq) {
   const size_t lists = (size_t)nq * (size_t)p.cap * sizeof(unsigned long long);
-  if (!p.filtered) return lists;
-  const size_t filt = align_up256((size_t)nq * (size_t)p.fcap * 8) + align_up256((size_t)nq * 4) + 256;
-  return std::max(lists, filt);
+  const size_t filt = align_up256((size_t)nq * (size_t)p.fcap * 8) + align_up256((size_t)nq * 4);
+  return align_up256(std::max(lists, filt));
 }
+// [0] the last level overflowed, [1] an earlier level did (harmless), [2] the repair did.
+int* dense_flags(const DensePlan& p, void* ws, int nq) {
+  return reinterpret_cast<int*>(static_cast<unsigned char*>(ws) + filtered_body_bytes(p, nq));
+}
+}  // namespace
 
-int* dense_overflow_counter(const DensePlan& p, void* ws, int nq) {
-  return reinterpret_cast<int*>(static_cast<unsigned char*>(ws) + align_up256((size_t)nq * (size_t)p.fcap * 8) +
-                                align_up256((size_t)nq * 4));
+size_t dense_workspace_bytes(const DensePlan& p, int nq) {
+  if (!p.filtered) return (size_t)nq * (size_t)p.cap * sizeof(unsigned long long);
+  return filtered_body_bytes(p, nq) + 256;
 }
 
 namespace {
@@ -1626,31 +1670,32 @@ hipError_t launch_kernel(const KernelInfo& ki, long long grid, DenseArgs& arg, h
 }
 
 // One filtered level: clear the counts, collect candidates, select.
-hipError_t filter_level(const DensePlan& p, const DenseArgs& a, int level, hipStream_t s, hipEvent_t ev0,
-                        hipEvent_t ev1) {
+// One filter pass over rows [0, rows): candidates >= th (every row when th is null) into the
+// buffers, then the exact top-k of each buffer.  The first pass (th null) sets the counts;
+// each selection zeroes its query's count for the next pass.  With a gate, nothing runs
+// unless *gate != 0.
+hipError_t filter_pass(const DensePlan& p, const DenseArgs& a, long long rows, const float* th, int* ovf,
+                       const int* gate, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
   const KernelInfo& ki = kKernels[p.kernel];
   unsigned long long* cbuf = a.partial;  // the workspace
   int* ccnt = reinterpret_cast<int*>(reinterpret_cast<unsigned char*>(cbuf) +
                                      align_up256((size_t)a.nq * (size_t)p.fcap * 8));
-  int* ovf = ccnt + align_up256((size_t)a.nq * 4) / 4;  // [0]: last level, [1]: earlier levels
-  const bool last = level == p.n_levels - 1;
-  hipLaunchKernelGGL(clear_ints_kernel, dim3((unsigned)std::min<long long>(1024, (a.nq + 255) / 256)), dim3(256), 0,
-                     s, ccnt, (long long)a.nq);
   DensePlan lp = p;
-  split_rows(lp, p.level_rows[level], p.chunk_bound, 1);
+  split_rows(lp, rows, p.chunk_bound, 1);
   DenseArgs arg = a;
-  arg.n_rows = p.level_rows[level];
+  arg.n_rows = rows;
   arg.n_chunks = lp.n_chunks;
   arg.rows_per_chunk = lp.rows_per_chunk;
-  arg.th = level == 0 ? nullptr : a.out_scores + (a.k - 1);
+  arg.th = th;
   arg.th_stride = a.k;
   arg.cbuf = cbuf;
   arg.ccnt = ccnt;
   arg.cap = p.fcap;
+  arg.gate = gate;
   hipError_t e = launch_kernel(ki, lp.grid, arg, s, ev0, ev1);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(select_topk_kernel, dim3((unsigned)a.nq), dim3(kThreads), 0, s, cbuf, ccnt, p.fcap, a.k,
-                     a.out_scores, a.out_ids, ovf + (last ? 0 : 1));
+                     a.out_scores, a.out_ids, ovf, gate);
   return hipGetLastError();
 }
 
@@ -1658,17 +1703,37 @@ hipError_t filter_level(const DensePlan& p, const DenseArgs& a, int level, hipSt
 
 hipError_t launch_dense(const DensePlan& p, int dtype, const DenseArgs& a, hipStream_t s, hipEvent_t ev0,
                         hipEvent_t ev1) {
-  (void)dtype;
   const KernelInfo& ki = kKernels[p.kernel];
   if (p.filtered) {
-    int* ovf = dense_overflow_counter(p, a.partial, a.nq);
-    hipLaunchKernelGGL(clear_ints_kernel, dim3(1), dim3(64), 0, s, ovf, 2ll);
+    int* fl = dense_flags(p, a.partial, a.nq);
+    hipLaunchKernelGGL(clear_ints_kernel, dim3(1), dim3(64), 0, s, fl, 4ll, nullptr);
     for (int l = 0; l < p.n_levels; ++l) {
       const bool last = l == p.n_levels - 1;
-      hipError_t e = filter_level(p, a, l, s, last ? ev0 : nullptr, last ? ev1 : nullptr);
+      // level l's threshold: the k-th score of level l - 1's exact result
+      hipError_t e = filter_pass(p, a, p.level_rows[l], l == 0 ? nullptr : a.out_scores + (a.k - 1), fl + (last ? 0 : 1),
+                                 nullptr, s, last ? ev0 : nullptr, last ? ev1 : nullptr);
       if (e != hipSuccess) return e;
     }
-    return hipSuccess;
+    // Exactness repair, decided on the device: only a buffer overflow in the last level can
+    // lose a row.  Then the last level runs again with the current k-th scores as thresholds
+    // (the lists are the top-k of a subset of the rows at or above the old thresholds, so
+    // their k-th scores are valid thresholds and no lower), and if that overflows too, the
+    // per-chunk-list plan runs.  Each repair launch returns at once when its flag is clear.
+    hipError_t e = filter_pass(p, a, a.n_rows, a.out_scores + (a.k - 1), fl + 2, fl, s, nullptr, nullptr);
+    if (e != hipSuccess) return e;
+    const DensePlan lp = plan_dense_lists(dtype, a.d, a.n_rows, a.nq, a.k);
+    DenseArgs la = a;
+    la.n_qblocks = lp.n_qblocks;
+    la.n_chunks = lp.n_chunks;
+    la.rows_per_chunk = lp.rows_per_chunk;
+    la.gate = fl + 2;
+    const KernelInfo& lk = kKernels[lp.kernel];
+    e = launch_kernel(lk, lp.grid, la, s, nullptr, nullptr);
+    if (e != hipSuccess) return e;
+    if (lp.n_chunks > 1)
+      hipLaunchKernelGGL(merge_large_kernel, dim3((unsigned)((a.nq + kWaves - 1) / kWaves)), dim3(kThreads), 0, s,
+                         a.partial, lp.n_chunks, a.nq, a.k, a.out_scores, a.out_ids, fl + 2);
+    return hipGetLastError();
   }
   DenseArgs arg = a;
   hipError_t e = launch_kernel(ki, p.grid, arg, s, ev0, ev1);
@@ -1678,39 +1743,10 @@ hipError_t launch_dense(const DensePlan& p, int dtype, const DenseArgs& a, hipSt
                        a.partial, p.n_chunks, a.nq, a.k, a.out_scores, a.out_ids);
   } else {
     hipLaunchKernelGGL(merge_large_kernel, dim3((unsigned)((a.nq + kWaves - 1) / kWaves)), dim3(kThreads), 0, s,
-                       a.partial, p.n_chunks, a.nq, a.k, a.out_scores, a.out_ids);
+                       a.partial, p.n_chunks, a.nq, a.k, a.out_scores, a.out_ids, nullptr);
   }
   return hipGetLastError();
 }
 
-hipError_t relaunch_dense_last_level(const DensePlan& p, int dtype, const DenseArgs& a, hipStream_t s) {
-  (void)dtype;
-  if (!p.filtered) return hipSuccess;
-  int* ovf = dense_overflow_counter(p, a.partial, a.nq);
-  hipLaunchKernelGGL(clear_ints_kernel, dim3(1), dim3(64), 0, s, ovf, 2ll);
-  // The current lists are the top-k of a subset of the rows at or above the last threshold:
-  // their k-th scores are valid thresholds again, and no lower than the last ones.
-  DenseArgs arg = a;
-  const KernelInfo& ki = kKernels[p.kernel];
-  unsigned long long* cbuf = a.partial;
-  int* ccnt = reinterpret_cast<int*>(reinterpret_cast<unsigned char*>(cbuf) +
-                                     align_up256((size_t)a.nq * (size_t)p.fcap * 8));
-  hipLaunchKernelGGL(clear_ints_kernel, dim3((unsigned)std::min<long long>(1024, (a.nq + 255) / 256)), dim3(256), 0,
-                     s, ccnt, (long long)a.nq);
-  DensePlan lp = p;
-  split_rows(lp, a.n_rows, p.chunk_bound, 1);
-  arg.n_chunks = lp.n_chunks;
-  arg.rows_per_chunk = lp.rows_per_chunk;
-  arg.th = a.out_scores + (a.k - 1);
-  arg.th_stride = a.k;
-  arg.cbuf = cbuf;
-  arg.ccnt = ccnt;
-  arg.cap = p.fcap;
-  hipError_t e = launch_kernel(ki, lp.grid, arg, s, nullptr, nullptr);
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(select_topk_kernel, dim3((unsigned)a.nq), dim3(kThreads), 0, s, cbuf, ccnt, p.fcap, a.k,
-                     a.out_scores, a.out_ids, ovf);
-  return hipGetLastError();
-}
 
 }  // namespace oprag

@@ -33,6 +33,8 @@ struct DenseArgs {
   unsigned long long* cbuf = nullptr;
   int* ccnt = nullptr;
   long long cap = 0;
+  // When set, the launch does nothing unless *gate != 0 (a device-side overflow flag).
+  const int* gate = nullptr;
 };
 
 struct DensePlan {
@@ -58,16 +60,11 @@ DensePlan plan_dense(int dtype, int d, long long n_rows, int nq, int k);
 // The per-chunk-list plan for any k (the exact fallback of the filtered mode).
 DensePlan plan_dense_lists(int dtype, int d, long long n_rows, int nq, int k);
 size_t dense_workspace_bytes(const DensePlan& p, int nq);
-// ev0 / ev1 (optional) are recorded on s right before and after the scoring kernel (the first
-// one, in filtered mode).
+// ev0 / ev1 (optional) are recorded on s right before and after the scoring kernel (in
+// filtered mode, the last level's).  Filtered mode also enqueues its exactness repair:
+// launches gated on device-side overflow flags, so the search never waits for the host.
 hipError_t launch_dense(const DensePlan& p, int dtype, const DenseArgs& a, hipStream_t s, hipEvent_t ev0 = nullptr,
                         hipEvent_t ev1 = nullptr);
-// Filtered mode: device address of the overflow counter inside the workspace (> 0 after a
-// launch when some query found more candidates than fcap).
-int* dense_overflow_counter(const DensePlan& p, void* ws, int nq);
-// Filtered mode: repeats the last level with the current k-th scores as thresholds.
-hipError_t relaunch_dense_last_level(const DensePlan& p, int dtype, const DenseArgs& a, hipStream_t s);
-
 
 // ---------------------------------------------------------------- sparse (BM25)
 struct SparseIndex {

@@ -129,6 +129,37 @@ def test_merge_with_candidates_concentrated(nq, k):
     assert np.array_equal(sc.numpy().astype(np.float64), ref_sc)
 
 
+@pytest.mark.parametrize("nq", [3, 70])
+@pytest.mark.parametrize("case", ["repair", "fallback"])
+def test_filtered_overflow_repair(case, nq):
+    """k > 16 runs in threshold levels with candidate buffers of max(4,096, 256 k) keys.
+    "repair": the first 4,096 rows score low, so the last level's threshold admits ~56,000
+    rows and the buffers overflow; the device-side repair reruns the last level with the
+    k-th scores found so far.  "fallback": a quarter of 120,000 rows tie at the top score,
+    so every repair overflows too and the per-chunk-list plan answers.  Exact either way."""
+    device()
+    g = np.random.default_rng(11 + nq)
+    k, d = 17, 128
+    if case == "repair":
+        n = 60_000
+        r = np.arange(n)
+        X = np.zeros((n, d), np.float32)
+        X[:, 0] = np.where(r < 4096, r % 7, 20 + (r * 7919) % 200)  # integers < 256: exact in bf16
+    else:
+        n = 120_000
+        X = g.integers(-2, 3, size=(4, d)).astype(np.float32)[g.integers(0, 4, size=n)]
+    X[:, 1] = g.integers(-1, 2, size=n)
+    Q = np.zeros((nq, d), np.float32)
+    Q[:, 0] = 1.0
+    Q[:, 2:] = g.integers(0, 2, size=(nq, d - 2)) if case == "fallback" else 0.0
+    log("overflow", case, nq)
+    _, sc, ids = _run(synth.to_storage(X, "bf16"), synth.to_storage(Q, "bf16"), k, "bf16")
+    S = Q.astype(np.float64) @ X.astype(np.float64).T
+    ref_ids, ref_sc = od.topk_from_scores(S, k)
+    assert np.array_equal(ids.numpy(), ref_ids)
+    assert np.array_equal(sc.numpy().astype(np.float64), ref_sc)
+
+
 def test_empty_index_pads():
     dev = device()
     from paper_2608_08340_amd import Index

@@ -124,10 +124,14 @@ def test_rrf_kernel_matches_exact_fractions():
         ref_ids, ref_f32, _ = rrf.fuse(D, S, 60, k)
         assert np.array_equal(ids.cpu().numpy(), ref_ids)
         assert np.array_equal(fused.cpu().numpy().view(np.uint32), ref_f32.view(np.uint32))
-    fused, ids = rrf_fuse(_t(D, dev), _t(S, dev), 0, 10)
-    torch.cuda.synchronize()
-    ref_ids, ref_f32, _ = rrf.fuse(D, S, 0, 10)
-    assert np.array_equal(ids.cpu().numpy(), ref_ids)
+    # rrf_k across the kernel's two orderings: correctly rounded quotients (rrf_k < 1e5) and
+    # quotients with exact int64 checks of near pairs (larger rrf_k)
+    for rk in (0, 99_999, 100_000, 1_000_000):
+        fused, ids = rrf_fuse(_t(D, dev), _t(S, dev), rk, 10)
+        torch.cuda.synchronize()
+        ref_ids, ref_f32, _ = rrf.fuse(D, S, rk, 10)
+        assert np.array_equal(ids.cpu().numpy(), ref_ids), rk
+        assert np.array_equal(fused.cpu().numpy().view(np.uint32), ref_f32.view(np.uint32)), rk
 
 
 @pytest.fixture(scope="module")
