@@ -130,9 +130,9 @@ oprag_status oprag_workspace_bytes(const oprag_index *idx, int32_t op, int64_t n
  *   q_dev      [nq x dim] in the index dtype;
  *   scores_dev [nq x k] fp32;  ids_dev [nq x k] int64 (row ids).
  * nq = 0 is a no-op.  workspace_dev must hold oprag_workspace_bytes(OPRAG_OP_DENSE) bytes.
- * Asynchronous on stream, except for bf16 / fp16 indexes with k > 16: that search runs in
- * threshold levels and reads one overflow counter back to the host, so it synchronises the
- * stream once before returning (and cannot be captured in a HIP graph).
+ * Asynchronous on stream for every k (bf16 / fp16 searches with k > 16 run in threshold
+ * levels whose exactness repair is decided on the device), so a search can be captured in a
+ * HIP graph.
  */
 oprag_status oprag_search_dense(oprag_index *idx, const void *q_dev, int64_t nq, int32_t k, float *scores_dev,
                                 int64_t *ids_dev, void *workspace_dev, size_t workspace_bytes, void *stream);
@@ -165,8 +165,7 @@ oprag_status oprag_rrf_fuse(const int64_t *dense_ids_dev, int32_t k_dense, const
 /*
  * Hybrid search (Section 4.4): exact dense top-k_dense and exact BM25 top-k_sparse over the
  * full corpus, fused by reciprocal rank fusion (rrf_k), cut at k.  Equivalent to
- * oprag_search_dense + oprag_search_sparse + oprag_rrf_fuse on the same stream, including
- * the one stream synchronisation of a bf16 / fp16 dense search with k_dense > 16.
+ * oprag_search_dense + oprag_search_sparse + oprag_rrf_fuse on the same stream.
  * workspace_dev must hold oprag_workspace_bytes(OPRAG_OP_HYBRID) bytes.
  */
 oprag_status oprag_search_hybrid(oprag_index *idx, const void *q_dev, const int32_t *qterm_indptr_dev,
