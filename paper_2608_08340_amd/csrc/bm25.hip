@@ -11,9 +11,10 @@
 // One workgroup scores one query over a range of up to 8,192 chunks held as an fp32
 // accumulator in LDS (32 KiB); a term's postings in the range are found by a 32-ary search.  Terms are applied one after another with a barrier in
 // between, and a term's postings name distinct chunks, so every chunk's score is summed
-// in query-term order with no atomics: the result is deterministic.  A 4 x 8-bit radix
-// select over the accumulator then finds the k-th best score, and the winners are sorted
-// (score desc, chunk asc) by a wave-wide bitonic network.
+// in query-term order with no atomics: the result is deterministic.  The range's top-k then
+// comes from a threshold (the k-th largest of the 256 thread maxima) and exact ranks of the
+// few scores above it; many equal scores at the threshold fall back to a 4 x 8-bit radix
+// select and a wave-wide bitonic sort (score desc, chunk asc).
 #include <algorithm>
 
 #include "oprag_internal.h"
@@ -163,11 +164,21 @@ __device__ __forceinline__ void range_bounds32(const int* chunk, long long lo, l
   *out_hi = b0;
 }
 
+// Candidates the threshold selection ranks directly.  With the 32 KiB accumulator this keeps
+// a workgroup under 40 KiB of LDS, four per CU.
+constexpr int kCandCap = 1000;
+
 __global__ __launch_bounds__(kNT) void bm25_kernel(SparseArgs a) {
   __shared__ __attribute__((aligned(16))) float acc[kSparseRange];
-  __shared__ unsigned int hist[256];
+  // One area, used in turn: the thread maxima (threshold step), the candidates (ranking),
+  // or the radix histogram and the winners (fallback path).
+  __shared__ u64 cand[kCandCap];
+  uint32_t* tmax = reinterpret_cast<uint32_t*>(cand);         // [kNT]
+  unsigned int* hist = reinterpret_cast<unsigned int*>(cand);  // [256]
+  u64* selbuf = cand + 128;                                    // [kMaxK]
+  __shared__ int s_nc;
+  __shared__ uint32_t s_tau;
   __shared__ int wave_tot[kNT / 64];
-  __shared__ unsigned long long selbuf[kMaxK];
   __shared__ unsigned int s_prefix, s_need, s_take_all, s_ngt;
   __shared__ long long s_lo[kTermBatch], s_hi[kTermBatch];
 
@@ -232,8 +243,69 @@ __global__ __launch_bounds__(kNT) void bm25_kernel(SparseArgs a) {
   }
   __syncthreads();
 
-  // ---- radix select of the k-th largest positive score (positive fp32 bits order as uints)
+  // ---- exact top-k of the range's positive scores (positive fp32 bits order as uints)
   const uint32_t* keys = reinterpret_cast<const uint32_t*>(acc);
+  // Threshold selection: tau = the k-th largest of the 256 thread maxima (slices i*256 + tid)
+  // is at most the k-th largest score, so only scores >= tau are candidates; when they fit
+  // in kCandCap, each one's rank is the number of larger composites (score, ~chunk), which
+  // are unique.  Otherwise (or with fewer than k positive maxima) the radix path below runs.
+  {
+    uint32_t m = 0u;
+    for (int i = tid; i < len; i += kNT) m = max(m, keys[i]);
+    tmax[tid] = m;
+    if (tid == 0) {
+      s_tau = 0u;
+      s_nc = 0;
+    }
+    __syncthreads();
+    int gt = 0, eq = 0;
+#pragma unroll 8
+    for (int u = 0; u < kNT; ++u) {
+      const uint32_t v = tmax[u];
+      gt += v > m ? 1 : 0;
+      eq += v == m ? 1 : 0;
+    }
+    if (m != 0u && gt <= a.k - 1 && a.k - 1 < gt + eq) s_tau = m;  // the k-th largest maximum
+    __syncthreads();
+  }
+  const uint32_t tau = s_tau;  // 0: fewer than k positive maxima
+  if (tau != 0u) {
+    int c = 0;
+    for (int i = tid; i < len; i += kNT) c += keys[i] >= tau ? 1 : 0;
+    const int before = block_excl_scan(c, wave_tot);
+    if (tid == kNT - 1) s_nc = before + c;
+    int pos = before;
+    if (before + c <= kCandCap)
+      for (int i = tid; i < len; i += kNT)
+        if (keys[i] >= tau) cand[pos++] = ((u64)keys[i] << 32) | (uint32_t)(~(uint32_t)(d0 + i));
+    __syncthreads();
+  }
+  const int nc = s_nc;
+  if (tau != 0u && nc <= kCandCap) {
+    // nc >= k (the k largest maxima are k distinct scores >= tau): ranks 0 .. k-1 all occur
+    for (int j = tid; j < nc; j += kNT) {
+      const u64 me = cand[j];
+      int r = 0;
+      for (int o = 0; o < nc; o += 8) {
+        u64 v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = cand[min(o + u, nc - 1)];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) r += (o + u < nc && v[u] > me) ? 1 : 0;
+      }
+      if (r < a.k) {
+        if (a.n_ranges == 1) {
+          a.out_ids[(long long)q * a.k + r] = (long long)comp_row(me);
+          a.out_scores[(long long)q * a.k + r] = __uint_as_float((uint32_t)(me >> 32));
+        } else {
+          a.partial[((long long)q * a.n_ranges + range) * a.k + r] = me;
+        }
+      }
+    }
+    return;  // workgroup-uniform
+  }
+
+  // ---- radix select of the k-th largest positive score
   if (tid == 0) {
     s_prefix = 0u;
     s_need = (unsigned)a.k;
