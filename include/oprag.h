@@ -18,8 +18,9 @@
  *    next synchronisation of the stream.
  *  - Memory: every large buffer (slab, CSR arrays, queries, outputs, workspace) is device
  *    memory owned by the caller and must stay valid while the index or call uses it.  The
- *    library allocates only the small BM25 statistics arrays at attach time and never in
- *    create, upsert or search.  Device pointers must be 16-byte aligned.
+ *    library allocates only the BM25 statistics arrays at attach time (4 bytes per term and
+ *    per posting) and never in create, upsert or search.  Device pointers must be 16-byte
+ *    aligned.
  *  - Streams: `stream` is a hipStream_t (NULL = default stream).  Calls are asynchronous on
  *    it.  An index keeps host-side state (row count), so calls on one index must be issued
  *    from one host thread at a time; an upsert is seen by searches ordered after it on the
@@ -105,7 +106,8 @@ oprag_status oprag_upsert(oprag_index *idx, const void *rows_dev, int32_t rows_d
  *   post_tf_dev     [nnz] int32 >= 1;  doc_len_dev [n_docs] int32 >= 0 (tokens per chunk).
  * The arrays stay caller-owned and are read by later searches.  The library checks them on
  * the device (E_INVALID on any violation), then computes idf(t) = ln(1 + (N - df + 0.5) /
- * (df + 0.5)) and per-chunk length norms k1 (1 - b + b dl / avgdl) into arrays it owns.
+ * (df + 0.5)) per term and tf / (tf + k1 (1 - b + b dl / avgdl)) per posting, in fp64 stored
+ * as fp32, into arrays it owns (4 bytes per term and per posting).
  * Synchronises `stream`.  Re-attaching replaces the previous sparse index.
  * k1 >= 0, 0 <= b <= 1.
  */

@@ -256,10 +256,10 @@ oprag_status oprag_sparse_attach(oprag_index* idx, int32_t vocab, int64_t n_docs
   DeviceScope ds(idx->device);
   if (ds.error() != hipSuccess) return hip_fail(ds.error(), "select device");
   hipStream_t s = static_cast<hipStream_t>(stream);
-  // Library-owned arrays: [flag u32 | sum u64 | idfk f32 x vocab | norm f32 x n_docs].
+  // Library-owned arrays: [flag u32 | sum u64 | idfk f32 x vocab | posting weights f32 x nnz].
   const size_t off_sum = 256, off_idf = 512;
-  const size_t off_norm = off_idf + align_up((size_t)vocab * 4);
-  const size_t bytes = off_norm + align_up((size_t)n_docs * 4);
+  const size_t off_wpost = off_idf + align_up((size_t)vocab * 4);
+  const size_t bytes = off_wpost + align_up((size_t)nnz * 4);
   void* mem = nullptr;
   hipError_t e = hipMalloc(&mem, bytes);
   if (e != hipSuccess) return hip_fail(e, "sparse arrays allocation");
@@ -286,7 +286,7 @@ oprag_status oprag_sparse_attach(oprag_index* idx, int32_t vocab, int64_t n_docs
   sp.post_chunk = post_chunk_dev;
   sp.post_tf = post_tf_dev;
   sp.idfk = reinterpret_cast<float*>(base + off_idf);
-  sp.norm = reinterpret_cast<float*>(base + off_norm);
+  sp.wpost = reinterpret_cast<float*>(base + off_wpost);
   sp.k1 = k1;
   sp.b = b;
   e = oprag::sparse_prepare(sp, doc_len_dev, reinterpret_cast<unsigned long long*>(base + off_sum), s);

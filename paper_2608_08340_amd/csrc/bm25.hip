@@ -5,8 +5,9 @@
 // Scoring reading (the paper does not fix the variant):
 //   idf(t)  = ln(1 + (N - df + 0.5) / (df + 0.5)),  df = postings of t,  N = chunks;
 //   score   = sum over query-term OCCURRENCES t of idf(t) tf (k1 + 1) / (tf + k1 (1 - b + b dl / avgdl)).
-// Per-term factors idf(t)(k1 + 1) and per-chunk length norms are computed once in fp64 at
-// attach time and stored as fp32; scores accumulate in fp32.
+// Per-term factors idf(t)(k1 + 1) and per-posting weights tf / (tf + k1 (1 - b + b dl /
+// avgdl)) are computed once in fp64 at attach time and stored as fp32, so a posting's
+// contribution is one product; scores accumulate in fp32.
 //
 // One workgroup scores one query over a range of up to 8,192 chunks held as an fp32
 // accumulator in LDS (32 KiB); a term's postings in the range are found by a 32-ary search.  Terms are applied one after another with a barrier in
@@ -69,8 +70,9 @@ __global__ void doclen_sum_kernel(const int* doc_len, long long n_docs, unsigned
   }
 }
 
-__global__ void prepare_kernel(int vocab, long long n_docs, const long long* indptr, const int* doc_len, double avgdl,
-                               double k1, double b, float* idfk, float* norm) {
+__global__ void prepare_kernel(int vocab, long long n_docs, long long nnz, const long long* indptr, const int* chunk,
+                               const int* tf, const int* doc_len, double avgdl, double k1, double b, float* idfk,
+                               float* wpost) {
   const long long tid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
   const long long stride = (long long)gridDim.x * blockDim.x;
   const double N = (double)n_docs;
@@ -78,8 +80,10 @@ __global__ void prepare_kernel(int vocab, long long n_docs, const long long* ind
     const double df = (double)(indptr[t + 1] - indptr[t]);
     idfk[t] = (float)(log(1.0 + (N - df + 0.5) / (df + 0.5)) * (k1 + 1.0));
   }
-  for (long long dd = tid; dd < n_docs; dd += stride)
-    norm[dd] = (float)(k1 * (1.0 - b + b * (double)doc_len[dd] / avgdl));
+  for (long long p = tid; p < nnz; p += stride) {
+    const double f = (double)tf[p];
+    wpost[p] = (float)(f / (f + k1 * (1.0 - b + b * (double)doc_len[chunk[p]] / avgdl)));
+  }
 }
 
 // First position p in [lo, hi) with chunk[p] >= key (chunks ascending within a term).
@@ -114,9 +118,8 @@ struct SparseArgs {
   long long n_docs;
   const long long* indptr;
   const int* chunk;
-  const int* tf;
   const float* idfk;
-  const float* norm;
+  const float* wpost;
   const int* qterm_indptr;
   const int* qterms;
   int nq;
@@ -218,25 +221,20 @@ __global__ __launch_bounds__(kNT) void bm25_kernel(SparseArgs a) {
       const long long lo = s_lo[g], hi = s_hi[g];
       if (lo < hi) {
         const float wt = a.idfk[a.qterms[j0 + g]];
+        // eight postings per thread per step, all loads issued before the first use
         long long p = lo + tid;
-        for (; p + 3 * kNT < hi; p += 4 * kNT) {
-          int c[4];
-          float f[4], nm[4];
+        for (; p + 7 * kNT < hi; p += 8 * kNT) {
+          int c[8];
+          float wp[8];
 #pragma unroll
-          for (int u = 0; u < 4; ++u) {
+          for (int u = 0; u < 8; ++u) {
             c[u] = a.chunk[p + u * kNT];
-            f[u] = (float)a.tf[p + u * kNT];
+            wp[u] = a.wpost[p + u * kNT];
           }
 #pragma unroll
-          for (int u = 0; u < 4; ++u) nm[u] = a.norm[c[u]];
-#pragma unroll
-          for (int u = 0; u < 4; ++u) acc[c[u] - d0] += (wt * f[u]) / (f[u] + nm[u]);
+          for (int u = 0; u < 8; ++u) acc[c[u] - d0] += wt * wp[u];
         }
-        for (; p < hi; p += kNT) {
-          const int c = a.chunk[p];
-          const float f = (float)a.tf[p];
-          acc[c - d0] += (wt * f) / (f + a.norm[c]);
-        }
+        for (; p < hi; p += kNT) acc[a.chunk[p] - d0] += wt * a.wpost[p];
       }
       __syncthreads();
     }
@@ -452,10 +450,11 @@ hipError_t sparse_prepare(SparseIndex& sp, const int* doc_len, unsigned long lon
   e = hipStreamSynchronize(s);
   if (e != hipSuccess) return e;
   sp.avgdl = (double)total / (double)sp.n_docs;
-  const long long work = std::max<long long>(sp.vocab, sp.n_docs);
-  const int blocks = (int)std::min<long long>(1024, (work + 255) / 256);
-  hipLaunchKernelGGL(prepare_kernel, dim3(std::max(1, blocks)), dim3(256), 0, s, sp.vocab, sp.n_docs, sp.term_indptr,
-                     doc_len, sp.avgdl, (double)sp.k1, (double)sp.b, sp.idfk, sp.norm);
+  const long long work = std::max<long long>(sp.vocab, sp.nnz);
+  const int blocks = (int)std::min<long long>(4096, (work + 255) / 256);
+  hipLaunchKernelGGL(prepare_kernel, dim3(std::max(1, blocks)), dim3(256), 0, s, sp.vocab, sp.n_docs, sp.nnz,
+                     sp.term_indptr, sp.post_chunk, sp.post_tf, doc_len, sp.avgdl, (double)sp.k1, (double)sp.b, sp.idfk,
+                     sp.wpost);
   return hipGetLastError();
 }
 
@@ -472,9 +471,8 @@ hipError_t launch_sparse(const SparseIndex& sp, const int* qterm_indptr, const i
   a.n_docs = sp.n_docs;
   a.indptr = sp.term_indptr;
   a.chunk = sp.post_chunk;
-  a.tf = sp.post_tf;
   a.idfk = sp.idfk;
-  a.norm = sp.norm;
+  a.wpost = sp.wpost;
   a.qterm_indptr = qterm_indptr;
   a.qterms = qterms;
   a.nq = nq;

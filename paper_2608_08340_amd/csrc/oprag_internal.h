@@ -75,7 +75,7 @@ struct SparseIndex {
   const int* post_chunk = nullptr;          // caller-owned
   const int* post_tf = nullptr;             // caller-owned
   float* idfk = nullptr;                    // library-owned [vocab]: idf(t) * (k1 + 1)
-  float* norm = nullptr;                    // library-owned [n_docs]: k1 * (1 - b + b * dl / avgdl)
+  float* wpost = nullptr;                   // library-owned [nnz]: tf / (tf + k1 (1 - b + b dl / avgdl))
   double avgdl = 0.0;
   float k1 = 0.f, b = 0.f;
 };
