@@ -404,6 +404,57 @@ __global__ __launch_bounds__(kNT) void bm25_kernel(SparseArgs a) {
   }
 }
 
+// Merge of the per-range lists when they hold at most kMergeCap composites per query.  Each
+// list is sorted (descending, empty 0 slots last) and the composites are unique, so the rank
+// of entry p of list i in the merged order is p plus, for every other list, the number of its
+// entries above it: a binary search in LDS.
+constexpr int kMergeCap = 1024;
+__global__ __launch_bounds__(kNT) void partial_rank_kernel(const unsigned long long* partial, int P, int kp, int nq,
+                                                           int k, float* out_scores, long long* out_ids) {
+  __shared__ u64 c[kMergeCap];
+  __shared__ int s_nv;
+  const int q = blockIdx.x, tid = threadIdx.x;
+  if (q >= nq) return;
+  const int n = P * kp;
+  const unsigned long long* src = partial + (long long)q * n;
+  if (tid == 0) s_nv = 0;
+  __syncthreads();
+  int nv = 0;
+  for (int i = tid; i < n; i += kNT) {
+    const u64 x = src[i];
+    c[i] = x;
+    nv += x != 0ull ? 1 : 0;
+  }
+  if (nv) atomicAdd(&s_nv, nv);
+  __syncthreads();
+  const int n_valid = s_nv;
+  const long long o = (long long)q * k;
+  for (int j = tid; j < n; j += kNT) {
+    const u64 me = c[j];
+    if (me == 0ull) continue;
+    const int li = j / kp;
+    int r = j - li * kp;
+    for (int l = 0; l < P; ++l) {
+      if (l == li) continue;
+      int lo = 0, hi = kp;  // entries of list l above me form a prefix
+      while (lo < hi) {
+        const int mid = (lo + hi) >> 1;
+        if (c[l * kp + mid] > me) lo = mid + 1;
+        else hi = mid;
+      }
+      r += lo;
+    }
+    if (r < k) {
+      out_ids[o + r] = (long long)comp_row(me);
+      out_scores[o + r] = __uint_as_float((uint32_t)(me >> 32));
+    }
+  }
+  for (int r = n_valid + tid; r < k; r += kNT) {
+    out_ids[o + r] = -1ll;
+    out_scores[o + r] = -__builtin_inff();
+  }
+}
+
 // Merge P partial lists of kp composites per query (raw positive-fp32 keys) into the top-k.
 __global__ __launch_bounds__(64) void partial_merge_kernel(const unsigned long long* partial, int P, int kp, int nq,
                                                            int k, float* out_scores, long long* out_ids) {
@@ -484,8 +535,12 @@ hipError_t launch_sparse(const SparseIndex& sp, const int* qterm_indptr, const i
   hipLaunchKernelGGL(bm25_kernel, dim3((unsigned)(nq * a.n_ranges)), dim3(kNT), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.n_ranges == 1) return e;
-  hipLaunchKernelGGL(partial_merge_kernel, dim3((unsigned)nq), dim3(64), 0, s, a.partial, a.n_ranges, k, nq, k,
-                     out_scores, out_ids);
+  if ((long long)a.n_ranges * k <= kMergeCap)
+    hipLaunchKernelGGL(partial_rank_kernel, dim3((unsigned)nq), dim3(kNT), 0, s, a.partial, a.n_ranges, k, nq, k,
+                       out_scores, out_ids);
+  else
+    hipLaunchKernelGGL(partial_merge_kernel, dim3((unsigned)nq), dim3(64), 0, s, a.partial, a.n_ranges, k, nq, k,
+                       out_scores, out_ids);
   return hipGetLastError();
 }
 

@@ -73,17 +73,19 @@ def test_bm25_parameters(k1, b):
     _check_sparse(B, ids, sc, 50, f"k1={k1} b={b}")
 
 
-def test_bm25_several_chunk_ranges():
-    """More chunks than one workgroup's LDS accumulator: per-range lists are merged."""
+@pytest.mark.parametrize("n_docs,k", [(70_001, 64), (140_001, 100)])
+def test_bm25_several_chunk_ranges(n_docs, k):
+    """More chunks than one workgroup's LDS accumulator: per-range lists are merged (9 x 64
+    composites per query fit the LDS ranking merge; 18 x 100 take the queue merge)."""
     dev = device()
-    ind, toks, csr, qi, qt = _small_corpus(700, 70001, 2000, 20.0, 30)
-    idx = make_index(torch.zeros((70001, 128), dtype=torch.bfloat16), "bf16")
+    ind, toks, csr, qi, qt = _small_corpus(700, n_docs, 2000, 20.0, 30)
+    idx = make_index(torch.zeros((n_docs, 128), dtype=torch.bfloat16), "bf16")
     _attach(idx, csr, dev)
-    sc, ids = idx.search_sparse(_t(qi, dev), _t(qt, dev), 64)
+    sc, ids = idx.search_sparse(_t(qi, dev), _t(qt, dev), k)
     torch.cuda.synchronize()
     qt_oracle = np.where((qt >= 0) & (qt < 2000), qt, 10 ** 6).astype(np.int64)
     B = bm25.scores_batch(ind, toks, qi, qt_oracle, 1.2, 0.75)
-    _check_sparse(B, ids, sc, 64, "multi-range")
+    _check_sparse(B, ids, sc, k, f"multi-range n_docs={n_docs}")
 
 
 def test_attach_rejects_malformed_csr():
