@@ -1288,7 +1288,12 @@ __global__ __launch_bounds__(kThreads) void dense_f32_kernel(DenseArgs a) {
 __global__ __launch_bounds__(kThreads) void select_topk_kernel(const unsigned long long* __restrict__ cbuf,
                                                                int* __restrict__ ccnt, long long cap, int k,
                                                                float* out_scores, long long* out_ids, int* overflow,
-                                                               const int* gate) {
+                                                               const int* gate, int threshold_only) {
+  constexpr int kCand = 1024;  // candidates the threshold path ranks directly
+  __shared__ u64 cand[kCand];
+  __shared__ u64 tmax[kThreads];
+  __shared__ u64 s_tau;
+  __shared__ int s_nc;
   __shared__ unsigned int hist[256];
   __shared__ int wtot[kWaves];
   __shared__ u64 sel[kMaxK];
@@ -1310,6 +1315,75 @@ __global__ __launch_bounds__(kThreads) void select_topk_kernel(const unsigned lo
   }
   __syncthreads();
   if (t == 0) ccnt[q] = 0;  // every thread has read it: the next pass starts from zero
+  // Threshold path: the keys are unique composites.  tau = the need-th largest of the thread
+  // maxima (lane-strided slices) bounds the need-th best key from below, and the keys >= tau
+  // (about 1-2 need) are ranked exactly.  Too many of them: the radix select below.
+  const int need = min(k, n);
+  if (need > 0) {
+    u64 m = 0ull;
+    for (int i = t; i < n; i += kThreads) m = umax64(m, src[i]);
+    tmax[t] = m;
+    if (t == 0) {
+      s_tau = 0ull;
+      s_nc = 0;
+    }
+    __syncthreads();
+    int gt = 0;
+#pragma unroll 8
+    for (int u = 0; u < kThreads; ++u) gt += tmax[u] > m ? 1 : 0;
+    if (m != 0ull && gt == need - 1) s_tau = m;  // nonzero maxima are unique; n >= need of them
+    __syncthreads();
+    const u64 tau = s_tau;
+    if (threshold_only) {
+      // An earlier level only hands its k-th score on as the next threshold, and tau is a
+      // valid one: at least k keys reach it (k <= n here, else the next level takes all rows).
+      if (t == 0) out_scores[(long long)q * k + (k - 1)] = need == k ? comp_score(tau) : kNegInf;
+      return;
+    }
+    int c = 0;
+    for (int i = t; i < n; i += kThreads) c += src[i] >= tau ? 1 : 0;
+    // exclusive scan of c over the workgroup
+    int x = c;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int y = __shfl_up(x, o, 64);
+      if (lane >= o) x += y;
+    }
+    if (lane == 63) wtot[w] = x;
+    __syncthreads();
+    int pos = x - c;
+    for (int i = 0; i < w; ++i) pos += wtot[i];
+    if (t == kThreads - 1) s_nc = pos + c;
+    if (pos + c <= kCand)
+      for (int i = t; i < n; i += kThreads) {
+        const u64 key = src[i];
+        if (key >= tau) cand[pos++] = key;
+      }
+    __syncthreads();
+    const int nc = s_nc;
+    if (nc <= kCand) {  // workgroup-uniform
+      for (int j = t; j < nc; j += kThreads) {
+        const u64 me = cand[j];
+        int r = 0;
+        for (int b = 0; b < nc; b += 8) {
+          u64 v[8];
+#pragma unroll
+          for (int u = 0; u < 8; ++u) v[u] = cand[min(b + u, nc - 1)];
+#pragma unroll
+          for (int u = 0; u < 8; ++u) r += (b + u < nc && v[u] > me) ? 1 : 0;
+        }
+        if (r < need) {
+          out_ids[(long long)q * k + r] = (long long)comp_row(me);
+          out_scores[(long long)q * k + r] = comp_score(me);
+        }
+      }
+      for (int r = need + t; r < k; r += kThreads) {
+        out_ids[(long long)q * k + r] = -1ll;
+        out_scores[(long long)q * k + r] = kNegInf;
+      }
+      return;
+    }
+  }
   for (int shift = 56; shift >= 0; shift -= 8) {
     if (s_done) break;  // block-uniform
     const u64 prefix = s_prefix, mask = s_mask;
@@ -1631,6 +1705,20 @@ DensePlan plan_dense(int dtype, int d, long long n_rows, int nq, int k) {
   }
   p.fcap = std::max(1ll, std::min(n_rows, std::max(kFilterFirst, 4 * kFilterGrow * (long long)k)));
   p.chunk_bound = chunk_bound(ki, d, n_rows, p.n_qblocks, nullptr);
+  p.kernel0 = p.kernel;
+  p.n_qblocks0 = p.n_qblocks;
+  p.chunk_bound0 = p.chunk_bound;
+  {
+    DensePlan l0 = p;
+    split_rows(l0, p.level_rows[0], p.chunk_bound, 1);
+    const int small = pick_kernel(dtype, d, 1, k, 2);
+    if (l0.grid < kNumCUs && small >= 0) {  // the main kernel would leave most CUs idle
+      const KernelInfo& ks = kKernels[small];
+      p.kernel0 = small;
+      p.n_qblocks0 = (nq + ks.bn - 1) / ks.bn;
+      p.chunk_bound0 = chunk_bound(ks, d, p.level_rows[0], p.n_qblocks0, nullptr);
+    }
+  }
   split_rows(p, n_rows, p.chunk_bound, 1);
   // the per-chunk-list plan is the exact fallback; the workspace covers it as well
   p.cap = plan_dense_lists(dtype, d, n_rows, nq, k).cap;
@@ -1671,18 +1759,23 @@ hipError_t launch_kernel(const KernelInfo& ki, long long grid, DenseArgs& arg, h
 
 // One filtered level: clear the counts, collect candidates, select.
 // One filter pass over rows [0, rows): candidates >= th (every row when th is null) into the
-// buffers, then the exact top-k of each buffer.  The first pass (th null) sets the counts;
+// buffers, then the exact top-k of each buffer (threshold_only: just a valid k-th score for
+// the next level).  The first pass (th null) sets the counts;
 // each selection zeroes its query's count for the next pass.  With a gate, nothing runs
 // unless *gate != 0.
 hipError_t filter_pass(const DensePlan& p, const DenseArgs& a, long long rows, const float* th, int* ovf,
-                       const int* gate, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
-  const KernelInfo& ki = kKernels[p.kernel];
+                       const int* gate, bool threshold_only, bool first, hipStream_t s, hipEvent_t ev0,
+                       hipEvent_t ev1) {
+  const KernelInfo& ki = kKernels[first ? p.kernel0 : p.kernel];
   unsigned long long* cbuf = a.partial;  // the workspace
   int* ccnt = reinterpret_cast<int*>(reinterpret_cast<unsigned char*>(cbuf) +
                                      align_up256((size_t)a.nq * (size_t)p.fcap * 8));
   DensePlan lp = p;
-  split_rows(lp, rows, p.chunk_bound, 1);
+  lp.tile_rows = ki.tile_rows;
+  lp.n_qblocks = first ? p.n_qblocks0 : p.n_qblocks;
+  split_rows(lp, rows, first ? p.chunk_bound0 : p.chunk_bound, 1);
   DenseArgs arg = a;
+  arg.n_qblocks = lp.n_qblocks;
   arg.n_rows = rows;
   arg.n_chunks = lp.n_chunks;
   arg.rows_per_chunk = lp.rows_per_chunk;
@@ -1695,7 +1788,7 @@ hipError_t filter_pass(const DensePlan& p, const DenseArgs& a, long long rows, c
   hipError_t e = launch_kernel(ki, lp.grid, arg, s, ev0, ev1);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(select_topk_kernel, dim3((unsigned)a.nq), dim3(kThreads), 0, s, cbuf, ccnt, p.fcap, a.k,
-                     a.out_scores, a.out_ids, ovf, gate);
+                     a.out_scores, a.out_ids, ovf, gate, threshold_only ? 1 : 0);
   return hipGetLastError();
 }
 
@@ -1709,9 +1802,9 @@ hipError_t launch_dense(const DensePlan& p, int dtype, const DenseArgs& a, hipSt
     hipLaunchKernelGGL(clear_ints_kernel, dim3(1), dim3(64), 0, s, fl, 4ll, nullptr);
     for (int l = 0; l < p.n_levels; ++l) {
       const bool last = l == p.n_levels - 1;
-      // level l's threshold: the k-th score of level l - 1's exact result
+      // level l's threshold: a lower bound of the k-th score over level l - 1's rows
       hipError_t e = filter_pass(p, a, p.level_rows[l], l == 0 ? nullptr : a.out_scores + (a.k - 1), fl + (last ? 0 : 1),
-                                 nullptr, s, last ? ev0 : nullptr, last ? ev1 : nullptr);
+                                 nullptr, !last, l == 0, s, last ? ev0 : nullptr, last ? ev1 : nullptr);
       if (e != hipSuccess) return e;
     }
     // Exactness repair, decided on the device: only a buffer overflow in the last level can
@@ -1719,7 +1812,8 @@ hipError_t launch_dense(const DensePlan& p, int dtype, const DenseArgs& a, hipSt
     // (the lists are the top-k of a subset of the rows at or above the old thresholds, so
     // their k-th scores are valid thresholds and no lower), and if that overflows too, the
     // per-chunk-list plan runs.  Each repair launch returns at once when its flag is clear.
-    hipError_t e = filter_pass(p, a, a.n_rows, a.out_scores + (a.k - 1), fl + 2, fl, s, nullptr, nullptr);
+    hipError_t e =
+        filter_pass(p, a, a.n_rows, a.out_scores + (a.k - 1), fl + 2, fl, false, false, s, nullptr, nullptr);
     if (e != hipSuccess) return e;
     const DensePlan lp = plan_dense_lists(dtype, a.d, a.n_rows, a.nq, a.k);
     DenseArgs la = a;

@@ -54,6 +54,11 @@ struct DensePlan {
   long long level_rows[8] = {};
   long long fcap = 0;           // candidate slots per query
   long long chunk_bound = 0;    // workgroups per query block the filter passes aim for
+  // The first level's kernel: a small-tile one when the main kernel would leave most CUs idle
+  // on the first level's few rows.
+  int kernel0 = 0;
+  int n_qblocks0 = 0;
+  long long chunk_bound0 = 0;
 };
 
 DensePlan plan_dense(int dtype, int d, long long n_rows, int nq, int k);
