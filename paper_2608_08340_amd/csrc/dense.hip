@@ -643,7 +643,8 @@ __device__ __forceinline__ bool reg_epilogue(const f32x4 (&acc)[MW][BN / 16], Se
 }
 
 // ------------------------------------------------------------------------------------
-// Selection against the running threshold (5 < k <= 16, every tile after a chunk's first).
+// Selection against the running threshold (k <= 16 except the larger k <= 5 kernels; every tile
+// after a chunk's first).
 // thr[n] holds the k-th best score of query slot n's running list (-inf while the list is
 // short, +inf past the batch); only a score reaching it can still enter the list.  A lane
 // first compares the maximum of its MW*4 scores of each query with the threshold, so a tile
@@ -1130,10 +1131,10 @@ __global__ __launch_bounds__(WV * 64) void dense_mfma_kernel(DenseArgs a) {
           filt_tile<BN, MW, WV>(acc, th, scratch, tile0, row_end, q0, a);
         done = true;
       } else if constexpr (SEL == 0) {
-        // k > 5: a chunk's first tile fills the lists through the group path, which leaves
-        // the running thresholds in place for the tiles after it.  (The k <= 5 kernels keep
-        // the block path for every tile: they already run close to the register limit.)
-        if constexpr (!kBlk)
+        // A chunk's first tile fills the lists through the group path, which leaves the
+        // running thresholds in place for the tiles after it.  (The larger k <= 5 kernels
+        // keep the block path for every tile: they already run close to the register limit.)
+        if constexpr (!kBlk || NW * MW <= 2)
           if (t > 0) done = thr_epilogue<BN, MW, WV>(acc, sel, scratch, tile0, row_end, q_lim, a.k);
         if (!done) {
           if constexpr (kBlk)
@@ -1171,7 +1172,7 @@ __global__ __launch_bounds__(WV * 64) void dense_mfma_kernel(DenseArgs a) {
           sel.pass(S, SR, RP, pr, q_lim, a.k, scratch);
         }
       }
-      if constexpr (SEL == 0 && !kBlk)
+      if constexpr (SEL == 0 && (!kBlk || NW * MW <= 2))
         if (refresh) thr_reset(sel, scratch, q_lim, a.k, BN);
     }
 #undef OPRAG_SUPER
@@ -1586,7 +1587,9 @@ __global__ __launch_bounds__(kThreads) void merge_large_kernel(const unsigned lo
 // ------------------------------------------------------------------------------------
 struct KernelInfo {
   void (*fn)(DenseArgs);
-  int dtype, bn, tile_rows, ks, sel, wgs_per_cu, min_nq, max_nq;
+  int dtype, bn, tile_rows, ks, sel;
+  int chunk_target;  // workgroups per CU the planner aims for (chunks x query blocks / CUs)
+  int min_nq, max_nq;
   int ring;     // MFMA kernels: k-steps per loop iteration, which must divide d / 32 (0: none)
   int threads;  // workgroup size
 };
@@ -1598,20 +1601,22 @@ struct KernelInfo {
 #define MF_KS(DT, NW, MW, RS, G, OCC, LO, HI)                                                   \
   MFK(DT, NW, MW, RS, G, 5, 0, OCC, LO, HI), MFK(DT, NW, MW, RS, G, 8, 0, OCC, LO, HI),          \
       MFK(DT, NW, MW, RS, G, 16, 0, OCC, LO, HI)
+// The single-query-block kernels aim for one workgroup per CU: two 64-row tiles each, so the
+// ring streams across a tile boundary and the second tile takes the running-threshold path.
 #define MF_SET(DT)                                                                              \
-  MF_KS(DT, 1, 1, 16, 1, 4, 1, 16), MF_KS(DT, 1, 1, 4, 1, 4, 1, 16), MF_KS(DT, 4, 2, 8, 1, 2, 17, 64), \
-      MF_KS(DT, 4, 2, 4, 1, 2, 17, 64), MFK(DT, 8, 4, 4, 2, 5, 0, 1, 65, 1 << 30),                \
-      MFK(DT, 8, 4, 4, 4, 8, 0, 1, 65, 1 << 30), MFK(DT, 8, 4, 4, 4, 16, 0, 1, 65, 1 << 30),         \
-      MFK(DT, 2, 4, 8, 1, 8, 1, 2, 1, 1 << 30), MFK(DT, 2, 4, 4, 1, 8, 1, 2, 1, 1 << 30),            \
-      MFK(DT, 1, 1, 16, 1, 5, 2, 4, 1, 16), MFK(DT, 1, 1, 4, 1, 5, 2, 4, 1, 16),                     \
-      MFK(DT, 4, 2, 8, 1, 5, 2, 2, 17, 64), MFK(DT, 4, 2, 4, 1, 5, 2, 2, 17, 64),                    \
-      MFK(DT, 8, 4, 4, 1, 5, 2, 1, 65, 1 << 30)
+  MF_KS(DT, 1, 1, 16, 1, 1, 1, 16), MF_KS(DT, 1, 1, 4, 1, 1, 1, 16), MF_KS(DT, 4, 2, 8, 1, 4, 17, 64), \
+      MF_KS(DT, 4, 2, 4, 1, 4, 17, 64), MFK(DT, 8, 4, 4, 2, 5, 0, 2, 65, 1 << 30),                \
+      MFK(DT, 8, 4, 4, 4, 8, 0, 2, 65, 1 << 30), MFK(DT, 8, 4, 4, 4, 16, 0, 2, 65, 1 << 30),         \
+      MFK(DT, 2, 4, 8, 1, 8, 1, 4, 1, 1 << 30), MFK(DT, 2, 4, 4, 1, 8, 1, 4, 1, 1 << 30),            \
+      MFK(DT, 1, 1, 16, 1, 5, 2, 8, 1, 16), MFK(DT, 1, 1, 4, 1, 5, 2, 8, 1, 16),                     \
+      MFK(DT, 4, 2, 8, 1, 5, 2, 4, 17, 64), MFK(DT, 4, 2, 4, 1, 5, 2, 4, 17, 64),                    \
+      MFK(DT, 8, 4, 4, 1, 5, 2, 2, 65, 1 << 30)
 
 const KernelInfo kKernels[] = {
-    {dense_f32_kernel<5, 0>, kDtypeF32, 32, 64, 5, 0, 2, 1, 1 << 30, 0, kThreads},
-    {dense_f32_kernel<8, 0>, kDtypeF32, 32, 64, 8, 0, 2, 1, 1 << 30, 0, kThreads},
-    {dense_f32_kernel<16, 0>, kDtypeF32, 32, 64, 16, 0, 2, 1, 1 << 30, 0, kThreads},
-    {dense_f32_kernel<8, 1>, kDtypeF32, 32, 64, 128, 1, 2, 1, 1 << 30, 0, kThreads},
+    {dense_f32_kernel<5, 0>, kDtypeF32, 32, 64, 5, 0, 4, 1, 1 << 30, 0, kThreads},
+    {dense_f32_kernel<8, 0>, kDtypeF32, 32, 64, 8, 0, 4, 1, 1 << 30, 0, kThreads},
+    {dense_f32_kernel<16, 0>, kDtypeF32, 32, 64, 16, 0, 4, 1, 1 << 30, 0, kThreads},
+    {dense_f32_kernel<8, 1>, kDtypeF32, 32, 64, 128, 1, 4, 1, 1 << 30, 0, kThreads},
     MF_SET(kDtypeBF16),
     MF_SET(kDtypeF16),
 };
@@ -1637,7 +1642,7 @@ constexpr long long kFilterGrow = 64;     // row growth from one level to the ne
 // Workgroups per query block that fill the chip twice over (at least enough to keep every
 // chunk of a ring kernel under 2^30 bytes of rows, the reach of its 32-bit offsets).
 long long chunk_bound(const KernelInfo& ki, int d, long long n_rows, int n_qblocks, long long* min_chunks) {
-  const long long target = (long long)kNumCUs * ki.wgs_per_cu * 2;
+  const long long target = (long long)kNumCUs * ki.chunk_target;
   long long bound = std::max(1ll, (target + n_qblocks - 1) / n_qblocks);
   long long mc = 1;
   if (ki.ring) {
