@@ -517,7 +517,7 @@ __device__ __forceinline__ void filt_all_tile(const f32x4 (&acc)[MW][BN / 16], l
 // acc[mi][ni][r] = score of row tile0 + 16*MW*wave + 16*mi + 4*(lane/16) + r against query
 // slot 16*ni + lane%16; th[ni] its threshold (+inf for slots past the batch).  One barrier;
 // then the owner of a stage at least half full flushes it.  The stage is next written in the
-// following tile's selection, after the barriers of its super-steps.
+// following tile's selection, after a barrier inside that tile's main loop.
 template <int BN, int MW, int WV>
 __device__ __forceinline__ void filt_tile(const f32x4 (&acc)[MW][BN / 16], const float (&th)[BN / 16],
                                           unsigned char* area, long long tile0, long long row_end, int q0,
@@ -778,14 +778,11 @@ __device__ __forceinline__ bool blk_epilogue(const f32x4 (&acc)[MW][BN / 16], Se
   constexpr int NW = BN / 16;
   constexpr int KS = 5;
   constexpr int NG = WV * 4;              // groups (lanes) per query
-  constexpr int TPQ = WV * 64 / BN;       // threads per query in the gathering step
   using B = BlockArea<MW, BN>;
   constexpr int SLOTS = B::SLOTS, VALS = B::VALS, QSTR = B::QSTR;
-  constexpr int CAP = Sel::CAP;
   float* blk = reinterpret_cast<float*>(area);                      // [BN][QSTR]: SLOTS x VALS
   unsigned* gmask = reinterpret_cast<unsigned*>(area + BN * QSTR * 4);  // [BN] active groups
-  float* gmax = reinterpret_cast<float*>(Sel::cand_of(scratch));    // [NG][BN], then
-  uint2* cand = reinterpret_cast<uint2*>(Sel::cand_of(scratch));    // [BN][CAP] (score, row offset)
+  float* gmax = reinterpret_cast<float*>(Sel::cand_of(scratch));    // [NG][BN]
   float* thr = Sel::tau_of(scratch);
   int* cnt = Sel::cnt_of(scratch);
   int* flag = Sel::flag_of(scratch);
@@ -852,70 +849,26 @@ __device__ __forceinline__ bool blk_epilogue(const f32x4 (&acc)[MW][BN / 16], Se
     }
   }
   lds_barrier();
-  // 4. TPQ threads per query gather the scores >= tau of its blocks into a short list
-  int over = 0;
-  {
-    const int q = tid % BN, sub = tid / BN;
-    if (q < q_lim) {
-      const float tau = thr[q];
-      const unsigned mask = gmask[q];
-      // this thread's blocks are the ranks sub, sub + TPQ, ...: count, reserve, write
-      int c = 0;
-      int rank = 0;
-      for (unsigned mm = mask; mm; mm &= mm - 1, ++rank) {
-        if (rank % TPQ != sub) continue;
-        const float* src = blk + q * QSTR + rank * VALS;
-#pragma unroll
-        for (int mi = 0; mi < MW; ++mi) {
-          const f32x4 v = *reinterpret_cast<const f32x4*>(src + mi * 4);
-#pragma unroll
-          for (int r = 0; r < 4; ++r) c += (v[r] >= tau && v[r] > kNegInf) ? 1 : 0;
-        }
-      }
-      if (c) {
-        int j = atomicAdd(&cnt[q], c);
-        if (j + c > CAP) {
-          over = 1;
-        } else {
-          rank = 0;
-          for (unsigned mm = mask; mm; mm &= mm - 1, ++rank) {
-            if (rank % TPQ != sub) continue;
-            const int gg = __builtin_ctz(mm);
-            const int r0 = (gg >> 2) * MW * 16 + (gg & 3) * 4;
-            const float* src = blk + q * QSTR + rank * VALS;
-#pragma unroll
-            for (int mi = 0; mi < MW; ++mi) {
-              const f32x4 v = *reinterpret_cast<const f32x4*>(src + mi * 4);
-#pragma unroll
-              for (int r = 0; r < 4; ++r)
-                if (v[r] >= tau && v[r] > kNegInf)
-                  cand[q * CAP + j++] = make_uint2(__float_as_uint(v[r]), (unsigned)(r0 + mi * 16 + r));
-            }
-          }
-        }
-      }
-    }
-  }
-  if (over) *flag = 1;
-  lds_barrier();
-  // 5. owners insert the list (or, after an overflow, every score >= tau of the blocks)
+  // 4. the owner takes the scores >= tau of its query's blocks: a mask of the hits of a block
+  // (one per active group, so usually a single bit), then one insertion per set bit with the
+  // score re-read at its offset
   if (tid < q_lim) {
-    if (!*flag) {
-      const int m = cnt[tid];
-      for (int j = 0; j < m; ++j) {
-        const uint2 e = cand[tid * CAP + j];
-        sel.run.insert(composite(__uint_as_float(e.x), (uint32_t)(tile0 + e.y)));
+    const float tau = thr[tid];
+    int rank = 0;
+    for (unsigned mm = gmask[tid]; mm; mm &= mm - 1, ++rank) {
+      const int gg = __builtin_ctz(mm);
+      const long long r0 = tile0 + (gg >> 2) * MW * 16 + (gg & 3) * 4;
+      const float* src = blk + tid * QSTR + rank * VALS;
+      unsigned hm = 0;
+#pragma unroll
+      for (int mi = 0; mi < MW; ++mi) {
+        const f32x4 v = *reinterpret_cast<const f32x4*>(src + mi * 4);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) hm |= (v[r] >= tau && v[r] > kNegInf) ? 1u << (mi * 4 + r) : 0u;
       }
-    } else {
-      const float tau = thr[tid];
-      int rank = 0;
-      for (unsigned mm = gmask[tid]; mm; mm &= mm - 1, ++rank) {
-        const int gg = __builtin_ctz(mm);
-        const long long r0 = tile0 + (gg >> 2) * MW * 16 + (gg & 3) * 4;
-        const float* src = blk + tid * QSTR + rank * VALS;
-        for (int p = 0; p < VALS; ++p)
-          if (src[p] >= tau && src[p] > kNegInf)
-            sel.run.insert(composite(src[p], (uint32_t)(r0 + (p >> 2) * 16 + (p & 3))));
+      for (; hm; hm &= hm - 1) {
+        const int pp = __builtin_ctz(hm);
+        sel.run.insert(composite(src[pp], (uint32_t)(r0 + (pp >> 2) * 16 + (pp & 3))));
       }
     }
   }
@@ -938,7 +891,7 @@ __device__ __forceinline__ bool blk_epilogue(const f32x4 (&acc)[MW][BN / 16], Se
 //    epilogue (or, when it declines, G passes through an LDS score tile) updates the
 //    running top-k of each query.
 // ------------------------------------------------------------------------------------
-template <int DT, int NW, int MW, int RS, int G, int KS, int SEL, int WV>
+template <int DT, int NW, int MW, int RS, int G, int KS, int SEL, int WV, int QR>
 __global__ __launch_bounds__(WV * 64) void dense_mfma_kernel(DenseArgs a) {
   if (a.gate != nullptr && *a.gate == 0) return;  // a repair launch with nothing to repair
   using M = Mfma<DT>;
@@ -959,7 +912,11 @@ __global__ __launch_bounds__(WV * 64) void dense_mfma_kernel(DenseArgs a) {
   constexpr int RP = WV * MWP * 16;             // rows per fallback pass
   constexpr int SR = RP + 4;                    // S row stride (floats)
   using Sel = typename SelOf<BN, KS, SEL, NT>::type;
-  constexpr int QBYTES = 2 * QSLOT;
+  // QR > 0: all d / 128 <= QR super-steps of the block's queries stay resident in LDS (loaded
+  // once), so the main loop has no query staging and no barrier.  Otherwise two slots
+  // alternate, one super-step ahead.
+  constexpr int QBYTES = (QR > 0 ? QR : 2) * QSLOT;
+  static_assert(QR == 0 || SEL == 2, "resident queries: filtered selection only");
   constexpr bool kBlk = SEL == 0 && KS == 5;
   constexpr int SB0 = SEL == 2 ? 0 : BN * SR * 4;
   constexpr int SBYTES = kBlk && BlockArea<MW, BN>::kBytes > SB0 ? BlockArea<MW, BN>::kBytes : SB0;
@@ -1078,29 +1035,54 @@ __global__ __launch_bounds__(WV * 64) void dense_mfma_kernel(DenseArgs a) {
   }
 #define OPRAG_SUPER(H)                                                                   \
   {                                                                                      \
-    const int sup = s0 / 4 + (H);                                                        \
-    unsigned char* qs = qslots + (sup & 1) * QSLOT;                                      \
-    unsigned char* qn = qslots + ((sup + 1) & 1) * QSLOT;                                \
-    OPRAG_KSTEP(4 * (H) + 0, 0, qs)                                                      \
-    OPRAG_KSTEP(4 * (H) + 1, 1, qs)                                                      \
-    OPRAG_KSTEP(4 * (H) + 2, 2, qs)                                                      \
-    OPRAG_KSTEP(4 * (H) + 3, 3, qs)                                                      \
-    _Pragma("unroll") for (int j = 0; j < QPT; ++j)                                      \
-        *reinterpret_cast<u32x4*>(qn + qdst[j]) = qr[j];                                 \
-    OPRAG_QUERIES()                                                                      \
-    lds_barrier();                                                                       \
-    OPRAG_BFRAG(qn, 0)                                                                   \
+    if constexpr (QR > 0) {                                                              \
+      unsigned char* qs = qslots + qsi * QSLOT;                                          \
+      qsi = qsi + 1 == nq4 ? 0 : qsi + 1;                                                \
+      unsigned char* qn = qslots + qsi * QSLOT;                                          \
+      OPRAG_KSTEP(4 * (H) + 0, 0, qs)                                                    \
+      OPRAG_KSTEP(4 * (H) + 1, 1, qs)                                                    \
+      OPRAG_KSTEP(4 * (H) + 2, 2, qs)                                                    \
+      OPRAG_KSTEP(4 * (H) + 3, 3, qs)                                                    \
+      if ((H) == 0 && s0 == t * nk) lds_barrier(); /* previous tile's stage flushes done */ \
+      OPRAG_BFRAG(qn, 0)                                                                 \
+    } else {                                                                             \
+      const int sup = s0 / 4 + (H);                                                      \
+      unsigned char* qs = qslots + (sup & 1) * QSLOT;                                    \
+      unsigned char* qn = qslots + ((sup + 1) & 1) * QSLOT;                              \
+      OPRAG_KSTEP(4 * (H) + 0, 0, qs)                                                    \
+      OPRAG_KSTEP(4 * (H) + 1, 1, qs)                                                    \
+      OPRAG_KSTEP(4 * (H) + 2, 2, qs)                                                    \
+      OPRAG_KSTEP(4 * (H) + 3, 3, qs)                                                    \
+      _Pragma("unroll") for (int j = 0; j < QPT; ++j)                                    \
+          *reinterpret_cast<u32x4*>(qn + qdst[j]) = qr[j];                               \
+      OPRAG_QUERIES()                                                                    \
+      lds_barrier();                                                                     \
+      OPRAG_BFRAG(qn, 0)                                                                 \
+    }                                                                                    \
   }
 
-    // prologue: queries of super-step 0 first (their wait then leaves the row loads in
-    // flight), rows of k-steps 0 .. PX-1, queries of super-step 0 to slot 0, queries of
-    // super-step 1
-    OPRAG_QUERIES()
+    int qsi = 0;  // resident queries: slot of the current super-step
+    if constexpr (QR > 0) {
+      // prologue: every super-step of the queries into its own slot, then rows of k-steps
+      // 0 .. PX-1
+      for (int u = 0; u < nq4; ++u) {
+        OPRAG_QUERIES()
 #pragma unroll
-    for (int u = 0; u < PX; ++u) OPRAG_ROWS(u)
+        for (int j = 0; j < QPT; ++j) *reinterpret_cast<u32x4*>(qslots + u * QSLOT + qdst[j]) = qr[j];
+      }
 #pragma unroll
-    for (int j = 0; j < QPT; ++j) *reinterpret_cast<u32x4*>(qslots + qdst[j]) = qr[j];
-    OPRAG_QUERIES()
+      for (int u = 0; u < PX; ++u) OPRAG_ROWS(u)
+    } else {
+      // prologue: queries of super-step 0 first (their wait then leaves the row loads in
+      // flight), rows of k-steps 0 .. PX-1, queries of super-step 0 to slot 0, queries of
+      // super-step 1
+      OPRAG_QUERIES()
+#pragma unroll
+      for (int u = 0; u < PX; ++u) OPRAG_ROWS(u)
+#pragma unroll
+      for (int j = 0; j < QPT; ++j) *reinterpret_cast<u32x4*>(qslots + qdst[j]) = qr[j];
+      OPRAG_QUERIES()
+    }
     lds_barrier();
     OPRAG_BFRAG(qslots, 0)
 
@@ -1592,10 +1574,13 @@ struct KernelInfo {
   int min_nq, max_nq;
   int ring;     // MFMA kernels: k-steps per loop iteration, which must divide d / 32 (0: none)
   int threads;  // workgroup size
+  int qres;     // resident query super-steps (0: streamed); the kernel serves d / 128 <= qres
 };
 
-#define MFKW(DT, NW, MW, RS, G, KS, SEL, OCC, LO, HI, WV) \
-  {dense_mfma_kernel<DT, NW, MW, RS, G, KS, SEL, WV>, DT, NW * 16, WV * MW * 16, KS, SEL, OCC, LO, HI, RS, WV * 64}
+#define MFKQ(DT, NW, MW, RS, G, KS, SEL, OCC, LO, HI, WV, QR)                                              \
+  {dense_mfma_kernel<DT, NW, MW, RS, G, KS, SEL, WV, QR>, DT, NW * 16, WV * MW * 16, KS, SEL, OCC, LO, HI, RS, \
+   WV * 64, QR}
+#define MFKW(DT, NW, MW, RS, G, KS, SEL, OCC, LO, HI, WV) MFKQ(DT, NW, MW, RS, G, KS, SEL, OCC, LO, HI, WV, 0)
 #define MFK(DT, NW, MW, RS, G, KS, SEL, OCC, LO, HI) MFKW(DT, NW, MW, RS, G, KS, SEL, OCC, LO, HI, kWaves)
 // Deep rings first; the 4-deep variants serve dimensions that are not multiples of the ring.
 #define MF_KS(DT, NW, MW, RS, G, OCC, LO, HI)                                                   \
@@ -1610,13 +1595,13 @@ struct KernelInfo {
       MFK(DT, 2, 4, 8, 1, 8, 1, 4, 1, 1 << 30), MFK(DT, 2, 4, 4, 1, 8, 1, 4, 1, 1 << 30),            \
       MFK(DT, 1, 1, 16, 1, 5, 2, 8, 1, 16), MFK(DT, 1, 1, 4, 1, 5, 2, 8, 1, 16),                     \
       MFK(DT, 4, 2, 8, 1, 5, 2, 4, 17, 64), MFK(DT, 4, 2, 4, 1, 5, 2, 4, 17, 64),                    \
-      MFK(DT, 8, 4, 4, 1, 5, 2, 2, 65, 1 << 30)
+      MFKQ(DT, 8, 4, 4, 1, 5, 2, 2, 65, 1 << 30, kWaves, 3), MFK(DT, 8, 4, 4, 1, 5, 2, 2, 65, 1 << 30)
 
 const KernelInfo kKernels[] = {
-    {dense_f32_kernel<5, 0>, kDtypeF32, 32, 64, 5, 0, 4, 1, 1 << 30, 0, kThreads},
-    {dense_f32_kernel<8, 0>, kDtypeF32, 32, 64, 8, 0, 4, 1, 1 << 30, 0, kThreads},
-    {dense_f32_kernel<16, 0>, kDtypeF32, 32, 64, 16, 0, 4, 1, 1 << 30, 0, kThreads},
-    {dense_f32_kernel<8, 1>, kDtypeF32, 32, 64, 128, 1, 4, 1, 1 << 30, 0, kThreads},
+    {dense_f32_kernel<5, 0>, kDtypeF32, 32, 64, 5, 0, 4, 1, 1 << 30, 0, kThreads, 0},
+    {dense_f32_kernel<8, 0>, kDtypeF32, 32, 64, 8, 0, 4, 1, 1 << 30, 0, kThreads, 0},
+    {dense_f32_kernel<16, 0>, kDtypeF32, 32, 64, 16, 0, 4, 1, 1 << 30, 0, kThreads, 0},
+    {dense_f32_kernel<8, 1>, kDtypeF32, 32, 64, 128, 1, 4, 1, 1 << 30, 0, kThreads, 0},
     MF_SET(kDtypeBF16),
     MF_SET(kDtypeF16),
 };
@@ -1630,6 +1615,7 @@ int pick_kernel(int dtype, int d, int nq, int k, int sel) {
     if (sel == 0 && ki.ks != ks) continue;
     if (nq < ki.min_nq || nq > ki.max_nq) continue;
     if (ki.ring && (d / 32) % ki.ring != 0) continue;
+    if (ki.qres && d / 128 > ki.qres) continue;
     return i;
   }
   return -1;
