@@ -1622,8 +1622,10 @@ int pick_kernel(int dtype, int d, int nq, int k, int sel) {
 }
 
 constexpr int kNumCUs = 256;
-constexpr long long kFilterFirst = 4096;  // rows of the first filtered level
-constexpr long long kFilterGrow = 64;     // row growth from one level to the next
+constexpr long long kFilterMin = 2048;        // fewest rows of a level that has a successor
+constexpr long long kFilterFirstMax = 16384;  // most rows of the first level
+constexpr long long kFilterLast = 16;         // row growth into the last level
+constexpr long long kFilterGrow = 64;         // row growth between earlier levels
 
 // Workgroups per query block that fill the chip twice over (at least enough to keep every
 // chunk of a ring kernel under 2^30 bytes of rows, the reach of its 32-bit offsets).
@@ -1684,17 +1686,29 @@ DensePlan plan_dense(int dtype, int d, long long n_rows, int nq, int k) {
   p.bn = ki.bn;
   p.tile_rows = ki.tile_rows;
   p.n_qblocks = (nq + p.bn - 1) / p.bn;
-  // Levels: the first kFilterFirst rows with every score a candidate, then prefixes growing
-  // kFilterGrow-fold, each filtered by the previous level's k-th score, then all rows.  A
-  // level then expects about k * kFilterGrow candidates per query; fcap allows four times that.
-  long long r = std::min(n_rows, kFilterFirst);
-  p.n_levels = 0;
-  p.level_rows[p.n_levels++] = r;
-  while (r < n_rows && p.n_levels < 8) {
-    r = (r * kFilterGrow >= n_rows || p.n_levels == 7) ? n_rows : r * kFilterGrow;
-    p.level_rows[p.n_levels++] = r;
+  // Levels: row prefixes, each filtered by the previous level's k-th score; the first takes
+  // every score as a candidate, the last is all rows.  Built from the end: the level before
+  // the last holds n_rows / kFilterLast rows (the last level, the one that streams the whole
+  // index, then admits about k * kFilterLast rows per query), earlier ones shrink
+  // kFilterGrow-fold (to no fewer than kFilterMin rows) until the first has at most
+  // kFilterFirstMax.  A level expects at most about k * kFilterGrow candidates per query; fcap
+  // allows four times that, and the whole first level.
+  long long back[8];
+  int nb = 0;
+  back[nb++] = n_rows;
+  {
+    long long r = std::max(kFilterMin, (n_rows + kFilterLast - 1) / kFilterLast);
+    if (4 * r <= n_rows) {  // else one level over all rows costs less
+      back[nb++] = r;
+      while (nb < 8 && r > kFilterFirstMax) {
+        r = std::max(kFilterMin, (r + kFilterGrow - 1) / kFilterGrow);
+        back[nb++] = r;
+      }
+    }
   }
-  p.fcap = std::max(1ll, std::min(n_rows, std::max(kFilterFirst, 4 * kFilterGrow * (long long)k)));
+  p.n_levels = nb;
+  for (int l = 0; l < nb; ++l) p.level_rows[l] = back[nb - 1 - l];
+  p.fcap = std::max(1ll, std::min(n_rows, std::max(p.level_rows[0], 4 * kFilterGrow * (long long)k)));
   p.chunk_bound = chunk_bound(ki, d, n_rows, p.n_qblocks, nullptr);
   p.kernel0 = p.kernel;
   p.n_qblocks0 = p.n_qblocks;

@@ -69,7 +69,8 @@ def test_exact_integer_scores_and_ties(dtype, k):
 
 @pytest.mark.parametrize("dtype", ["bf16", "f16"])
 @pytest.mark.parametrize("n,nq,k", [(3000, 1, 7), (3000, 17, 8), (3000, 65, 9), (2500, 130, 16), (3000, 40, 17),
-                                    (4100, 33, 64), (5000, 70, 100), (3000, 9, 128), (64, 5, 100), (1, 3, 4)])
+                                    (4100, 33, 64), (5000, 70, 100), (3000, 9, 128), (64, 5, 100), (1, 3, 4),
+                                    (9000, 21, 40), (20000, 130, 128)])
 def test_ragged_sizes_and_k(dtype, n, nq, k):
     """Row counts that are not tile multiples, query counts that are not block multiples, k across
     both selection strategies, k larger than the index (padding)."""

@@ -178,3 +178,39 @@ def test_hybrid_32k_bm25_rrf_top5(c3, correlated):
     assert same.mean() > 0.2
     assert np.array_equal(fids.cpu().numpy()[same], o_ids[same])
     log("queries whose stage lists equal the oracle's exactly:", int(same.sum()), "of", len(same))
+
+
+@pytest.mark.timeout(300)
+def test_hybrid_other_stream_and_graph_replay(c3):
+    """A hybrid search (threshold levels with device-side repair gates, BM25, RRF) issued on a
+    non-default stream, and captured in a HIP graph replayed three times (outputs cleared and
+    other searches run in between), equals the eager result bit for bit."""
+    dev = device()
+    h = c3
+    w = h.dense
+    idx = make_index(w.rows, "bf16")
+    _attach(idx, h.csr, dev, h.k1, h.b)
+    q = w.queries.to(dev)
+    qi, qt = _t(h.qterm_indptr, dev), _t(h.qterms, dev)
+    ref_f, ref_i = idx.search_hybrid(q, qi, qt, 100, 100, 60, 5)
+    torch.cuda.synchronize()
+    log("hybrid on another stream")
+    s = torch.cuda.Stream(device=dev)
+    s.wait_stream(torch.cuda.current_stream(dev))
+    with torch.cuda.stream(s):
+        f2, i2 = idx.search_hybrid(q, qi, qt, 100, 100, 60, 5)
+    s.synchronize()
+    assert torch.equal(i2, ref_i) and torch.equal(f2.view(torch.int32), ref_f.view(torch.int32))
+    log("hybrid captured in a graph")
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        fg, ig = idx.search_hybrid(q, qi, qt, 100, 100, 60, 5)
+    torch.cuda.synchronize()
+    for rep in range(3):
+        fg.fill_(-1.0)
+        ig.fill_(-2)
+        g.replay()
+        idx.search_dense(q[:7], 5)  # eager work between replays
+        torch.cuda.synchronize()
+        assert torch.equal(ig, ref_i), f"replay {rep}"
+        assert torch.equal(fg.view(torch.int32), ref_f.view(torch.int32)), f"replay {rep}"
