@@ -96,8 +96,7 @@ size_t align_up(size_t x) { return (x + 255) & ~size_t(255); }
 
 size_t dense_ws(const oprag_index* idx, int64_t nq, int32_t k) {
   const int nql = (int)std::min<int64_t>(nq, kMaxQPerLaunch);
-  const oprag::DensePlan p = oprag::plan_dense(idx->dtype, idx->dim, idx->capacity, nql, k);
-  return oprag::dense_workspace_bytes(p, nql);
+  return oprag::dense_workspace_bound(idx->dtype, idx->dim, idx->capacity, nql, k);
 }
 
 size_t sparse_ws(const oprag_index* idx, int64_t nq, int32_t k) {

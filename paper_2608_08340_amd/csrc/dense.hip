@@ -1623,9 +1623,10 @@ int pick_kernel(int dtype, int d, int nq, int k, int sel) {
 
 constexpr int kNumCUs = 256;
 constexpr long long kFilterMin = 2048;        // fewest rows of a level that has a successor
-constexpr long long kFilterFirstMax = 16384;  // most rows of the first level
+constexpr long long kFilterFirstMax = 4096;   // most rows of the first level
 constexpr long long kFilterLast = 16;         // row growth into the last level
 constexpr long long kFilterGrow = 64;         // row growth between earlier levels
+constexpr long long kFilterAllRows = 32768;   // up to this many rows a buffer holds every row
 
 // Workgroups per query block that fill the chip twice over (at least enough to keep every
 // chunk of a ring kernel under 2^30 bytes of rows, the reach of its 32-bit offsets).
@@ -1692,7 +1693,9 @@ DensePlan plan_dense(int dtype, int d, long long n_rows, int nq, int k) {
   // index, then admits about k * kFilterLast rows per query), earlier ones shrink
   // kFilterGrow-fold (to no fewer than kFilterMin rows) until the first has at most
   // kFilterFirstMax.  A level expects at most about k * kFilterGrow candidates per query; fcap
-  // allows four times that, and the whole first level.
+  // allows four times that, and the whole first level.  Up to kFilterAllRows rows a buffer
+  // holds every row (at most 256 KB per query), so no level can overflow and the repair
+  // launches are left out.
   long long back[8];
   int nb = 0;
   back[nb++] = n_rows;
@@ -1708,7 +1711,10 @@ DensePlan plan_dense(int dtype, int d, long long n_rows, int nq, int k) {
   }
   p.n_levels = nb;
   for (int l = 0; l < nb; ++l) p.level_rows[l] = back[nb - 1 - l];
-  p.fcap = std::max(1ll, std::min(n_rows, std::max(p.level_rows[0], 4 * kFilterGrow * (long long)k)));
+  p.fcap = n_rows <= kFilterAllRows
+               ? std::max(1ll, n_rows)
+               : std::max(1ll, std::min(n_rows, std::max(p.level_rows[0], 4 * kFilterGrow * (long long)k)));
+  p.repair = p.fcap < n_rows;
   p.chunk_bound = chunk_bound(ki, d, n_rows, p.n_qblocks, nullptr);
   p.kernel0 = p.kernel;
   p.n_qblocks0 = p.n_qblocks;
@@ -1747,6 +1753,15 @@ int* dense_flags(const DensePlan& p, void* ws, int nq) {
 size_t dense_workspace_bytes(const DensePlan& p, int nq) {
   if (!p.filtered) return (size_t)nq * (size_t)p.cap * sizeof(unsigned long long);
   return filtered_body_bytes(p, nq) + 256;
+}
+
+// The plan's workspace grows with the row count except where buffers stop holding every row
+// (fcap drops from kFilterAllRows to max(kFilterFirstMax, 256 k)), so the bound over all row
+// counts up to `capacity` is the larger of the two plans on either side.
+size_t dense_workspace_bound(int dtype, int d, long long capacity, int nq, int k) {
+  size_t b = dense_workspace_bytes(plan_dense(dtype, d, capacity, nq, k), nq);
+  if (capacity > kFilterAllRows) b = std::max(b, dense_workspace_bytes(plan_dense(dtype, d, kFilterAllRows, nq, k), nq));
+  return b;
 }
 
 namespace {
@@ -1812,6 +1827,7 @@ hipError_t launch_dense(const DensePlan& p, int dtype, const DenseArgs& a, hipSt
                                  nullptr, !last, l == 0, s, last ? ev0 : nullptr, last ? ev1 : nullptr);
       if (e != hipSuccess) return e;
     }
+    if (!p.repair) return hipGetLastError();  // every buffer holds all rows: nothing can overflow
     // Exactness repair, decided on the device: only a buffer overflow in the last level can
     // lose a row.  Then the last level runs again with the current k-th scores as thresholds
     // (the lists are the top-k of a subset of the rows at or above the old thresholds, so

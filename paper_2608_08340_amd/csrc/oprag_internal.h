@@ -53,6 +53,7 @@ struct DensePlan {
   int n_levels = 0;
   long long level_rows[8] = {};
   long long fcap = 0;           // candidate slots per query
+  bool repair = false;          // a level can overflow fcap: enqueue the device-gated repair
   long long chunk_bound = 0;    // workgroups per query block the filter passes aim for
   // The first level's kernel: a small-tile one when the main kernel would leave most CUs idle
   // on the first level's few rows.
@@ -65,6 +66,8 @@ DensePlan plan_dense(int dtype, int d, long long n_rows, int nq, int k);
 // The per-chunk-list plan for any k (the exact fallback of the filtered mode).
 DensePlan plan_dense_lists(int dtype, int d, long long n_rows, int nq, int k);
 size_t dense_workspace_bytes(const DensePlan& p, int nq);
+// Enough workspace for a search of nq queries at any row count up to `capacity`.
+size_t dense_workspace_bound(int dtype, int d, long long capacity, int nq, int k);
 // ev0 / ev1 (optional) are recorded on s right before and after the scoring kernel (in
 // filtered mode, the last level's).  Filtered mode also enqueues its exactness repair:
 // launches gated on device-side overflow flags, so the search never waits for the host.

@@ -161,6 +161,31 @@ def test_filtered_overflow_repair(case, nq):
     assert np.array_equal(sc.numpy().astype(np.float64), ref_sc)
 
 
+@pytest.mark.parametrize("k", [17, 100])
+def test_workspace_sized_from_capacity_covers_every_row_count(k):
+    """The workspace size a search reports depends on the capacity only.  Filtered searches
+    keep every row in their buffers up to 32,768 rows (no repair launches) and switch to
+    max(4,096, 256 k) slots per query above, so a workspace sized for a 60,000-row capacity
+    must still cover 32,768 rows: the index grows through both regimes with one workspace."""
+    dev = device()
+    from paper_2608_08340_amd import OP_DENSE
+    cap, d, nq = 60_000, 128, 40
+    w = synth.mixture_dense(900 + k, cap, d, 32, nq, k, "bf16")
+    idx = make_index(w.rows[:0], "bf16", capacity=cap)
+    need = idx.workspace_bytes(OP_DENSE, nq, k)
+    ws = idx.workspace(OP_DENSE, nq, k)
+    assert ws.numel() == need
+    done = 0
+    for n in (5_000, 32_768, 40_000, 60_000):
+        idx.upsert(w.rows[done:n].to(dev))
+        done = n
+        log("capacity workspace", k, n)
+        sc, ids = idx.search_dense(w.queries.to(dev), k)
+        assert idx.workspace(OP_DENSE, nq, k).data_ptr() == ws.data_ptr()  # never regrown
+        S, X, Q = oracle_scores(w.rows[:n], w.queries, "bf16")
+        check_dense(S, X, Q, ids, sc, k, "bf16", label=f"n={n} k={k}")
+
+
 def test_empty_index_pads():
     dev = device()
     from paper_2608_08340_amd import Index
