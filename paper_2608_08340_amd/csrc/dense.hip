@@ -886,10 +886,13 @@ __device__ __forceinline__ bool blk_epilogue(const f32x4 (&acc)[MW][BN / 16], Se
 //  - The query block of a super-step (BN x 128 dimensions) is loaded one super-step
 //    ahead into VGPRs, written to one of two LDS slots at the end of the previous
 //    super-step, and read by every wave as B operands, one k-step ahead of its MFMAs.
-//    One barrier per super-step.
+//    One barrier per super-step.  With QR > 0 (d <= 128 QR) every super-step of the
+//    queries instead stays resident in its own LDS slot, loaded once before the first
+//    tile, and the loop has one barrier per tile.
 //  - After the last k-step of a tile the scores sit in the accumulators; the register
 //    epilogue (or, when it declines, G passes through an LDS score tile) updates the
-//    running top-k of each query.
+//    running top-k of each query, or (SEL 2) the filtered mode collects the scores that
+//    reach the query's threshold.
 // ------------------------------------------------------------------------------------
 template <int DT, int NW, int MW, int RS, int G, int KS, int SEL, int WV, int QR>
 __global__ __launch_bounds__(WV * 64) void dense_mfma_kernel(DenseArgs a) {
