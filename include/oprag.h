@@ -54,7 +54,12 @@ typedef enum oprag_status {
 
 typedef enum oprag_dtype { OPRAG_F32 = 0, OPRAG_BF16 = 1, OPRAG_F16 = 2 } oprag_dtype;
 
-typedef enum oprag_op { OPRAG_OP_DENSE = 0, OPRAG_OP_SPARSE = 1, OPRAG_OP_HYBRID = 2 } oprag_op;
+typedef enum oprag_op {
+  OPRAG_OP_DENSE = 0,
+  OPRAG_OP_SPARSE = 1,
+  OPRAG_OP_HYBRID = 2,
+  OPRAG_OP_DENSE_FIRST = 3
+} oprag_op;
 
 typedef struct oprag_index oprag_index; /* opaque handle */
 
@@ -118,8 +123,8 @@ oprag_status oprag_sparse_attach(oprag_index *idx, int32_t vocab, int64_t n_docs
 
 /*
  * Workspace bytes a search of nq queries needs (op: oprag_op; k_dense is the dense k for
- * OPRAG_OP_DENSE and OPRAG_OP_HYBRID, k_sparse the sparse k for OPRAG_OP_SPARSE and
- * OPRAG_OP_HYBRID).  The value does not depend on the current row count, so a workspace
+ * OPRAG_OP_DENSE and OPRAG_OP_HYBRID and the candidate count n_cand for
+ * OPRAG_OP_DENSE_FIRST, k_sparse the sparse k for OPRAG_OP_SPARSE and OPRAG_OP_HYBRID).  The value does not depend on the current row count, so a workspace
  * sized once stays valid as the index grows.
  */
 oprag_status oprag_workspace_bytes(const oprag_index *idx, int32_t op, int64_t nq, int32_t k_dense, int32_t k_sparse,
@@ -174,6 +179,26 @@ oprag_status oprag_search_hybrid(oprag_index *idx, const void *q_dev, const int3
                                  const int32_t *qterms_dev, int64_t nq, int32_t k_dense, int32_t k_sparse,
                                  int32_t rrf_k, int32_t k, float *fused_dev, int64_t *ids_dev, void *workspace_dev,
                                  size_t workspace_bytes, void *stream);
+
+/*
+ * Dense-first hybrid search (the serving schedule of Section 4.1, "Retrieval", whose latency
+ * and quality against full hybrid retrieval Section 5.5 reports): the exact dense top-n_cand
+ * candidates (as oprag_search_dense), their BM25 scores over the attached sparse index (the
+ * full-corpus statistics of oprag_sparse_attach; a candidate's postings are found by binary
+ * search), and reciprocal rank fusion (rrf_k) of the candidates' dense order with their
+ * lexical order (the candidates with a positive score, by score desc then id asc), cut at k
+ * by (fused desc, id asc) and compared exactly as in oprag_rrf_fuse.  Only candidates can be
+ * returned.
+ *   q_dev [nq x dim]; qterm_indptr_dev / qterms_dev as in oprag_search_sparse;
+ *   fused_dev [nq x k] fp32, ids_dev [nq x k] int64 (-1 / -inf past the candidates).
+ * 1 <= n_cand <= 128.  workspace_dev must hold
+ * oprag_workspace_bytes(OPRAG_OP_DENSE_FIRST, k_dense = n_cand) bytes.  E_STATE without an
+ * attached sparse index.
+ */
+oprag_status oprag_search_hybrid_dense_first(oprag_index *idx, const void *q_dev, const int32_t *qterm_indptr_dev,
+                                             const int32_t *qterms_dev, int64_t nq, int32_t n_cand, int32_t rrf_k,
+                                             int32_t k, float *fused_dev, int64_t *ids_dev, void *workspace_dev,
+                                             size_t workspace_bytes, void *stream);
 
 /*
  * Kernel timing (diagnostics: measuring the scoring kernel against its roofline).  Arms a

@@ -20,10 +20,11 @@ import threading
 
 import torch
 
-__all__ = ["Index", "OpragError", "rrf_fuse", "library", "LIB_PATH", "OP_DENSE", "OP_SPARSE", "OP_HYBRID"]
+__all__ = ["Index", "OpragError", "rrf_fuse", "library", "LIB_PATH", "OP_DENSE", "OP_SPARSE", "OP_HYBRID",
+           "OP_DENSE_FIRST"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "liboprag.so")
-OP_DENSE, OP_SPARSE, OP_HYBRID = 0, 1, 2
+OP_DENSE, OP_SPARSE, OP_HYBRID, OP_DENSE_FIRST = 0, 1, 2, 3
 _DTYPE = {torch.float32: 0, torch.bfloat16: 1, torch.float16: 2}
 STATUS = {0: "OK", -1: "E_INVALID", -2: "E_CAPACITY", -3: "E_STATE", -4: "E_UNSUPPORTED", -5: "E_DEVICE"}
 
@@ -54,6 +55,7 @@ _SIGS = {
     "oprag_search_sparse": ([_P, _P, _P, _I64, _I32, _P, _P, _P, _SZ, _P], _I32),
     "oprag_rrf_fuse": ([_P, _I32, _P, _I32, _I64, _I32, _I32, _P, _P, _P], _I32),
     "oprag_search_hybrid": ([_P, _P, _P, _P, _I64, _I32, _I32, _I32, _I32, _P, _P, _P, _SZ, _P], _I32),
+    "oprag_search_hybrid_dense_first": ([_P, _P, _P, _P, _I64, _I32, _I32, _I32, _P, _P, _P, _SZ, _P], _I32),
     "oprag_time_next_dense_kernel": ([_P, _P], _I32),
 }
 _lib = None
@@ -216,6 +218,25 @@ class Index:
         _check(library().oprag_search_hybrid(self._h, _ptr(q), _ptr(qterm_indptr), _ptr(qterms), nq, k_dense,
                                              k_sparse, rrf_k, k, _ptr(fused), _ptr(ids), _ptr(ws), ws.numel(),
                                              _stream(self.device)))
+        return fused, ids
+
+    def search_hybrid_dense_first(self, q: torch.Tensor, qterm_indptr: torch.Tensor, qterms: torch.Tensor,
+                                  n_cand: int = 128, rrf_k: int = 60, k: int = 5, out: tuple | None = None):
+        """Dense top-n_cand candidates reranked by BM25 and fused with their dense order by RRF.
+        Returns (fused fp32, ids int64), [nq x k]."""
+        _dev_tensor(q, self.dtype, self.device, "q")
+        _dev_tensor(qterm_indptr, torch.int32, self.device, "qterm_indptr")
+        _dev_tensor(qterms, torch.int32, self.device, "qterms")
+        nq = q.shape[0]
+        if qterm_indptr.numel() != nq + 1:
+            raise OpragError(-1, "qterm_indptr must have nq + 1 entries")
+        fused, ids = out if out is not None else (
+            torch.empty((nq, k), dtype=torch.float32, device=self.device),
+            torch.empty((nq, k), dtype=torch.int64, device=self.device))
+        ws = self.workspace(OP_DENSE_FIRST, nq, n_cand, 1)
+        _check(library().oprag_search_hybrid_dense_first(self._h, _ptr(q), _ptr(qterm_indptr), _ptr(qterms), nq,
+                                                         n_cand, rrf_k, k, _ptr(fused), _ptr(ids), _ptr(ws),
+                                                         ws.numel(), _stream(self.device)))
         return fused, ids
 
 

@@ -109,6 +109,11 @@ size_t hybrid_ws(const oprag_index* idx, int64_t nq, int32_t kd, int32_t ks) {
   return lists + std::max(align_up(dense_ws(idx, nq, kd)), align_up(sparse_ws(idx, nq, ks)));
 }
 
+// Dense-first: the candidates' ids and scores, then the dense search's own area.
+size_t dense_first_ws(const oprag_index* idx, int64_t nq, int32_t n_cand) {
+  return align_up((size_t)nq * n_cand * 8) + align_up((size_t)nq * n_cand * 4) + align_up(dense_ws(idx, nq, n_cand));
+}
+
 oprag_status do_dense(oprag_index* idx, const void* q, int64_t nq, int32_t k, float* scores, int64_t* ids, void* ws,
                       size_t ws_bytes, hipStream_t s) {
   const size_t es = elem_size(idx->dtype);
@@ -324,6 +329,10 @@ oprag_status oprag_workspace_bytes(const oprag_index* idx, int32_t op, int64_t n
       if (oprag_status st = check_k(k_sparse, "k_sparse")) return st;
       *bytes = nq ? hybrid_ws(idx, nq, k_dense, k_sparse) : 0;
       return ok();
+    case OPRAG_OP_DENSE_FIRST:
+      if (oprag_status st = check_k(k_dense, "k_dense (n_cand)")) return st;
+      *bytes = nq ? dense_first_ws(idx, nq, k_dense) : 0;
+      return ok();
     default:
       return fail(OPRAG_E_INVALID, "op %d is not an oprag_op", op);
   }
@@ -435,6 +444,42 @@ oprag_status oprag_search_hybrid(oprag_index* idx, const void* q_dev, const int3
   e = oprag::launch_rrf(reinterpret_cast<const long long*>(d_ids), k_dense, reinterpret_cast<const long long*>(s_ids),
                         k_sparse, nq, rrf_k, k, fused_dev, reinterpret_cast<long long*>(ids_dev), s);
   if (e != hipSuccess) return hip_fail(e, "rrf launch");
+  return ok();
+}
+
+oprag_status oprag_search_hybrid_dense_first(oprag_index* idx, const void* q_dev, const int32_t* qterm_indptr_dev,
+                                             const int32_t* qterms_dev, int64_t nq, int32_t n_cand, int32_t rrf_k,
+                                             int32_t k, float* fused_dev, int64_t* ids_dev, void* workspace_dev,
+                                             size_t workspace_bytes, void* stream) {
+  if (oprag_status st = check_index(idx)) return st;
+  if (!idx->has_sparse) return fail(OPRAG_E_STATE, "no sparse index attached");
+  if (oprag_status st = check_k(n_cand, "n_cand")) return st;
+  if (oprag_status st = check_k(k, "k")) return st;
+  if (rrf_k < 0 || rrf_k > 1000000) return fail(OPRAG_E_INVALID, "rrf_k %d outside [0, 1000000]", rrf_k);
+  if (nq < 0 || nq > (int64_t)1 << 24) return fail(OPRAG_E_INVALID, "nq %lld out of range", (long long)nq);
+  if (nq == 0) return ok();
+  if (oprag_status st = check_buf(q_dev, "q_dev")) return st;
+  if (oprag_status st = check_buf(qterm_indptr_dev, "qterm_indptr_dev")) return st;
+  if (!qterms_dev) return fail(OPRAG_E_INVALID, "qterms_dev is NULL");
+  if (oprag_status st = check_buf(fused_dev, "fused_dev")) return st;
+  if (oprag_status st = check_buf(ids_dev, "ids_dev")) return st;
+  const size_t need = dense_first_ws(idx, nq, n_cand);
+  if (!workspace_dev || !aligned16(workspace_dev) || workspace_bytes < need)
+    return fail(OPRAG_E_INVALID, "workspace missing or too small (%zu < %zu bytes)", workspace_bytes, need);
+  DeviceScope ds(idx->device);
+  if (ds.error() != hipSuccess) return hip_fail(ds.error(), "select device");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  unsigned char* w = static_cast<unsigned char*>(workspace_dev);
+  int64_t* c_ids = reinterpret_cast<int64_t*>(w);
+  w += align_up((size_t)nq * n_cand * 8);
+  float* c_sc = reinterpret_cast<float*>(w);
+  w += align_up((size_t)nq * n_cand * 4);
+  const size_t inner = workspace_bytes - (size_t)(w - static_cast<unsigned char*>(workspace_dev));
+  if (oprag_status st = do_dense(idx, q_dev, nq, n_cand, c_sc, c_ids, w, inner, s)) return st;
+  const hipError_t e =
+      oprag::launch_dense_first(idx->sp, qterm_indptr_dev, qterms_dev, reinterpret_cast<const long long*>(c_ids),
+                                n_cand, nq, rrf_k, k, fused_dev, reinterpret_cast<long long*>(ids_dev), s);
+  if (e != hipSuccess) return hip_fail(e, "dense-first rerank launch");
   return ok();
 }
 

@@ -478,6 +478,120 @@ __global__ __launch_bounds__(64) void partial_merge_kernel(const unsigned long l
   }
 }
 
+// ------------------------------------------------------------------------------------
+// Dense-first hybrid (the serving schedule of Section 4.1, "Retrieval", measured in Section
+// 5.5: lexical reranking of the dense top-n candidates only).  One workgroup of 1,024 threads per query: thread
+// (c, j) = (t % 128, t / 128) takes the dense candidate of rank c + 1 and the query's terms
+// j, j + 8, j + 16, ...  A term's posting of the candidate is found by binary search over the
+// term's ascending chunk ids; the candidate's BM25 score is the sum of idfk * wpost over its
+// matching term occurrences, added in query order (for up to 8 terms exactly the order of the
+// full BM25 kernel).  The candidates with a positive score are ranked by (score desc, id asc);
+// reciprocal rank fusion of that order with the dense order, compared exactly as fractions
+// (as rrf_kernel does), gives the top k.
+// ------------------------------------------------------------------------------------
+constexpr int kDfThreads = 1024;
+constexpr int kRrfExactMax = 100000;  // below this rrf_k the fused quotients order exactly
+constexpr int kDfCand = 128;
+constexpr int kDfLanes = kDfThreads / kDfCand;
+__global__ __launch_bounds__(kDfThreads) void dense_first_kernel(int vocab, const long long* __restrict__ indptr,
+                                                                 const int* __restrict__ chunk,
+                                                                 const float* __restrict__ idfk,
+                                                                 const float* __restrict__ wpost,
+                                                                 const int* qterm_indptr, const int* qterms,
+                                                                 const long long* cand, int n_cand, int rrf_k, int k,
+                                                                 float* out_fused, long long* out_ids) {
+  __shared__ float part[kDfLanes][kDfCand];
+  __shared__ float lex[kDfCand];
+  __shared__ long long cid[kDfCand];
+  __shared__ long long fnum[kDfCand];
+  __shared__ long long fden[kDfCand];
+  __shared__ double fval[kDfCand];
+  const long long q = blockIdx.x;
+  const int t = threadIdx.x, c = t % kDfCand, j = t / kDfCand;
+  const long long id = c < n_cand ? cand[q * n_cand + c] : -1;
+  float sc = 0.f;
+  if (id >= 0) {
+    for (int e = qterm_indptr[q] + j; e < qterm_indptr[q + 1]; e += kDfLanes) {
+      const int term = qterms[e];
+      if (term < 0 || term >= vocab) continue;  // unknown terms match nothing
+      const long long end = indptr[term + 1];
+      long long lo = indptr[term], hi = end;  // first posting whose chunk is >= id
+      while (lo < hi) {
+        const long long mid = (lo + hi) >> 1;
+        if (chunk[mid] < id)
+          lo = mid + 1;
+        else
+          hi = mid;
+      }
+      if (lo < end && chunk[lo] == id) sc += idfk[term] * wpost[lo];
+    }
+  }
+  part[j][c] = sc;
+  __syncthreads();
+  if (t < kDfCand) {
+    float total = 0.f;
+#pragma unroll
+    for (int u = 0; u < kDfLanes; ++u) total += part[u][c];
+    lex[c] = id >= 0 ? total : 0.f;
+    cid[c] = id;
+  }
+  __syncthreads();
+  if (t < kDfCand && id >= 0) {
+    // lexical rank among the candidates with a positive score, then the fused fraction
+    const float me = lex[c];
+    int rs = 0;
+    if (me > 0.f) {
+      for (int u = 0; u < n_cand; ++u) {
+        const float o = lex[u];
+        const long long oi = cid[u];
+        rs += (oi >= 0 && o > 0.f && (o > me || (o == me && oi < id))) ? 1 : 0;
+      }
+    }
+    const long long a = (long long)rrf_k + c + 1;
+    long long num = 1, den = a;
+    if (me > 0.f) {
+      const long long b = (long long)rrf_k + rs + 1;
+      num = a + b;
+      den = a * b;
+    }
+    fnum[c] = num;
+    fden[c] = den;
+    fval[c] = (double)num / (double)den;
+  }
+  __syncthreads();
+  if (t < kDfCand && id >= 0) {
+    const long long n0 = fnum[c], d0 = fden[c];
+    const double v0 = fval[c];
+    int r = 0;
+    for (int u = 0; u < n_cand; ++u) {
+      if (u == c || cid[u] < 0) continue;
+      bool beats;
+      if (rrf_k < kRrfExactMax) {
+        // distinct fused values differ by at least (rrf_k + 129)^-4, more than the rounding of
+        // the correctly rounded quotients, and equal values round alike
+        beats = fval[u] > v0 || (fval[u] == v0 && cid[u] < id);
+      } else {
+        const long long lhs = fnum[u] * d0, rhs = n0 * fden[u];
+        beats = lhs > rhs || (lhs == rhs && cid[u] < id);
+      }
+      r += beats ? 1 : 0;
+    }
+    if (r < k) {
+      out_ids[q * k + r] = id;
+      out_fused[q * k + r] = (float)((double)n0 / (double)d0);
+    }
+  }
+  // slots past the valid candidates
+  if (t < k) {
+    int nv = 0;
+    for (int u = 0; u < n_cand; ++u) nv += cand[q * n_cand + u] >= 0 ? 1 : 0;
+    if (t >= nv) {
+      out_ids[q * k + t] = -1;
+      out_fused[q * k + t] = -__builtin_inff();
+    }
+  }
+}
+
 }  // namespace
 
 hipError_t sparse_validate(int vocab, long long n_docs, long long nnz, const long long* indptr, const int* chunk,
@@ -541,6 +655,16 @@ hipError_t launch_sparse(const SparseIndex& sp, const int* qterm_indptr, const i
   else
     hipLaunchKernelGGL(partial_merge_kernel, dim3((unsigned)nq), dim3(64), 0, s, a.partial, a.n_ranges, k, nq, k,
                        out_scores, out_ids);
+  return hipGetLastError();
+}
+
+hipError_t launch_dense_first(const SparseIndex& sp, const int* qterm_indptr, const int* qterms,
+                              const long long* cand, int n_cand, long long nq, int rrf_k, int k, float* out_fused,
+                              long long* out_ids, hipStream_t s) {
+  if (n_cand < 1 || n_cand > kDfCand) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(dense_first_kernel, dim3((unsigned)nq), dim3(kDfThreads), 0, s, sp.vocab, sp.term_indptr,
+                     sp.post_chunk, sp.idfk, sp.wpost, qterm_indptr, qterms, cand, n_cand, rrf_k, k, out_fused,
+                     out_ids);
   return hipGetLastError();
 }
 

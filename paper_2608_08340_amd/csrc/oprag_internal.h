@@ -100,6 +100,11 @@ hipError_t launch_sparse(const SparseIndex& sp, const int* qterm_indptr, const i
                          float* out_scores, long long* out_ids, void* ws, hipStream_t s);
 
 // ---------------------------------------------------------------- fusion and upsert
+// Dense-first hybrid: BM25 of the dense candidates cand [nq x n_cand] (dense order, -1 padded,
+// 1 <= n_cand <= 128), reciprocal rank fusion with their dense order, top k.
+hipError_t launch_dense_first(const SparseIndex& sp, const int* qterm_indptr, const int* qterms,
+                              const long long* cand, int n_cand, long long nq, int rrf_k, int k, float* out_fused,
+                              long long* out_ids, hipStream_t s);
 hipError_t launch_rrf(const long long* dense_ids, int k_dense, const long long* sparse_ids, int k_sparse,
                       long long nq, int rrf_k, int k, float* out_fused, long long* out_ids, hipStream_t s);
 hipError_t launch_upsert(void* slab, int slab_dtype, int d, long long first_row, const void* rows,

@@ -4,7 +4,7 @@ import pytest
 import torch
 
 import synth
-from oracle import accept, bm25, rrf
+from oracle import accept, bm25, dense_first, rrf
 from oracle import dense as od
 from tests.gpu_helpers import check_dense, device, log, make_index, oracle_scores
 
@@ -214,3 +214,113 @@ def test_hybrid_other_stream_and_graph_replay(c3):
         torch.cuda.synchronize()
         assert torch.equal(ig, ref_i), f"replay {rep}"
         assert torch.equal(fg.view(torch.int32), ref_f.view(torch.int32)), f"replay {rep}"
+
+
+def _dense_first_expect(dids, B, rrf_k, k, rel=2e-6):
+    """Exact RRF of the GPU's own dense candidates with their lexical order from the fp64
+    oracle BM25.  ok[q] is False where two distinct positive candidate scores lie within rel
+    of each other (each fp32 contribution idf (k1 + 1) * w carries at most three roundings and
+    a sum of up to 8 of them seven more, so fp32 keeps the order of scores further apart than
+    about 1.2e-6 relative); those queries are compared loosely.  Exactly equal scores come from equal (term, tf, length) contributions, which
+    the GPU computes identically, so their id order is checked."""
+    ids, f32, _ = dense_first.batch(dids, B, rrf_k, k)
+    ok = np.ones(dids.shape[0], dtype=bool)
+    for q in range(dids.shape[0]):
+        c = dids[q][dids[q] >= 0]
+        s = np.unique(B[q, c][B[q, c] > 0])
+        if s.size > 1 and np.any(np.diff(s) <= rel * s[1:]):
+            ok[q] = False
+    return ids, f32, ok
+
+
+def _check_dense_first(fused, fids, dids, B, rrf_k, k, label, min_exact=0.5):
+    dids = dids.cpu().numpy()
+    g_ids, g_f = fids.cpu().numpy(), fused.cpu().numpy()
+    e_ids, e_f, ok = _dense_first_expect(dids, B, rrf_k, k)
+    log(f"{label}: {ok.sum()} of {len(ok)} queries compared exactly")
+    assert ok.mean() > min_exact, label
+    assert np.array_equal(g_ids[ok], e_ids[ok]), label
+    assert np.array_equal(g_f[ok].view(np.uint32), e_f[ok].view(np.uint32)), label
+    for q in np.nonzero(~ok)[0]:  # near ties: same candidates returned, valid order
+        cand = set(dids[q][dids[q] >= 0].tolist())
+        got = [i for i in g_ids[q] if i >= 0]
+        assert set(got) <= cand and len(got) == min(k, len(cand)), label
+        assert np.all(np.diff(g_f[q][: len(got)]) <= 0), label
+    return ok
+
+
+@pytest.mark.parametrize("n_cand,k", [(128, 5), (37, 10), (8, 20)])
+def test_dense_first_small_corpus(n_cand, k):
+    """Dense-first hybrid on 3,000 chunks (d = 128, 400 terms): the GPU's dense top-n_cand
+    candidates, reranked by their BM25 scores and fused with their dense order by RRF(60),
+    equal the oracle's fusion of the same candidates with fp64 BM25, fraction for fraction.
+    Queries 0-3 have no terms, only unknown terms, repeats, and a mix."""
+    dev = device()
+    n, nq = 3000, 60
+    ind, toks, csr, qi, qt = _small_corpus(900 + n_cand, n, 400, 40.0, nq)
+    w = synth.mixture_dense(950 + n_cand, n, 128, 16, nq, n_cand, "bf16")
+    idx = make_index(w.rows, "bf16")
+    _attach(idx, csr, dev)
+    q = w.queries.to(dev)
+    log("dense-first small", n_cand, k)
+    fused, fids = idx.search_hybrid_dense_first(q, _t(qi, dev), _t(qt, dev), n_cand, 60, k)
+    dsc, dids = idx.search_dense(q, n_cand)
+    torch.cuda.synchronize()
+    S, X, Q = oracle_scores(w.rows, w.queries, "bf16")
+    check_dense(S, X, Q, dids, dsc, n_cand, "bf16", label="candidates")
+    qt_oracle = np.where((qt >= 0) & (qt < 400), qt, 10 ** 6).astype(np.int64)
+    B = bm25.scores_batch(ind, toks, qi, qt_oracle, 1.2, 0.75)
+    _check_dense_first(fused, fids, dids, B, 60, k, f"n_cand={n_cand} k={k}")
+    # no lexical evidence: the dense order alone
+    d0 = dids.cpu().numpy()[0]
+    assert np.array_equal(fids.cpu().numpy()[0][: min(k, n_cand)], d0[: min(k, n_cand)])
+
+
+def test_dense_first_fewer_rows_than_candidates():
+    """50 chunks, 128 candidates asked, k = 60: the 50 valid candidates are fused and the rest
+    of each row is padding (-1, -inf)."""
+    dev = device()
+    n, nq = 50, 12
+    ind, toks, csr, qi, qt = _small_corpus(1300, n, 30, 8.0, nq)
+    w = synth.mixture_dense(1301, n, 128, 4, nq, 16, "bf16")
+    idx = make_index(w.rows, "bf16")
+    _attach(idx, csr, dev)
+    q = w.queries.to(dev)
+    fused, fids = idx.search_hybrid_dense_first(q, _t(qi, dev), _t(qt, dev), 128, 60, 60)
+    dsc, dids = idx.search_dense(q, 128)
+    torch.cuda.synchronize()
+    qt_oracle = np.where((qt >= 0) & (qt < 30), qt, 10 ** 6).astype(np.int64)
+    B = bm25.scores_batch(ind, toks, qi, qt_oracle, 1.2, 0.75)
+    _check_dense_first(fused, fids, dids, B, 60, 60, "50 rows")
+    assert (fids.cpu().numpy()[:, 50:] == -1).all()
+    assert np.isneginf(fused.cpu().numpy()[:, 50:]).all()
+
+
+@pytest.mark.timeout(300)
+@pytest.mark.parametrize("correlated", [False, True])
+def test_dense_first_32k_against_oracle_and_full_hybrid(c3, correlated):
+    """The 32,768 x 1,024 bf16 hybrid workload, 256 queries of 8 terms: dense-first with 128
+    candidates and k = 5 matches the oracle's fusion of the GPU's candidates; Recall@5 and
+    Jaccard overlap against full hybrid retrieval (RRF of dense and BM25 top-100 lists over
+    the whole corpus) are logged, as the paper reports them.  They depend on how far the
+    lexical and dense signals agree: little with independent synthetic queries, more when the
+    query terms are drawn from the chunk the dense query was made from."""
+    dev = device()
+    h = c3 if not correlated else synth.hybrid_32k(correlated=True, dense=synth.dense_32k())
+    w = h.dense
+    idx = make_index(w.rows, "bf16")
+    _attach(idx, h.csr, dev, h.k1, h.b)
+    q = w.queries.to(dev)
+    qi, qt = _t(h.qterm_indptr, dev), _t(h.qterms, dev)
+    fused, fids = idx.search_hybrid_dense_first(q, qi, qt, 128, 60, 5)
+    dsc, dids = idx.search_dense(q, 128)
+    full_f, full_ids = idx.search_hybrid(q, qi, qt, 100, 100, 60, 5)
+    torch.cuda.synchronize()
+    B = bm25.scores_batch(h.doc_indptr, h.tokens, h.qterm_indptr, h.qterms, h.k1, h.b)
+    _check_dense_first(fused, fids, dids, B, 60, 5, "32k", min_exact=0.25)
+    a, b = fids.cpu().numpy(), full_ids.cpu().numpy()
+    recall = np.mean([len(set(a[i]) & set(b[i])) / 5 for i in range(len(a))])
+    jacc = np.mean([len(set(a[i]) & set(b[i])) / len(set(a[i]) | set(b[i])) for i in range(len(a))])
+    log(f"dense-first vs full hybrid ({'correlated' if correlated else 'independent'} terms): "
+        f"Recall@5 {recall:.3f}, Jaccard {jacc:.3f}")
+    assert 0.0 <= jacc <= recall <= 1.0
