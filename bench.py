@@ -303,6 +303,16 @@ def suite() -> int:
     ms_h = _timed(lambda: nxt().search_hybrid(qd, qi, qterms, 100, 100, 60, 5), 64, stream)
     report("hybrid: full oprag_search_hybrid, batch 256, cold", ms_h, nq,
            algorithmic_bytes(N_ROWS, DIM, nq, 5) + sparse_bytes, 2.0 * nq * N_ROWS * DIM)
+    # dense-first: dense top-128, BM25 of those candidates only, RRF(60) -> 5; quality against
+    # the full hybrid result as Recall@5 and Jaccard overlap
+    ms_f = _timed(lambda: nxt().search_hybrid_dense_first(qd, qi, qterms, 128, 60, 5), 64, stream)
+    a = nxt().search_hybrid_dense_first(qd, qi, qterms, 128, 60, 5)[1].cpu().numpy()
+    b = nxt().search_hybrid(qd, qi, qterms, 100, 100, 60, 5)[1].cpu().numpy()
+    inter = [len(set(a[i]) & set(b[i])) for i in range(nq)]
+    report("hybrid dense-first: dense top-128 -> BM25 of the candidates -> RRF(60) -> 5, batch 256, cold", ms_f, nq,
+           algorithmic_bytes(N_ROWS, DIM, nq, 128), 2.0 * nq * N_ROWS * DIM,
+           recall_at_5_vs_full=round(float(np.mean(inter)) / 5, 3),
+           jaccard_vs_full=round(float(np.mean([x / len(set(a[i]) | set(b[i])) for i, x in enumerate(inter)])), 3))
     for ix in idxs:
         ix.close()
     del idxs, rows

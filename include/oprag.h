@@ -112,7 +112,8 @@ oprag_status oprag_upsert(oprag_index *idx, const void *rows_dev, int32_t rows_d
  * The arrays stay caller-owned and are read by later searches.  The library checks them on
  * the device (E_INVALID on any violation), then computes idf(t) = ln(1 + (N - df + 0.5) /
  * (df + 0.5)) per term and tf / (tf + k1 (1 - b + b dl / avgdl)) per posting, in fp64 stored
- * as fp32, into arrays it owns (4 bytes per term and per posting).
+ * as fp32, and a chunk-major copy of (term, weight) pairs for scoring given chunks, into
+ * arrays it owns (4 bytes per term, 12 per posting and 8 per chunk).
  * Synchronises `stream`.  Re-attaching replaces the previous sparse index.
  * k1 >= 0, 0 <= b <= 1.
  */
@@ -184,8 +185,8 @@ oprag_status oprag_search_hybrid(oprag_index *idx, const void *q_dev, const int3
  * Dense-first hybrid search (the serving schedule of Section 4.1, "Retrieval", whose latency
  * and quality against full hybrid retrieval Section 5.5 reports): the exact dense top-n_cand
  * candidates (as oprag_search_dense), their BM25 scores over the attached sparse index (the
- * full-corpus statistics of oprag_sparse_attach; a candidate's postings are found by binary
- * search), and reciprocal rank fusion (rrf_k) of the candidates' dense order with their
+ * full-corpus statistics of oprag_sparse_attach; a candidate's terms are read from the
+ * chunk-major copy the attach builds), and reciprocal rank fusion (rrf_k) of the candidates' dense order with their
  * lexical order (the candidates with a positive score, by score desc then id asc), cut at k
  * by (fused desc, id asc) and compared exactly as in oprag_rrf_fuse.  Only candidates can be
  * returned.

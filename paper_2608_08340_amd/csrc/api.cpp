@@ -260,10 +260,14 @@ oprag_status oprag_sparse_attach(oprag_index* idx, int32_t vocab, int64_t n_docs
   DeviceScope ds(idx->device);
   if (ds.error() != hipSuccess) return hip_fail(ds.error(), "select device");
   hipStream_t s = static_cast<hipStream_t>(stream);
-  // Library-owned arrays: [flag u32 | sum u64 | idfk f32 x vocab | posting weights f32 x nnz].
+  // Library-owned arrays: [flag u32 | sum u64 | idfk f32 x vocab | posting weights f32 x nnz |
+  // chunk-major copy: list offsets i64 x (n_docs + 1), terms i32 x nnz, weights f32 x nnz].
   const size_t off_sum = 256, off_idf = 512;
   const size_t off_wpost = off_idf + align_up((size_t)vocab * 4);
-  const size_t bytes = off_wpost + align_up((size_t)nnz * 4);
+  const size_t off_fptr = off_wpost + align_up((size_t)nnz * 4);
+  const size_t off_fterm = off_fptr + align_up((size_t)(n_docs + 1) * 8);
+  const size_t off_fw = off_fterm + align_up((size_t)nnz * 4);
+  const size_t bytes = off_fw + align_up((size_t)nnz * 4);
   void* mem = nullptr;
   hipError_t e = hipMalloc(&mem, bytes);
   if (e != hipSuccess) return hip_fail(e, "sparse arrays allocation");
@@ -291,9 +295,22 @@ oprag_status oprag_sparse_attach(oprag_index* idx, int32_t vocab, int64_t n_docs
   sp.post_tf = post_tf_dev;
   sp.idfk = reinterpret_cast<float*>(base + off_idf);
   sp.wpost = reinterpret_cast<float*>(base + off_wpost);
+  sp.fwd_ptr = reinterpret_cast<long long*>(base + off_fptr);
+  sp.fwd_term = reinterpret_cast<int*>(base + off_fterm);
+  sp.fwd_w = reinterpret_cast<float*>(base + off_fw);
   sp.k1 = k1;
   sp.b = b;
   e = oprag::sparse_prepare(sp, doc_len_dev, reinterpret_cast<unsigned long long*>(base + off_sum), s);
+  if (e == hipSuccess) {  // the chunk-major copy, with per-chunk counters as scratch
+    int* cnt = nullptr;
+    e = hipMalloc(&cnt, (size_t)n_docs * sizeof(int));
+    if (e == hipSuccess) {
+      e = oprag::sparse_forward(sp, cnt, s);
+      const hipError_t es = hipStreamSynchronize(s);
+      if (e == hipSuccess) e = es;
+      (void)hipFree(cnt);
+    }
+  }
   if (e == hipSuccess) e = hipStreamSynchronize(s);
   if (e != hipSuccess) {
     (void)hipFree(mem);

@@ -479,74 +479,167 @@ __global__ __launch_bounds__(64) void partial_merge_kernel(const unsigned long l
 }
 
 // ------------------------------------------------------------------------------------
+// Chunk-major copy of the postings (built once at attach) for the lexical scoring of given
+// chunks: counts per chunk, exclusive prefix sums, then every posting placed in its chunk's
+// list (positions by atomics, so a list is in no particular order; the CSR holds a
+// (term, chunk) pair at most once, so a list holds each term at most once).
+// ------------------------------------------------------------------------------------
+__global__ void fwd_count_kernel(long long nnz, const int* __restrict__ chunk, int* cnt) {
+  const long long stride = (long long)gridDim.x * blockDim.x;
+  for (long long p = (long long)blockIdx.x * blockDim.x + threadIdx.x; p < nnz; p += stride) atomicAdd(&cnt[chunk[p]], 1);
+}
+
+// One workgroup: ptr[i] = sum of cnt[0 .. i), ptr[n] = total, in tiles of 1,024 x 4 counts.
+__global__ __launch_bounds__(1024) void fwd_scan_kernel(long long n, const int* __restrict__ cnt, long long* ptr) {
+  __shared__ long long part[1024];
+  const int t = threadIdx.x;
+  long long carry = 0;
+  for (long long base = 0; base < n; base += 4096) {
+    long long v[4], sum = 0;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const long long i = base + (long long)t * 4 + u;
+      v[u] = i < n ? cnt[i] : 0;
+      sum += v[u];
+    }
+    part[t] = sum;
+    __syncthreads();
+    for (int off = 1; off < 1024; off <<= 1) {  // inclusive scan of the 1,024 tile sums
+      const long long x = t >= off ? part[t - off] : 0;
+      __syncthreads();
+      part[t] += x;
+      __syncthreads();
+    }
+    long long excl = carry + part[t] - sum;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const long long i = base + (long long)t * 4 + u;
+      if (i < n) ptr[i] = excl;
+      excl += v[u];
+    }
+    carry += part[1023];
+    __syncthreads();  // part is rewritten by the next tile
+  }
+  if (t == 0) ptr[n] = carry;
+}
+
+// Workgroups take terms in turn; a term's postings go to their chunks' lists.
+__global__ void fwd_fill_kernel(int vocab, const long long* __restrict__ indptr, const int* __restrict__ chunk,
+                                const float* __restrict__ wpost, const long long* __restrict__ ptr, int* fill,
+                                int* fwd_term, float* fwd_w) {
+  for (long long t = blockIdx.x; t < vocab; t += gridDim.x) {
+    const long long p1 = indptr[t + 1];
+    for (long long p = indptr[t] + threadIdx.x; p < p1; p += blockDim.x) {
+      const int d = chunk[p];
+      const long long pos = ptr[d] + atomicAdd(&fill[d], 1);
+      fwd_term[pos] = (int)t;
+      fwd_w[pos] = wpost[p];
+    }
+  }
+}
+
+// ------------------------------------------------------------------------------------
 // Dense-first hybrid (the serving schedule of Section 4.1, "Retrieval", measured in Section
-// 5.5: lexical reranking of the dense top-n candidates only).  One workgroup of 1,024 threads per query: thread
-// (c, j) = (t % 128, t / 128) takes the dense candidate of rank c + 1 and the query's terms
-// j, j + 8, j + 16, ...  A term's posting of the candidate is found by binary search over the
-// term's ascending chunk ids; the candidate's BM25 score is the sum of idfk * wpost over its
-// matching term occurrences, added in query order (for up to 8 terms exactly the order of the
-// full BM25 kernel).  The candidates with a positive score are ranked by (score desc, id asc);
-// reciprocal rank fusion of that order with the dense order, compared exactly as fractions
-// (as rrf_kernel does), gives the top k.
+// 5.5: lexical reranking of the dense top-n candidates only).  One workgroup of 1,024 threads
+// per query: the eight threads (c, j) = (t / 8, t % 8) share the dense candidate of rank c + 1
+// and read its chunk-major (term, weight) list together, entries j, j + 8, ..., comparing each
+// entry with up to 32 query term occurrences at a time held in LDS; a match stores the weight
+// in the candidate's slot for that occurrence.  The candidate's BM25 score is then the sum of
+// idfk * weight over the occurrences in query order (the order of the full BM25 kernel).  The
+// candidates with a positive score are ranked by (score desc, id asc); reciprocal rank fusion
+// of that order with the dense order, compared exactly as fractions (as rrf_kernel does),
+// gives the top k.
 // ------------------------------------------------------------------------------------
 constexpr int kDfThreads = 1024;
 constexpr int kRrfExactMax = 100000;  // below this rrf_k the fused quotients order exactly
 constexpr int kDfCand = 128;
 constexpr int kDfLanes = kDfThreads / kDfCand;
-__global__ __launch_bounds__(kDfThreads) void dense_first_kernel(int vocab, const long long* __restrict__ indptr,
-                                                                 const int* __restrict__ chunk,
+__global__ __launch_bounds__(kDfThreads) void dense_first_kernel(int vocab, const long long* __restrict__ fwd_ptr,
+                                                                 const int* __restrict__ fwd_term,
                                                                  const float* __restrict__ idfk,
-                                                                 const float* __restrict__ wpost,
+                                                                 const float* __restrict__ fwd_w,
                                                                  const int* qterm_indptr, const int* qterms,
                                                                  const long long* cand, int n_cand, int rrf_k, int k,
                                                                  float* out_fused, long long* out_ids) {
-  __shared__ float part[kDfLanes][kDfCand];
+  constexpr int kTerms = 32;  // query term occurrences per pass
+  __shared__ int qt_s[kTerms];
+  __shared__ float wq[kDfCand][kTerms + 1];
   __shared__ float lex[kDfCand];
   __shared__ long long cid[kDfCand];
   __shared__ long long fnum[kDfCand];
   __shared__ long long fden[kDfCand];
   __shared__ double fval[kDfCand];
+  __shared__ int s_nv;  // valid candidates (the dense list pads with -1 at its end)
   const long long q = blockIdx.x;
-  const int t = threadIdx.x, c = t % kDfCand, j = t / kDfCand;
+  const int t = threadIdx.x, c = t / kDfLanes, j = t % kDfLanes;
   const long long id = c < n_cand ? cand[q * n_cand + c] : -1;
-  float sc = 0.f;
-  if (id >= 0) {
-    for (int e = qterm_indptr[q] + j; e < qterm_indptr[q + 1]; e += kDfLanes) {
-      const int term = qterms[e];
-      if (term < 0 || term >= vocab) continue;  // unknown terms match nothing
-      const long long end = indptr[term + 1];
-      long long lo = indptr[term], hi = end;  // first posting whose chunk is >= id
-      while (lo < hi) {
-        const long long mid = (lo + hi) >> 1;
-        if (chunk[mid] < id)
-          lo = mid + 1;
-        else
-          hi = mid;
-      }
-      if (lo < end && chunk[lo] == id) sc += idfk[term] * wpost[lo];
-    }
-  }
-  part[j][c] = sc;
-  __syncthreads();
-  if (t < kDfCand) {
-    float total = 0.f;
+  const long long f0 = id >= 0 ? fwd_ptr[id] : 0, f1 = id >= 0 ? fwd_ptr[id + 1] : 0;
+  float sc = 0.f;  // thread j == 0 of a candidate: its score
+  const int e_end = qterm_indptr[q + 1];
+  for (int e0 = qterm_indptr[q]; e0 < e_end; e0 += kTerms) {
+    const int ne = min(kTerms, e_end - e0);
+    if (t < kTerms) qt_s[t] = t < ne ? qterms[e0 + t] : -1;
+    for (int i = t; i < kDfCand * kTerms; i += kDfThreads) wq[i / kTerms][i % kTerms] = 0.f;
+    __syncthreads();
+    // sixteen entries per thread and step, all loads issued before any comparison; per query term
+    // occurrence the weights of matching entries are summed (a list holds a term once, so
+    // the sum is that weight or 0) and a match is stored
+    constexpr int kStep = 16;
+    for (long long f = f0 + j; f < f1; f += kStep * kDfLanes) {
+      int tm[kStep];
+      float wt[kStep];
 #pragma unroll
-    for (int u = 0; u < kDfLanes; ++u) total += part[u][c];
-    lex[c] = id >= 0 ? total : 0.f;
-    cid[c] = id;
-  }
-  __syncthreads();
-  if (t < kDfCand && id >= 0) {
-    // lexical rank among the candidates with a positive score, then the fused fraction
-    const float me = lex[c];
-    int rs = 0;
-    if (me > 0.f) {
-      for (int u = 0; u < n_cand; ++u) {
-        const float o = lex[u];
-        const long long oi = cid[u];
-        rs += (oi >= 0 && o > 0.f && (o > me || (o == me && oi < id))) ? 1 : 0;
+      for (int v = 0; v < kStep; ++v) {
+        const long long g = f + v * kDfLanes;
+        tm[v] = g < f1 ? fwd_term[g] : -1;
+        wt[v] = g < f1 ? fwd_w[g] : 0.f;
+      }
+      for (int u = 0; u < ne; ++u) {
+        const int tu = qt_s[u];
+        float m = 0.f;
+#pragma unroll
+        for (int v = 0; v < kStep; ++v) m += tm[v] == tu ? wt[v] : 0.f;
+        if (m != 0.f) wq[c][u] = m;
       }
     }
+    __syncthreads();
+    if (j == 0 && id >= 0) {
+      for (int u = 0; u < ne; ++u) {
+        const int term = qt_s[u];
+        if (term >= 0 && term < vocab) sc += idfk[term] * wq[c][u];  // unknown terms match nothing
+      }
+    }
+    __syncthreads();  // qt_s and wq are rewritten by the next pass
+  }
+  if (t == 0) s_nv = 0;
+  __syncthreads();
+  if (j == 0) {
+    lex[c] = id >= 0 ? sc : 0.f;
+    cid[c] = id;
+    if (id >= 0) atomicAdd(&s_nv, 1);
+  }
+  __syncthreads();
+  // ranking: the eight threads of candidate c each compare it with 16 of the candidates
+  // (u = 16 j .. 16 j + 15); the counts are summed across the eight adjacent lanes
+  auto sum8 = [](int x) {
+    x += __shfl_xor(x, 1);
+    x += __shfl_xor(x, 2);
+    x += __shfl_xor(x, 4);
+    return x;
+  };
+  constexpr int kPer = kDfCand / kDfLanes;
+  const float me = lex[c];
+  int rs = 0;  // lexical rank among the candidates with a positive score (invalid ones score 0)
+  if (id >= 0 && me > 0.f) {
+#pragma unroll
+    for (int v = 0; v < kPer; ++v) {
+      const int u = j * kPer + v;
+      const float o = lex[u];
+      rs += (o > 0.f && (o > me || (o == me && cid[u] < id))) ? 1 : 0;
+    }
+  }
+  rs = sum8(rs);
+  if (j == 0 && id >= 0) {
     const long long a = (long long)rrf_k + c + 1;
     long long num = 1, den = a;
     if (me > 0.f) {
@@ -559,32 +652,39 @@ __global__ __launch_bounds__(kDfThreads) void dense_first_kernel(int vocab, cons
     fval[c] = (double)num / (double)den;
   }
   __syncthreads();
-  if (t < kDfCand && id >= 0) {
-    const long long n0 = fnum[c], d0 = fden[c];
+  int r = 0;  // final rank: candidates that beat this one in (fused desc, id asc)
+  long long n0 = 0, d0 = 1;
+  if (id >= 0) {
+    n0 = fnum[c];
+    d0 = fden[c];
     const double v0 = fval[c];
-    int r = 0;
-    for (int u = 0; u < n_cand; ++u) {
-      if (u == c || cid[u] < 0) continue;
-      bool beats;
-      if (rrf_k < kRrfExactMax) {
-        // distinct fused values differ by at least (rrf_k + 129)^-4, more than the rounding of
-        // the correctly rounded quotients, and equal values round alike
-        beats = fval[u] > v0 || (fval[u] == v0 && cid[u] < id);
-      } else {
-        const long long lhs = fnum[u] * d0, rhs = n0 * fden[u];
-        beats = lhs > rhs || (lhs == rhs && cid[u] < id);
+#pragma unroll
+    for (int v = 0; v < kPer; ++v) {
+      const int u = j * kPer + v;
+      const long long oi = cid[u];
+      bool beats = false;
+      if (oi >= 0) {
+        if (rrf_k < kRrfExactMax) {
+          // distinct fused values differ by at least (rrf_k + 129)^-4, more than the rounding
+          // of the correctly rounded quotients, and equal values round alike
+          const double fv = fval[u];
+          beats = fv > v0 || (fv == v0 && oi < id);
+        } else {
+          const long long lhs = fnum[u] * d0, rhs = n0 * fden[u];
+          beats = lhs > rhs || (lhs == rhs && oi < id);
+        }
       }
       r += beats ? 1 : 0;
     }
-    if (r < k) {
-      out_ids[q * k + r] = id;
-      out_fused[q * k + r] = (float)((double)n0 / (double)d0);
-    }
+  }
+  r = sum8(r);
+  if (j == 0 && id >= 0 && r < k) {
+    out_ids[q * k + r] = id;
+    out_fused[q * k + r] = (float)((double)n0 / (double)d0);
   }
   // slots past the valid candidates
   if (t < k) {
-    int nv = 0;
-    for (int u = 0; u < n_cand; ++u) nv += cand[q * n_cand + u] >= 0 ? 1 : 0;
+    const int nv = s_nv;
     if (t >= nv) {
       out_ids[q * k + t] = -1;
       out_fused[q * k + t] = -__builtin_inff();
@@ -620,6 +720,21 @@ hipError_t sparse_prepare(SparseIndex& sp, const int* doc_len, unsigned long lon
   hipLaunchKernelGGL(prepare_kernel, dim3(std::max(1, blocks)), dim3(256), 0, s, sp.vocab, sp.n_docs, sp.nnz,
                      sp.term_indptr, sp.post_chunk, sp.post_tf, doc_len, sp.avgdl, (double)sp.k1, (double)sp.b, sp.idfk,
                      sp.wpost);
+  return hipGetLastError();
+}
+
+hipError_t sparse_forward(const SparseIndex& sp, int* cnt, hipStream_t s) {
+  hipError_t e = hipMemsetAsync(cnt, 0, (size_t)sp.n_docs * sizeof(int), s);
+  if (e != hipSuccess) return e;
+  const int blocks = (int)std::min<long long>(4096, std::max<long long>(1, (sp.nnz + 255) / 256));
+  hipLaunchKernelGGL(fwd_count_kernel, dim3(blocks), dim3(256), 0, s, sp.nnz, sp.post_chunk, cnt);
+  hipLaunchKernelGGL(fwd_scan_kernel, dim3(1), dim3(1024), 0, s, sp.n_docs, cnt, sp.fwd_ptr);
+  e = hipGetLastError();
+  if (e == hipSuccess) e = hipMemsetAsync(cnt, 0, (size_t)sp.n_docs * sizeof(int), s);
+  if (e != hipSuccess) return e;
+  const int tblocks = (int)std::min<long long>(65536, std::max(1, sp.vocab));
+  hipLaunchKernelGGL(fwd_fill_kernel, dim3(tblocks), dim3(256), 0, s, sp.vocab, sp.term_indptr, sp.post_chunk,
+                     sp.wpost, sp.fwd_ptr, cnt, sp.fwd_term, sp.fwd_w);
   return hipGetLastError();
 }
 
@@ -662,8 +777,8 @@ hipError_t launch_dense_first(const SparseIndex& sp, const int* qterm_indptr, co
                               const long long* cand, int n_cand, long long nq, int rrf_k, int k, float* out_fused,
                               long long* out_ids, hipStream_t s) {
   if (n_cand < 1 || n_cand > kDfCand) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(dense_first_kernel, dim3((unsigned)nq), dim3(kDfThreads), 0, s, sp.vocab, sp.term_indptr,
-                     sp.post_chunk, sp.idfk, sp.wpost, qterm_indptr, qterms, cand, n_cand, rrf_k, k, out_fused,
+  hipLaunchKernelGGL(dense_first_kernel, dim3((unsigned)nq), dim3(kDfThreads), 0, s, sp.vocab, sp.fwd_ptr,
+                     sp.fwd_term, sp.idfk, sp.fwd_w, qterm_indptr, qterms, cand, n_cand, rrf_k, k, out_fused,
                      out_ids);
   return hipGetLastError();
 }

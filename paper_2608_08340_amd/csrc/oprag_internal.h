@@ -84,6 +84,10 @@ struct SparseIndex {
   const int* post_tf = nullptr;             // caller-owned
   float* idfk = nullptr;                    // library-owned [vocab]: idf(t) * (k1 + 1)
   float* wpost = nullptr;                   // library-owned [nnz]: tf / (tf + k1 (1 - b + b dl / avgdl))
+  // library-owned chunk-major copy: chunk d's (term, weight) pairs at [fwd_ptr[d], fwd_ptr[d + 1])
+  long long* fwd_ptr = nullptr;             // [n_docs + 1]
+  int* fwd_term = nullptr;                  // [nnz]
+  float* fwd_w = nullptr;                   // [nnz]
   double avgdl = 0.0;
   float k1 = 0.f, b = 0.f;
 };
@@ -95,6 +99,9 @@ hipError_t sparse_validate(int vocab, long long n_docs, long long nnz, const lon
                            const int* chunk, const int* tf, const int* doc_len, unsigned int* d_flag,
                            hipStream_t s);
 hipError_t sparse_prepare(SparseIndex& sp, const int* doc_len, unsigned long long* d_sum, hipStream_t s);
+// Builds the chunk-major copy (fwd_ptr / fwd_term / fwd_w) from the postings and their
+// weights; cnt is scratch of n_docs ints.
+hipError_t sparse_forward(const SparseIndex& sp, int* cnt, hipStream_t s);
 size_t sparse_workspace_bytes(long long n_docs, int nq, int k);
 hipError_t launch_sparse(const SparseIndex& sp, const int* qterm_indptr, const int* qterms, int nq, int k,
                          float* out_scores, long long* out_ids, void* ws, hipStream_t s);
