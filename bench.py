@@ -313,6 +313,10 @@ def suite() -> int:
            algorithmic_bytes(N_ROWS, DIM, nq, 128), 2.0 * nq * N_ROWS * DIM,
            recall_at_5_vs_full=round(float(np.mean(inter)) / 5, 3),
            jaccard_vs_full=round(float(np.mean([x / len(set(a[i]) | set(b[i])) for i, x in enumerate(inter)])), 3))
+    # the paper's weighted fusion over every chunk (min-max normalised, 0.5 / 0.5), top-5
+    ms_w = _timed(lambda: nxt().search_hybrid_weighted(qd, qi, qterms, 0.5, 0.5, 5), 64, stream)
+    report("hybrid weighted: 0.5 minmax(dense) + 0.5 minmax(BM25) over all chunks -> 5, batch 256, cold", ms_w, nq,
+           algorithmic_bytes(N_ROWS, DIM, nq, 5) + sparse_bytes, 2.0 * nq * N_ROWS * DIM)
     for ix in idxs:
         ix.close()
     del idxs, rows

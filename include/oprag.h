@@ -58,7 +58,8 @@ typedef enum oprag_op {
   OPRAG_OP_DENSE = 0,
   OPRAG_OP_SPARSE = 1,
   OPRAG_OP_HYBRID = 2,
-  OPRAG_OP_DENSE_FIRST = 3
+  OPRAG_OP_DENSE_FIRST = 3,
+  OPRAG_OP_WEIGHTED = 4
 } oprag_op;
 
 typedef struct oprag_index oprag_index; /* opaque handle */
@@ -200,6 +201,25 @@ oprag_status oprag_search_hybrid_dense_first(oprag_index *idx, const void *q_dev
                                              const int32_t *qterms_dev, int64_t nq, int32_t n_cand, int32_t rrf_k,
                                              int32_t k, float *fused_dev, int64_t *ids_dev, void *workspace_dev,
                                              size_t workspace_bytes, void *stream);
+
+/*
+ * Weighted score fusion over the whole corpus (Section 4.4): score(d, q) = w_dense *
+ * s^_dense(d, q) + w_lex * s^_lexical(d, q) for every chunk 0 <= d < n_rows, where s^ is the
+ * per-query min-max normalisation over all chunks, (s - min) / (max - min), and 0 for every
+ * chunk when max == min (the paper states the formula but neither s^ nor the weights).
+ * s_dense is the inner product (fp32 accumulation), s_lexical the BM25 score of the attached
+ * sparse index (0 for chunks without a matching term and for chunks past its n_docs).  The
+ * weighted sum is formed in fp64 and rounded to fp32; top k by (score desc, id asc).
+ *   q_dev [nq x dim] (bf16 / fp16 index); qterm_indptr_dev / qterms_dev as in
+ *   oprag_search_sparse; scores_dev [nq x k] fp32, ids_dev [nq x k] int64.
+ * w_dense, w_lex finite and >= 0.  The scores of every chunk pass through the workspace
+ * (oprag_workspace_bytes(OPRAG_OP_WEIGHTED): 16 bytes per query and unit of capacity).
+ * E_STATE without an attached sparse index, E_UNSUPPORTED for an fp32 index.
+ */
+oprag_status oprag_search_hybrid_weighted(oprag_index *idx, const void *q_dev, const int32_t *qterm_indptr_dev,
+                                          const int32_t *qterms_dev, int64_t nq, float w_dense, float w_lex, int32_t k,
+                                          float *scores_dev, int64_t *ids_dev, void *workspace_dev,
+                                          size_t workspace_bytes, void *stream);
 
 /*
  * Kernel timing (diagnostics: measuring the scoring kernel against its roofline).  Arms a

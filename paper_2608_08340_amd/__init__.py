@@ -21,10 +21,10 @@ import threading
 import torch
 
 __all__ = ["Index", "OpragError", "rrf_fuse", "library", "LIB_PATH", "OP_DENSE", "OP_SPARSE", "OP_HYBRID",
-           "OP_DENSE_FIRST"]
+           "OP_DENSE_FIRST", "OP_WEIGHTED"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "liboprag.so")
-OP_DENSE, OP_SPARSE, OP_HYBRID, OP_DENSE_FIRST = 0, 1, 2, 3
+OP_DENSE, OP_SPARSE, OP_HYBRID, OP_DENSE_FIRST, OP_WEIGHTED = 0, 1, 2, 3, 4
 _DTYPE = {torch.float32: 0, torch.bfloat16: 1, torch.float16: 2}
 STATUS = {0: "OK", -1: "E_INVALID", -2: "E_CAPACITY", -3: "E_STATE", -4: "E_UNSUPPORTED", -5: "E_DEVICE"}
 
@@ -56,6 +56,8 @@ _SIGS = {
     "oprag_rrf_fuse": ([_P, _I32, _P, _I32, _I64, _I32, _I32, _P, _P, _P], _I32),
     "oprag_search_hybrid": ([_P, _P, _P, _P, _I64, _I32, _I32, _I32, _I32, _P, _P, _P, _SZ, _P], _I32),
     "oprag_search_hybrid_dense_first": ([_P, _P, _P, _P, _I64, _I32, _I32, _I32, _P, _P, _P, _SZ, _P], _I32),
+    "oprag_search_hybrid_weighted": ([_P, _P, _P, _P, _I64, ctypes.c_float, ctypes.c_float, _I32, _P, _P, _P, _SZ, _P],
+                                     _I32),
     "oprag_time_next_dense_kernel": ([_P, _P], _I32),
 }
 _lib = None
@@ -238,6 +240,25 @@ class Index:
                                                          n_cand, rrf_k, k, _ptr(fused), _ptr(ids), _ptr(ws),
                                                          ws.numel(), _stream(self.device)))
         return fused, ids
+
+    def search_hybrid_weighted(self, q: torch.Tensor, qterm_indptr: torch.Tensor, qterms: torch.Tensor,
+                               w_dense: float = 0.5, w_lex: float = 0.5, k: int = 5, out: tuple | None = None):
+        """w_dense * minmax(dense) + w_lex * minmax(BM25) over every chunk, top k.
+        Returns (scores fp32, ids int64), [nq x k]."""
+        _dev_tensor(q, self.dtype, self.device, "q")
+        _dev_tensor(qterm_indptr, torch.int32, self.device, "qterm_indptr")
+        _dev_tensor(qterms, torch.int32, self.device, "qterms")
+        nq = q.shape[0]
+        if qterm_indptr.numel() != nq + 1:
+            raise OpragError(-1, "qterm_indptr must have nq + 1 entries")
+        scores, ids = out if out is not None else (
+            torch.empty((nq, k), dtype=torch.float32, device=self.device),
+            torch.empty((nq, k), dtype=torch.int64, device=self.device))
+        ws = self.workspace(OP_WEIGHTED, nq, 1, 1)
+        _check(library().oprag_search_hybrid_weighted(self._h, _ptr(q), _ptr(qterm_indptr), _ptr(qterms), nq,
+                                                      w_dense, w_lex, k, _ptr(scores), _ptr(ids), _ptr(ws),
+                                                      ws.numel(), _stream(self.device)))
+        return scores, ids
 
 
 def rrf_fuse(dense_ids: torch.Tensor, sparse_ids: torch.Tensor, rrf_k: int = 60, k: int = 5):

@@ -114,6 +114,14 @@ size_t dense_first_ws(const oprag_index* idx, int64_t nq, int32_t n_cand) {
   return align_up((size_t)nq * n_cand * 8) + align_up((size_t)nq * n_cand * 4) + align_up(dense_ws(idx, nq, n_cand));
 }
 
+// Weighted fusion: dense scores, lexical scores (each [nq x ld], ld = capacity rounded up to
+// 4), composites [nq x capacity], counts [nq].
+long long weighted_ld(const oprag_index* idx) { return (idx->capacity + 3) & ~3ll; }
+size_t weighted_ws(const oprag_index* idx, int64_t nq) {
+  const size_t ld = (size_t)weighted_ld(idx);
+  return 2 * align_up((size_t)nq * ld * 4) + align_up((size_t)nq * (size_t)idx->capacity * 8) + align_up((size_t)nq * 4);
+}
+
 oprag_status do_dense(oprag_index* idx, const void* q, int64_t nq, int32_t k, float* scores, int64_t* ids, void* ws,
                       size_t ws_bytes, hipStream_t s) {
   const size_t es = elem_size(idx->dtype);
@@ -346,6 +354,9 @@ oprag_status oprag_workspace_bytes(const oprag_index* idx, int32_t op, int64_t n
       if (oprag_status st = check_k(k_sparse, "k_sparse")) return st;
       *bytes = nq ? hybrid_ws(idx, nq, k_dense, k_sparse) : 0;
       return ok();
+    case OPRAG_OP_WEIGHTED:
+      *bytes = nq ? weighted_ws(idx, nq) : 0;
+      return ok();
     case OPRAG_OP_DENSE_FIRST:
       if (oprag_status st = check_k(k_dense, "k_dense (n_cand)")) return st;
       *bytes = nq ? dense_first_ws(idx, nq, k_dense) : 0;
@@ -497,6 +508,59 @@ oprag_status oprag_search_hybrid_dense_first(oprag_index* idx, const void* q_dev
       oprag::launch_dense_first(idx->sp, qterm_indptr_dev, qterms_dev, reinterpret_cast<const long long*>(c_ids),
                                 n_cand, nq, rrf_k, k, fused_dev, reinterpret_cast<long long*>(ids_dev), s);
   if (e != hipSuccess) return hip_fail(e, "dense-first rerank launch");
+  return ok();
+}
+
+oprag_status oprag_search_hybrid_weighted(oprag_index* idx, const void* q_dev, const int32_t* qterm_indptr_dev,
+                                          const int32_t* qterms_dev, int64_t nq, float w_dense, float w_lex, int32_t k,
+                                          float* scores_dev, int64_t* ids_dev, void* workspace_dev,
+                                          size_t workspace_bytes, void* stream) {
+  if (oprag_status st = check_index(idx)) return st;
+  if (!idx->has_sparse) return fail(OPRAG_E_STATE, "no sparse index attached");
+  if (idx->dtype == OPRAG_F32) return fail(OPRAG_E_UNSUPPORTED, "weighted fusion needs a bf16 or fp16 index");
+  if (oprag_status st = check_k(k, "k")) return st;
+  if (!(std::isfinite(w_dense) && w_dense >= 0.f && std::isfinite(w_lex) && w_lex >= 0.f))
+    return fail(OPRAG_E_INVALID, "weights must be finite and >= 0");
+  if (nq < 0 || nq > (int64_t)1 << 24) return fail(OPRAG_E_INVALID, "nq %lld out of range", (long long)nq);
+  if (nq == 0) return ok();
+  if (oprag_status st = check_buf(q_dev, "q_dev")) return st;
+  if (oprag_status st = check_buf(qterm_indptr_dev, "qterm_indptr_dev")) return st;
+  if (!qterms_dev) return fail(OPRAG_E_INVALID, "qterms_dev is NULL");
+  if (oprag_status st = check_buf(scores_dev, "scores_dev")) return st;
+  if (oprag_status st = check_buf(ids_dev, "ids_dev")) return st;
+  const size_t need = weighted_ws(idx, nq);
+  if (!workspace_dev || !aligned16(workspace_dev) || workspace_bytes < need)
+    return fail(OPRAG_E_INVALID, "workspace missing or too small (%zu < %zu bytes)", workspace_bytes, need);
+  const oprag::DensePlan p = oprag::plan_dense_dump(idx->dtype, idx->dim, idx->n_rows, (int)nq);
+  if (p.kernel < 0) return fail(OPRAG_E_UNSUPPORTED, "no scoring kernel for dtype %d", idx->dtype);
+  DeviceScope ds(idx->device);
+  if (ds.error() != hipSuccess) return hip_fail(ds.error(), "select device");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const long long ld = weighted_ld(idx);
+  unsigned char* w = static_cast<unsigned char*>(workspace_dev);
+  float* D = reinterpret_cast<float*>(w);
+  w += align_up((size_t)nq * (size_t)ld * 4);
+  float* B = reinterpret_cast<float*>(w);
+  w += align_up((size_t)nq * (size_t)ld * 4);
+  unsigned long long* cbuf = reinterpret_cast<unsigned long long*>(w);
+  w += align_up((size_t)nq * (size_t)idx->capacity * 8);
+  int* ccnt = reinterpret_cast<int*>(w);
+  oprag::DenseArgs a;
+  a.X = idx->slab;
+  a.n_rows = idx->n_rows;
+  a.d = idx->dim;
+  a.Q = q_dev;
+  a.nq = (int)nq;
+  a.k = 1;
+  a.dump = D;
+  a.dump_ld = ld;
+  hipError_t e = oprag::launch_dense_dump(p, a, s);
+  if (e == hipSuccess) e = oprag::launch_sparse_dump(idx->sp, qterm_indptr_dev, qterms_dev, (int)nq, B, ld, s);
+  if (e == hipSuccess)
+    e = oprag::launch_weighted_fuse(D, B, ld, idx->n_rows, std::min<long long>(idx->sp.n_docs, idx->n_rows), (int)nq,
+                                    (double)w_dense, (double)w_lex, k, cbuf, ccnt, scores_dev,
+                                    reinterpret_cast<long long*>(ids_dev), s);
+  if (e != hipSuccess) return hip_fail(e, "weighted fusion launch");
   return ok();
 }
 

@@ -125,6 +125,8 @@ struct SparseArgs {
   int nq;
   int k;
   int n_ranges;
+  float* dump = nullptr;         // when set: every chunk's score to dump[q * dump_ld + chunk], no top-k
+  long long dump_ld = 0;
   float* out_scores;            // final output when n_ranges == 1
   long long* out_ids;
   unsigned long long* partial;  // [nq x n_ranges x k] when n_ranges > 1
@@ -240,6 +242,11 @@ __global__ __launch_bounds__(kNT) void bm25_kernel(SparseArgs a) {
     }
   }
   __syncthreads();
+  if (a.dump != nullptr) {  // launch-uniform: the range's scores, no selection
+    float* dst = a.dump + (long long)q * a.dump_ld + d0;
+    for (int i = tid; i < len; i += kNT) dst[i] = acc[i];
+    return;
+  }
 
   // ---- exact top-k of the range's positive scores (positive fp32 bits order as uints)
   const uint32_t* keys = reinterpret_cast<const uint32_t*>(acc);
@@ -735,6 +742,29 @@ hipError_t sparse_forward(const SparseIndex& sp, int* cnt, hipStream_t s) {
   const int tblocks = (int)std::min<long long>(65536, std::max(1, sp.vocab));
   hipLaunchKernelGGL(fwd_fill_kernel, dim3(tblocks), dim3(256), 0, s, sp.vocab, sp.term_indptr, sp.post_chunk,
                      sp.wpost, sp.fwd_ptr, cnt, sp.fwd_term, sp.fwd_w);
+  return hipGetLastError();
+}
+
+hipError_t launch_sparse_dump(const SparseIndex& sp, const int* qterm_indptr, const int* qterms, int nq, float* dump,
+                              long long ld, hipStream_t s) {
+  SparseArgs a;
+  a.vocab = sp.vocab;
+  a.n_docs = sp.n_docs;
+  a.indptr = sp.term_indptr;
+  a.chunk = sp.post_chunk;
+  a.idfk = sp.idfk;
+  a.wpost = sp.wpost;
+  a.qterm_indptr = qterm_indptr;
+  a.qterms = qterms;
+  a.nq = nq;
+  a.k = 1;
+  a.n_ranges = (int)((sp.n_docs + kSparseRange - 1) / kSparseRange);
+  a.dump = dump;
+  a.dump_ld = ld;
+  a.out_scores = nullptr;
+  a.out_ids = nullptr;
+  a.partial = nullptr;
+  hipLaunchKernelGGL(bm25_kernel, dim3((unsigned)(nq * a.n_ranges)), dim3(kNT), 0, s, a);
   return hipGetLastError();
 }
 

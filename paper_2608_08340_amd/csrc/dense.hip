@@ -424,6 +424,46 @@ struct SelOf<BN, KS, 2, NT> {
   typedef SelFilter<BN> type;
 };
 
+// Score dump (SEL 3): no selection; every score of the tile goes to a.dump.
+struct SelDump {
+  static constexpr int kBytes = 16;
+  __device__ __forceinline__ void init() {}
+  __device__ __forceinline__ void pass(const float*, int, int, const PassRows&, int, int, unsigned char*) {}
+  __device__ __forceinline__ void write(const DenseArgs&, int, long long) const {}
+};
+template <int BN, int KS, int NT>
+struct SelOf<BN, KS, 3, NT> {
+  typedef SelDump type;
+};
+
+// acc[mi][ni][r] is the score of row tile0 + 16*MW*wave + 16*mi + 4*(lane/16) + r against
+// query slot 16*ni + lane%16: four consecutive rows per lane and query, stored as one 16-byte
+// write when all four exist (dump_ld is a multiple of 4).
+template <int BN, int MW, int WV>
+__device__ __forceinline__ void dump_tile(const f32x4 (&acc)[MW][BN / 16], long long tile0, long long row_end,
+                                          int q0, int q_lim, const DenseArgs& a) {
+  constexpr int NW = BN / 16;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const long long r0 = tile0 + w * MW * 16 + (lane >> 4) * 4;
+#pragma unroll
+  for (int ni = 0; ni < NW; ++ni) {
+    const int n = ni * 16 + (lane & 15);
+    if (n >= q_lim) continue;
+    float* dst = a.dump + (long long)(q0 + n) * a.dump_ld;
+#pragma unroll
+    for (int mi = 0; mi < MW; ++mi) {
+      const long long row = r0 + mi * 16;
+      if (row + 3 < row_end) {
+        *reinterpret_cast<f32x4*>(dst + row) = acc[mi][ni];
+      } else {
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (row + r < row_end) dst[row + r] = acc[mi][ni][r];
+      }
+    }
+  }
+}
+
 // Owner thread of query slot n: append its staged keys (the stage's first SCAP slots; a count
 // beyond SCAP means the rest already went out directly) to the global buffer.
 template <int BN>
@@ -921,7 +961,7 @@ __global__ __launch_bounds__(WV * 64) void dense_mfma_kernel(DenseArgs a) {
   constexpr int QBYTES = (QR > 0 ? QR : 2) * QSLOT;
   static_assert(QR == 0 || SEL == 2, "resident queries: filtered selection only");
   constexpr bool kBlk = SEL == 0 && KS == 5;
-  constexpr int SB0 = SEL == 2 ? 0 : BN * SR * 4;
+  constexpr int SB0 = SEL >= 2 ? 0 : BN * SR * 4;
   constexpr int SBYTES = kBlk && BlockArea<MW, BN>::kBytes > SB0 ? BlockArea<MW, BN>::kBytes : SB0;
   constexpr int SMEM = QBYTES + SBYTES + Sel::kBytes;
   static_assert(MW % G == 0 && ((MWP * 16) & (MWP * 16 - 1)) == 0, "pass shape");
@@ -1109,7 +1149,10 @@ __global__ __launch_bounds__(WV * 64) void dense_mfma_kernel(DenseArgs a) {
       const long long tile0 = row_begin + (long long)t * TR;
       bool refresh = false;  // the group path ran: thresholds and lists of the fast path to restore
       bool done = false;
-      if constexpr (SEL == 2) {
+      if constexpr (SEL == 3) {
+        dump_tile<BN, MW, WV>(acc, tile0, row_end, q0, q_lim, a);
+        done = true;
+      } else if constexpr (SEL == 2) {
         if (a.th == nullptr)  // launch-uniform
           filt_all_tile<BN, MW, WV>(acc, tile0, row_end, q0, q_lim, a);
         else
@@ -1428,6 +1471,58 @@ __global__ __launch_bounds__(kThreads) void select_topk_kernel(const unsigned lo
   }
 }
 
+// Weighted fusion (Section 4.4): per query, the dense and lexical scores of every chunk,
+// min-max normalised over all chunks (a constant row normalises to 0), weighted and summed in
+// fp64, rounded to fp32 and written as composites for the exact selection.  Lexical scores
+// past n_lex chunks are 0.  One workgroup per query.
+__global__ __launch_bounds__(kThreads) void weighted_fuse_kernel(const float* __restrict__ D,
+                                                                 const float* __restrict__ B, long long ld,
+                                                                 long long n, long long n_lex, double wd, double wl,
+                                                                 unsigned long long* cbuf, int* ccnt) {
+  __shared__ float red[4][kThreads / 64];
+  const long long q = blockIdx.x;
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const float* d = D + q * ld;
+  const float* b = B + q * ld;
+  float mnd = __builtin_inff(), mxd = -__builtin_inff(), mnl = __builtin_inff(), mxl = -__builtin_inff();
+  for (long long i = t; i < n; i += kThreads) {
+    const float x = d[i], y = i < n_lex ? b[i] : 0.f;
+    mnd = fminf(mnd, x);
+    mxd = fmaxf(mxd, x);
+    mnl = fminf(mnl, y);
+    mxl = fmaxf(mxl, y);
+  }
+  for (int o = 32; o > 0; o >>= 1) {
+    mnd = fminf(mnd, __shfl_xor(mnd, o));
+    mxd = fmaxf(mxd, __shfl_xor(mxd, o));
+    mnl = fminf(mnl, __shfl_xor(mnl, o));
+    mxl = fmaxf(mxl, __shfl_xor(mxl, o));
+  }
+  if (lane == 0) {
+    red[0][w] = mnd;
+    red[1][w] = mxd;
+    red[2][w] = mnl;
+    red[3][w] = mxl;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int u = 0; u < kThreads / 64; ++u) {
+    mnd = fminf(mnd, red[0][u]);
+    mxd = fmaxf(mxd, red[1][u]);
+    mnl = fminf(mnl, red[2][u]);
+    mxl = fmaxf(mxl, red[3][u]);
+  }
+  const double sd = mxd > mnd ? wd / ((double)mxd - (double)mnd) : 0.0;
+  const double sl = mxl > mnl ? wl / ((double)mxl - (double)mnl) : 0.0;
+  unsigned long long* dst = cbuf + q * n;
+  for (long long i = t; i < n; i += kThreads) {
+    const double x = d[i], y = i < n_lex ? b[i] : 0.f;
+    const float f = (float)(sd * (x - mnd) + sl * (y - mnl));
+    dst[i] = composite(f, (uint32_t)i);
+  }
+  if (t == 0) ccnt[q] = (int)n;
+}
+
 // Clears the filtered-mode counters (a kernel, not a memset: safe inside captured graphs).
 __global__ void clear_ints_kernel(int* p, long long n, const int* gate) {
   if (gate != nullptr && *gate == 0) return;
@@ -1598,7 +1693,8 @@ struct KernelInfo {
       MFK(DT, 2, 4, 8, 1, 8, 1, 4, 1, 1 << 30), MFK(DT, 2, 4, 4, 1, 8, 1, 4, 1, 1 << 30),            \
       MFK(DT, 1, 1, 16, 1, 5, 2, 8, 1, 16), MFK(DT, 1, 1, 4, 1, 5, 2, 8, 1, 16),                     \
       MFK(DT, 4, 2, 8, 1, 5, 2, 4, 17, 64), MFK(DT, 4, 2, 4, 1, 5, 2, 4, 17, 64),                    \
-      MFKQ(DT, 8, 4, 4, 1, 5, 2, 2, 65, 1 << 30, kWaves, 3), MFK(DT, 8, 4, 4, 1, 5, 2, 2, 65, 1 << 30)
+      MFKQ(DT, 8, 4, 4, 1, 5, 2, 2, 65, 1 << 30, kWaves, 3), MFK(DT, 8, 4, 4, 1, 5, 2, 2, 65, 1 << 30), \
+      MFK(DT, 8, 4, 4, 1, 5, 3, 2, 1, 1 << 30)
 
 const KernelInfo kKernels[] = {
     {dense_f32_kernel<5, 0>, kDtypeF32, 32, 64, 5, 0, 4, 1, 1 << 30, 0, kThreads, 0},
@@ -1866,5 +1962,37 @@ hipError_t launch_dense(const DensePlan& p, int dtype, const DenseArgs& a, hipSt
   return hipGetLastError();
 }
 
+
+DensePlan plan_dense_dump(int dtype, int d, long long n_rows, int nq) {
+  DensePlan p;
+  p.kernel = pick_kernel(dtype, d, nq, 5, 3);
+  if (p.kernel < 0) return p;
+  const KernelInfo& ki = kKernels[p.kernel];
+  p.bn = ki.bn;
+  p.tile_rows = ki.tile_rows;
+  p.n_qblocks = (nq + p.bn - 1) / p.bn;
+  long long mc = 1;
+  const long long bound = chunk_bound(ki, d, n_rows, p.n_qblocks, &mc);
+  split_rows(p, n_rows, bound, mc);
+  return p;
+}
+
+hipError_t launch_dense_dump(const DensePlan& p, const DenseArgs& a, hipStream_t s) {
+  DenseArgs arg = a;
+  arg.n_qblocks = p.n_qblocks;
+  arg.n_chunks = p.n_chunks;
+  arg.rows_per_chunk = p.rows_per_chunk;
+  return launch_kernel(kKernels[p.kernel], p.grid, arg, s, nullptr, nullptr);
+}
+
+hipError_t launch_weighted_fuse(const float* D, const float* B, long long ld, long long n, long long n_lex, int nq,
+                                double wd, double wl, int k, unsigned long long* cbuf, int* ccnt, float* out_scores,
+                                long long* out_ids, hipStream_t s) {
+  hipLaunchKernelGGL(weighted_fuse_kernel, dim3((unsigned)nq), dim3(kThreads), 0, s, D, B, ld, n, n_lex, wd, wl, cbuf,
+                     ccnt);
+  hipLaunchKernelGGL(select_topk_kernel, dim3((unsigned)nq), dim3(kThreads), 0, s, cbuf, ccnt, n, k, out_scores, out_ids,
+                     nullptr, nullptr, 0);
+  return hipGetLastError();
+}
 
 }  // namespace oprag

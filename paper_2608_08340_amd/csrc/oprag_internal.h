@@ -35,6 +35,9 @@ struct DenseArgs {
   long long cap = 0;
   // When set, the launch does nothing unless *gate != 0 (a device-side overflow flag).
   const int* gate = nullptr;
+  // Score dump (SEL 3): every score to dump[q * dump_ld + row].
+  float* dump = nullptr;
+  long long dump_ld = 0;
 };
 
 struct DensePlan {
@@ -66,6 +69,14 @@ DensePlan plan_dense(int dtype, int d, long long n_rows, int nq, int k);
 // The per-chunk-list plan for any k (the exact fallback of the filtered mode).
 DensePlan plan_dense_lists(int dtype, int d, long long n_rows, int nq, int k);
 size_t dense_workspace_bytes(const DensePlan& p, int nq);
+// Score dump: every score of nq queries against rows [0, a.n_rows) into a.dump (SEL 3 kernel).
+DensePlan plan_dense_dump(int dtype, int d, long long n_rows, int nq);
+hipError_t launch_dense_dump(const DensePlan& p, const DenseArgs& a, hipStream_t s);
+// Weighted fusion of dense scores D and lexical scores B ([nq x ld], lexical 0 past n_lex),
+// min-max normalised per query over n chunks, then the exact top k (cbuf [nq x n], ccnt [nq]).
+hipError_t launch_weighted_fuse(const float* D, const float* B, long long ld, long long n, long long n_lex, int nq,
+                                double wd, double wl, int k, unsigned long long* cbuf, int* ccnt, float* out_scores,
+                                long long* out_ids, hipStream_t s);
 // Enough workspace for a search of nq queries at any row count up to `capacity`.
 size_t dense_workspace_bound(int dtype, int d, long long capacity, int nq, int k);
 // ev0 / ev1 (optional) are recorded on s right before and after the scoring kernel (in
@@ -109,6 +120,9 @@ hipError_t launch_sparse(const SparseIndex& sp, const int* qterm_indptr, const i
 // ---------------------------------------------------------------- fusion and upsert
 // Dense-first hybrid: BM25 of the dense candidates cand [nq x n_cand] (dense order, -1 padded,
 // 1 <= n_cand <= 128), reciprocal rank fusion with their dense order, top k.
+// BM25 scores of every chunk [0, n_docs) for nq queries into dump [nq x ld].
+hipError_t launch_sparse_dump(const SparseIndex& sp, const int* qterm_indptr, const int* qterms, int nq, float* dump,
+                              long long ld, hipStream_t s);
 hipError_t launch_dense_first(const SparseIndex& sp, const int* qterm_indptr, const int* qterms,
                               const long long* cand, int n_cand, long long nq, int rrf_k, int k, float* out_fused,
                               long long* out_ids, hipStream_t s);

@@ -324,3 +324,49 @@ def test_dense_first_32k_against_oracle_and_full_hybrid(c3, correlated):
     log(f"dense-first vs full hybrid ({'correlated' if correlated else 'independent'} terms): "
         f"Recall@5 {recall:.3f}, Jaccard {jacc:.3f}")
     assert 0.0 <= jacc <= recall <= 1.0
+
+
+def _check_weighted(F, sc, ids, k, label):
+    reps = accept.check_batch(F, ids.cpu().numpy(), sc.cpu().numpy(), k, rtol=1e-3)
+    bad = [(q, r.problems) for q, r in enumerate(reps) if not r.ok]
+    assert not bad, f"{label}: {len(bad)} queries fail, first {bad[:2]}"
+
+
+@pytest.mark.parametrize("w_d,w_l,k", [(0.5, 0.5, 5), (0.8, 0.2, 17), (1.0, 0.0, 10), (0.0, 1.0, 10)])
+def test_weighted_fusion_small_corpus(w_d, w_l, k):
+    """Weighted fusion (min-max normalised dense and BM25 over every chunk) on a 3,000-row
+    d = 128 index whose sparse corpus covers only the first 2,500 chunks (the rest score 0
+    lexically): the GPU top-k passes the acceptance rules against the fp64 oracle's fused
+    scores.  Queries 0-3 have no terms, only unknown terms, repeats and a mix."""
+    from oracle import weighted
+    dev = device()
+    n, n_docs, nq = 3000, 2500, 40
+    ind, toks, csr, qi, qt = _small_corpus(1500 + k, n_docs, 300, 30.0, nq)
+    w = synth.mixture_dense(1501 + k, n, 128, 16, nq, k, "bf16")
+    idx = make_index(w.rows, "bf16")
+    _attach(idx, csr, dev)
+    log("weighted small", w_d, w_l, k)
+    sc, ids = idx.search_hybrid_weighted(w.queries.to(dev), _t(qi, dev), _t(qt, dev), w_d, w_l, k)
+    torch.cuda.synchronize()
+    S, X, Q = oracle_scores(w.rows, w.queries, "bf16")
+    qt_oracle = np.where((qt >= 0) & (qt < 300), qt, 10 ** 6).astype(np.int64)
+    B = np.zeros((nq, n))
+    B[:, :n_docs] = bm25.scores_batch(ind, toks, qi, qt_oracle, 1.2, 0.75)
+    _check_weighted(weighted.fused(S, B, w_d, w_l), sc, ids, k, f"w=({w_d},{w_l}) k={k}")
+
+
+@pytest.mark.timeout(300)
+def test_weighted_fusion_32k(c3):
+    """The 32,768 x 1,024 bf16 hybrid workload with weights 0.5 / 0.5, top-5, every query
+    against the fp64 oracle."""
+    from oracle import weighted
+    dev = device()
+    h = c3
+    w = h.dense
+    idx = make_index(w.rows, "bf16")
+    _attach(idx, h.csr, dev, h.k1, h.b)
+    sc, ids = idx.search_hybrid_weighted(w.queries.to(dev), _t(h.qterm_indptr, dev), _t(h.qterms, dev), 0.5, 0.5, 5)
+    torch.cuda.synchronize()
+    S, X, Q = oracle_scores(w.rows, w.queries, "bf16")
+    B = bm25.scores_batch(h.doc_indptr, h.tokens, h.qterm_indptr, h.qterms, h.k1, h.b)
+    _check_weighted(weighted.fused(S, B), sc, ids, 5, "32k weighted")
