@@ -321,6 +321,20 @@ def suite() -> int:
         ix.close()
     del idxs, rows
 
+    # embedding tail fused with the upsert: 256 chunks x 512 tokens of 1,024-wide bf16 hidden
+    # states (seeded synthetic; lengths uniform in [64, 512]) -> mean pool -> L2 -> bf16 rows
+    g = np.random.default_rng(11)
+    m_e, t_e = 256, 512
+    hid = torch.randn((m_e, t_e, DIM), generator=torch.Generator().manual_seed(11)).to(torch.bfloat16).to(dev)
+    lens = torch.from_numpy(g.integers(64, t_e + 1, size=m_e).astype(np.int32)).to(dev)
+    ixe = Index(DIM, m_e * 40, torch.bfloat16)
+    ms_e = _timed(lambda: ixe.upsert_pooled(hid, lens), 32, stream)
+    tok = int(lens.sum().item())
+    report("embedding tail: mean pool + L2 + upsert, 256 chunks x <=512 tokens x 1,024 bf16 hidden", ms_e, m_e,
+           tok * DIM * 2 + m_e * DIM * 2, 0.0, valid_tokens=tok)
+    ixe.close()
+    del hid
+
     # 1,048,576 x 768 bf16, batch 1,024, top-10 (larger than the Infinity Cache)
     w4 = synth.mixture_dense(4, 1 << 20, 768, 4096, 1024, 10, "bf16")
     ix = Index(768, 1 << 20, torch.bfloat16)

@@ -105,6 +105,21 @@ oprag_status oprag_upsert(oprag_index *idx, const void *rows_dev, int32_t rows_d
                           int64_t *first_row);
 
 /*
+ * Embedding tail fused with the upsert: Op_embed's last two steps (Section 4.3: mean pool of
+ * the model's hidden states over the chunk's tokens, then L2 normalisation) followed by
+ * Op_upsert of the resulting vectors (appended as in oprag_upsert, all or nothing).
+ *   hidden_dev  [m x T x dim] in hidden_dtype (OPRAG_BF16 or OPRAG_F32), chunk-major;
+ *   lengths_dev [m] int32: chunk i's tokens are 0 .. lengths[i] - 1 (right padding; values
+ *               outside [0, T] are clamped).
+ * Row n_rows + i becomes sum / ||sum|| of chunk i's valid hidden states (sums in fp32 in token
+ * order, the norm in fp64; the mean's 1/len cancels), rounded to nearest even to the index
+ * dtype; a chunk with no tokens or a zero sum becomes the zero vector.  *first_row (optional)
+ * receives the first new id.  Asynchronous on `stream`.
+ */
+oprag_status oprag_upsert_pooled(oprag_index *idx, const void *hidden_dev, int32_t hidden_dtype,
+                                 const int32_t *lengths_dev, int64_t m, int32_t T, void *stream, int64_t *first_row);
+
+/*
  * Attach the inverted-postings index BM25 scores from (Section 4.4): CSR term -> (chunk, tf)
  * over chunk ids [0, n_docs) (the same ids as the dense rows; n_docs <= capacity).
  *   term_indptr_dev [vocab + 1] int64, term_indptr[0] = 0, term_indptr[vocab] = nnz;

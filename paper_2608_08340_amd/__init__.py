@@ -56,6 +56,7 @@ _SIGS = {
     "oprag_rrf_fuse": ([_P, _I32, _P, _I32, _I64, _I32, _I32, _P, _P, _P], _I32),
     "oprag_search_hybrid": ([_P, _P, _P, _P, _I64, _I32, _I32, _I32, _I32, _P, _P, _P, _SZ, _P], _I32),
     "oprag_search_hybrid_dense_first": ([_P, _P, _P, _P, _I64, _I32, _I32, _I32, _P, _P, _P, _SZ, _P], _I32),
+    "oprag_upsert_pooled": ([_P, _P, _I32, _P, _I64, _I32, _P, ctypes.POINTER(_I64)], _I32),
     "oprag_search_hybrid_weighted": ([_P, _P, _P, _P, _I64, ctypes.c_float, ctypes.c_float, _I32, _P, _P, _P, _SZ, _P],
                                      _I32),
     "oprag_time_next_dense_kernel": ([_P, _P], _I32),
@@ -150,6 +151,24 @@ class Index:
         first = ctypes.c_int64()
         _check(library().oprag_upsert(self._h, _ptr(rows) if rows.numel() else None, _DTYPE[rows.dtype],
                                       rows.shape[0], _stream(self.device), ctypes.byref(first)))
+        return first.value
+
+    def upsert_pooled(self, hidden: torch.Tensor, lengths: torch.Tensor) -> int:
+        """Mean-pool hidden states [m x T x dim] (bf16 or fp32) over each chunk's first lengths[i]
+        tokens, L2-normalise, append; returns the first new id."""
+        if hidden.dtype not in (torch.bfloat16, torch.float32):
+            raise OpragError(-1, f"hidden states must be bf16 or fp32, not {hidden.dtype}")
+        if hidden.dim() != 3 or hidden.shape[2] != self.dim:
+            raise OpragError(-1, f"hidden must be [m x T x {self.dim}]")
+        _dev_tensor(hidden, hidden.dtype, self.device, "hidden")
+        _dev_tensor(lengths, torch.int32, self.device, "lengths")
+        if lengths.numel() != hidden.shape[0]:
+            raise OpragError(-1, "lengths must have m entries")
+        first = ctypes.c_int64()
+        m = hidden.shape[0]
+        _check(library().oprag_upsert_pooled(self._h, _ptr(hidden) if m else None, _DTYPE[hidden.dtype],
+                                             _ptr(lengths) if m else None, m, max(1, hidden.shape[1]),
+                                             _stream(self.device), ctypes.byref(first)))
         return first.value
 
     def attach_sparse(self, term_indptr: torch.Tensor, post_chunk: torch.Tensor, post_tf: torch.Tensor,

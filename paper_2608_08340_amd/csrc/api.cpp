@@ -248,6 +248,32 @@ oprag_status oprag_upsert(oprag_index* idx, const void* rows_dev, int32_t rows_d
   return ok();
 }
 
+oprag_status oprag_upsert_pooled(oprag_index* idx, const void* hidden_dev, int32_t hidden_dtype,
+                                 const int32_t* lengths_dev, int64_t m, int32_t T, void* stream, int64_t* first_row) {
+  if (oprag_status st = check_index(idx)) return st;
+  if (m < 0) return fail(OPRAG_E_INVALID, "m = %lld < 0", (long long)m);
+  if (hidden_dtype != OPRAG_BF16 && hidden_dtype != OPRAG_F32)
+    return fail(OPRAG_E_INVALID, "hidden_dtype %d must be OPRAG_BF16 or OPRAG_F32", hidden_dtype);
+  if (T < 1 || T > (1 << 20)) return fail(OPRAG_E_INVALID, "T = %d outside [1, 2^20]", T);
+  if (m > idx->capacity - idx->n_rows)
+    return fail(OPRAG_E_CAPACITY, "upsert of %lld rows exceeds capacity (%lld of %lld used)", (long long)m,
+                (long long)idx->n_rows, (long long)idx->capacity);
+  if (m == 0) {
+    if (first_row) *first_row = idx->n_rows;
+    return ok();
+  }
+  if (oprag_status st = check_buf(hidden_dev, "hidden_dev")) return st;
+  if (oprag_status st = check_buf(lengths_dev, "lengths_dev")) return st;
+  DeviceScope ds(idx->device);
+  if (ds.error() != hipSuccess) return hip_fail(ds.error(), "select device");
+  const hipError_t e = oprag::launch_pool_upsert(idx->slab, idx->dtype, idx->dim, idx->n_rows, hidden_dev,
+                                                 hidden_dtype, lengths_dev, m, T, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "pooled upsert launch");
+  if (first_row) *first_row = idx->n_rows;
+  idx->n_rows += m;
+  return ok();
+}
+
 oprag_status oprag_sparse_attach(oprag_index* idx, int32_t vocab, int64_t n_docs, int64_t nnz,
                                  const int64_t* term_indptr_dev, const int32_t* post_chunk_dev,
                                  const int32_t* post_tf_dev, const int32_t* doc_len_dev, float k1, float b,

@@ -128,6 +128,11 @@ hipError_t launch_dense_first(const SparseIndex& sp, const int* qterm_indptr, co
                               long long* out_ids, hipStream_t s);
 hipError_t launch_rrf(const long long* dense_ids, int k_dense, const long long* sparse_ids, int k_sparse,
                       long long nq, int rrf_k, int k, float* out_fused, long long* out_ids, hipStream_t s);
+// Mean pool over each chunk's first lengths[i] (clamped to [0, T]) tokens of hidden states
+// [m x T x d] (bf16 or fp32), L2 normalisation, round to the slab dtype into rows
+// [first_row, first_row + m).
+hipError_t launch_pool_upsert(void* slab, int slab_dtype, int d, long long first_row, const void* hidden,
+                              int hidden_dtype, const int* lengths, long long m, int T, hipStream_t s);
 hipError_t launch_upsert(void* slab, int slab_dtype, int d, long long first_row, const void* rows,
                          int rows_dtype, long long m, hipStream_t s);
 

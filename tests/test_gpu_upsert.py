@@ -159,3 +159,65 @@ def test_streaming_upsert_and_search_small():
 def test_streaming_8m_x_384_f16_top100_full_size():
     """8,388,608 x 384 fp16 rows (8,192 clusters), 16 rounds of +65,536 rows and 4,096 queries, top-100."""
     _streaming(n0=8388608, rounds=16, m=65536, d=384, clusters=8192, nq=4096, k=100, sample=4)
+
+
+def _ulp(x: np.ndarray, dtype: str) -> np.ndarray:
+    """One unit in the last place of the storage dtype at |x| (normal range)."""
+    mant = {"bf16": 7, "f16": 10, "f32": 23}[dtype]
+    e = np.floor(np.log2(np.maximum(np.abs(x), 1e-30)))
+    return np.exp2(e - mant)
+
+
+@pytest.mark.parametrize("dtype,hidden_dtype,d", [(a, b, 128) for a in ("bf16", "f16", "f32") for b in ("bf16", "f32")]
+                         + [("bf16", "bf16", 1152), ("f32", "f32", 260)])
+def test_pooled_upsert_matches_mean_pool_l2_oracle(dtype, hidden_dtype, d):
+    """Embedding tail fused with the upsert: 45 chunks of up to 50 hidden states of width d
+    (128; 1,152 = one full and one partial block of 1,024 dimensions; 260, not a multiple of
+    eight, for the element-wise path) (lengths include 0, 1, T, above T and negative, clamped to [0, T]), appended after 11
+    existing rows.  Each stored element is within one unit in the last place of the storage
+    dtype, plus the fp32 summation bound len * 2^-24 * sum|h| / ||sum||, of the fp64 mean-pool
+    + L2 oracle; zero chunks are stored as zeros, and a pooled row used as a query finds
+    itself."""
+    from oracle import embed_tail
+    from paper_2608_08340_amd import Index
+    dev = device()
+    g = np.random.default_rng(77)
+    m, T = 45, 50
+    H = g.standard_normal((m, T, d)).astype(np.float32) + 0.3
+    lengths = g.integers(1, T + 1, size=m).astype(np.int32)
+    lengths[:6] = [0, 1, T, T + 9, -3, 2]
+    H[5, :2] = 0.0  # zero sum
+    Ht = torch.from_numpy(H)
+    if hidden_dtype == "bf16":
+        Ht = Ht.to(torch.bfloat16)
+    H64 = Ht.float().numpy().astype(np.float64)
+    idx = Index(d, 100, DT[dtype])
+    base = g.standard_normal((11, d))
+    base /= np.linalg.norm(base, axis=1, keepdims=True)
+    idx.upsert(synth.to_storage(base.astype(np.float32), dtype).to(dev))
+    log("pooled upsert", dtype, hidden_dtype)
+    first = idx.upsert_pooled(Ht.to(dev), torch.from_numpy(lengths).to(dev))
+    torch.cuda.synchronize()
+    assert first == 11 and idx.n_rows == 11 + m
+    got = decode(synth.storage_bits(idx.slab[11:11 + m].cpu()), dtype)
+    ref = embed_tail.pool(H64, lengths)
+    n = np.clip(lengths, 0, T)
+    bound = np.zeros_like(ref)
+    for i in range(m):
+        if n[i] == 0:
+            continue
+        tot = H64[i, : n[i]].sum(axis=0)
+        nrm = np.linalg.norm(tot)
+        if nrm > 0:
+            bound[i] = 2 * n[i] * 2.0 ** -24 * np.abs(H64[i, : n[i]]).sum(axis=0) / nrm
+    err = np.abs(got - ref)
+    tol = _ulp(ref, dtype) * (ref != 0) + bound
+    assert np.all(err <= tol), float(np.max(err - tol))
+    assert np.all(got[[0, 4, 5]] == 0.0)
+    norms = np.linalg.norm(got[6:], axis=1)
+    assert np.allclose(norms, 1.0, atol=4 * {"bf16": 2 ** -8, "f16": 2 ** -11, "f32": 2 ** -23}[dtype])
+    if dtype != "f32":
+        q = idx.slab[11 + 10:11 + 14].clone()
+        sc, ids = idx.search_dense(q, 1)
+        torch.cuda.synchronize()
+        assert ids[:, 0].cpu().tolist() == [21, 22, 23, 24]
