@@ -2,13 +2,17 @@
  * oprag.h - C ABI of the MI355X (gfx950) exact-retrieval core of OpRAG.
  *
  * The paper's operator model (Section 3.2) states the three calls this library implements:
- *   E  = Op_embed(D; b_e)          - outside the library: callers pass unit-norm vectors
- *                                    (the embedding path ends in an L2 normalisation, Section 4.3);
+ *   E  = Op_embed(D; b_e)          - the model forward pass is outside the library; its tail
+ *                                    (mean pool, L2 normalisation, Section 4.3) is fused with
+ *                                    the insertion in oprag_upsert_pooled, and oprag_upsert
+ *                                    takes vectors that are already unit-norm;
  *   I' = Op_upsert(I, E; b_u)      - oprag_upsert: bulk insertion of new embeddings;
  *   R_k = Op_retrieve(q, I)        - oprag_search_dense: exact top-k by inner product;
  * and the hybrid retrieval of Section 4.4 (dense scores plus inverted-postings BM25 over the
  * full corpus, fused, then partial top-k): oprag_sparse_attach / oprag_search_sparse /
- * oprag_rrf_fuse / oprag_search_hybrid.
+ * oprag_rrf_fuse / oprag_search_hybrid (reciprocal rank fusion) and
+ * oprag_search_hybrid_weighted (the paper's weighted score fusion), plus the dense-first
+ * serving schedule of Sections 4.1 and 5.5, oprag_search_hybrid_dense_first.
  *
  * Conventions for every function:
  *  - Return value: OPRAG_OK (0) or a negative oprag_status; the reason is available from
@@ -18,9 +22,9 @@
  *    next synchronisation of the stream.
  *  - Memory: every large buffer (slab, CSR arrays, queries, outputs, workspace) is device
  *    memory owned by the caller and must stay valid while the index or call uses it.  The
- *    library allocates only the BM25 statistics arrays at attach time (4 bytes per term and
- *    per posting) and never in create, upsert or search.  Device pointers must be 16-byte
- *    aligned.
+ *    library allocates only its BM25 arrays at attach time (4 bytes per term, 12 per posting
+ *    and 8 per chunk, plus temporary counters) and never in create, upsert or search.
+ *    Device pointers must be 16-byte aligned.
  *  - Streams: `stream` is a hipStream_t (NULL = default stream).  Calls are asynchronous on
  *    it.  An index keeps host-side state (row count), so calls on one index must be issued
  *    from one host thread at a time; an upsert is seen by searches ordered after it on the
