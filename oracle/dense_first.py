@@ -1,8 +1,8 @@
 """Dense-first hybrid retrieval: lexical scoring of the dense candidates only.  Test
 infrastructure only.
 
-The paper's serving schedule (Section 3.2, "Retrieval", and the query-serving experiment of
-Section 5) first takes a dense top-n candidate set and applies lexical reranking to those
+The paper's serving schedule (Section 4.1, "Retrieval", and the query-serving experiment of
+Section 5.5) first takes a dense top-n candidate set and applies lexical reranking to those
 candidates alone, then reports Recall@k and Jaccard overlap against full hybrid retrieval.
 It names the schedule, not the formula; the reading used here:
 

@@ -1473,24 +1473,53 @@ __global__ __launch_bounds__(kThreads) void select_topk_kernel(const unsigned lo
 
 // Weighted fusion (Section 4.4): per query, the dense and lexical scores of every chunk,
 // min-max normalised over all chunks (a constant row normalises to 0), weighted and summed in
-// fp64, rounded to fp32 and written as composites for the exact selection.  Lexical scores
-// past n_lex chunks are 0.  One workgroup per query.
-__global__ __launch_bounds__(kThreads) void weighted_fuse_kernel(const float* __restrict__ D,
+// fp64 and rounded to fp32.  Lexical scores past n_lex chunks are 0.  One workgroup of 1,024
+// threads per query; eight chunks per thread and step, their loads issued before use.
+//   pass 1: the minima and maxima of both rows;
+//   pass 2: every chunk's fused composite; tau = the need-th largest of the maxima of the 128
+//           eight-thread groups (need = min(k, n) <= 128) bounds the need-th best composite
+//           from below;
+//   pass 3: the same composites again, and those >= tau go to cbuf[q] (in any order) with
+//           their count in ccnt[q], for the exact selection.
+// Pass 2 keeps the score keys of the first kFuseLds chunks in LDS for pass 3 and the rest are
+// computed again; every operation is rounded explicitly, so both ways give the same composites.
+constexpr int kFuseThreads = 1024, kFuseGroups = kFuseThreads / 8, kFuseLds = 32768;
+static_assert(kFuseLds % (8 * kFuseThreads) == 0, "whole steps come from LDS");
+static_assert(kMaxK <= kFuseGroups, "tau needs k group maxima");
+__device__ __forceinline__ u64 fused_composite(double sd, double sl, double mnd, double mnl, float x, float y,
+                                               long long i) {
+  const double v = __dadd_rn(__dmul_rn(sd, __dsub_rn((double)x, mnd)), __dmul_rn(sl, __dsub_rn((double)y, mnl)));
+  return composite(__double2float_rn(v), (uint32_t)i);
+}
+__global__ __launch_bounds__(kFuseThreads) void weighted_fuse_kernel(const float* __restrict__ D,
                                                                  const float* __restrict__ B, long long ld,
                                                                  long long n, long long n_lex, double wd, double wl,
-                                                                 unsigned long long* cbuf, int* ccnt) {
-  __shared__ float red[4][kThreads / 64];
+                                                                 int k, unsigned long long* cbuf, int* ccnt) {
+  __shared__ float red[4][kFuseThreads / 64];
+  __shared__ uint32_t skey[kFuseLds];
+  __shared__ u64 gmax[kFuseGroups];
+  __shared__ u64 s_tau;
+  __shared__ int s_cnt;
   const long long q = blockIdx.x;
   const int t = threadIdx.x, lane = t & 63, w = t >> 6;
   const float* d = D + q * ld;
   const float* b = B + q * ld;
   float mnd = __builtin_inff(), mxd = -__builtin_inff(), mnl = __builtin_inff(), mxl = -__builtin_inff();
-  for (long long i = t; i < n; i += kThreads) {
-    const float x = d[i], y = i < n_lex ? b[i] : 0.f;
-    mnd = fminf(mnd, x);
-    mxd = fmaxf(mxd, x);
-    mnl = fminf(mnl, y);
-    mxl = fmaxf(mxl, y);
+  for (long long i0 = t; i0 < n; i0 += 8 * kFuseThreads) {
+    float x[8], y[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const long long i = i0 + (long long)u * kFuseThreads;
+      x[u] = i < n ? d[i] : d[i0];
+      y[u] = i < n_lex ? b[i] : 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      mnd = fminf(mnd, x[u]);
+      mxd = fmaxf(mxd, x[u]);
+      mnl = fminf(mnl, y[u]);
+      mxl = fmaxf(mxl, y[u]);
+    }
   }
   for (int o = 32; o > 0; o >>= 1) {
     mnd = fminf(mnd, __shfl_xor(mnd, o));
@@ -1506,7 +1535,7 @@ __global__ __launch_bounds__(kThreads) void weighted_fuse_kernel(const float* __
   }
   __syncthreads();
 #pragma unroll
-  for (int u = 0; u < kThreads / 64; ++u) {
+  for (int u = 0; u < kFuseThreads / 64; ++u) {
     mnd = fminf(mnd, red[0][u]);
     mxd = fmaxf(mxd, red[1][u]);
     mnl = fminf(mnl, red[2][u]);
@@ -1514,13 +1543,79 @@ __global__ __launch_bounds__(kThreads) void weighted_fuse_kernel(const float* __
   }
   const double sd = mxd > mnd ? wd / ((double)mxd - (double)mnd) : 0.0;
   const double sl = mxl > mnl ? wl / ((double)mxl - (double)mnl) : 0.0;
-  unsigned long long* dst = cbuf + q * n;
-  for (long long i = t; i < n; i += kThreads) {
-    const double x = d[i], y = i < n_lex ? b[i] : 0.f;
-    const float f = (float)(sd * (x - mnd) + sl * (y - mnl));
-    dst[i] = composite(f, (uint32_t)i);
+  const double mnd64 = mnd, mnl64 = mnl;
+  // pass 2: this thread's largest composite, then its group's
+  u64 m = 0ull;
+  for (long long i0 = t; i0 < n; i0 += 8 * kFuseThreads) {
+    float x[8], y[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const long long i = i0 + (long long)u * kFuseThreads;
+      x[u] = i < n ? d[i] : 0.f;
+      y[u] = i < n_lex ? b[i] : 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const long long i = i0 + (long long)u * kFuseThreads;
+      if (i < n) {
+        const u64 c = fused_composite(sd, sl, mnd64, mnl64, x[u], y[u], i);
+        m = umax64(m, c);
+        if (i < kFuseLds) skey[i] = comp_key(c);
+      }
+    }
   }
-  if (t == 0) ccnt[q] = (int)n;
+#pragma unroll
+  for (int o = 1; o < 8; o <<= 1) m = umax64(m, __shfl_xor(m, o));
+  if ((t & 7) == 0) gmax[t >> 3] = m;
+  if (t == 0) {
+    s_tau = 0ull;
+    s_cnt = 0;
+  }
+  __syncthreads();
+  // Nonzero group maxima are distinct composites; when fewer than need of them exist, tau
+  // stays 0 and every chunk is a candidate.
+  const int need = (int)min((long long)k, n);
+  if (t < kFuseGroups && need > 0) {
+    const u64 g = gmax[t];
+    int gt = 0;
+#pragma unroll 8
+    for (int u = 0; u < kFuseGroups; ++u) gt += gmax[u] > g ? 1 : 0;
+    if (g != 0ull && gt == need - 1) s_tau = g;
+  }
+  __syncthreads();
+  const u64 tau = s_tau;
+  // pass 3: compact the composites >= tau, one LDS reservation per wave and step
+  unsigned long long* dst = cbuf + q * n;
+  for (long long i0 = t; i0 < n; i0 += 8 * kFuseThreads) {
+    float x[8], y[8];
+    const bool from_lds = i0 + 7ll * kFuseThreads < kFuseLds;  // uniform: whole steps
+    if (!from_lds) {
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const long long i = i0 + (long long)u * kFuseThreads;
+        x[u] = i < n ? d[i] : 0.f;
+        y[u] = i < n_lex ? b[i] : 0.f;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const long long i = i0 + (long long)u * kFuseThreads;
+      u64 c = 0ull;
+      if (i < n)
+        c = from_lds ? ((u64)skey[i] << 32) | (u64)(uint32_t)(~(uint32_t)i)
+                     : fused_composite(sd, sl, mnd64, mnl64, x[u], y[u], i);
+      const bool take = i < n && c >= tau;
+      const u64 bal = __ballot(take);
+      if (bal != 0ull) {
+        int base = 0;
+        if (lane == __ffsll((long long)bal) - 1) base = atomicAdd(&s_cnt, __popcll(bal));
+        base = __shfl(base, __ffsll((long long)bal) - 1);
+        if (take) dst[base + __popcll(bal & ((1ull << lane) - 1ull))] = c;
+      }
+    }
+  }
+  __syncthreads();
+  if (t == 0) ccnt[q] = s_cnt;
 }
 
 // Clears the filtered-mode counters (a kernel, not a memset: safe inside captured graphs).
@@ -1988,8 +2083,8 @@ hipError_t launch_dense_dump(const DensePlan& p, const DenseArgs& a, hipStream_t
 hipError_t launch_weighted_fuse(const float* D, const float* B, long long ld, long long n, long long n_lex, int nq,
                                 double wd, double wl, int k, unsigned long long* cbuf, int* ccnt, float* out_scores,
                                 long long* out_ids, hipStream_t s) {
-  hipLaunchKernelGGL(weighted_fuse_kernel, dim3((unsigned)nq), dim3(kThreads), 0, s, D, B, ld, n, n_lex, wd, wl, cbuf,
-                     ccnt);
+  hipLaunchKernelGGL(weighted_fuse_kernel, dim3((unsigned)nq), dim3(kFuseThreads), 0, s, D, B, ld, n, n_lex, wd, wl,
+                     k, cbuf, ccnt);
   hipLaunchKernelGGL(select_topk_kernel, dim3((unsigned)nq), dim3(kThreads), 0, s, cbuf, ccnt, n, k, out_scores, out_ids,
                      nullptr, nullptr, 0);
   return hipGetLastError();

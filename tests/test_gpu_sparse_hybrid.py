@@ -332,20 +332,23 @@ def _check_weighted(F, sc, ids, k, label):
     assert not bad, f"{label}: {len(bad)} queries fail, first {bad[:2]}"
 
 
-@pytest.mark.parametrize("w_d,w_l,k", [(0.5, 0.5, 5), (0.8, 0.2, 17), (1.0, 0.0, 10), (0.0, 1.0, 10)])
-def test_weighted_fusion_small_corpus(w_d, w_l, k):
-    """Weighted fusion (min-max normalised dense and BM25 over every chunk) on a 3,000-row
-    d = 128 index whose sparse corpus covers only the first 2,500 chunks (the rest score 0
-    lexically): the GPU top-k passes the acceptance rules against the fp64 oracle's fused
-    scores.  Queries 0-3 have no terms, only unknown terms, repeats and a mix."""
+@pytest.mark.parametrize("w_d,w_l,k,n,n_docs", [(0.5, 0.5, 5, 3000, 2500), (0.8, 0.2, 17, 3000, 2500),
+                                               (1.0, 0.0, 10, 3000, 2500), (0.0, 1.0, 10, 3000, 2500),
+                                               (0.3, 0.7, 128, 3000, 2500), (0.5, 0.5, 100, 70, 50)])
+def test_weighted_fusion_small_corpus(w_d, w_l, k, n, n_docs):
+    """Weighted fusion (min-max normalised dense and BM25 over every chunk) on a d = 128 index
+    whose sparse corpus covers only its first n_docs chunks (the rest score 0 lexically): the
+    GPU top-k passes the acceptance rules against the fp64 oracle's fused scores.  Queries 0-3
+    have no terms, only unknown terms, repeats and a mix (with w_l = 1 and no terms every
+    chunk ties at 0).  k = 128 is the largest k; the last case has fewer chunks than k."""
     from oracle import weighted
     dev = device()
-    n, n_docs, nq = 3000, 2500, 40
+    nq = 40
     ind, toks, csr, qi, qt = _small_corpus(1500 + k, n_docs, 300, 30.0, nq)
     w = synth.mixture_dense(1501 + k, n, 128, 16, nq, k, "bf16")
     idx = make_index(w.rows, "bf16")
     _attach(idx, csr, dev)
-    log("weighted small", w_d, w_l, k)
+    log("weighted small", w_d, w_l, k, n)
     sc, ids = idx.search_hybrid_weighted(w.queries.to(dev), _t(qi, dev), _t(qt, dev), w_d, w_l, k)
     torch.cuda.synchronize()
     S, X, Q = oracle_scores(w.rows, w.queries, "bf16")
