@@ -163,28 +163,46 @@ def pmc_summarize(out_dir: str) -> int:
 STATS_FILE = os.path.join(ROOT, "profiles", "dense_scoring_32k_x_1024_bf16_b256_kernel_stats.txt")
 
 
-def trace_summarize(out_dir: str) -> int:
-    """Write the kernel-trace statistics of a rocprofv3 --kernel-trace --stats run of bench.py."""
+SUITE_STATS_FILE = os.path.join(ROOT, "profiles", "suite_every_workload_kernel_stats.txt")
+
+
+def trace_summarize(out_dir: str, suite: bool = False) -> int:
+    """Write the kernel-trace statistics of a rocprofv3 --kernel-trace --stats run of bench.py
+    (of ``bench.py --suite`` when suite is set)."""
     files = glob.glob(os.path.join(out_dir, "**", "*kernel_stats.csv"), recursive=True)
     if not files:
         print(f"no kernel_stats.csv under {out_dir}", file=sys.stderr)
         return 1
     rows = list(csv.DictReader(open(files[0])))
-    lines = [
-        "rocprofv3 kernel statistics of the default bench.py run (32,768 x 1,024 bf16, batch 256, k 5)",
-        "command: cd /tmp && export TMPDIR=/tmp && timeout -k 10 300 rocprofv3 --kernel-trace --stats "
-        "--output-format csv -d $GRAFT_REPO_ROOT/gpurun_out/kt_bench -o bench -- python3 $GRAFT_REPO_ROOT/bench.py "
-        "&& python3 $GRAFT_REPO_ROOT/bench.py --trace-summarize $GRAFT_REPO_ROOT/gpurun_out/kt_bench",
+    if suite:
+        head = [
+            "rocprofv3 kernel statistics of bench.py --suite (every workload: 32K x 1,024 bf16 batches 1 / 16 / 256 / "
+            "1,024, hybrid dense / BM25 / RRF / full, dense-first, weighted fusion, embedding tail, 1M x 768, "
+            "streaming upsert and search); calls include warm-up and the eager timing passes",
+            "command: cd /tmp && export TMPDIR=/tmp && timeout -k 10 600 rocprofv3 --kernel-trace --stats "
+            "--output-format csv -d $GRAFT_REPO_ROOT/gpurun_out/kt_suite -o suite -- python3 $GRAFT_REPO_ROOT/bench.py "
+            "--suite && python3 $GRAFT_REPO_ROOT/bench.py --suite-trace-summarize $GRAFT_REPO_ROOT/gpurun_out/kt_suite",
+        ]
+        out_file, n_show = SUITE_STATS_FILE, 40
+    else:
+        head = [
+            "rocprofv3 kernel statistics of the default bench.py run (32,768 x 1,024 bf16, batch 256, k 5)",
+            "command: cd /tmp && export TMPDIR=/tmp && timeout -k 10 300 rocprofv3 --kernel-trace --stats "
+            "--output-format csv -d $GRAFT_REPO_ROOT/gpurun_out/kt_bench -o bench -- python3 $GRAFT_REPO_ROOT/bench.py "
+            "&& python3 $GRAFT_REPO_ROOT/bench.py --trace-summarize $GRAFT_REPO_ROOT/gpurun_out/kt_bench",
+        ]
+        out_file, n_show = STATS_FILE, 12
+    lines = head + [
         f"kernel source sha256[:16] of dense.hip: {kernel_source_sha()}",
         "",
         f"{'calls':>7} {'avg_us':>9} {'min_us':>9} {'max_us':>9} {'share%':>7}  kernel",
     ]
-    for r in rows[:12]:
+    for r in rows[:n_show]:
         name = r["Name"].replace("(anonymous namespace)::", "")
         lines.append(f"{int(r['Calls']):7d} {float(r['AverageNs']) / 1e3:9.2f} {float(r['MinNs']) / 1e3:9.2f} "
                      f"{float(r['MaxNs']) / 1e3:9.2f} {float(r['Percentage']):7.2f}  {name[:150]}")
-    os.makedirs(os.path.dirname(STATS_FILE), exist_ok=True)
-    open(STATS_FILE, "w").write("\n".join(lines) + "\n")
+    os.makedirs(os.path.dirname(out_file), exist_ok=True)
+    open(out_file, "w").write("\n".join(lines) + "\n")
     print("\n".join(lines))
     return 0
 
@@ -260,6 +278,7 @@ def suite() -> int:
         ix = Index(DIM, N_ROWS, torch.bfloat16)
         ix.upsert(rows)
         idxs.append(ix)
+    sweep = []
     for b in (1, 16, 256, 1024):
         q = w.queries[:b].contiguous().to(dev)
         outs = [(torch.empty((b, K), device=dev), torch.empty((b, K), dtype=torch.int64, device=dev))
@@ -271,8 +290,18 @@ def suite() -> int:
             it[0] += 1
             idxs[c].search_dense(q, K, out=outs[c])
         ms = _timed(step, 256, stream)
+        sweep.append((b, ms))
         report(f"32,768 x 1,024 bf16, batch {b}, top-5, cold", ms, b, algorithmic_bytes(N_ROWS, DIM, b, K),
                2.0 * b * N_ROWS * DIM, _kernel_ms(step, 128, stream))
+    # cost model t(B) = alpha + beta * B over the batch sweep (least squares)
+    bs = np.array([b for b, _ in sweep], dtype=np.float64)
+    ts = np.array([m * 1e3 for _, m in sweep], dtype=np.float64)
+    beta, alpha = np.polyfit(bs, ts, 1)
+    fit = {"workload": "32,768 x 1,024 bf16 batch sweep, fit t(B) = alpha + beta * B", "alpha_us": round(float(alpha), 2),
+           "beta_us_per_query": round(float(beta), 4),
+           "max_rel_residual": round(float(np.max(np.abs(alpha + beta * bs - ts) / ts)), 3)}
+    out.append(fit)
+    print(json.dumps(fit), flush=True)
 
     # hybrid: the same index + 32,768-chunk Zipf corpus; dense 100 + BM25 100 -> RRF(60) -> 5
     hw = synth.hybrid_32k(dense=w)
@@ -377,12 +406,16 @@ def main() -> int:
                     help="a short run for counter collection: one reference copy, then 8 cold searches")
     ap.add_argument("--pmc-summarize", metavar="DIR", help="write the traffic record from two --pmc runs")
     ap.add_argument("--trace-summarize", metavar="DIR", help="write the kernel statistics of a traced run")
+    ap.add_argument("--suite-trace-summarize", metavar="DIR",
+                    help="write the kernel statistics of a traced --suite run")
     ap.add_argument("--suite", action="store_true", help="time every workload (one JSON line each)")
     args = ap.parse_args()
     if args.pmc_summarize:
         return pmc_summarize(args.pmc_summarize)
     if args.trace_summarize:
         return trace_summarize(args.trace_summarize)
+    if args.suite_trace_summarize:
+        return trace_summarize(args.suite_trace_summarize, suite=True)
     if args.suite:
         if args.gpus != 1:
             print("the suite runs on one GPU only", file=sys.stderr)

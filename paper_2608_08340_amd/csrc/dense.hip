@@ -1510,15 +1510,17 @@ __global__ __launch_bounds__(kFuseThreads) void weighted_fuse_kernel(const float
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
       const long long i = i0 + (long long)u * kFuseThreads;
-      x[u] = i < n ? d[i] : d[i0];
+      x[u] = i < n ? d[i] : 0.f;
       y[u] = i < n_lex ? b[i] : 0.f;
     }
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
-      mnd = fminf(mnd, x[u]);
-      mxd = fmaxf(mxd, x[u]);
-      mnl = fminf(mnl, y[u]);
-      mxl = fmaxf(mxl, y[u]);
+      if (i0 + (long long)u * kFuseThreads < n) {  // slots past the last chunk take no part
+        mnd = fminf(mnd, x[u]);
+        mxd = fmaxf(mxd, x[u]);
+        mnl = fminf(mnl, y[u]);
+        mxl = fmaxf(mxl, y[u]);
+      }
     }
   }
   for (int o = 32; o > 0; o >>= 1) {

@@ -332,27 +332,30 @@ def _check_weighted(F, sc, ids, k, label):
     assert not bad, f"{label}: {len(bad)} queries fail, first {bad[:2]}"
 
 
-@pytest.mark.parametrize("w_d,w_l,k,n,n_docs", [(0.5, 0.5, 5, 3000, 2500), (0.8, 0.2, 17, 3000, 2500),
-                                               (1.0, 0.0, 10, 3000, 2500), (0.0, 1.0, 10, 3000, 2500),
-                                               (0.3, 0.7, 128, 3000, 2500), (0.5, 0.5, 100, 70, 50)])
-def test_weighted_fusion_small_corpus(w_d, w_l, k, n, n_docs):
+@pytest.mark.parametrize("w_d,w_l,k,n,n_docs,vocab", [(0.5, 0.5, 5, 3000, 2500, 300), (0.8, 0.2, 17, 3000, 2500, 300),
+                                                     (1.0, 0.0, 10, 3000, 2500, 300), (0.0, 1.0, 10, 3000, 2500, 300),
+                                                     (0.3, 0.7, 128, 3000, 2500, 300), (0.5, 0.5, 100, 70, 50, 300),
+                                                     (0.5, 0.5, 5, 3000, 3000, 8)])
+def test_weighted_fusion_small_corpus(w_d, w_l, k, n, n_docs, vocab):
     """Weighted fusion (min-max normalised dense and BM25 over every chunk) on a d = 128 index
-    whose sparse corpus covers only its first n_docs chunks (the rest score 0 lexically): the
-    GPU top-k passes the acceptance rules against the fp64 oracle's fused scores.  Queries 0-3
+    whose sparse corpus covers its first n_docs chunks (the rest score 0 lexically): the GPU
+    top-k passes the acceptance rules against the fp64 oracle's fused scores.  Queries 0-3
     have no terms, only unknown terms, repeats and a mix (with w_l = 1 and no terms every
-    chunk ties at 0).  k = 128 is the largest k; the last case has fewer chunks than k."""
+    chunk ties at 0).  k = 128 is the largest k; one case has fewer chunks than k; in the last
+    the corpus covers every chunk with an 8-term vocabulary, so most queries have a lexical
+    minimum above 0 (which padding past the last chunk must not lower)."""
     from oracle import weighted
     dev = device()
     nq = 40
-    ind, toks, csr, qi, qt = _small_corpus(1500 + k, n_docs, 300, 30.0, nq)
+    ind, toks, csr, qi, qt = _small_corpus(1500 + k, n_docs, vocab, 30.0, nq)
     w = synth.mixture_dense(1501 + k, n, 128, 16, nq, k, "bf16")
     idx = make_index(w.rows, "bf16")
     _attach(idx, csr, dev)
-    log("weighted small", w_d, w_l, k, n)
+    log("weighted small", w_d, w_l, k, n, vocab)
     sc, ids = idx.search_hybrid_weighted(w.queries.to(dev), _t(qi, dev), _t(qt, dev), w_d, w_l, k)
     torch.cuda.synchronize()
     S, X, Q = oracle_scores(w.rows, w.queries, "bf16")
-    qt_oracle = np.where((qt >= 0) & (qt < 300), qt, 10 ** 6).astype(np.int64)
+    qt_oracle = np.where((qt >= 0) & (qt < vocab), qt, 10 ** 6).astype(np.int64)
     B = np.zeros((nq, n))
     B[:, :n_docs] = bm25.scores_batch(ind, toks, qi, qt_oracle, 1.2, 0.75)
     _check_weighted(weighted.fused(S, B, w_d, w_l), sc, ids, k, f"w=({w_d},{w_l}) k={k}")
