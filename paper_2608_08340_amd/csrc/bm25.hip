@@ -169,9 +169,10 @@ __device__ __forceinline__ void range_bounds32(const int* chunk, long long lo, l
   *out_hi = b0;
 }
 
-// Candidates the threshold selection ranks directly.  With the 32 KiB accumulator this keeps
-// a workgroup under 40 KiB of LDS, four per CU.
-constexpr int kCandCap = 1000;
+// Candidates the threshold selection ranks directly.  With the 32 KiB accumulator and the
+// kernel's other shared arrays (about 200 bytes) a workgroup stays within 40 KiB of LDS, so
+// four fit on a CU; a few bytes more drop that to three and cost a third of the speed.
+constexpr int kCandCap = 992;
 
 __global__ __launch_bounds__(kNT) void bm25_kernel(SparseArgs a) {
   __shared__ __attribute__((aligned(16))) float acc[kSparseRange];
@@ -186,6 +187,7 @@ __global__ __launch_bounds__(kNT) void bm25_kernel(SparseArgs a) {
   __shared__ int wave_tot[kNT / 64];
   __shared__ unsigned int s_prefix, s_need, s_take_all, s_ngt;
   __shared__ long long s_lo[kTermBatch], s_hi[kTermBatch];
+  __shared__ float s_wt[kTermBatch];
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int q = blockIdx.x / a.n_ranges;
@@ -197,23 +199,41 @@ __global__ __launch_bounds__(kNT) void bm25_kernel(SparseArgs a) {
 
   const int tb = a.qterm_indptr[q], te = a.qterm_indptr[q + 1];
   for (int j0 = tb; j0 < te; j0 += kTermBatch) {
-    // 1. posting bounds of up to kTermBatch terms at once, 32 threads per term
+    // 1. posting bounds of up to kTermBatch terms at once, 32 threads per term.  A term that
+    // occurs m times in the query is walked once, at its first occurrence, with weight
+    // m * idf(t) * (k1 + 1); its later occurrences walk nothing.
     {
       const int g = tid >> 5, sub = tid & 31;
       const int j = j0 + g;
       if (g < kTermBatch) {
         long long lo = 0, hi = 0;
-        if (j < te) {
+        float wt = 0.f;
+        if (j < te) {  // uniform over the group's 32 threads
           const int t = a.qterms[j];
           if (t >= 0 && t < a.vocab) {  // unknown terms match nothing
-            lo = a.indptr[t];
-            hi = a.indptr[t + 1];
-            if (a.n_ranges > 1) range_bounds32(a.chunk, lo, hi, d0, d0 + len, sub, &lo, &hi);
+            int earlier = 0, mult = 0;
+            for (int jj = tb + sub; jj < te; jj += 32)
+              if (a.qterms[jj] == t) {
+                if (jj < j) earlier = 1;
+                else mult += 1;
+              }
+#pragma unroll
+            for (int o = 16; o > 0; o >>= 1) {
+              earlier |= __shfl_xor(earlier, o, 32);
+              mult += __shfl_xor(mult, o, 32);
+            }
+            if (!earlier) {
+              lo = a.indptr[t];
+              hi = a.indptr[t + 1];
+              wt = a.idfk[t] * (float)mult;
+              if (a.n_ranges > 1) range_bounds32(a.chunk, lo, hi, d0, d0 + len, sub, &lo, &hi);
+            }
           }
         }
         if (sub == 0) {
           s_lo[g] = lo;
           s_hi[g] = hi;
+          s_wt[g] = wt;
         }
       }
     }
@@ -222,7 +242,7 @@ __global__ __launch_bounds__(kNT) void bm25_kernel(SparseArgs a) {
     for (int g = 0; g < kTermBatch && j0 + g < te; ++g) {
       const long long lo = s_lo[g], hi = s_hi[g];
       if (lo < hi) {
-        const float wt = a.idfk[a.qterms[j0 + g]];
+        const float wt = s_wt[g];
         // eight postings per thread per step, all loads issued before the first use
         long long p = lo + tid;
         for (; p + 7 * kNT < hi; p += 8 * kNT) {
