@@ -1332,7 +1332,7 @@ __global__ __launch_bounds__(kThreads) void select_topk_kernel(const unsigned lo
   const int t = threadIdx.x, lane = t & 63, w = t >> 6;
   const int q = blockIdx.x;
   const int cnt = ccnt[q];
-  if (t == 0 && cnt > cap) atomicAdd(overflow, 1);
+  if (t == 0 && cnt > cap && overflow != nullptr) atomicAdd(overflow, 1);
   const int n = (int)min((long long)cnt, cap);
   const u64* src = cbuf + (long long)q * cap;
   if (t == 0) {
@@ -2014,12 +2014,15 @@ hipError_t launch_dense(const DensePlan& p, int dtype, const DenseArgs& a, hipSt
                         hipEvent_t ev1) {
   const KernelInfo& ki = kKernels[p.kernel];
   if (p.filtered) {
-    int* fl = dense_flags(p, a.partial, a.nq);
-    hipLaunchKernelGGL(clear_ints_kernel, dim3(1), dim3(64), 0, s, fl, 4ll, nullptr);
+    // The overflow flags matter only where a buffer can overflow; otherwise no flag is
+    // passed, and there is nothing to clear.
+    int* fl = p.repair ? dense_flags(p, a.partial, a.nq) : nullptr;
+    if (p.repair) hipLaunchKernelGGL(clear_ints_kernel, dim3(1), dim3(64), 0, s, fl, 4ll, nullptr);
     for (int l = 0; l < p.n_levels; ++l) {
       const bool last = l == p.n_levels - 1;
       // level l's threshold: a lower bound of the k-th score over level l - 1's rows
-      hipError_t e = filter_pass(p, a, p.level_rows[l], l == 0 ? nullptr : a.out_scores + (a.k - 1), fl + (last ? 0 : 1),
+      hipError_t e = filter_pass(p, a, p.level_rows[l], l == 0 ? nullptr : a.out_scores + (a.k - 1),
+                                 fl ? fl + (last ? 0 : 1) : nullptr,
                                  nullptr, !last, l == 0, s, last ? ev0 : nullptr, last ? ev1 : nullptr);
       if (e != hipSuccess) return e;
     }
