@@ -1348,9 +1348,26 @@ __global__ __launch_bounds__(kThreads) void select_topk_kernel(const unsigned lo
   // maxima (lane-strided slices) bounds the need-th best key from below, and the keys >= tau
   // (about 1-2 need) are ranked exactly.  Too many of them: the radix select below.
   const int need = min(k, n);
+  // Up to kRegKeys keys per thread are read once, all loads in flight together, and kept in
+  // registers for the three passes below; larger buffers are read again in each pass.
+  constexpr int kRegKeys = 16;
+  const bool in_reg = n <= kRegKeys * kThreads;  // workgroup-uniform
+  u64 kv[kRegKeys];
+  if (in_reg) {
+#pragma unroll
+    for (int u = 0; u < kRegKeys; ++u) {
+      const int i = t + u * kThreads;
+      kv[u] = i < n ? src[i] : 0ull;
+    }
+  }
   if (need > 0) {
     u64 m = 0ull;
-    for (int i = t; i < n; i += kThreads) m = umax64(m, src[i]);
+    if (in_reg) {
+#pragma unroll
+      for (int u = 0; u < kRegKeys; ++u) m = umax64(m, kv[u]);
+    } else {
+      for (int i = t; i < n; i += kThreads) m = umax64(m, src[i]);
+    }
     tmax[t] = m;
     if (t == 0) {
       s_tau = 0ull;
@@ -1370,7 +1387,12 @@ __global__ __launch_bounds__(kThreads) void select_topk_kernel(const unsigned lo
       return;
     }
     int c = 0;
-    for (int i = t; i < n; i += kThreads) c += src[i] >= tau ? 1 : 0;
+    if (in_reg) {
+#pragma unroll
+      for (int u = 0; u < kRegKeys; ++u) c += (t + u * kThreads < n && kv[u] >= tau) ? 1 : 0;
+    } else {
+      for (int i = t; i < n; i += kThreads) c += src[i] >= tau ? 1 : 0;
+    }
     // exclusive scan of c over the workgroup
     int x = c;
 #pragma unroll
@@ -1383,11 +1405,18 @@ __global__ __launch_bounds__(kThreads) void select_topk_kernel(const unsigned lo
     int pos = x - c;
     for (int i = 0; i < w; ++i) pos += wtot[i];
     if (t == kThreads - 1) s_nc = pos + c;
-    if (pos + c <= kCand)
-      for (int i = t; i < n; i += kThreads) {
-        const u64 key = src[i];
-        if (key >= tau) cand[pos++] = key;
+    if (pos + c <= kCand) {
+      if (in_reg) {
+#pragma unroll
+        for (int u = 0; u < kRegKeys; ++u)
+          if (t + u * kThreads < n && kv[u] >= tau) cand[pos++] = kv[u];
+      } else {
+        for (int i = t; i < n; i += kThreads) {
+          const u64 key = src[i];
+          if (key >= tau) cand[pos++] = key;
+        }
       }
+    }
     __syncthreads();
     const int nc = s_nc;
     if (nc <= kCand) {  // workgroup-uniform
