@@ -361,6 +361,28 @@ def test_weighted_fusion_small_corpus(w_d, w_l, k, n, n_docs, vocab):
     _check_weighted(weighted.fused(S, B, w_d, w_l), sc, ids, k, f"w=({w_d},{w_l}) k={k}")
 
 
+def test_weighted_fusion_past_the_lds_key_cache():
+    """45,001 chunks, more than the 32,768 score keys the fusion kernel keeps in LDS: the
+    steps past them compute the composites again from the score rows, and both halves must
+    agree with the oracle (top-5 and top-100, every chunk in the sparse corpus)."""
+    from oracle import weighted
+    dev = device()
+    n, nq = 45_001, 24
+    ind, toks, csr, qi, qt = _small_corpus(4501, n, 500, 12.0, nq)
+    w = synth.mixture_dense(4502, n, 128, 32, nq, 100, "bf16")
+    idx = make_index(w.rows, "bf16")
+    _attach(idx, csr, dev)
+    S, X, Q = oracle_scores(w.rows, w.queries, "bf16")
+    qt_oracle = np.where((qt >= 0) & (qt < 500), qt, 10 ** 6).astype(np.int64)
+    B = bm25.scores_batch(ind, toks, qi, qt_oracle, 1.2, 0.75)
+    F = weighted.fused(S, B)
+    for k in (5, 100):
+        log("weighted past the LDS cache", n, k)
+        sc, ids = idx.search_hybrid_weighted(w.queries.to(dev), _t(qi, dev), _t(qt, dev), 0.5, 0.5, k)
+        torch.cuda.synchronize()
+        _check_weighted(F, sc, ids, k, f"n={n} k={k}")
+
+
 @pytest.mark.timeout(300)
 def test_weighted_fusion_32k(c3):
     """The 32,768 x 1,024 bf16 hybrid workload with weights 0.5 / 0.5, top-5, every query
