@@ -232,7 +232,8 @@ oprag_status oprag_search_hybrid_dense_first(oprag_index *idx, const void *q_dev
  *   q_dev [nq x dim] (bf16 / fp16 index); qterm_indptr_dev / qterms_dev as in
  *   oprag_search_sparse; scores_dev [nq x k] fp32, ids_dev [nq x k] int64.
  * w_dense, w_lex finite and >= 0.  The scores of every chunk pass through the workspace
- * (oprag_workspace_bytes(OPRAG_OP_WEIGHTED): 16 bytes per query and unit of capacity).
+ * (oprag_workspace_bytes(OPRAG_OP_WEIGHTED): 16 bytes per query and unit of capacity, plus
+ * 8 bytes per query for each partial minimum / maximum pair of the two score dumps).
  * E_STATE without an attached sparse index, E_UNSUPPORTED for an fp32 index.
  */
 oprag_status oprag_search_hybrid_weighted(oprag_index *idx, const void *q_dev, const int32_t *qterm_indptr_dev,

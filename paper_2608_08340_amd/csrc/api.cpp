@@ -117,9 +117,18 @@ size_t dense_first_ws(const oprag_index* idx, int64_t nq, int32_t n_cand) {
 // Weighted fusion: dense scores, lexical scores (each [nq x ld], ld = capacity rounded up to
 // 4), composites [nq x capacity], counts [nq].
 long long weighted_ld(const oprag_index* idx) { return (idx->capacity + 3) & ~3ll; }
+// Partial minima and maxima per query: of the dense dump's chunks (at most as many as its plan
+// at full capacity has) and of the BM25 ranges.
+int weighted_pd(const oprag_index* idx, int64_t nq) {
+  return std::max(1, oprag::plan_dense_dump(idx->dtype, idx->dim, idx->capacity, (int)nq).n_chunks);
+}
+int weighted_pl(const oprag_index* idx) {
+  return (int)((idx->capacity + oprag::kSparseRange - 1) / oprag::kSparseRange);
+}
 size_t weighted_ws(const oprag_index* idx, int64_t nq) {
   const size_t ld = (size_t)weighted_ld(idx);
-  return 2 * align_up((size_t)nq * ld * 4) + align_up((size_t)nq * (size_t)idx->capacity * 8) + align_up((size_t)nq * 4);
+  return 2 * align_up((size_t)nq * ld * 4) + align_up((size_t)nq * (size_t)idx->capacity * 8) + align_up((size_t)nq * 4) +
+         align_up((size_t)nq * (size_t)weighted_pd(idx, nq) * 8) + align_up((size_t)nq * (size_t)weighted_pl(idx) * 8);
 }
 
 oprag_status do_dense(oprag_index* idx, const void* q, int64_t nq, int32_t k, float* scores, int64_t* ids, void* ws,
@@ -571,6 +580,12 @@ oprag_status oprag_search_hybrid_weighted(oprag_index* idx, const void* q_dev, c
   unsigned long long* cbuf = reinterpret_cast<unsigned long long*>(w);
   w += align_up((size_t)nq * (size_t)idx->capacity * 8);
   int* ccnt = reinterpret_cast<int*>(w);
+  w += align_up((size_t)nq * 4);
+  float* mm_d = reinterpret_cast<float*>(w);
+  w += align_up((size_t)nq * (size_t)weighted_pd(idx, nq) * 8);
+  float* mm_l = reinterpret_cast<float*>(w);
+  if (p.n_chunks > weighted_pd(idx, nq)) return fail(OPRAG_E_INVALID, "internal: dump plan exceeds its bound");
+  const int pl = (int)((idx->sp.n_docs + oprag::kSparseRange - 1) / oprag::kSparseRange);
   oprag::DenseArgs a;
   a.X = idx->slab;
   a.n_rows = idx->n_rows;
@@ -580,12 +595,14 @@ oprag_status oprag_search_hybrid_weighted(oprag_index* idx, const void* q_dev, c
   a.k = 1;
   a.dump = D;
   a.dump_ld = ld;
+  a.dump_mm = mm_d;
   hipError_t e = oprag::launch_dense_dump(p, a, s);
-  if (e == hipSuccess) e = oprag::launch_sparse_dump(idx->sp, qterm_indptr_dev, qterms_dev, (int)nq, B, ld, s);
+  if (e == hipSuccess)
+    e = oprag::launch_sparse_dump(idx->sp, qterm_indptr_dev, qterms_dev, (int)nq, B, ld, mm_l, idx->n_rows, s);
   if (e == hipSuccess)
     e = oprag::launch_weighted_fuse(D, B, ld, idx->n_rows, std::min<long long>(idx->sp.n_docs, idx->n_rows), (int)nq,
-                                    (double)w_dense, (double)w_lex, k, cbuf, ccnt, scores_dev,
-                                    reinterpret_cast<long long*>(ids_dev), s);
+                                    mm_d, p.n_chunks, mm_l, pl, (double)w_dense, (double)w_lex, k, cbuf, ccnt,
+                                    scores_dev, reinterpret_cast<long long*>(ids_dev), s);
   if (e != hipSuccess) return hip_fail(e, "weighted fusion launch");
   return ok();
 }

@@ -127,6 +127,8 @@ struct SparseArgs {
   int n_ranges;
   float* dump = nullptr;         // when set: every chunk's score to dump[q * dump_ld + chunk], no top-k
   long long dump_ld = 0;
+  float* dump_mm = nullptr;      // with dump: (min, max) over chunks < mm_rows per (query, range)
+  long long mm_rows = 0;
   float* out_scores;            // final output when n_ranges == 1
   long long* out_ids;
   unsigned long long* partial;  // [nq x n_ranges x k] when n_ranges > 1
@@ -264,7 +266,37 @@ __global__ __launch_bounds__(kNT) void bm25_kernel(SparseArgs a) {
   __syncthreads();
   if (a.dump != nullptr) {  // launch-uniform: the range's scores, no selection
     float* dst = a.dump + (long long)q * a.dump_ld + d0;
-    for (int i = tid; i < len; i += kNT) dst[i] = acc[i];
+    const int mm_len = (int)std::max<long long>(0, std::min<long long>(len, a.mm_rows - d0));
+    float mn = __builtin_inff(), mx = -__builtin_inff();
+    for (int i = tid; i < len; i += kNT) {
+      const float v = acc[i];
+      dst[i] = v;
+      if (i < mm_len) {
+        mn = fminf(mn, v);
+        mx = fmaxf(mx, v);
+      }
+    }
+    if (a.dump_mm != nullptr) {  // launch-uniform
+      for (int o = 32; o > 0; o >>= 1) {
+        mn = fminf(mn, __shfl_xor(mn, o));
+        mx = fmaxf(mx, __shfl_xor(mx, o));
+      }
+      float* red = reinterpret_cast<float*>(cand);  // [kNT / 64][2], the candidate area is unused here
+      if (lane == 0) {
+        red[2 * w] = mn;
+        red[2 * w + 1] = mx;
+      }
+      __syncthreads();
+      if (tid == 0) {
+        for (int u = 1; u < kNT / 64; ++u) {
+          mn = fminf(mn, red[2 * u]);
+          mx = fmaxf(mx, red[2 * u + 1]);
+        }
+        float* o = a.dump_mm + ((long long)q * a.n_ranges + range) * 2;
+        o[0] = mn;
+        o[1] = mx;
+      }
+    }
     return;
   }
 
@@ -766,7 +798,7 @@ hipError_t sparse_forward(const SparseIndex& sp, int* cnt, hipStream_t s) {
 }
 
 hipError_t launch_sparse_dump(const SparseIndex& sp, const int* qterm_indptr, const int* qterms, int nq, float* dump,
-                              long long ld, hipStream_t s) {
+                              long long ld, float* dump_mm, long long mm_rows, hipStream_t s) {
   SparseArgs a;
   a.vocab = sp.vocab;
   a.n_docs = sp.n_docs;
@@ -781,6 +813,8 @@ hipError_t launch_sparse_dump(const SparseIndex& sp, const int* qterm_indptr, co
   a.n_ranges = (int)((sp.n_docs + kSparseRange - 1) / kSparseRange);
   a.dump = dump;
   a.dump_ld = ld;
+  a.dump_mm = dump_mm;
+  a.mm_rows = mm_rows;
   a.out_scores = nullptr;
   a.out_ids = nullptr;
   a.partial = nullptr;

@@ -438,10 +438,12 @@ struct SelOf<BN, KS, 3, NT> {
 
 // acc[mi][ni][r] is the score of row tile0 + 16*MW*wave + 16*mi + 4*(lane/16) + r against
 // query slot 16*ni + lane%16: four consecutive rows per lane and query, stored as one 16-byte
-// write when all four exist (dump_ld is a multiple of 4).
+// write when all four exist (dump_ld is a multiple of 4).  mn / mx take the lane's running
+// minimum and maximum per query slot over the rows that exist.
 template <int BN, int MW, int WV>
 __device__ __forceinline__ void dump_tile(const f32x4 (&acc)[MW][BN / 16], long long tile0, long long row_end,
-                                          int q0, int q_lim, const DenseArgs& a) {
+                                          int q0, int q_lim, const DenseArgs& a, float (&mn)[BN / 16],
+                                          float (&mx)[BN / 16]) {
   constexpr int NW = BN / 16;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const long long r0 = tile0 + w * MW * 16 + (lane >> 4) * 4;
@@ -455,10 +457,19 @@ __device__ __forceinline__ void dump_tile(const f32x4 (&acc)[MW][BN / 16], long 
       const long long row = r0 + mi * 16;
       if (row + 3 < row_end) {
         *reinterpret_cast<f32x4*>(dst + row) = acc[mi][ni];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          mn[ni] = fminf(mn[ni], acc[mi][ni][r]);
+          mx[ni] = fmaxf(mx[ni], acc[mi][ni][r]);
+        }
       } else {
 #pragma unroll
         for (int r = 0; r < 4; ++r)
-          if (row + r < row_end) dst[row + r] = acc[mi][ni][r];
+          if (row + r < row_end) {
+            dst[row + r] = acc[mi][ni][r];
+            mn[ni] = fminf(mn[ni], acc[mi][ni][r]);
+            mx[ni] = fmaxf(mx[ni], acc[mi][ni][r]);
+          }
       }
     }
   }
@@ -995,6 +1006,12 @@ __global__ __launch_bounds__(WV * 64) void dense_mfma_kernel(DenseArgs a) {
     if (tid < BN) reinterpret_cast<int*>(scratch + BN * SelFilter<BN>::SCAP * 8)[tid] = 0;
     // no barrier needed here: the first tile's epilogue follows several barriers
   }
+  float dmn[NW], dmx[NW];  // score dump: this lane's minimum and maximum per query slot
+#pragma unroll
+  for (int ni = 0; ni < NW; ++ni) {
+    dmn[ni] = __builtin_inff();
+    dmx[ni] = -__builtin_inff();
+  }
   float th[NW];  // filtered mode: thresholds of this lane's query slots
 #pragma unroll
   for (int ni = 0; ni < NW; ++ni) {
@@ -1150,7 +1167,7 @@ __global__ __launch_bounds__(WV * 64) void dense_mfma_kernel(DenseArgs a) {
       bool refresh = false;  // the group path ran: thresholds and lists of the fast path to restore
       bool done = false;
       if constexpr (SEL == 3) {
-        dump_tile<BN, MW, WV>(acc, tile0, row_end, q0, q_lim, a);
+        dump_tile<BN, MW, WV>(acc, tile0, row_end, q0, q_lim, a, dmn, dmx);
         done = true;
       } else if constexpr (SEL == 2) {
         if (a.th == nullptr)  // launch-uniform
@@ -1214,6 +1231,39 @@ __global__ __launch_bounds__(WV * 64) void dense_mfma_kernel(DenseArgs a) {
       if (chunk == 0 && tid < q_lim) a.ccnt[q0 + tid] = (int)a.n_rows;  // every row is a candidate
     } else if (tid < q_lim) {
       filt_flush<BN>(tid, q0 + tid, scratch, a);
+    }
+  } else if constexpr (SEL == 3) {
+    if (a.dump_mm != nullptr) {  // launch-uniform
+      // the four lanes of a query slot in a wave, then the waves through LDS
+#pragma unroll
+      for (int ni = 0; ni < NW; ++ni) {
+        dmn[ni] = fminf(dmn[ni], __shfl_xor(dmn[ni], 16));
+        dmx[ni] = fmaxf(dmx[ni], __shfl_xor(dmx[ni], 16));
+        dmn[ni] = fminf(dmn[ni], __shfl_xor(dmn[ni], 32));
+        dmx[ni] = fmaxf(dmx[ni], __shfl_xor(dmx[ni], 32));
+      }
+      __syncthreads();  // every wave is done with the query slots, reused here
+      float* red = reinterpret_cast<float*>(qslots);  // [WV][BN][2]
+      static_assert(WV * BN * 2 * 4 <= QBYTES, "reduction area");
+      if (lane < 16) {
+#pragma unroll
+        for (int ni = 0; ni < NW; ++ni) {
+          red[(w * BN + ni * 16 + lane) * 2] = dmn[ni];
+          red[(w * BN + ni * 16 + lane) * 2 + 1] = dmx[ni];
+        }
+      }
+      __syncthreads();
+      if (tid < q_lim) {
+        float mn = __builtin_inff(), mx = -__builtin_inff();
+#pragma unroll
+        for (int u = 0; u < WV; ++u) {
+          mn = fminf(mn, red[(u * BN + tid) * 2]);
+          mx = fmaxf(mx, red[(u * BN + tid) * 2 + 1]);
+        }
+        float* o = a.dump_mm + ((long long)(q0 + tid) * a.n_chunks + chunk) * 2;
+        o[0] = mn;
+        o[1] = mx;
+      }
     }
   } else {
     sel.write(a, q0, chunk);
@@ -1504,7 +1554,8 @@ __global__ __launch_bounds__(kThreads) void select_topk_kernel(const unsigned lo
 // min-max normalised over all chunks (a constant row normalises to 0), weighted and summed in
 // fp64 and rounded to fp32.  Lexical scores past n_lex chunks are 0.  One workgroup of 1,024
 // threads per query; eight chunks per thread and step, their loads issued before use.
-//   pass 1: the minima and maxima of both rows;
+//   pass 1: the minima and maxima of both rows, from the dumps' per-chunk / per-range
+//           partials (and 0 for the lexical row when chunks past n_lex exist);
 //   pass 2: every chunk's fused composite; tau = the need-th largest of the maxima of the 128
 //           eight-thread groups (need = min(k, n) <= 128) bounds the need-th best composite
 //           from below;
@@ -1522,8 +1573,10 @@ __device__ __forceinline__ u64 fused_composite(double sd, double sl, double mnd,
 }
 __global__ __launch_bounds__(kFuseThreads) void weighted_fuse_kernel(const float* __restrict__ D,
                                                                  const float* __restrict__ B, long long ld,
-                                                                 long long n, long long n_lex, double wd, double wl,
-                                                                 int k, unsigned long long* cbuf, int* ccnt) {
+                                                                 long long n, long long n_lex,
+                                                                 const float* __restrict__ mm_d, int pd,
+                                                                 const float* __restrict__ mm_l, int pl, double wd,
+                                                                 double wl, int k, unsigned long long* cbuf, int* ccnt) {
   __shared__ float red[4][kFuseThreads / 64];
   __shared__ uint32_t skey[kFuseLds];
   __shared__ u64 gmax[kFuseGroups];
@@ -1534,23 +1587,17 @@ __global__ __launch_bounds__(kFuseThreads) void weighted_fuse_kernel(const float
   const float* d = D + q * ld;
   const float* b = B + q * ld;
   float mnd = __builtin_inff(), mxd = -__builtin_inff(), mnl = __builtin_inff(), mxl = -__builtin_inff();
-  for (long long i0 = t; i0 < n; i0 += 8 * kFuseThreads) {
-    float x[8], y[8];
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const long long i = i0 + (long long)u * kFuseThreads;
-      x[u] = i < n ? d[i] : 0.f;
-      y[u] = i < n_lex ? b[i] : 0.f;
-    }
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      if (i0 + (long long)u * kFuseThreads < n) {  // slots past the last chunk take no part
-        mnd = fminf(mnd, x[u]);
-        mxd = fmaxf(mxd, x[u]);
-        mnl = fminf(mnl, y[u]);
-        mxl = fmaxf(mxl, y[u]);
-      }
-    }
+  for (int i = t; i < pd; i += kFuseThreads) {
+    mnd = fminf(mnd, mm_d[(q * pd + i) * 2]);
+    mxd = fmaxf(mxd, mm_d[(q * pd + i) * 2 + 1]);
+  }
+  for (int i = t; i < pl; i += kFuseThreads) {
+    mnl = fminf(mnl, mm_l[(q * pl + i) * 2]);
+    mxl = fmaxf(mxl, mm_l[(q * pl + i) * 2 + 1]);
+  }
+  if (n_lex < n) {  // chunks past the sparse corpus score 0 lexically
+    mnl = fminf(mnl, 0.f);
+    mxl = fmaxf(mxl, 0.f);
   }
   for (int o = 32; o > 0; o >>= 1) {
     mnd = fminf(mnd, __shfl_xor(mnd, o));
@@ -2115,10 +2162,11 @@ hipError_t launch_dense_dump(const DensePlan& p, const DenseArgs& a, hipStream_t
 }
 
 hipError_t launch_weighted_fuse(const float* D, const float* B, long long ld, long long n, long long n_lex, int nq,
-                                double wd, double wl, int k, unsigned long long* cbuf, int* ccnt, float* out_scores,
-                                long long* out_ids, hipStream_t s) {
-  hipLaunchKernelGGL(weighted_fuse_kernel, dim3((unsigned)nq), dim3(kFuseThreads), 0, s, D, B, ld, n, n_lex, wd, wl,
-                     k, cbuf, ccnt);
+                                const float* mm_d, int pd, const float* mm_l, int pl, double wd, double wl, int k,
+                                unsigned long long* cbuf, int* ccnt, float* out_scores, long long* out_ids,
+                                hipStream_t s) {
+  hipLaunchKernelGGL(weighted_fuse_kernel, dim3((unsigned)nq), dim3(kFuseThreads), 0, s, D, B, ld, n, n_lex, mm_d, pd,
+                     mm_l, pl, wd, wl, k, cbuf, ccnt);
   hipLaunchKernelGGL(select_topk_kernel, dim3((unsigned)nq), dim3(kThreads), 0, s, cbuf, ccnt, n, k, out_scores, out_ids,
                      nullptr, nullptr, 0);
   return hipGetLastError();

@@ -35,9 +35,11 @@ struct DenseArgs {
   long long cap = 0;
   // When set, the launch does nothing unless *gate != 0 (a device-side overflow flag).
   const int* gate = nullptr;
-  // Score dump (SEL 3): every score to dump[q * dump_ld + row].
+  // Score dump (SEL 3): every score to dump[q * dump_ld + row]; with dump_mm set, also the
+  // minimum and maximum of each (query, chunk) to dump_mm[(q * n_chunks + chunk) * 2 + {0, 1}].
   float* dump = nullptr;
   long long dump_ld = 0;
+  float* dump_mm = nullptr;
 };
 
 struct DensePlan {
@@ -74,9 +76,11 @@ DensePlan plan_dense_dump(int dtype, int d, long long n_rows, int nq);
 hipError_t launch_dense_dump(const DensePlan& p, const DenseArgs& a, hipStream_t s);
 // Weighted fusion of dense scores D and lexical scores B ([nq x ld], lexical 0 past n_lex),
 // min-max normalised per query over n chunks, then the exact top k (cbuf [nq x n], ccnt [nq]).
+// The minima and maxima come from the dumps' partials mm_d [nq x pd x 2] and mm_l [nq x pl x 2].
 hipError_t launch_weighted_fuse(const float* D, const float* B, long long ld, long long n, long long n_lex, int nq,
-                                double wd, double wl, int k, unsigned long long* cbuf, int* ccnt, float* out_scores,
-                                long long* out_ids, hipStream_t s);
+                                const float* mm_d, int pd, const float* mm_l, int pl, double wd, double wl, int k,
+                                unsigned long long* cbuf, int* ccnt, float* out_scores, long long* out_ids,
+                                hipStream_t s);
 // Enough workspace for a search of nq queries at any row count up to `capacity`.
 size_t dense_workspace_bound(int dtype, int d, long long capacity, int nq, int k);
 // ev0 / ev1 (optional) are recorded on s right before and after the scoring kernel (in
@@ -120,9 +124,11 @@ hipError_t launch_sparse(const SparseIndex& sp, const int* qterm_indptr, const i
 // ---------------------------------------------------------------- fusion and upsert
 // Dense-first hybrid: BM25 of the dense candidates cand [nq x n_cand] (dense order, -1 padded,
 // 1 <= n_cand <= 128), reciprocal rank fusion with their dense order, top k.
-// BM25 scores of every chunk [0, n_docs) for nq queries into dump [nq x ld].
+// BM25 scores of every chunk [0, n_docs) for nq queries into dump [nq x ld], and the minimum
+// and maximum over chunks [0, mm_rows) of each (query, range of kSparseRange chunks) into
+// dump_mm [nq x ranges x 2] (+inf / -inf for a range with none of them).
 hipError_t launch_sparse_dump(const SparseIndex& sp, const int* qterm_indptr, const int* qterms, int nq, float* dump,
-                              long long ld, hipStream_t s);
+                              long long ld, float* dump_mm, long long mm_rows, hipStream_t s);
 hipError_t launch_dense_first(const SparseIndex& sp, const int* qterm_indptr, const int* qterms,
                               const long long* cand, int n_cand, long long nq, int rrf_k, int k, float* out_fused,
                               long long* out_ids, hipStream_t s);
