@@ -383,6 +383,36 @@ def test_weighted_fusion_past_the_lds_key_cache():
         _check_weighted(F, sc, ids, k, f"n={n} k={k}")
 
 
+def test_weighted_fusion_index_growing_inside_a_larger_corpus():
+    """A 40,000-chunk sparse corpus attached to an index of capacity 40,000 that holds 5,000,
+    then 33,000, then 40,000 rows: the normalisation covers the chunks with a dense row only
+    (the lexical minimum and maximum of the corpus's other chunks must not enter), and the
+    workspace sized from the capacity serves every row count."""
+    from paper_2608_08340_amd import OP_WEIGHTED
+    from oracle import weighted
+    dev = device()
+    cap, nq = 40_000, 24
+    ind, toks, csr, qi, qt = _small_corpus(5001, cap, 400, 14.0, nq)
+    w = synth.mixture_dense(5002, cap, 128, 32, nq, 100, "bf16")
+    idx = make_index(w.rows[:0], "bf16", capacity=cap)
+    _attach(idx, csr, dev)
+    ws = idx.workspace(OP_WEIGHTED, nq)
+    qt_oracle = np.where((qt >= 0) & (qt < 400), qt, 10 ** 6).astype(np.int64)
+    B = bm25.scores_batch(ind, toks, qi, qt_oracle, 1.2, 0.75)  # statistics over the whole corpus
+    done = 0
+    for n in (5_000, 33_000, 40_000):
+        idx.upsert(w.rows[done:n].to(dev))
+        done = n
+        S, X, Q = oracle_scores(w.rows[:n], w.queries, "bf16")
+        F = weighted.fused(S, B[:, :n])
+        for k in (5, 100):
+            log("weighted growing", n, k)
+            sc, ids = idx.search_hybrid_weighted(w.queries.to(dev), _t(qi, dev), _t(qt, dev), 0.5, 0.5, k)
+            torch.cuda.synchronize()
+            assert idx.workspace(OP_WEIGHTED, nq).data_ptr() == ws.data_ptr()  # never regrown
+            _check_weighted(F, sc, ids, k, f"n={n} k={k}")
+
+
 @pytest.mark.timeout(300)
 def test_weighted_fusion_32k(c3):
     """The 32,768 x 1,024 bf16 hybrid workload with weights 0.5 / 0.5, top-5, every query
