@@ -17,7 +17,9 @@ values, with no blocking, fusion or pruning:
 * ``upsert`` - append-only Op_upsert (Section 3.2, "Upsert") on a host copy of the index,
   with the fp32 -> bf16 / fp16 rounding the library applies when the source dtype differs.
 * ``accept`` - the tie-aware acceptance rules the GPU results are held to.
+* ``dense_first``, ``weighted``, ``embed_tail`` - the dense-first hybrid schedule, the
+  paper's weighted score fusion and the mean-pool + L2 tail of the embedding step.
 
-Readings where the paper is silent are listed in the design doc of the repository.
+Where the paper is silent, each module's docstring states the reading it takes.
 """
 from . import accept, bm25, dense, rrf, storage, upsert  # noqa: F401
