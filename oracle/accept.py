@@ -159,21 +159,32 @@ def check_batch(S: np.ndarray, gpu_ids, gpu_scores, k: int, **kw):
     return reps
 
 
-def certificate(s_returned: np.ndarray, gpu_ids, gpu_scores, err_returned: np.ndarray,
-                s_best_unreturned: float | None = None, err_best_unreturned: float = 0.0) -> Report:
+def certificate(s_returned: np.ndarray, gpu_ids, gpu_scores, err_returned: np.ndarray, k: int, n_rows: int,
+                s_unreturned=None, err_unreturned=None) -> Report:
     """Sort-free check for one query at full size.
 
-    ``s_returned`` are the oracle scores of the returned ids.  When the oracle's best score
-    among the rows NOT returned is given, nothing may beat the k-th returned row by more than
-    the two error bounds.
+    ``s_returned`` [k] are the oracle scores of the returned ids (any value in padding slots)
+    and ``err_returned`` their error bounds.  The list must hold exactly min(k, n_rows)
+    distinct ids in [0, n_rows) followed by -1 padding with -inf scores, match the oracle
+    scores within the bounds, and be ordered.  ``s_unreturned`` / ``err_unreturned`` give
+    oracle scores and bounds of rows NOT returned (every row that could matter: at least
+    those scoring above the k-th returned score plus its bound); none of them may beat the
+    k-th returned row by more than the two bounds.
     """
     rep = Report()
-    g = np.asarray(gpu_ids, dtype=np.int64)
-    sh = np.asarray(gpu_scores, dtype=np.float64)
-    v = g >= 0
-    kk = int(v.sum())
-    if np.any(g[:kk] < 0) or len(set(g[:kk].tolist())) != kk:
-        rep.fail("ids not a distinct valid prefix")
+    g = np.asarray(gpu_ids, dtype=np.int64).reshape(-1)
+    sh = np.asarray(gpu_scores, dtype=np.float64).reshape(-1)
+    s_returned = np.asarray(s_returned, dtype=np.float64).reshape(-1)
+    err_returned = np.asarray(err_returned, dtype=np.float64).reshape(-1)
+    kk = min(k, n_rows)
+    if g.shape[0] != k:
+        rep.fail(f"list has {g.shape[0]} slots, expected {k}")
+        return rep
+    if np.any(g[:kk] < 0) or np.any(g[:kk] >= n_rows) or len(set(g[:kk].tolist())) != kk:
+        rep.fail(f"ids are not {kk} distinct rows of [0, {n_rows}): {g[:kk].tolist()}")
+        return rep
+    if np.any(g[kk:] != -1) or np.any(np.isfinite(sh[kk:])):
+        rep.fail(f"padding past {kk} entries is not (-1, -inf): {g[kk:].tolist()}")
         return rep
     for r in range(kk):
         if not abs(sh[r] - s_returned[r]) <= err_returned[r]:
@@ -181,9 +192,182 @@ def certificate(s_returned: np.ndarray, gpu_ids, gpu_scores, err_returned: np.nd
     for r in range(kk - 1):
         if sh[r] < sh[r + 1] or (sh[r] == sh[r + 1] and g[r] > g[r + 1]):
             rep.fail(f"gpu list not ordered at r={r}")
-    if s_best_unreturned is not None and kk:
-        kth = float(np.min(s_returned[:kk]))
+    if s_unreturned is not None and kk:
+        s_u = np.asarray(s_unreturned, dtype=np.float64).reshape(-1)
+        e_u = np.zeros_like(s_u) if err_unreturned is None else np.asarray(err_unreturned, dtype=np.float64).reshape(-1)
         j = int(np.argmin(s_returned[:kk]))
-        if s_best_unreturned > kth + err_returned[j] + err_best_unreturned:
-            rep.fail(f"missed a row scoring {s_best_unreturned!r} above the k-th returned {kth!r}")
+        kth = float(s_returned[j])
+        beat = s_u > kth + err_returned[j] + e_u
+        if np.any(beat):
+            rep.fail(f"missed {int(beat.sum())} row(s), best scoring {float(s_u[beat].max())!r}, "
+                     f"above the k-th returned {kth!r}")
+    return rep
+
+
+def bm25_f32_err(B: np.ndarray, n_terms) -> np.ndarray:
+    """Bound on |fp32 BM25 - B| for a sum of positive contributions over at most ``n_terms``
+    query terms.  Each contribution's factors are rounded to fp32 three times (idf (k1 + 1),
+    the query multiplicity, the posting weight) and each of the at most n_terms additions
+    rounds once, all relative errors of at most u = 2^-24 on positive values, so the sum is
+    within gamma_{n_terms + 3}(u) B; the factor 2 absorbs the fp64 rounding of the attach-time
+    factors."""
+    n = np.asarray(n_terms, dtype=np.float64)
+    u = 2.0 ** -24
+    return 2.0 * (n + 3) * u / (1.0 - (n + 3) * u) * np.abs(np.asarray(B, dtype=np.float64))
+
+
+def _rank_order_exists(items, above, fixed, release) -> bool:
+    """Is there a bijection rank: items -> 1..n with rank[x] < rank[y] whenever above(x, y),
+    rank[x] == fixed[x] where given and rank[x] >= release[x] where given?
+
+    Unit jobs on one machine with precedence, release times and deadlines (a fixed rank is a
+    release and a deadline at once, every other job may finish by n): release times are
+    pushed forward and deadlines backward along the precedence relation, then the slots are
+    filled in order by earliest modified deadline among the released jobs whose predecessors
+    are placed.  For unit jobs with integer release times this rule finds a schedule whenever
+    one exists (Lageweg, Lenstra and Rinnooy Kan, 1976), and here every slot must be used."""
+    items = list(items)
+    n = len(items)
+    preds = {y: [x for x in items if x != y and above(x, y)] for y in items}
+    succs = {x: [y for y in items if y != x and above(x, y)] for x in items}
+    r = {x: fixed.get(x, release.get(x, 1)) for x in items}
+    d = {x: fixed.get(x, n) for x in items}
+    # the relation is a strict order (transitive), so one pass in a linear extension suffices
+    topo = sorted(items, key=lambda x: len(preds[x]))
+    for y in topo:
+        for x in preds[y]:
+            r[y] = max(r[y], r[x] + 1)
+    for x in reversed(topo):
+        for y in succs[x]:
+            d[x] = min(d[x], d[y] - 1)
+    if any(r[x] > d[x] for x in items):
+        return False
+    placed = set()
+    for t in range(1, n + 1):
+        ready = [x for x in items if x not in placed and r[x] <= t and all(p in placed for p in preds[x])]
+        if not ready:
+            return False
+        x = min(ready, key=lambda z: (d[z], z))
+        if d[x] < t:
+            return False
+        placed.add(x)
+    return True
+
+
+def check_dense_first(cand_ids, lex, lex_err, gpu_ids, gpu_fused, rrf_k: int, k: int, sig=None) -> Report:
+    """Tie-aware check of a dense-first fused list for one query.
+
+    ``cand_ids`` are the dense candidates in dense order (-1 = empty slot), ``lex`` their
+    fp64 oracle lexical scores, ``lex_err`` bounds on the computed (fp32) scores' errors, and
+    ``sig`` (optional) one hashable per candidate such that equal signatures guarantee
+    bitwise equal computed scores (then only the id order is admissible between them).
+
+    The lexical rank of a candidate with a positive score is known only up to the
+    candidates whose scores lie within the two bounds of its own: its admissible ranks run
+    from 1 + (candidates certainly above) to 1 + (candidates possibly above).  Accepted iff
+      * the list holds min(k, candidates) distinct candidates, then (-1, -inf) padding;
+      * each returned fused value is exactly fp32(1/(rrf_k + a) + 1/(rrf_k + r)) for the
+        id's dense rank a and an admissible lexical rank r (1/(rrf_k + a) alone for a
+        candidate without a positive score), and the recovered ranks are distinct;
+      * the list is ordered by (exact fused value desc, id asc);
+      * some admissible lexical order (ranks consistent with the candidates certainly above
+        one another, the returned candidates at their recovered ranks) leaves every candidate
+        that is not returned behind the k-th returned entry in (fused desc, id asc).
+    Without near ties every interval is a single rank, and this is exact equality with the
+    reranking of the candidates by their exact scores.
+    """
+    from fractions import Fraction
+
+    rep = Report()
+    cand = [int(c) for c in cand_ids]
+    valid = [c for c in cand if c >= 0]
+    a_of = {c: i + 1 for i, c in enumerate(valid)}
+    lex_of = {c: float(v) for c, v in zip(cand, lex) if c >= 0}
+    err_of = {c: float(e) for c, e in zip(cand, lex_err) if c >= 0}
+    sig_of = {c: s for c, s in zip(cand, sig)} if sig is not None else {}
+    pos = [c for c in valid if lex_of[c] > 0]
+
+    def certainly_above(x, y):  # x's computed score beats y's, whatever the rounding
+        if sig_of and sig_of.get(x) == sig_of.get(y) and lex_of[x] == lex_of[y]:
+            return x < y
+        return lex_of[x] - err_of[x] > lex_of[y] + err_of[y]
+
+    rmin, rmax = {}, {}
+    for c in pos:
+        above = sum(1 for o in pos if o != c and certainly_above(o, c))
+        below = sum(1 for o in pos if o != c and certainly_above(c, o))
+        rmin[c], rmax[c] = 1 + above, len(pos) - below
+
+    def dense_part(c):
+        return Fraction(1, rrf_k + a_of[c])
+
+    g = [int(x) for x in np.asarray(gpu_ids).reshape(-1)]
+    f = np.asarray(gpu_fused, dtype=np.float32).reshape(-1)
+    kk = min(k, len(valid))
+    if len(g) != k or any(x < 0 for x in g[:kk]) or any(x != -1 for x in g[kk:]):
+        rep.fail(f"expected {kk} ids then -1 padding: {g}")
+        return rep
+    if np.any(np.isfinite(f[kk:])):
+        rep.fail("padding slots carry finite fused values")
+    got = g[:kk]
+    if len(set(got)) != kk or any(x not in a_of for x in got):
+        rep.fail(f"ids repeated or not candidates: {got}")
+        return rep
+    exact, ranks = [], []
+    for r, c in enumerate(got):
+        if c in rmin:
+            hit = None
+            for lr in range(rmin[c], rmax[c] + 1):
+                v = dense_part(c) + Fraction(1, rrf_k + lr)
+                if np.float32(float(v)) == f[r]:
+                    hit = (v, lr)
+                    break
+            if hit is None:
+                rep.fail(f"slot {r}: id {c} (dense rank {a_of[c]}, lexical ranks {rmin[c]}..{rmax[c]}) "
+                         f"has fused {f[r]!r}, no admissible value")
+                return rep
+            exact.append(hit[0])
+            ranks.append(hit[1])
+        else:
+            v = dense_part(c)
+            if np.float32(float(v)) != f[r]:
+                rep.fail(f"slot {r}: id {c} has no lexical score, fused {f[r]!r} != 1/({rrf_k}+{a_of[c]})")
+                return rep
+            exact.append(v)
+    if len(set(ranks)) != len(ranks):
+        rep.fail(f"two returned candidates share a lexical rank: {ranks}")
+    for r in range(kk - 1):
+        if exact[r] < exact[r + 1] or (exact[r] == exact[r + 1] and got[r] > got[r + 1]):
+            rep.fail(f"list not ordered at slot {r}")
+    if kk:
+        # Completeness: some admissible lexical order must put every candidate left out behind
+        # the k-th returned entry.  The returned candidates keep their recovered ranks; a
+        # candidate c left out needs a rank of at least m_c (the first at which its fused value
+        # loses to the k-th); ranks are a permutation of 1..|positive| consistent with the
+        # "certainly above" relations.
+        fk, ik = exact[-1], got[-1]
+
+        def loses(v, c):
+            return v < fk or (v == fk and c > ik)
+
+        fixed = {c: lr for c, lr in zip([c for c in got if c in rmin], ranks)}
+        release = {}
+        for c in valid:
+            if c in got:
+                continue
+            if c not in rmin:
+                if not loses(dense_part(c), c):
+                    rep.fail(f"candidate {c} without a lexical score (fused {float(dense_part(c))!r}) beats the "
+                             f"k-th returned {ik} ({float(fk)!r})")
+                    return rep
+                continue
+            m = next((lr for lr in range(1, len(pos) + 1) if loses(dense_part(c) + Fraction(1, rrf_k + lr), c)), None)
+            if m is None:
+                rep.fail(f"candidate {c} beats the k-th returned {ik} at every lexical rank")
+                return rep
+            release[c] = m
+        if not _rank_order_exists(pos, certainly_above, fixed, release):
+            rep.fail(f"no admissible lexical order leaves the unreturned candidates behind the k-th returned {ik} "
+                     f"({float(fk)!r}) with the returned ranks {dict(fixed)}")
+    rep.n_subst = sum(1 for c in pos if rmax[c] > rmin[c])  # candidates with an uncertain rank
     return rep

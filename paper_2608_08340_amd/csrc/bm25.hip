@@ -256,9 +256,9 @@ __global__ __launch_bounds__(kNT) void bm25_kernel(SparseArgs a) {
             wp[u] = a.wpost[p + u * kNT];
           }
 #pragma unroll
-          for (int u = 0; u < 8; ++u) acc[c[u] - d0] += wt * wp[u];
+          for (int u = 0; u < 8; ++u) acc[c[u] - d0] = __builtin_fmaf(wt, wp[u], acc[c[u] - d0]);
         }
-        for (; p < hi; p += kNT) acc[a.chunk[p] - d0] += wt * a.wpost[p];
+        for (; p < hi; p += kNT) acc[a.chunk[p] - d0] = __builtin_fmaf(wt, a.wpost[p], acc[a.chunk[p] - d0]);
       }
       __syncthreads();
     }
@@ -602,18 +602,22 @@ __global__ void fwd_fill_kernel(int vocab, const long long* __restrict__ indptr,
 // 5.5: lexical reranking of the dense top-n candidates only).  One workgroup of 1,024 threads
 // per query: the eight threads (c, j) = (t / 8, t % 8) share the dense candidate of rank c + 1
 // and read its chunk-major (term, weight) list together, entries j, j + 8, ..., comparing each
-// entry with up to 32 query term occurrences at a time held in LDS; a match stores the weight
-// in the candidate's slot for that occurrence.  The candidate's BM25 score is then the sum of
-// idfk * weight over the occurrences in query order (the order of the full BM25 kernel).  The
-// candidates with a positive score are ranked by (score desc, id asc); reciprocal rank fusion
-// of that order with the dense order, compared exactly as fractions (as rrf_kernel does),
-// gives the top k.
+// entry with up to 32 query terms at a time held in LDS; a match stores the weight in the
+// candidate's slot for that term.  Like bm25_kernel, a term that occurs m times in the query
+// takes part once, at its first occurrence, with factor m * idf(t) (k1 + 1), and the
+// candidate's score is fma(factor, weight, score) over the distinct terms in first-occurrence
+// order: the same fp32 operations in the same order, so a candidate scores exactly what the
+// full BM25 search gives its chunk.  Candidates at or past the sparse corpus's n_docs chunks
+// hold no postings and score 0.  The candidates with a positive score are ranked by (score
+// desc, id asc); reciprocal rank fusion of that order with the dense order, compared exactly
+// as fractions (as rrf_kernel does), gives the top k.
 // ------------------------------------------------------------------------------------
 constexpr int kDfThreads = 1024;
 constexpr int kRrfExactMax = 100000;  // below this rrf_k the fused quotients order exactly
 constexpr int kDfCand = 128;
 constexpr int kDfLanes = kDfThreads / kDfCand;
-__global__ __launch_bounds__(kDfThreads) void dense_first_kernel(int vocab, const long long* __restrict__ fwd_ptr,
+__global__ __launch_bounds__(kDfThreads) void dense_first_kernel(int vocab, long long n_docs,
+                                                                 const long long* __restrict__ fwd_ptr,
                                                                  const int* __restrict__ fwd_term,
                                                                  const float* __restrict__ idfk,
                                                                  const float* __restrict__ fwd_w,
@@ -621,7 +625,9 @@ __global__ __launch_bounds__(kDfThreads) void dense_first_kernel(int vocab, cons
                                                                  const long long* cand, int n_cand, int rrf_k, int k,
                                                                  float* out_fused, long long* out_ids) {
   constexpr int kTerms = 32;  // query term occurrences per pass
-  __shared__ int qt_s[kTerms];
+  static_assert(kTerms * 32 == kDfThreads, "32 threads find the multiplicity of each occurrence");
+  __shared__ int qt_s[kTerms];    // the pass's distinct-term occurrences (-1: repeat or unknown)
+  __shared__ float fw_s[kTerms];  // their factors m * idf(t) (k1 + 1)
   __shared__ float wq[kDfCand][kTerms + 1];
   __shared__ float lex[kDfCand];
   __shared__ long long cid[kDfCand];
@@ -632,17 +638,41 @@ __global__ __launch_bounds__(kDfThreads) void dense_first_kernel(int vocab, cons
   const long long q = blockIdx.x;
   const int t = threadIdx.x, c = t / kDfLanes, j = t % kDfLanes;
   const long long id = c < n_cand ? cand[q * n_cand + c] : -1;
-  const long long f0 = id >= 0 ? fwd_ptr[id] : 0, f1 = id >= 0 ? fwd_ptr[id + 1] : 0;
+  const bool has_terms = id >= 0 && id < n_docs;  // chunks past the sparse corpus have none
+  const long long f0 = has_terms ? fwd_ptr[id] : 0, f1 = has_terms ? fwd_ptr[id + 1] : 0;
   float sc = 0.f;  // thread j == 0 of a candidate: its score
-  const int e_end = qterm_indptr[q + 1];
-  for (int e0 = qterm_indptr[q]; e0 < e_end; e0 += kTerms) {
+  const int tb = qterm_indptr[q], e_end = qterm_indptr[q + 1];
+  for (int e0 = tb; e0 < e_end; e0 += kTerms) {
     const int ne = min(kTerms, e_end - e0);
-    if (t < kTerms) qt_s[t] = t < ne ? qterms[e0 + t] : -1;
+    {
+      // occurrence u = t / 32 of the pass: is it its term's first, and how often does the
+      // term occur from here on (32 threads scan the query's terms, as bm25_kernel does)
+      const int u = t >> 5, sub = t & 31;
+      int term = -1, earlier = 0, mult = 0;
+      if (u < ne) {
+        term = qterms[e0 + u];
+        for (int jj = tb + sub; jj < e_end; jj += 32)
+          if (qterms[jj] == term) {
+            if (jj < e0 + u) earlier = 1;
+            else mult += 1;
+          }
+      }
+#pragma unroll
+      for (int o = 16; o > 0; o >>= 1) {
+        earlier |= __shfl_xor(earlier, o, 32);
+        mult += __shfl_xor(mult, o, 32);
+      }
+      if (sub == 0) {
+        const bool use = u < ne && !earlier && term >= 0 && term < vocab;  // unknown terms match nothing
+        qt_s[u] = use ? term : -1;
+        fw_s[u] = use ? idfk[term] * (float)mult : 0.f;
+      }
+    }
     for (int i = t; i < kDfCand * kTerms; i += kDfThreads) wq[i / kTerms][i % kTerms] = 0.f;
     __syncthreads();
-    // sixteen entries per thread and step, all loads issued before any comparison; per query term
-    // occurrence the weights of matching entries are summed (a list holds a term once, so
-    // the sum is that weight or 0) and a match is stored
+    // sixteen entries per thread and step, all loads issued before any comparison; per query
+    // term the weights of matching entries are summed (a list holds a term once, so the sum
+    // is that weight or 0) and a match is stored
     constexpr int kStep = 16;
     for (long long f = f0 + j; f < f1; f += kStep * kDfLanes) {
       int tm[kStep];
@@ -655,6 +685,7 @@ __global__ __launch_bounds__(kDfThreads) void dense_first_kernel(int vocab, cons
       }
       for (int u = 0; u < ne; ++u) {
         const int tu = qt_s[u];
+        if (tu < 0) continue;  // uniform: the term takes part at an earlier occurrence, or never
         float m = 0.f;
 #pragma unroll
         for (int v = 0; v < kStep; ++v) m += tm[v] == tu ? wt[v] : 0.f;
@@ -662,13 +693,11 @@ __global__ __launch_bounds__(kDfThreads) void dense_first_kernel(int vocab, cons
       }
     }
     __syncthreads();
-    if (j == 0 && id >= 0) {
-      for (int u = 0; u < ne; ++u) {
-        const int term = qt_s[u];
-        if (term >= 0 && term < vocab) sc += idfk[term] * wq[c][u];  // unknown terms match nothing
-      }
+    if (j == 0 && has_terms) {
+      for (int u = 0; u < ne; ++u)
+        if (qt_s[u] >= 0) sc = __builtin_fmaf(fw_s[u], wq[c][u], sc);  // an unmatched term adds 0 exactly
     }
-    __syncthreads();  // qt_s and wq are rewritten by the next pass
+    __syncthreads();  // qt_s, fw_s and wq are rewritten by the next pass
   }
   if (t == 0) s_nv = 0;
   __syncthreads();
@@ -861,7 +890,7 @@ hipError_t launch_dense_first(const SparseIndex& sp, const int* qterm_indptr, co
                               const long long* cand, int n_cand, long long nq, int rrf_k, int k, float* out_fused,
                               long long* out_ids, hipStream_t s) {
   if (n_cand < 1 || n_cand > kDfCand) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(dense_first_kernel, dim3((unsigned)nq), dim3(kDfThreads), 0, s, sp.vocab, sp.fwd_ptr,
+  hipLaunchKernelGGL(dense_first_kernel, dim3((unsigned)nq), dim3(kDfThreads), 0, s, sp.vocab, sp.n_docs, sp.fwd_ptr,
                      sp.fwd_term, sp.idfk, sp.fwd_w, qterm_indptr, qterms, cand, n_cand, rrf_k, k, out_fused,
                      out_ids);
   return hipGetLastError();

@@ -136,12 +136,13 @@ def _streaming(n0, rounds, m, d, clusters, nq, k, sample, workload=5):
         assert (sids[:, 0].cpu().numpy() == np.arange(n - m, n - m + 64)).all()
         sc, ids = sc.cpu().numpy(), ids.cpu().numpy()
         Q = decode(synth.storage_bits(q), "f16")
-        # every query: fp64 score of each returned row and list order
-        Xr = decode(bits[ids.reshape(-1)], "f16").reshape(nq, k, d)
-        s_ret = np.einsum("qkd,qd->qk", Xr, Q)
+        # every query: fp64 score of each returned row, list length and order
+        valid = ids >= 0
+        Xr = decode(bits[np.where(valid, ids, 0).reshape(-1)], "f16").reshape(nq, k, d)
+        s_ret = np.where(valid, np.einsum("qkd,qd->qk", Xr, Q), 0.0)
         err = accept.strict_err(np.einsum("qkd,qd->qk", np.abs(Xr), np.abs(Q)), d)
         for qq in range(nq):
-            rep = accept.certificate(s_ret[qq], ids[qq], sc[qq], err[qq])
+            rep = accept.certificate(s_ret[qq], ids[qq], sc[qq], err[qq], k, n)
             assert rep.ok, (r, qq, rep.problems)
         # sampled queries: full oracle (row blocks scored on a thread pool)
         samp = np.random.default_rng(100 + r).choice(nq, sample, replace=False)
@@ -157,8 +158,10 @@ def test_streaming_upsert_and_search_small():
 
 @pytest.mark.timeout(1200)
 def test_streaming_8m_x_384_f16_top100_full_size():
-    """8,388,608 x 384 fp16 rows (8,192 clusters), 16 rounds of +65,536 rows and 4,096 queries, top-100."""
-    _streaming(n0=8388608, rounds=16, m=65536, d=384, clusters=8192, nq=4096, k=100, sample=4)
+    """8,388,608 x 384 fp16 rows (8,192 clusters), 16 rounds of +65,536 rows and 4,096 queries, top-100.
+    Every query of every round: returned scores against fp64, list length and order; 16
+    sampled queries per round: fp64 scores of every row and the full acceptance rules."""
+    _streaming(n0=8388608, rounds=16, m=65536, d=384, clusters=8192, nq=4096, k=100, sample=16)
 
 
 def _ulp(x: np.ndarray, dtype: str) -> np.ndarray:

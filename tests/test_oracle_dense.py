@@ -58,6 +58,21 @@ def test_bruteforce_float_rows():
         np.testing.assert_allclose(sc[b], [fs[i] for i in ref], rtol=0, atol=1e-14)
 
 
+def test_abs_dot_hand_case():
+    """sum_j |q_j x_ij| by hand: row 0 -> 1 + 2 + 6 = 9, row 1 -> 0.5 + 0 + 8 = 8.5 (the plain
+    dots are 3 and -8.5, so an absolute value taken after the sum fails row 0)."""
+    X = np.array([[1.0, -2.0, 3.0], [0.5, 0.0, -4.0]])
+    q = np.array([[-1.0, 1.0, 2.0], [0.0, 0.0, 0.0]])
+    A = od.abs_dot(X, q)
+    assert A.tolist() == [[9.0, 8.5], [0.0, 0.0]]
+    assert od.scores(X, q)[0].tolist() == [3.0, -8.5]
+    # never below |score|, equal for sign-consistent rows
+    rnd = np.random.default_rng(8)
+    Xr, Qr = rnd.standard_normal((30, 16)), rnd.standard_normal((4, 16))
+    assert np.all(od.abs_dot(Xr, Qr) >= np.abs(od.scores(Xr, Qr)) - 1e-12)
+    assert np.allclose(od.abs_dot(np.abs(Xr), np.abs(Qr)), od.scores(np.abs(Xr), np.abs(Qr)))
+
+
 def test_padding_when_k_exceeds_rows():
     X = np.eye(3)
     ids, sc = od.topk_from_scores(od.scores(X, np.array([[0.1, 0.3, 0.2]])), 5)
