@@ -166,6 +166,25 @@ oprag_status oprag_search_dense(oprag_index *idx, const void *q_dev, int64_t nq,
                                 int64_t *ids_dev, void *workspace_dev, size_t workspace_bytes, void *stream);
 
 /*
+ * For callers that cannot allocate device memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc): oprag_search_dense with the same
+ * arguments, kernels and results, but no workspace argument.  The intermediate per-chunk
+ * lists (or threshold-level candidates) go to a fixed array of OPRAG_NOALLOC_SCRATCH_BYTES
+ * in device memory that the library defines once per GPU and keeps until the process ends;
+ * the call allocates nothing.  A search whose plan at the current row count needs more
+ * returns E_CAPACITY with nothing enqueued: split the batch.  The need never exceeds what
+ * oprag_workspace_bytes(OPRAG_OP_DENSE) reports; with k <= 16 and up to 1,024 queries it
+ * stays within 8 MiB (2.6 MB for 256 queries and k = 5), while k > 16 needs 8 bytes per
+ * query and candidate slot (every row up to 32,768 rows) and can exceed the array at a few
+ * hundred queries.  Every call on one GPU shares its array, and nothing in it has to start
+ * at any value (each call writes what it later reads), so calls that may overlap on one GPU
+ * (different streams, or several host threads) race and must be ordered by the caller.
+ */
+#define OPRAG_NOALLOC_SCRATCH_BYTES (32u << 20)
+oprag_status oprag_search_dense_noalloc(oprag_index *idx, const void *q_dev, int64_t nq, int32_t k,
+                                        float *scores_dev, int64_t *ids_dev, void *stream);
+
+/*
  * Exact BM25 top-k (Section 4.4) over the attached sparse index.  Query q's terms are
  * qterms_dev[qterm_indptr_dev[q] .. qterm_indptr_dev[q + 1]) (int32; repeated terms count
  * once per occurrence; ids outside [0, vocab) match nothing).  Only chunks with a positive

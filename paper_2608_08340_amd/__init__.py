@@ -52,6 +52,7 @@ _SIGS = {
     "oprag_sparse_attach": ([_P, _I32, _I64, _I64, _P, _P, _P, _P, _F, _F, _P], _I32),
     "oprag_workspace_bytes": ([_P, _I32, _I64, _I32, _I32, ctypes.POINTER(_SZ)], _I32),
     "oprag_search_dense": ([_P, _P, _I64, _I32, _P, _P, _P, _SZ, _P], _I32),
+    "oprag_search_dense_noalloc": ([_P, _P, _I64, _I32, _P, _P, _P], _I32),
     "oprag_search_sparse": ([_P, _P, _P, _I64, _I32, _P, _P, _P, _SZ, _P], _I32),
     "oprag_rrf_fuse": ([_P, _I32, _P, _I32, _I64, _I32, _I32, _P, _P, _P], _I32),
     "oprag_search_hybrid": ([_P, _P, _P, _P, _I64, _I32, _I32, _I32, _I32, _P, _P, _P, _SZ, _P], _I32),
@@ -208,6 +209,18 @@ class Index:
         ws = self.workspace(OP_DENSE, nq, k, 1)
         _check(library().oprag_search_dense(self._h, _ptr(q), nq, k, _ptr(scores), _ptr(ids), _ptr(ws),
                                             ws.numel(), _stream(self.device)))
+        return scores, ids
+
+    def search_dense_noalloc(self, q: torch.Tensor, k: int, out: tuple | None = None):
+        """search_dense without a workspace: the library's fixed per-GPU scratch array holds the
+        intermediate lists (for callers that cannot allocate; concurrent calls on one GPU race)."""
+        _dev_tensor(q, self.dtype, self.device, "q")
+        nq = q.shape[0]
+        scores, ids = out if out is not None else (
+            torch.empty((nq, k), dtype=torch.float32, device=self.device),
+            torch.empty((nq, k), dtype=torch.int64, device=self.device))
+        _check(library().oprag_search_dense_noalloc(self._h, _ptr(q), nq, k, _ptr(scores), _ptr(ids),
+                                                    _stream(self.device)))
         return scores, ids
 
     def search_sparse(self, qterm_indptr: torch.Tensor, qterms: torch.Tensor, k: int, out: tuple | None = None):

@@ -7,6 +7,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 
 #include "../../include/oprag.h"
@@ -163,6 +164,39 @@ oprag_status do_dense(oprag_index* idx, const void* q, int64_t nq, int32_t k, fl
     hipError_t e = oprag::launch_dense(p, idx->dtype, a, s, ev0, ev1);
     if (e != hipSuccess) return hip_fail(e, "dense search launch");
   }
+  return OPRAG_OK;
+}
+
+// Largest workspace one call of a dense search without allocation may need.  The plan of
+// one launch (at most kMaxQPerLaunch queries) at the current row count decides it.
+size_t dense_ws_now(const oprag_index* idx, int64_t nq, int32_t k) {
+  const int nql = (int)std::min<int64_t>(nq, kMaxQPerLaunch);
+  const oprag::DensePlan p = oprag::plan_dense(idx->dtype, idx->dim, idx->n_rows, nql, k);
+  return p.kernel < 0 ? 0 : oprag::dense_workspace_bytes(p, nql);
+}
+
+// The workspace of oprag_search_dense_noalloc: a fixed device array, one copy per GPU the
+// library runs on, held until the process ends.  Host code never passes `scratch` itself to
+// a kernel (on the host the name is only a stand-in for the symbol): it takes the device
+// address that hipGetSymbolAddress returns, once per device, with that device current.
+constexpr size_t kNoallocScratchBytes = (size_t)OPRAG_NOALLOC_SCRATCH_BYTES;
+__device__ __align__(256) static unsigned char scratch[kNoallocScratchBytes];
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of this device's scratch array (the device must be current).
+oprag_status scratch_of(int device, void** out) {
+  if (device < 0 || device >= kMaxDevices) return fail(OPRAG_E_UNSUPPORTED, "device %d >= %d", device, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[device]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    if (!p) return fail(OPRAG_E_DEVICE, "hipGetSymbolAddress(scratch) returned NULL");
+    g_scratch_ptr[device] = p;
+  }
+  *out = g_scratch_ptr[device];
   return OPRAG_OK;
 }
 
@@ -417,6 +451,29 @@ oprag_status oprag_search_dense(oprag_index* idx, const void* q_dev, int64_t nq,
   DeviceScope ds(idx->device);
   if (ds.error() != hipSuccess) return hip_fail(ds.error(), "select device");
   if (oprag_status st = do_dense(idx, q_dev, nq, k, scores_dev, ids_dev, workspace_dev, workspace_bytes,
+                                 static_cast<hipStream_t>(stream)))
+    return st;
+  return ok();
+}
+
+oprag_status oprag_search_dense_noalloc(oprag_index* idx, const void* q_dev, int64_t nq, int32_t k, float* scores_dev,
+                                        int64_t* ids_dev, void* stream) {
+  if (oprag_status st = check_index(idx)) return st;
+  if (oprag_status st = check_k(k, "k")) return st;
+  if (nq < 0 || nq > (int64_t)1 << 31) return fail(OPRAG_E_INVALID, "nq %lld out of range", (long long)nq);
+  if (nq == 0) return ok();
+  if (oprag_status st = check_buf(q_dev, "q_dev")) return st;
+  if (oprag_status st = check_buf(scores_dev, "scores_dev")) return st;
+  if (oprag_status st = check_buf(ids_dev, "ids_dev")) return st;
+  const size_t need = dense_ws_now(idx, nq, k);
+  if (need > kNoallocScratchBytes)
+    return fail(OPRAG_E_CAPACITY, "search needs %zu bytes of scratch, the fixed array holds %zu (fewer queries per call)",
+                need, kNoallocScratchBytes);
+  DeviceScope ds(idx->device);
+  if (ds.error() != hipSuccess) return hip_fail(ds.error(), "select device");
+  void* ws = nullptr;
+  if (oprag_status st = scratch_of(idx->device, &ws)) return st;
+  if (oprag_status st = do_dense(idx, q_dev, nq, k, scores_dev, ids_dev, ws, kNoallocScratchBytes,
                                  static_cast<hipStream_t>(stream)))
     return st;
   return ok();
