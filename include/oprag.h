@@ -43,7 +43,7 @@
 extern "C" {
 #endif
 
-#define OPRAG_ABI_VERSION 1
+#define OPRAG_ABI_VERSION 2
 #define OPRAG_MAX_K 128
 #define OPRAG_MAX_DIM 8192
 
@@ -162,7 +162,7 @@ oprag_status oprag_workspace_bytes(const oprag_index *idx, int32_t op, int64_t n
  * levels whose exactness repair is decided on the device), so a search can be captured in a
  * HIP graph.
  */
-oprag_status oprag_search_dense(oprag_index *idx, const void *q_dev, int64_t nq, int32_t k, float *scores_dev,
+oprag_status oprag_search_dense(const oprag_index *idx, const void *q_dev, int64_t nq, int32_t k, float *scores_dev,
                                 int64_t *ids_dev, void *workspace_dev, size_t workspace_bytes, void *stream);
 
 /*
@@ -181,7 +181,7 @@ oprag_status oprag_search_dense(oprag_index *idx, const void *q_dev, int64_t nq,
  * (different streams, or several host threads) race and must be ordered by the caller.
  */
 #define OPRAG_NOALLOC_SCRATCH_BYTES (32u << 20)
-oprag_status oprag_search_dense_noalloc(oprag_index *idx, const void *q_dev, int64_t nq, int32_t k,
+oprag_status oprag_search_dense_noalloc(const oprag_index *idx, const void *q_dev, int64_t nq, int32_t k,
                                         float *scores_dev, int64_t *ids_dev, void *stream);
 
 /*
@@ -191,7 +191,7 @@ oprag_status oprag_search_dense_noalloc(oprag_index *idx, const void *q_dev, int
  * score are ranked.  scores_dev [nq x k] fp32, ids_dev [nq x k] int64.
  * E_STATE without an attached sparse index.
  */
-oprag_status oprag_search_sparse(oprag_index *idx, const int32_t *qterm_indptr_dev, const int32_t *qterms_dev,
+oprag_status oprag_search_sparse(const oprag_index *idx, const int32_t *qterm_indptr_dev, const int32_t *qterms_dev,
                                  int64_t nq, int32_t k, float *scores_dev, int64_t *ids_dev, void *workspace_dev,
                                  size_t workspace_bytes, void *stream);
 
@@ -215,10 +215,10 @@ oprag_status oprag_rrf_fuse(const int64_t *dense_ids_dev, int32_t k_dense, const
  * oprag_search_dense + oprag_search_sparse + oprag_rrf_fuse on the same stream.
  * workspace_dev must hold oprag_workspace_bytes(OPRAG_OP_HYBRID) bytes.
  */
-oprag_status oprag_search_hybrid(oprag_index *idx, const void *q_dev, const int32_t *qterm_indptr_dev,
-                                 const int32_t *qterms_dev, int64_t nq, int32_t k_dense, int32_t k_sparse,
-                                 int32_t rrf_k, int32_t k, float *fused_dev, int64_t *ids_dev, void *workspace_dev,
-                                 size_t workspace_bytes, void *stream);
+oprag_status oprag_search_hybrid(const oprag_index *idx, const void *q_dev, int64_t nq, const int32_t *qterm_indptr_dev,
+                                 const int32_t *qterms_dev, int32_t k_dense, int32_t k_sparse, int32_t rrf_k, int32_t k,
+                                 float *fused_dev, int64_t *ids_dev, void *workspace_dev, size_t workspace_bytes,
+                                 void *stream);
 
 /*
  * Dense-first hybrid search (the serving schedule of Section 4.1, "Retrieval", whose latency
@@ -235,10 +235,10 @@ oprag_status oprag_search_hybrid(oprag_index *idx, const void *q_dev, const int3
  * oprag_workspace_bytes(OPRAG_OP_DENSE_FIRST, k_dense = n_cand) bytes.  E_STATE without an
  * attached sparse index.
  */
-oprag_status oprag_search_hybrid_dense_first(oprag_index *idx, const void *q_dev, const int32_t *qterm_indptr_dev,
-                                             const int32_t *qterms_dev, int64_t nq, int32_t n_cand, int32_t rrf_k,
-                                             int32_t k, float *fused_dev, int64_t *ids_dev, void *workspace_dev,
-                                             size_t workspace_bytes, void *stream);
+oprag_status oprag_search_hybrid_dense_first(const oprag_index *idx, const void *q_dev, int64_t nq,
+                                             const int32_t *qterm_indptr_dev, const int32_t *qterms_dev, int32_t n_cand,
+                                             int32_t rrf_k, int32_t k, float *fused_dev, int64_t *ids_dev,
+                                             void *workspace_dev, size_t workspace_bytes, void *stream);
 
 /*
  * Weighted score fusion over the whole corpus (Section 4.4): score(d, q) = w_dense *
@@ -255,10 +255,10 @@ oprag_status oprag_search_hybrid_dense_first(oprag_index *idx, const void *q_dev
  * 8 bytes per query for each partial minimum / maximum pair of the two score dumps).
  * E_STATE without an attached sparse index, E_UNSUPPORTED for an fp32 index.
  */
-oprag_status oprag_search_hybrid_weighted(oprag_index *idx, const void *q_dev, const int32_t *qterm_indptr_dev,
-                                          const int32_t *qterms_dev, int64_t nq, float w_dense, float w_lex, int32_t k,
-                                          float *scores_dev, int64_t *ids_dev, void *workspace_dev,
-                                          size_t workspace_bytes, void *stream);
+oprag_status oprag_search_hybrid_weighted(const oprag_index *idx, const void *q_dev, int64_t nq,
+                                          const int32_t *qterm_indptr_dev, const int32_t *qterms_dev, float w_dense,
+                                          float w_lex, int32_t k, float *scores_dev, int64_t *ids_dev,
+                                          void *workspace_dev, size_t workspace_bytes, void *stream);
 
 /*
  * Kernel timing (diagnostics: measuring the scoring kernel against its roofline).  Arms a

@@ -55,10 +55,10 @@ _SIGS = {
     "oprag_search_dense_noalloc": ([_P, _P, _I64, _I32, _P, _P, _P], _I32),
     "oprag_search_sparse": ([_P, _P, _P, _I64, _I32, _P, _P, _P, _SZ, _P], _I32),
     "oprag_rrf_fuse": ([_P, _I32, _P, _I32, _I64, _I32, _I32, _P, _P, _P], _I32),
-    "oprag_search_hybrid": ([_P, _P, _P, _P, _I64, _I32, _I32, _I32, _I32, _P, _P, _P, _SZ, _P], _I32),
-    "oprag_search_hybrid_dense_first": ([_P, _P, _P, _P, _I64, _I32, _I32, _I32, _P, _P, _P, _SZ, _P], _I32),
+    "oprag_search_hybrid": ([_P, _P, _I64, _P, _P, _I32, _I32, _I32, _I32, _P, _P, _P, _SZ, _P], _I32),
+    "oprag_search_hybrid_dense_first": ([_P, _P, _I64, _P, _P, _I32, _I32, _I32, _P, _P, _P, _SZ, _P], _I32),
     "oprag_upsert_pooled": ([_P, _P, _I32, _P, _I64, _I32, _P, ctypes.POINTER(_I64)], _I32),
-    "oprag_search_hybrid_weighted": ([_P, _P, _P, _P, _I64, ctypes.c_float, ctypes.c_float, _I32, _P, _P, _P, _SZ, _P],
+    "oprag_search_hybrid_weighted": ([_P, _P, _I64, _P, _P, ctypes.c_float, ctypes.c_float, _I32, _P, _P, _P, _SZ, _P],
                                      _I32),
     "oprag_time_next_dense_kernel": ([_P, _P], _I32),
 }
@@ -249,7 +249,7 @@ class Index:
             torch.empty((nq, k), dtype=torch.float32, device=self.device),
             torch.empty((nq, k), dtype=torch.int64, device=self.device))
         ws = self.workspace(OP_HYBRID, nq, k_dense, k_sparse)
-        _check(library().oprag_search_hybrid(self._h, _ptr(q), _ptr(qterm_indptr), _ptr(qterms), nq, k_dense,
+        _check(library().oprag_search_hybrid(self._h, _ptr(q), nq, _ptr(qterm_indptr), _ptr(qterms), k_dense,
                                              k_sparse, rrf_k, k, _ptr(fused), _ptr(ids), _ptr(ws), ws.numel(),
                                              _stream(self.device)))
         return fused, ids
@@ -268,7 +268,7 @@ class Index:
             torch.empty((nq, k), dtype=torch.float32, device=self.device),
             torch.empty((nq, k), dtype=torch.int64, device=self.device))
         ws = self.workspace(OP_DENSE_FIRST, nq, n_cand, 1)
-        _check(library().oprag_search_hybrid_dense_first(self._h, _ptr(q), _ptr(qterm_indptr), _ptr(qterms), nq,
+        _check(library().oprag_search_hybrid_dense_first(self._h, _ptr(q), nq, _ptr(qterm_indptr), _ptr(qterms),
                                                          n_cand, rrf_k, k, _ptr(fused), _ptr(ids), _ptr(ws),
                                                          ws.numel(), _stream(self.device)))
         return fused, ids
@@ -287,7 +287,7 @@ class Index:
             torch.empty((nq, k), dtype=torch.float32, device=self.device),
             torch.empty((nq, k), dtype=torch.int64, device=self.device))
         ws = self.workspace(OP_WEIGHTED, nq, 1, 1)
-        _check(library().oprag_search_hybrid_weighted(self._h, _ptr(q), _ptr(qterm_indptr), _ptr(qterms), nq,
+        _check(library().oprag_search_hybrid_weighted(self._h, _ptr(q), nq, _ptr(qterm_indptr), _ptr(qterms),
                                                       w_dense, w_lex, k, _ptr(scores), _ptr(ids), _ptr(ws),
                                                       ws.numel(), _stream(self.device)))
         return scores, ids

@@ -18,6 +18,7 @@ using oprag::kMaxQPerLaunch;
 
 struct oprag_index {
   int32_t dim = 0, dtype = 0, device = 0;
+  int32_t n_cus = 0;  // compute units of the device (kernel grids are planned for it)
   int64_t capacity = 0;
   void* slab = nullptr;
   size_t slab_bytes = 0;
@@ -97,7 +98,7 @@ size_t align_up(size_t x) { return (x + 255) & ~size_t(255); }
 
 size_t dense_ws(const oprag_index* idx, int64_t nq, int32_t k) {
   const int nql = (int)std::min<int64_t>(nq, kMaxQPerLaunch);
-  return oprag::dense_workspace_bound(idx->dtype, idx->dim, idx->capacity, nql, k);
+  return oprag::dense_workspace_bound(idx->dtype, idx->dim, idx->capacity, nql, k, idx->n_cus);
 }
 
 size_t sparse_ws(const oprag_index* idx, int64_t nq, int32_t k) {
@@ -121,7 +122,7 @@ long long weighted_ld(const oprag_index* idx) { return (idx->capacity + 3) & ~3l
 // Partial minima and maxima per query: of the dense dump's chunks (at most as many as its plan
 // at full capacity has) and of the BM25 ranges.
 int weighted_pd(const oprag_index* idx, int64_t nq) {
-  return std::max(1, oprag::plan_dense_dump(idx->dtype, idx->dim, idx->capacity, (int)nq).n_chunks);
+  return std::max(1, oprag::plan_dense_dump(idx->dtype, idx->dim, idx->capacity, (int)nq, idx->n_cus).n_chunks);
 }
 int weighted_pl(const oprag_index* idx) {
   return (int)((idx->capacity + oprag::kSparseRange - 1) / oprag::kSparseRange);
@@ -132,12 +133,12 @@ size_t weighted_ws(const oprag_index* idx, int64_t nq) {
          align_up((size_t)nq * (size_t)weighted_pd(idx, nq) * 8) + align_up((size_t)nq * (size_t)weighted_pl(idx) * 8);
 }
 
-oprag_status do_dense(oprag_index* idx, const void* q, int64_t nq, int32_t k, float* scores, int64_t* ids, void* ws,
+oprag_status do_dense(const oprag_index* idx, const void* q, int64_t nq, int32_t k, float* scores, int64_t* ids, void* ws,
                       size_t ws_bytes, hipStream_t s) {
   const size_t es = elem_size(idx->dtype);
   for (int64_t q0 = 0; q0 < nq; q0 += kMaxQPerLaunch) {
     const int nql = (int)std::min<int64_t>(kMaxQPerLaunch, nq - q0);
-    const oprag::DensePlan p = oprag::plan_dense(idx->dtype, idx->dim, idx->n_rows, nql, k);
+    const oprag::DensePlan p = oprag::plan_dense(idx->dtype, idx->dim, idx->n_rows, nql, k, idx->n_cus);
     if (p.kernel < 0) return fail(OPRAG_E_UNSUPPORTED, "no dense kernel for dtype %d, k %d", idx->dtype, k);
     if (oprag::dense_workspace_bytes(p, nql) > ws_bytes)
       return fail(OPRAG_E_INVALID, "workspace too small: %zu < %zu bytes", ws_bytes,
@@ -171,7 +172,7 @@ oprag_status do_dense(oprag_index* idx, const void* q, int64_t nq, int32_t k, fl
 // one launch (at most kMaxQPerLaunch queries) at the current row count decides it.
 size_t dense_ws_now(const oprag_index* idx, int64_t nq, int32_t k) {
   const int nql = (int)std::min<int64_t>(nq, kMaxQPerLaunch);
-  const oprag::DensePlan p = oprag::plan_dense(idx->dtype, idx->dim, idx->n_rows, nql, k);
+  const oprag::DensePlan p = oprag::plan_dense(idx->dtype, idx->dim, idx->n_rows, nql, k, idx->n_cus);
   return p.kernel < 0 ? 0 : oprag::dense_workspace_bytes(p, nql);
 }
 
@@ -238,7 +239,12 @@ oprag_status oprag_index_create(const oprag_index_desc* desc, void* slab_dev, si
   const hipError_t e = hipGetDeviceCount(&n_dev);
   if (e != hipSuccess) return hip_fail(e, "device count");
   if (desc->device >= n_dev) return fail(OPRAG_E_INVALID, "device %d does not exist (%d devices)", desc->device, n_dev);
+  int n_cus = 0;
+  const hipError_t ea = hipDeviceGetAttribute(&n_cus, hipDeviceAttributeMultiprocessorCount, desc->device);
+  if (ea != hipSuccess) return hip_fail(ea, "compute unit count");
+  if (n_cus < 1) return fail(OPRAG_E_DEVICE, "device %d reports %d compute units", desc->device, n_cus);
   oprag_index* idx = new oprag_index;
+  idx->n_cus = n_cus;
   idx->dim = desc->dim;
   idx->dtype = desc->dtype;
   idx->device = desc->device;
@@ -435,7 +441,7 @@ oprag_status oprag_workspace_bytes(const oprag_index* idx, int32_t op, int64_t n
   }
 }
 
-oprag_status oprag_search_dense(oprag_index* idx, const void* q_dev, int64_t nq, int32_t k, float* scores_dev,
+oprag_status oprag_search_dense(const oprag_index* idx, const void* q_dev, int64_t nq, int32_t k, float* scores_dev,
                                 int64_t* ids_dev, void* workspace_dev, size_t workspace_bytes, void* stream) {
   if (oprag_status st = check_index(idx)) return st;
   if (oprag_status st = check_k(k, "k")) return st;
@@ -456,7 +462,7 @@ oprag_status oprag_search_dense(oprag_index* idx, const void* q_dev, int64_t nq,
   return ok();
 }
 
-oprag_status oprag_search_dense_noalloc(oprag_index* idx, const void* q_dev, int64_t nq, int32_t k, float* scores_dev,
+oprag_status oprag_search_dense_noalloc(const oprag_index* idx, const void* q_dev, int64_t nq, int32_t k, float* scores_dev,
                                         int64_t* ids_dev, void* stream) {
   if (oprag_status st = check_index(idx)) return st;
   if (oprag_status st = check_k(k, "k")) return st;
@@ -479,7 +485,7 @@ oprag_status oprag_search_dense_noalloc(oprag_index* idx, const void* q_dev, int
   return ok();
 }
 
-oprag_status oprag_search_sparse(oprag_index* idx, const int32_t* qterm_indptr_dev, const int32_t* qterms_dev,
+oprag_status oprag_search_sparse(const oprag_index* idx, const int32_t* qterm_indptr_dev, const int32_t* qterms_dev,
                                  int64_t nq, int32_t k, float* scores_dev, int64_t* ids_dev, void* workspace_dev,
                                  size_t workspace_bytes, void* stream) {
   if (oprag_status st = check_index(idx)) return st;
@@ -524,10 +530,10 @@ oprag_status oprag_rrf_fuse(const int64_t* dense_ids_dev, int32_t k_dense, const
   return ok();
 }
 
-oprag_status oprag_search_hybrid(oprag_index* idx, const void* q_dev, const int32_t* qterm_indptr_dev,
-                                 const int32_t* qterms_dev, int64_t nq, int32_t k_dense, int32_t k_sparse,
-                                 int32_t rrf_k, int32_t k, float* fused_dev, int64_t* ids_dev, void* workspace_dev,
-                                 size_t workspace_bytes, void* stream) {
+oprag_status oprag_search_hybrid(const oprag_index* idx, const void* q_dev, int64_t nq, const int32_t* qterm_indptr_dev,
+                                 const int32_t* qterms_dev, int32_t k_dense, int32_t k_sparse, int32_t rrf_k, int32_t k,
+                                 float* fused_dev, int64_t* ids_dev, void* workspace_dev, size_t workspace_bytes,
+                                 void* stream) {
   if (oprag_status st = check_index(idx)) return st;
   if (!idx->has_sparse) return fail(OPRAG_E_STATE, "no sparse index attached");
   if (oprag_status st = check_k(k_dense, "k_dense")) return st;
@@ -567,10 +573,10 @@ oprag_status oprag_search_hybrid(oprag_index* idx, const void* q_dev, const int3
   return ok();
 }
 
-oprag_status oprag_search_hybrid_dense_first(oprag_index* idx, const void* q_dev, const int32_t* qterm_indptr_dev,
-                                             const int32_t* qterms_dev, int64_t nq, int32_t n_cand, int32_t rrf_k,
-                                             int32_t k, float* fused_dev, int64_t* ids_dev, void* workspace_dev,
-                                             size_t workspace_bytes, void* stream) {
+oprag_status oprag_search_hybrid_dense_first(const oprag_index* idx, const void* q_dev, int64_t nq,
+                                             const int32_t* qterm_indptr_dev, const int32_t* qterms_dev, int32_t n_cand,
+                                             int32_t rrf_k, int32_t k, float* fused_dev, int64_t* ids_dev,
+                                             void* workspace_dev, size_t workspace_bytes, void* stream) {
   if (oprag_status st = check_index(idx)) return st;
   if (!idx->has_sparse) return fail(OPRAG_E_STATE, "no sparse index attached");
   if (oprag_status st = check_k(n_cand, "n_cand")) return st;
@@ -603,10 +609,10 @@ oprag_status oprag_search_hybrid_dense_first(oprag_index* idx, const void* q_dev
   return ok();
 }
 
-oprag_status oprag_search_hybrid_weighted(oprag_index* idx, const void* q_dev, const int32_t* qterm_indptr_dev,
-                                          const int32_t* qterms_dev, int64_t nq, float w_dense, float w_lex, int32_t k,
-                                          float* scores_dev, int64_t* ids_dev, void* workspace_dev,
-                                          size_t workspace_bytes, void* stream) {
+oprag_status oprag_search_hybrid_weighted(const oprag_index* idx, const void* q_dev, int64_t nq,
+                                          const int32_t* qterm_indptr_dev, const int32_t* qterms_dev, float w_dense,
+                                          float w_lex, int32_t k, float* scores_dev, int64_t* ids_dev,
+                                          void* workspace_dev, size_t workspace_bytes, void* stream) {
   if (oprag_status st = check_index(idx)) return st;
   if (!idx->has_sparse) return fail(OPRAG_E_STATE, "no sparse index attached");
   if (idx->dtype == OPRAG_F32) return fail(OPRAG_E_UNSUPPORTED, "weighted fusion needs a bf16 or fp16 index");
@@ -623,7 +629,7 @@ oprag_status oprag_search_hybrid_weighted(oprag_index* idx, const void* q_dev, c
   const size_t need = weighted_ws(idx, nq);
   if (!workspace_dev || !aligned16(workspace_dev) || workspace_bytes < need)
     return fail(OPRAG_E_INVALID, "workspace missing or too small (%zu < %zu bytes)", workspace_bytes, need);
-  const oprag::DensePlan p = oprag::plan_dense_dump(idx->dtype, idx->dim, idx->n_rows, (int)nq);
+  const oprag::DensePlan p = oprag::plan_dense_dump(idx->dtype, idx->dim, idx->n_rows, (int)nq, idx->n_cus);
   if (p.kernel < 0) return fail(OPRAG_E_UNSUPPORTED, "no scoring kernel for dtype %d", idx->dtype);
   DeviceScope ds(idx->device);
   if (ds.error() != hipSuccess) return hip_fail(ds.error(), "select device");

@@ -10,23 +10,26 @@
 // with a single chunk the first kernel writes the final list itself.  The score matrix
 // never leaves the chip.
 //
-// Data movement for bf16 / fp16: each stage of KC = 64 dimensions is copied straight from
-// global memory into an LDS ring slot with global_load_lds_dwordx4 (no VGPR round trip),
-// already in MFMA fragment order (one 1 KiB fragment = 16 rows x 32 dims, lane i's 16 bytes
-// at offset 16 i), so every fragment read is a linear, conflict-free ds_read_b128.  The
-// waves form a WM x WN grid over (rows x queries); each loads the fragments of a 32-dim step
-// for its subtile before issuing that step's MFMAs, and the next step's fragments while the
-// MFMAs run.
+// Data movement for bf16 / fp16: each wave owns MW 16-row subtiles of a tile and loads their
+// rows with 16-byte buffer loads straight into VGPRs, already in the MFMA A-operand layout
+// (lane l: row l % 16, eight dimensions 8 (l / 16) of a 32-dimension k-step); a register ring
+// of RS k-steps keeps RS - 1 of them in flight.  The query block is shared by the waves: each
+// 128-dimension super-step of it is loaded one super-step ahead into VGPRs and written to one
+// of two LDS slots (16-byte pieces swizzled by row so writes and fragment reads use all
+// banks), from which every wave reads its B operands one k-step ahead of the MFMAs.
 //
-// Selection (k <= 16): per tile, the score subtile goes to LDS query-major.  Pass 1 keeps the
-// top-KS *values* of each thread's row slice with a branch-free v_med3 insertion network
-// (one instruction per slot), and the values are combined per query with the running list
-// to give the k-th best value tau.  Pass 2 appends only rows scoring above tau, plus the
-// smallest-id rows equal to tau that may still be needed, to a small per-query candidate
-// list, which the query's owner thread inserts into its running (score desc, id asc) list.
-// Exact, and the 64-bit composite compares run on at most 2k - 1 candidates per query and
-// pass.  Selection (k <= 128): one wave per query keeps a 128-entry sorted queue and merges
-// batches of 64 candidates above its k-th entry with a bitonic network.
+// Selection (k <= 16) runs after each tile on the accumulators.  A chunk's first tile, and
+// any tile the faster test declines, takes the group path: the k-th largest of the lanes'
+// group maxima (with the running list) bounds the k-th best score from below, only the
+// scores reaching it go to LDS, and each query's owner thread inserts them into its running
+// (score desc, id asc) list of 64-bit composites.  Later tiles compare each lane's group
+// maximum with the running k-th score and hand over the rare hits.  Heavy ties fall back to
+// passes over an LDS score tile: the top-KS values of each slice (a v_med3 insertion
+// network), then the rows above the exact k-th value and the smallest-id rows equal to it.
+// Filtered mode (bf16 / fp16, 16 < k <= 128): threshold levels over growing row prefixes
+// collect candidate keys per query and select_topk_kernel ranks them.  fp32 with k > 16: one
+// wave per query keeps a 128-entry sorted queue and merges batches of 64 candidates above
+// its k-th entry with a bitonic network.
 #include <algorithm>
 
 #include <hip/hip_ext.h>
@@ -63,13 +66,6 @@ struct Mfma<kDtypeF16> {
   }
 };
 
-#define OPRAG_LDS(p) ((__attribute__((address_space(3))) void*)(p))
-
-// 16 bytes per lane, global -> LDS; lane i's bytes land at lds_base + 16 * i.
-__device__ __forceinline__ void dma16(const void* g, void* lds_base) {
-  __builtin_amdgcn_global_load_lds(g, OPRAG_LDS(lds_base), 16, 0, 0);
-}
-
 // Raw buffer resource over [base, base + bytes): 16-byte loads at offsets past the end
 // return zeros instead of touching memory (gfx9 descriptor word 3: 32-bit data format).
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base, long long bytes) {
@@ -79,12 +75,6 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base, 
 
 __device__ __forceinline__ u32x4 buffer_load16(__amdgpu_buffer_rsrc_t r, int voffset) {
   return __builtin_amdgcn_raw_buffer_load_b128(r, voffset, 0, 0);
-}
-
-template <int N>
-__device__ __forceinline__ void wait_vm() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
 // Workgroup barrier that leaves in-flight ring loads in flight (a full __syncthreads()
@@ -1893,7 +1883,6 @@ int pick_kernel(int dtype, int d, int nq, int k, int sel) {
   return -1;
 }
 
-constexpr int kNumCUs = 256;
 constexpr long long kFilterMin = 2048;        // fewest rows of a level that has a successor
 constexpr long long kFilterFirstMax = 4096;   // most rows of the first level
 constexpr long long kFilterLast = 16;         // row growth into the last level
@@ -1902,8 +1891,8 @@ constexpr long long kFilterAllRows = 32768;   // up to this many rows a buffer h
 
 // Workgroups per query block that fill the chip twice over (at least enough to keep every
 // chunk of a ring kernel under 2^30 bytes of rows, the reach of its 32-bit offsets).
-long long chunk_bound(const KernelInfo& ki, int d, long long n_rows, int n_qblocks, long long* min_chunks) {
-  const long long target = (long long)kNumCUs * ki.chunk_target;
+long long chunk_bound(const KernelInfo& ki, int d, long long n_rows, int n_qblocks, int n_cus, long long* min_chunks) {
+  const long long target = (long long)n_cus * ki.chunk_target;
   long long bound = std::max(1ll, (target + n_qblocks - 1) / n_qblocks);
   long long mc = 1;
   if (ki.ring) {
@@ -1930,8 +1919,9 @@ size_t align_up256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 }  // namespace
 
-DensePlan plan_dense_lists(int dtype, int d, long long n_rows, int nq, int k) {
+DensePlan plan_dense_lists(int dtype, int d, long long n_rows, int nq, int k, int n_cus) {
   DensePlan p;
+  p.n_cus = n_cus;
   p.kernel = pick_kernel(dtype, d, nq, k, k <= 16 ? 0 : 1);
   if (p.kernel < 0) return p;
   const KernelInfo& ki = kKernels[p.kernel];
@@ -1939,7 +1929,7 @@ DensePlan plan_dense_lists(int dtype, int d, long long n_rows, int nq, int k) {
   p.tile_rows = ki.tile_rows;
   p.n_qblocks = (nq + p.bn - 1) / p.bn;
   long long min_chunks = 1;
-  const long long bound = chunk_bound(ki, d, n_rows, p.n_qblocks, &min_chunks);
+  const long long bound = chunk_bound(ki, d, n_rows, p.n_qblocks, n_cus, &min_chunks);
   const long long n_tiles = (n_rows + p.tile_rows - 1) / p.tile_rows;
   long long chunks = bound;
   // the queue-based large-k selector wants several tiles per chunk so its queues amortise
@@ -1949,11 +1939,12 @@ DensePlan plan_dense_lists(int dtype, int d, long long n_rows, int nq, int k) {
   return p;
 }
 
-DensePlan plan_dense(int dtype, int d, long long n_rows, int nq, int k) {
-  if (dtype == kDtypeF32 || k <= 16) return plan_dense_lists(dtype, d, n_rows, nq, k);
+DensePlan plan_dense(int dtype, int d, long long n_rows, int nq, int k, int n_cus) {
+  if (dtype == kDtypeF32 || k <= 16) return plan_dense_lists(dtype, d, n_rows, nq, k, n_cus);
   DensePlan p;
+  p.n_cus = n_cus;
   p.kernel = pick_kernel(dtype, d, nq, k, 2);
-  if (p.kernel < 0) return plan_dense_lists(dtype, d, n_rows, nq, k);
+  if (p.kernel < 0) return plan_dense_lists(dtype, d, n_rows, nq, k, n_cus);
   const KernelInfo& ki = kKernels[p.kernel];
   p.filtered = true;
   p.bn = ki.bn;
@@ -1987,7 +1978,7 @@ DensePlan plan_dense(int dtype, int d, long long n_rows, int nq, int k) {
                ? std::max(1ll, n_rows)
                : std::max(1ll, std::min(n_rows, std::max(p.level_rows[0], 4 * kFilterGrow * (long long)k)));
   p.repair = p.fcap < n_rows;
-  p.chunk_bound = chunk_bound(ki, d, n_rows, p.n_qblocks, nullptr);
+  p.chunk_bound = chunk_bound(ki, d, n_rows, p.n_qblocks, n_cus, nullptr);
   p.kernel0 = p.kernel;
   p.n_qblocks0 = p.n_qblocks;
   p.chunk_bound0 = p.chunk_bound;
@@ -1995,16 +1986,16 @@ DensePlan plan_dense(int dtype, int d, long long n_rows, int nq, int k) {
     DensePlan l0 = p;
     split_rows(l0, p.level_rows[0], p.chunk_bound, 1);
     const int small = pick_kernel(dtype, d, 1, k, 2);
-    if (l0.grid < kNumCUs && small >= 0) {  // the main kernel would leave most CUs idle
+    if (l0.grid < n_cus && small >= 0) {  // the main kernel would leave most CUs idle
       const KernelInfo& ks = kKernels[small];
       p.kernel0 = small;
       p.n_qblocks0 = (nq + ks.bn - 1) / ks.bn;
-      p.chunk_bound0 = chunk_bound(ks, d, p.level_rows[0], p.n_qblocks0, nullptr);
+      p.chunk_bound0 = chunk_bound(ks, d, p.level_rows[0], p.n_qblocks0, n_cus, nullptr);
     }
   }
   split_rows(p, n_rows, p.chunk_bound, 1);
   // the per-chunk-list plan is the exact fallback; the workspace covers it as well
-  p.cap = plan_dense_lists(dtype, d, n_rows, nq, k).cap;
+  p.cap = plan_dense_lists(dtype, d, n_rows, nq, k, n_cus).cap;
   return p;
 }
 
@@ -2030,9 +2021,10 @@ size_t dense_workspace_bytes(const DensePlan& p, int nq) {
 // The plan's workspace grows with the row count except where buffers stop holding every row
 // (fcap drops from kFilterAllRows to max(kFilterFirstMax, 256 k)), so the bound over all row
 // counts up to `capacity` is the larger of the two plans on either side.
-size_t dense_workspace_bound(int dtype, int d, long long capacity, int nq, int k) {
-  size_t b = dense_workspace_bytes(plan_dense(dtype, d, capacity, nq, k), nq);
-  if (capacity > kFilterAllRows) b = std::max(b, dense_workspace_bytes(plan_dense(dtype, d, kFilterAllRows, nq, k), nq));
+size_t dense_workspace_bound(int dtype, int d, long long capacity, int nq, int k, int n_cus) {
+  size_t b = dense_workspace_bytes(plan_dense(dtype, d, capacity, nq, k, n_cus), nq);
+  if (capacity > kFilterAllRows)
+    b = std::max(b, dense_workspace_bytes(plan_dense(dtype, d, kFilterAllRows, nq, k, n_cus), nq));
   return b;
 }
 
@@ -2111,7 +2103,7 @@ hipError_t launch_dense(const DensePlan& p, int dtype, const DenseArgs& a, hipSt
     hipError_t e =
         filter_pass(p, a, a.n_rows, a.out_scores + (a.k - 1), fl + 2, fl, false, false, s, nullptr, nullptr);
     if (e != hipSuccess) return e;
-    const DensePlan lp = plan_dense_lists(dtype, a.d, a.n_rows, a.nq, a.k);
+    const DensePlan lp = plan_dense_lists(dtype, a.d, a.n_rows, a.nq, a.k, p.n_cus);
     DenseArgs la = a;
     la.n_qblocks = lp.n_qblocks;
     la.n_chunks = lp.n_chunks;
@@ -2139,8 +2131,9 @@ hipError_t launch_dense(const DensePlan& p, int dtype, const DenseArgs& a, hipSt
 }
 
 
-DensePlan plan_dense_dump(int dtype, int d, long long n_rows, int nq) {
+DensePlan plan_dense_dump(int dtype, int d, long long n_rows, int nq, int n_cus) {
   DensePlan p;
+  p.n_cus = n_cus;
   p.kernel = pick_kernel(dtype, d, nq, 5, 3);
   if (p.kernel < 0) return p;
   const KernelInfo& ki = kKernels[p.kernel];
@@ -2148,7 +2141,7 @@ DensePlan plan_dense_dump(int dtype, int d, long long n_rows, int nq) {
   p.tile_rows = ki.tile_rows;
   p.n_qblocks = (nq + p.bn - 1) / p.bn;
   long long mc = 1;
-  const long long bound = chunk_bound(ki, d, n_rows, p.n_qblocks, &mc);
+  const long long bound = chunk_bound(ki, d, n_rows, p.n_qblocks, n_cus, &mc);
   split_rows(p, n_rows, bound, mc);
   return p;
 }

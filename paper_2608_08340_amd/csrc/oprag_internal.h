@@ -43,6 +43,7 @@ struct DenseArgs {
 };
 
 struct DensePlan {
+  int n_cus = 0;                // compute units of the device the plan is for
   int kernel = 0;               // index into the dense kernel table
   int bn = 0;                   // queries per workgroup
   int tile_rows = 0;            // rows per tile
@@ -67,12 +68,12 @@ struct DensePlan {
   long long chunk_bound0 = 0;
 };
 
-DensePlan plan_dense(int dtype, int d, long long n_rows, int nq, int k);
+DensePlan plan_dense(int dtype, int d, long long n_rows, int nq, int k, int n_cus);
 // The per-chunk-list plan for any k (the exact fallback of the filtered mode).
-DensePlan plan_dense_lists(int dtype, int d, long long n_rows, int nq, int k);
+DensePlan plan_dense_lists(int dtype, int d, long long n_rows, int nq, int k, int n_cus);
 size_t dense_workspace_bytes(const DensePlan& p, int nq);
 // Score dump: every score of nq queries against rows [0, a.n_rows) into a.dump (SEL 3 kernel).
-DensePlan plan_dense_dump(int dtype, int d, long long n_rows, int nq);
+DensePlan plan_dense_dump(int dtype, int d, long long n_rows, int nq, int n_cus);
 hipError_t launch_dense_dump(const DensePlan& p, const DenseArgs& a, hipStream_t s);
 // Weighted fusion of dense scores D and lexical scores B ([nq x ld], lexical 0 past n_lex),
 // min-max normalised per query over n chunks, then the exact top k (cbuf [nq x n], ccnt [nq]).
@@ -81,8 +82,9 @@ hipError_t launch_weighted_fuse(const float* D, const float* B, long long ld, lo
                                 const float* mm_d, int pd, const float* mm_l, int pl, double wd, double wl, int k,
                                 unsigned long long* cbuf, int* ccnt, float* out_scores, long long* out_ids,
                                 hipStream_t s);
+// Plans take the compute-unit count of the index's device (the grid aims at a multiple of it).
 // Enough workspace for a search of nq queries at any row count up to `capacity`.
-size_t dense_workspace_bound(int dtype, int d, long long capacity, int nq, int k);
+size_t dense_workspace_bound(int dtype, int d, long long capacity, int nq, int k, int n_cus);
 // ev0 / ev1 (optional) are recorded on s right before and after the scoring kernel (in
 // filtered mode, the last level's).  Filtered mode also enqueues its exactness repair:
 // launches gated on device-side overflow flags, so the search never waits for the host.

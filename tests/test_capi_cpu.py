@@ -33,7 +33,7 @@ def test_exports_every_declared_symbol(lib):
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(P._SIGS), "binding and header disagree"
-    assert lib.oprag_abi_version() == 1
+    assert lib.oprag_abi_version() == 2
 
 
 def _desc(dim=1024, dtype=1, cap=100, dev=0, res=0):
@@ -90,7 +90,7 @@ def test_null_handle_everywhere(lib):
     assert lib.oprag_workspace_bytes(None, 0, 1, 5, 5, ctypes.byref(sz)) == E_INVALID
     assert lib.oprag_search_dense(None, None, 1, 5, None, None, None, 0, None) == E_INVALID
     assert lib.oprag_search_sparse(None, None, None, 1, 5, None, None, None, 0, None) == E_INVALID
-    assert lib.oprag_search_hybrid(None, None, None, None, 1, 100, 100, 60, 5, None, None, None, 0, None) == E_INVALID
+    assert lib.oprag_search_hybrid(None, None, 1, None, None, 100, 100, 60, 5, None, None, None, 0, None) == E_INVALID
     assert lib.oprag_index_destroy(None) == 0
 
 
