@@ -917,6 +917,114 @@ __device__ __forceinline__ bool blk_epilogue(const f32x4 (&acc)[MW][BN / 16], Se
 }
 
 // ------------------------------------------------------------------------------------
+// k <= 8, group path: tau = the k-th largest of the lanes' group maxima and the running list
+// is a lower bound of the k-th best score (k distinct rows reach it), so the query's top k
+// lies among its running entries and the tile's scores >= tau.  Every lane writes its scores
+// >= tau to the query's candidate list in LDS (slot-major, [CAPR][BN]; count, reserve once,
+// write); the query's owner thread then reads all of them at once, with every load in flight
+// before the first insertion, and inserts them into its running list.  Returns false, with
+// the running lists untouched, when a query has more than CAPR candidates (many equal scores
+// at tau).
+// ------------------------------------------------------------------------------------
+template <int BN, int WV>
+struct RankArea {
+  static constexpr int NG = WV * 4;  // groups (lane quarters of a wave) per query
+  static constexpr int CAPR = 16;
+  static constexpr int kBytes = NG * BN * 4 + CAPR * BN * 8;
+};
+
+template <int BN, int MW, int KS, int WV, typename Sel>
+__device__ __forceinline__ bool rank_epilogue(const f32x4 (&acc)[MW][BN / 16], Sel& sel, unsigned char* area,
+                                              unsigned char* scratch, long long tile0, long long row_end, int q_lim,
+                                              int k) {
+  constexpr int NW = BN / 16;
+  using RA = RankArea<BN, WV>;
+  constexpr int NG = RA::NG, CAPR = RA::CAPR;
+  static_assert(KS <= 8, "the group maxima bound the k-th score for small k");
+  float* gmax = reinterpret_cast<float*>(area);                    // [NG][BN]
+  u64* cand = reinterpret_cast<u64*>(area + NG * BN * 4);          // [CAPR][BN]
+  float* thr = Sel::tau_of(scratch);
+  int* cnt = Sel::cnt_of(scratch);
+  int* flag = Sel::flag_of(scratch);
+  constexpr int TR = WV * MW * 16;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int g = w * 4 + (lane >> 4);
+  const int row0 = w * MW * 16 + (lane >> 4) * 4;  // tile offset of this lane's value (0, r = 0)
+  // element (mi, r) of this lane is a valid row iff 16 mi + r < lim
+  const int lim = (int)min((long long)TR, row_end - tile0) - row0;
+
+  // 1. group maxima
+#pragma unroll
+  for (int ni = 0; ni < NW; ++ni) {
+    float m = kNegInf;
+#pragma unroll
+    for (int mi = 0; mi < MW; ++mi)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) m = __builtin_fmaxf(m, mi * 16 + r < lim ? acc[mi][ni][r] : kNegInf);
+    gmax[g * BN + ni * 16 + (lane & 15)] = m;
+  }
+  if (tid == 0) *flag = 0;
+  lds_barrier();
+  // 2. owners: tau
+  if (tid < BN) {
+    float tau = __builtin_inff();  // queries past the batch take no candidates
+    if (tid < q_lim) {
+      float gm[NG];
+#pragma unroll
+      for (int j = 0; j < NG; ++j) gm[j] = gmax[j * BN + tid];
+      ValTop<KS> L;
+      L.clear();
+#pragma unroll
+      for (int j = 0; j < NG; ++j) L.insert(gm[j]);
+#pragma unroll
+      for (int i = 0; i < KS; ++i)
+        if (i < k && sel.run.v[i]) L.insert(comp_score(sel.run.v[i]));
+      tau = L.at(k);
+    }
+    thr[tid] = tau;
+    cnt[tid] = 0;
+  }
+  lds_barrier();
+  // 3. this lane's scores reaching tau: count, reserve once per query, write
+#pragma unroll
+  for (int ni = 0; ni < NW; ++ni) {
+    const int n = ni * 16 + (lane & 15);
+    const float th = thr[n];
+    int c = 0;
+#pragma unroll
+    for (int mi = 0; mi < MW; ++mi)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) c += (mi * 16 + r < lim && acc[mi][ni][r] >= th) ? 1 : 0;
+    if (c == 0) continue;
+    int j = atomicAdd(&cnt[n], c);
+    if (j + c > CAPR) {
+      *flag = 1;
+      continue;
+    }
+#pragma unroll
+    for (int mi = 0; mi < MW; ++mi)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float x = acc[mi][ni][r];
+        if (mi * 16 + r < lim && x >= th) cand[(j++) * BN + n] = composite(x, (uint32_t)(tile0 + row0 + mi * 16 + r));
+      }
+  }
+  lds_barrier();
+  if (*flag) return false;
+  // 4. owners: every candidate read at once, then inserted (a wave stops at its largest count)
+  if (tid < q_lim) {
+    const int n = cnt[tid];
+    u64 c[CAPR];
+#pragma unroll
+    for (int j = 0; j < CAPR; ++j) c[j] = j < n ? cand[j * BN + tid] : 0ull;
+#pragma unroll
+    for (int j = 0; j < CAPR; ++j)
+      if (c[j]) sel.run.insert(c[j]);
+  }
+  return true;
+}
+
+// ------------------------------------------------------------------------------------
 // bf16 / fp16 MFMA kernel.  Four waves split a tile of TR = 4*MW*16 rows (each wave owns
 // MW distinct 16-row subtiles) and share a block of BN = NW*16 queries.  A k-step is one
 // MFMA depth (32 dimensions); four k-steps form a super-step of 128 dimensions.
@@ -961,9 +1069,15 @@ __global__ __launch_bounds__(WV * 64) void dense_mfma_kernel(DenseArgs a) {
   // alternate, one super-step ahead.
   constexpr int QBYTES = (QR > 0 ? QR : 2) * QSLOT;
   static_assert(QR == 0 || SEL == 2, "resident queries: filtered selection only");
-  constexpr bool kBlk = SEL == 0 && KS == 5;
+  // k <= 5: the small-tile kernels take the one-pass rank epilogue (and the running-threshold
+  // test for later tiles); the 128-query kernel keeps the block epilogue on every tile, which
+  // leaves its main loop the register budget it is scheduled for.
+  constexpr bool kBlk = SEL == 0 && KS == 5 && NW * MW > 2;
+  constexpr bool kRank = SEL == 0 && KS == 5 && !kBlk;
   constexpr int SB0 = SEL >= 2 ? 0 : BN * SR * 4;
-  constexpr int SBYTES = kBlk && BlockArea<MW, BN>::kBytes > SB0 ? BlockArea<MW, BN>::kBytes : SB0;
+  constexpr int SBYTES = kBlk && BlockArea<MW, BN>::kBytes > SB0   ? BlockArea<MW, BN>::kBytes
+                         : kRank && RankArea<BN, WV>::kBytes > SB0 ? RankArea<BN, WV>::kBytes
+                                                                   : SB0;
   constexpr int SMEM = QBYTES + SBYTES + Sel::kBytes;
   static_assert(MW % G == 0 && ((MWP * 16) & (MWP * 16 - 1)) == 0, "pass shape");
   static_assert(SEL != 0 || RP % (4 * (NT / BN)) == 0, "slice shape");
@@ -1166,15 +1280,18 @@ __global__ __launch_bounds__(WV * 64) void dense_mfma_kernel(DenseArgs a) {
           filt_tile<BN, MW, WV>(acc, th, scratch, tile0, row_end, q0, a);
         done = true;
       } else if constexpr (SEL == 0) {
-        // A chunk's first tile fills the lists through the group path, which leaves the
-        // running thresholds in place for the tiles after it.  (The larger k <= 5 kernels
-        // keep the block path for every tile: they already run close to the register limit.)
-        if constexpr (!kBlk || NW * MW <= 2)
+        // A chunk's first tile fills the lists through the group path; the tiles after it
+        // test against the running thresholds, and take the group path only when a query has
+        // too many hits.  (The 128-query k <= 5 kernel keeps the block path for every tile.)
+        if constexpr (!kBlk)
           if (t > 0) done = thr_epilogue<BN, MW, WV>(acc, sel, scratch, tile0, row_end, q_lim, a.k);
         if (!done) {
           if constexpr (kBlk)
             done = blk_epilogue<BN, MW, WV>(acc, sel, reinterpret_cast<unsigned char*>(S), scratch, tile0, row_end,
-                                        q_lim, a.k);
+                                            q_lim, a.k);
+          else if constexpr (kRank)
+            done = rank_epilogue<BN, MW, KS, WV>(acc, sel, reinterpret_cast<unsigned char*>(S), scratch, tile0,
+                                                 row_end, q_lim, a.k);
           else
             done = reg_epilogue<BN, MW, KS, WV>(acc, sel, S, scratch, tile0, row_end, q_lim, a.k);
           refresh = true;
@@ -1207,7 +1324,7 @@ __global__ __launch_bounds__(WV * 64) void dense_mfma_kernel(DenseArgs a) {
           sel.pass(S, SR, RP, pr, q_lim, a.k, scratch);
         }
       }
-      if constexpr (SEL == 0 && (!kBlk || NW * MW <= 2))
+      if constexpr (SEL == 0 && !kBlk)
         if (refresh) thr_reset(sel, scratch, q_lim, a.k, BN);
     }
 #undef OPRAG_SUPER
