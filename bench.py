@@ -333,10 +333,11 @@ def trace_summarize(out_dir: str, suite: bool = False) -> int:
         out_file, n_show = SUITE_STATS_FILE, 40
     else:
         head = [
-            "rocprofv3 kernel statistics of the default bench.py run (32,768 x 1,024 bf16, batch 256, k 5)",
-            "command: cd /tmp && export TMPDIR=/tmp && timeout -k 10 300 rocprofv3 --kernel-trace --stats "
+            "rocprofv3 kernel statistics of the default bench.py run (32,768 x 1,024 bf16, batch 256, k 5; "
+            "the CPU oracle leg left out)",
+            "command: cd /tmp && export TMPDIR=/tmp && timeout -k 10 400 rocprofv3 --kernel-trace --stats "
             "--output-format csv -d $GRAFT_REPO_ROOT/gpurun_out/kt_bench -o bench -- python3 $GRAFT_REPO_ROOT/bench.py "
-            "&& python3 $GRAFT_REPO_ROOT/bench.py --trace-summarize $GRAFT_REPO_ROOT/gpurun_out/kt_bench",
+            "--no-cpu && python3 $GRAFT_REPO_ROOT/bench.py --trace-summarize $GRAFT_REPO_ROOT/gpurun_out/kt_bench",
         ]
         out_file, n_show = STATS_FILE, 12
     lines = head + [
