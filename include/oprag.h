@@ -22,8 +22,9 @@
  *    next synchronisation of the stream.
  *  - Memory: every large buffer (slab, CSR arrays, queries, outputs, workspace) is device
  *    memory owned by the caller and must stay valid while the index or call uses it.  The
- *    library allocates only its BM25 arrays at attach time (4 bytes per term, 12 per posting
- *    and 8 per chunk, plus temporary counters) and never in create, upsert or search.
+ *    library allocates only its BM25 arrays at attach time (8 bytes per term, 12 per posting,
+ *    8 per chunk and at most 64 MiB of dense rows for the most frequent terms, plus temporary
+ *    counters) and never in create, upsert or search.
  *    Device pointers must be 16-byte aligned.
  *  - Streams: `stream` is a hipStream_t (NULL = default stream).  Calls are asynchronous on
  *    it.  An index keeps host-side state (row count), so calls on one index must be issued
@@ -132,8 +133,10 @@ oprag_status oprag_upsert_pooled(oprag_index *idx, const void *hidden_dev, int32
  * The arrays stay caller-owned and are read by later searches.  The library checks them on
  * the device (E_INVALID on any violation), then computes idf(t) = ln(1 + (N - df + 0.5) /
  * (df + 0.5)) per term and tf / (tf + k1 (1 - b + b dl / avgdl)) per posting, in fp64 stored
- * as fp32, and a chunk-major copy of (term, weight) pairs for scoring given chunks, into
- * arrays it owns (4 bytes per term, 12 per posting and 8 per chunk).
+ * as fp32, a chunk-major copy of (term, weight) pairs for scoring given chunks, and dense
+ * per-chunk weight rows of the most frequent terms (df >= max(64, n_docs / 8), at most 992 rows
+ * and 64 MiB), into arrays it owns (8 bytes per term, 12 per posting, 8 per chunk, plus the
+ * rows).
  * Synchronises `stream`.  Re-attaching replaces the previous sparse index.
  * k1 >= 0, 0 <= b <= 1.
  */

@@ -9,6 +9,7 @@
 #include <cstring>
 #include <mutex>
 #include <string>
+#include <vector>
 
 #include "../../include/oprag.h"
 #include "oprag_internal.h"
@@ -343,32 +344,57 @@ oprag_status oprag_sparse_attach(oprag_index* idx, int32_t vocab, int64_t n_docs
   DeviceScope ds(idx->device);
   if (ds.error() != hipSuccess) return hip_fail(ds.error(), "select device");
   hipStream_t s = static_cast<hipStream_t>(stream);
-  // Library-owned arrays: [flag u32 | sum u64 | idfk f32 x vocab | posting weights f32 x nnz |
-  // chunk-major copy: list offsets i64 x (n_docs + 1), terms i32 x nnz, weights f32 x nnz].
-  const size_t off_sum = 256, off_idf = 512;
+  // Validation first, with a small flag buffer of its own.
+  hipError_t e = hipSuccess;
+  {
+    unsigned int* d_flag = nullptr;
+    e = hipMalloc(&d_flag, 256);
+    if (e != hipSuccess) return hip_fail(e, "sparse validation flag allocation");
+    e = oprag::sparse_validate(vocab, n_docs, nnz, reinterpret_cast<const long long*>(term_indptr_dev),
+                               post_chunk_dev, post_tf_dev, doc_len_dev, d_flag, s);
+    unsigned int bad = 0;
+    if (e == hipSuccess) e = hipMemcpyAsync(&bad, d_flag, sizeof(bad), hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    (void)hipFree(d_flag);
+    if (e != hipSuccess) return hip_fail(e, "sparse index validation");
+    if (bad)
+      return fail(OPRAG_E_INVALID, "sparse index fails %u structural checks (indptr/chunk order/range/tf/doc_len)",
+                  bad);
+  }
+  // Head terms: document frequency at least n_docs / 8 (and 64), the most frequent first, as
+  // many as fit kMaxHead rows and kHeadBytes of dense weight rows.
+  std::vector<long long> indptr((size_t)vocab + 1);
+  e = hipMemcpy(indptr.data(), term_indptr_dev, indptr.size() * sizeof(long long), hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return hip_fail(e, "term offsets to host");
+  const long long head_ld = (n_docs + 3) & ~3ll;
+  std::vector<int> head;
+  for (int t = 0; t < vocab; ++t) {
+    const long long df = indptr[t + 1] - indptr[t];
+    if (df >= 64 && 8 * df >= n_docs) head.push_back(t);
+  }
+  std::stable_sort(head.begin(), head.end(),
+                   [&](int a, int b2) { return indptr[a + 1] - indptr[a] > indptr[b2 + 1] - indptr[b2]; });
+  const long long head_cap = std::min<long long>(oprag::kMaxHead, oprag::kHeadBytes / (head_ld * 4));
+  if ((long long)head.size() > head_cap) head.resize((size_t)std::max(0ll, head_cap));
+  std::vector<int> hidx((size_t)vocab, -1);
+  for (size_t h = 0; h < head.size(); ++h) hidx[(size_t)head[h]] = (int)h;
+  const int n_head = (int)head.size();
+  // Library-owned arrays: [sum u64 | idfk f32 x vocab | posting weights f32 x nnz |
+  // chunk-major copy: list offsets i64 x (n_docs + 1), terms i32 x nnz, weights f32 x nnz |
+  // head rows of term t i32 x vocab | head terms i32 x n_head | head rows f32 x n_head x head_ld].
+  const size_t off_sum = 0, off_idf = 256;
   const size_t off_wpost = off_idf + align_up((size_t)vocab * 4);
   const size_t off_fptr = off_wpost + align_up((size_t)nnz * 4);
   const size_t off_fterm = off_fptr + align_up((size_t)(n_docs + 1) * 8);
   const size_t off_fw = off_fterm + align_up((size_t)nnz * 4);
-  const size_t bytes = off_fw + align_up((size_t)nnz * 4);
+  const size_t off_hidx = off_fw + align_up((size_t)nnz * 4);
+  const size_t off_hterm = off_hidx + align_up((size_t)vocab * 4);
+  const size_t off_whead = off_hterm + align_up((size_t)std::max(1, n_head) * 4);
+  const size_t bytes = off_whead + align_up((size_t)n_head * (size_t)head_ld * 4);
   void* mem = nullptr;
-  hipError_t e = hipMalloc(&mem, bytes);
+  e = hipMalloc(&mem, bytes);
   if (e != hipSuccess) return hip_fail(e, "sparse arrays allocation");
   unsigned char* base = static_cast<unsigned char*>(mem);
-  unsigned int* d_flag = reinterpret_cast<unsigned int*>(base);
-  e = oprag::sparse_validate(vocab, n_docs, nnz, reinterpret_cast<const long long*>(term_indptr_dev), post_chunk_dev,
-                             post_tf_dev, doc_len_dev, d_flag, s);
-  unsigned int bad = 0;
-  if (e == hipSuccess) e = hipMemcpyAsync(&bad, d_flag, sizeof(bad), hipMemcpyDeviceToHost, s);
-  if (e == hipSuccess) e = hipStreamSynchronize(s);
-  if (e != hipSuccess) {
-    (void)hipFree(mem);
-    return hip_fail(e, "sparse index validation");
-  }
-  if (bad) {
-    (void)hipFree(mem);
-    return fail(OPRAG_E_INVALID, "sparse index fails %u structural checks (indptr/chunk order/range/tf/doc_len)", bad);
-  }
   oprag::SparseIndex sp;
   sp.vocab = vocab;
   sp.n_docs = n_docs;
@@ -381,9 +407,18 @@ oprag_status oprag_sparse_attach(oprag_index* idx, int32_t vocab, int64_t n_docs
   sp.fwd_ptr = reinterpret_cast<long long*>(base + off_fptr);
   sp.fwd_term = reinterpret_cast<int*>(base + off_fterm);
   sp.fwd_w = reinterpret_cast<float*>(base + off_fw);
+  sp.n_head = n_head;
+  sp.head_ld = head_ld;
+  sp.hidx = reinterpret_cast<int*>(base + off_hidx);
+  sp.whead = reinterpret_cast<float*>(base + off_whead);
   sp.k1 = k1;
   sp.b = b;
-  e = oprag::sparse_prepare(sp, doc_len_dev, reinterpret_cast<unsigned long long*>(base + off_sum), s);
+  e = hipMemcpy(sp.hidx, hidx.data(), (size_t)vocab * 4, hipMemcpyHostToDevice);
+  if (e == hipSuccess && n_head > 0)
+    e = hipMemcpy(base + off_hterm, head.data(), (size_t)n_head * 4, hipMemcpyHostToDevice);
+  if (e == hipSuccess)
+    e = oprag::sparse_prepare(sp, doc_len_dev, reinterpret_cast<unsigned long long*>(base + off_sum), s);
+  if (e == hipSuccess && n_head > 0) e = oprag::sparse_head_rows(sp, reinterpret_cast<const int*>(base + off_hterm), s);
   if (e == hipSuccess) {  // the chunk-major copy, with per-chunk counters as scratch
     int* cnt = nullptr;
     e = hipMalloc(&cnt, (size_t)n_docs * sizeof(int));

@@ -9,13 +9,19 @@
 // avgdl)) are computed once in fp64 at attach time and stored as fp32, so a posting's
 // contribution is one product; scores accumulate in fp32.
 //
-// One workgroup scores one query over a range of up to 8,192 chunks held as an fp32
-// accumulator in LDS (32 KiB); a term's postings in the range are found by a 32-ary search.  Terms are applied one after another with a barrier in
-// between, and a term's postings name distinct chunks, so every chunk's score is summed
-// in query-term order with no atomics: the result is deterministic.  The range's top-k then
-// comes from a threshold (the k-th largest of the 256 thread maxima) and exact ranks of the
-// few scores above it; many equal scores at the threshold fall back to a 4 x 8-bit radix
-// select and a wave-wide bitonic sort (score desc, chunk asc).
+// One workgroup scores one query over a range of up to 32,768 chunks.  A query's distinct terms
+// each contribute once, with m times their factor for m occurrences, in a fixed order: first
+// the head terms (the most frequent ones, df >= N / 8, whose weights the attach keeps as dense
+// per-chunk rows), then the others, each group in the query's first-occurrence order.  The
+// head terms are summed from their rows in registers, each thread over its own chunks (about
+// nine in ten postings a batch touches belong to them, and walking them made every query read
+// the same long lists again).  The remaining terms add their postings in the range, found by a
+// 32-ary search, to an fp32 accumulator in LDS (128 KiB), one term after another with a barrier
+// in between; a term's postings name distinct chunks, so there are no atomics and the result
+// is deterministic.  The range's top-k then comes from a threshold (the k-th largest of the
+// 256 thread maxima) and exact ranks of the few scores above it; many equal scores at the
+// threshold fall back to a 4 x 8-bit radix select and a wave-wide bitonic sort (score desc,
+// chunk asc).
 #include <algorithm>
 
 #include "oprag_internal.h"
@@ -25,6 +31,8 @@ namespace oprag {
 namespace {
 
 using namespace dev;
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kNT = 256;         // threads per scoring workgroup (one per radix bin)
 constexpr int kTermBatch = kNT / 32;  // query terms whose posting bounds are found together
@@ -86,16 +94,6 @@ __global__ void prepare_kernel(int vocab, long long n_docs, long long nnz, const
   }
 }
 
-// First position p in [lo, hi) with chunk[p] >= key (chunks ascending within a term).
-__device__ __forceinline__ long long lower_bound(const int* chunk, long long lo, long long hi, long long key) {
-  while (lo < hi) {
-    const long long mid = (lo + hi) >> 1;
-    if (chunk[mid] < key) lo = mid + 1;
-    else hi = mid;
-  }
-  return lo;
-}
-
 // Block-wide exclusive prefix sum of one int per thread (kNT threads).
 __device__ __forceinline__ int block_excl_scan(int v, int* wave_tot) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -120,6 +118,9 @@ struct SparseArgs {
   const int* chunk;
   const float* idfk;
   const float* wpost;
+  const int* hidx;               // head row of each term, -1 for the others
+  const float* whead;            // dense head rows [n_head x head_ld]
+  long long head_ld;
   const int* qterm_indptr;
   const int* qterms;
   int nq;
@@ -171,9 +172,9 @@ __device__ __forceinline__ void range_bounds32(const int* chunk, long long lo, l
   *out_hi = b0;
 }
 
-// Candidates the threshold selection ranks directly.  With the 32 KiB accumulator and the
-// kernel's other shared arrays (about 200 bytes) a workgroup stays within 40 KiB of LDS, so
-// four fit on a CU; a few bytes more drop that to three and cost a third of the speed.
+// Candidates the threshold selection ranks directly (their area also holds a query's head-term
+// list while the scores are summed).  With the 128 KiB accumulator one workgroup fits a CU:
+// a query of the 32K-chunk corpus takes one workgroup, one selection and no list merge.
 constexpr int kCandCap = 992;
 
 __global__ __launch_bounds__(kNT) void bm25_kernel(SparseArgs a) {
@@ -197,9 +198,99 @@ __global__ __launch_bounds__(kNT) void bm25_kernel(SparseArgs a) {
   const long long d0 = (long long)range * kSparseRange;
   const int len = (int)std::min<long long>(kSparseRange, a.n_docs - d0);
 
-  for (int i = tid; i < kSparseRange; i += kNT) acc[i] = 0.f;
-
   const int tb = a.qterm_indptr[q], te = a.qterm_indptr[q + 1];
+  // 1. head terms, from their dense rows.  The query's distinct head terms are listed in
+  // first-occurrence order (in the candidate area, unused until the selection), each with
+  // factor m * idf(t) (k1 + 1) for its m occurrences; then every thread sums, term after term,
+  // the rows over its own chunks (16 bytes = 4 consecutive chunks from each of 8 column groups)
+  // in registers.  A row holds 0 where the term is absent and fma(f, 0, s) = s, so these are
+  // exactly the fp32 operations of walking the terms' postings, without searches, scattered
+  // LDS updates or barriers.
+  {
+    int* hl_row = reinterpret_cast<int*>(cand);               // [kMaxHead]
+    float* hl_wt = reinterpret_cast<float*>(cand) + kMaxHead;  // [kMaxHead]
+    static_assert(2 * kMaxHead * 4 <= kCandCap * 8, "the head list fits the candidate area");
+    int nh = 0;
+    for (int j0 = tb; j0 < te; j0 += kNT) {
+      const int j = j0 + tid;
+      int row = -1;
+      float wt = 0.f;
+      if (j < te) {
+        const int t = a.qterms[j];
+        if (t >= 0 && t < a.vocab && a.hidx[t] >= 0) {
+          bool earlier = false;
+          int mult = 0;
+          for (int jj = tb; jj < te; ++jj)
+            if (a.qterms[jj] == t) {
+              if (jj < j) earlier = true;
+              else ++mult;
+            }
+          if (!earlier) {
+            row = a.hidx[t];
+            wt = a.idfk[t] * (float)mult;
+          }
+        }
+      }
+      const int f = row >= 0 ? 1 : 0;
+      const int pos = nh + block_excl_scan(f, wave_tot);
+      if (f) {  // distinct head terms <= kMaxHead
+        hl_row[pos] = row;
+        hl_wt[pos] = wt;
+      }
+      if (tid == kNT - 1) s_nc = pos + f;  // the count so far, shared
+      __syncthreads();
+      nh = s_nc;
+      __syncthreads();
+    }
+    // Thread tid owns chunks 4 tid + 1024 g + (0 .. 3) of each sub-range of kSub chunks; the
+    // rows of two terms over the whole range (up to 4 sub-ranges) are in flight at once.
+    constexpr int kSub = 8 * 4 * kNT;
+    constexpr int kNS = kSparseRange / kSub;
+    static_assert(kSparseRange % kSub == 0, "whole sub-ranges");
+    f32x4 hs[kNS][8];
+#pragma unroll
+    for (int r = 0; r < kNS; ++r)
+#pragma unroll
+      for (int g = 0; g < 8; ++g) hs[r][g] = f32x4{0.f, 0.f, 0.f, 0.f};
+    auto load_row = [&](int i, f32x4 (&v)[kNS][8]) __attribute__((always_inline)) {
+      const float* row = a.whead + (long long)hl_row[i] * a.head_ld + d0;
+#pragma unroll
+      for (int r = 0; r < kNS; ++r)
+#pragma unroll
+        for (int g = 0; g < 8; ++g) {
+          const int c = r * kSub + 4 * tid + 1024 * g;  // d0 + c < n_docs: c .. c + 3 lie inside the padded row
+          v[r][g] = c < len ? *reinterpret_cast<const f32x4*>(row + c) : f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+    };
+    auto add_row = [&](float wt, const f32x4 (&v)[kNS][8]) __attribute__((always_inline)) {
+#pragma unroll
+      for (int r = 0; r < kNS; ++r)
+#pragma unroll
+        for (int g = 0; g < 8; ++g)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) hs[r][g][e] = __builtin_fmaf(wt, v[r][g][e], hs[r][g][e]);
+    };
+    int i = 0;
+    for (; i + 1 < nh; i += 2) {
+      f32x4 v0[kNS][8], v1[kNS][8];
+      load_row(i, v0);
+      load_row(i + 1, v1);
+      add_row(hl_wt[i], v0);
+      add_row(hl_wt[i + 1], v1);
+    }
+    if (i < nh) {
+      f32x4 v0[kNS][8];
+      load_row(i, v0);
+      add_row(hl_wt[i], v0);
+    }
+#pragma unroll
+    for (int r = 0; r < kNS; ++r)
+#pragma unroll
+      for (int g = 0; g < 8; ++g) *reinterpret_cast<f32x4*>(acc + r * kSub + 4 * tid + 1024 * g) = hs[r][g];
+    __syncthreads();  // the accumulator is complete; the head list area is free again
+  }
+
+  // 2. the other (tail) terms, from their postings
   for (int j0 = tb; j0 < te; j0 += kTermBatch) {
     // 1. posting bounds of up to kTermBatch terms at once, 32 threads per term.  A term that
     // occurs m times in the query is walked once, at its first occurrence, with weight
@@ -224,7 +315,7 @@ __global__ __launch_bounds__(kNT) void bm25_kernel(SparseArgs a) {
               earlier |= __shfl_xor(earlier, o, 32);
               mult += __shfl_xor(mult, o, 32);
             }
-            if (!earlier) {
+            if (!earlier && a.hidx[t] < 0) {  // head terms were summed from their rows
               lo = a.indptr[t];
               hi = a.indptr[t + 1];
               wt = a.idfk[t] * (float)mult;
@@ -240,10 +331,10 @@ __global__ __launch_bounds__(kNT) void bm25_kernel(SparseArgs a) {
       }
     }
     __syncthreads();
-    // 2. one term after another (a term's postings name distinct chunks: no atomics)
+    // one term after another (a term's postings name distinct chunks: no atomics)
     for (int g = 0; g < kTermBatch && j0 + g < te; ++g) {
       const long long lo = s_lo[g], hi = s_hi[g];
-      if (lo < hi) {
+      if (lo < hi) {  // workgroup-uniform
         const float wt = s_wt[g];
         // eight postings per thread per step, all loads issued before the first use
         long long p = lo + tid;
@@ -259,8 +350,8 @@ __global__ __launch_bounds__(kNT) void bm25_kernel(SparseArgs a) {
           for (int u = 0; u < 8; ++u) acc[c[u] - d0] = __builtin_fmaf(wt, wp[u], acc[c[u] - d0]);
         }
         for (; p < hi; p += kNT) acc[a.chunk[p] - d0] = __builtin_fmaf(wt, a.wpost[p], acc[a.chunk[p] - d0]);
+        __syncthreads();
       }
-      __syncthreads();
     }
   }
   __syncthreads();
@@ -306,9 +397,20 @@ __global__ __launch_bounds__(kNT) void bm25_kernel(SparseArgs a) {
   // is at most the k-th largest score, so only scores >= tau are candidates; when they fit
   // in kCandCap, each one's rank is the number of larger composites (score, ~chunk), which
   // are unique.  Otherwise (or with fewer than k positive maxima) the radix path below runs.
+  // The passes over the keys read 8 of a thread's slice per step, all before the first use, so
+  // a step waits for one LDS round trip instead of eight.
+  auto slice8 = [&](int i0, uint32_t (&v)[8]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = i0 + u * kNT < len ? keys[i0 + u * kNT] : 0u;
+  };
   {
     uint32_t m = 0u;
-    for (int i = tid; i < len; i += kNT) m = max(m, keys[i]);
+    for (int i0 = tid; i0 < len; i0 += 8 * kNT) {
+      uint32_t v[8];
+      slice8(i0, v);
+#pragma unroll
+      for (int u = 0; u < 8; ++u) m = max(m, v[u]);
+    }
     tmax[tid] = m;
     if (tid == 0) {
       s_tau = 0u;
@@ -326,20 +428,50 @@ __global__ __launch_bounds__(kNT) void bm25_kernel(SparseArgs a) {
     __syncthreads();
   }
   const uint32_t tau = s_tau;  // 0: fewer than k positive maxima
+  // At least k scores reach tau (the k largest maxima), so the top k are the G scores above tau
+  // (ranked exactly, as unique composites) and, when G < k, the k - G chunks of smallest id
+  // among the E scores equal to tau (equal scores order by id).  Many chunks can share tau
+  // exactly (equal term frequencies and lengths), which is why the two are taken apart.
+  auto emit = [&](int r, u64 key) __attribute__((always_inline)) {
+    if (a.n_ranges == 1) {
+      a.out_ids[(long long)q * a.k + r] = (long long)comp_row(key);
+      a.out_scores[(long long)q * a.k + r] = __uint_as_float((uint32_t)(key >> 32));
+    } else {
+      a.partial[((long long)q * a.n_ranges + range) * a.k + r] = key;
+    }
+  };
   if (tau != 0u) {
+    // a thread's keys above tau: a mask bit per slice position (at most 128 per thread)
+    static_assert(kSparseRange <= 128 * kNT, "a slice fits the mask");
+    uint32_t mk[4] = {0u, 0u, 0u, 0u};
     int c = 0;
-    for (int i = tid; i < len; i += kNT) c += keys[i] >= tau ? 1 : 0;
+    for (int i0 = tid, j0 = 0; i0 < len; i0 += 8 * kNT, j0 += 8) {
+      uint32_t v[8];
+      slice8(i0, v);
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (v[u] > tau) {
+          ++c;
+          const int j = j0 + u;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) mk[e] |= (j >> 5) == e ? 1u << (j & 31) : 0u;
+        }
+    }
     const int before = block_excl_scan(c, wave_tot);
     if (tid == kNT - 1) s_nc = before + c;
     int pos = before;
-    if (before + c <= kCandCap)
-      for (int i = tid; i < len; i += kNT)
-        if (keys[i] >= tau) cand[pos++] = ((u64)keys[i] << 32) | (uint32_t)(~(uint32_t)(d0 + i));
+    if (before + c <= kCandCap) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        for (uint32_t m = mk[e]; m != 0u; m &= m - 1u) {
+          const int i = tid + (32 * e + __builtin_ctz(m)) * kNT;
+          cand[pos++] = ((u64)keys[i] << 32) | (uint32_t)(~(uint32_t)(d0 + i));
+        }
+    }
     __syncthreads();
   }
-  const int nc = s_nc;
-  if (tau != 0u && nc <= kCandCap) {
-    // nc >= k (the k largest maxima are k distinct scores >= tau): ranks 0 .. k-1 all occur
+  const int nc = s_nc;  // G
+  if (tau != 0u && nc <= kCandCap) {  // workgroup-uniform
     for (int j = tid; j < nc; j += kNT) {
       const u64 me = cand[j];
       int r = 0;
@@ -350,16 +482,34 @@ __global__ __launch_bounds__(kNT) void bm25_kernel(SparseArgs a) {
 #pragma unroll
         for (int u = 0; u < 8; ++u) r += (o + u < nc && v[u] > me) ? 1 : 0;
       }
-      if (r < a.k) {
-        if (a.n_ranges == 1) {
-          a.out_ids[(long long)q * a.k + r] = (long long)comp_row(me);
-          a.out_scores[(long long)q * a.k + r] = __uint_as_float((uint32_t)(me >> 32));
-        } else {
-          a.partial[((long long)q * a.n_ranges + range) * a.k + r] = me;
+      if (r < a.k) emit(r, me);
+    }
+    if (nc < a.k) {
+      // ranks nc .. k - 1: the scores equal to tau in chunk order.  Each thread owns a
+      // contiguous block of at most 128 chunks; it reads the block starting at a rotated offset
+      // (lanes then hit different LDS banks instead of one) and marks the equal scores in a
+      // 128-bit mask, whose set bits it then emits in order after a scan of the counts.
+      static_assert(kSparseRange <= 128 * kNT, "a block fits the mask");
+      const int per = (len + kNT - 1) / kNT;
+      const int b0 = min(len, tid * per), nb = min(len, b0 + per) - b0;
+      uint32_t mk[4] = {0u, 0u, 0u, 0u};
+      int ce = 0;
+      for (int i = 0; i < nb; ++i) {
+        int o = i + tid;
+        o = o >= nb ? o % nb : o;
+        if (keys[b0 + o] == tau) {
+          ++ce;
+#pragma unroll
+          for (int u = 0; u < 4; ++u) mk[u] |= (o >> 5) == u ? 1u << (o & 31) : 0u;
         }
       }
+      int r = nc + block_excl_scan(ce, wave_tot);
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        for (uint32_t m = mk[u]; m != 0u && r < a.k; m &= m - 1u)
+          emit(r++, ((u64)tau << 32) | (uint32_t)(~(uint32_t)(d0 + b0 + 32 * u + __builtin_ctz(m))));
     }
-    return;  // workgroup-uniform
+    return;
   }
 
   // ---- radix select of the k-th largest positive score
@@ -597,6 +747,16 @@ __global__ void fwd_fill_kernel(int vocab, const long long* __restrict__ indptr,
   }
 }
 
+// Dense head rows: row h holds the posting weight of term head_terms[h] for every chunk (the
+// rows are zeroed first, so a chunk without the term reads 0).  One workgroup per head term.
+__global__ void head_rows_kernel(const long long* indptr, const int* chunk, const float* wpost, const int* head_terms,
+                                 long long ld, float* whead) {
+  const int h = blockIdx.x;
+  const int t = head_terms[h];
+  float* row = whead + (long long)h * ld;
+  for (long long p = indptr[t] + threadIdx.x; p < indptr[t + 1]; p += blockDim.x) row[chunk[p]] = wpost[p];
+}
+
 // ------------------------------------------------------------------------------------
 // Dense-first hybrid (the serving schedule of Section 4.1, "Retrieval", measured in Section
 // 5.5: lexical reranking of the dense top-n candidates only).  One workgroup of 1,024 threads
@@ -605,9 +765,9 @@ __global__ void fwd_fill_kernel(int vocab, const long long* __restrict__ indptr,
 // entry with up to 32 query terms at a time held in LDS; a match stores the weight in the
 // candidate's slot for that term.  Like bm25_kernel, a term that occurs m times in the query
 // takes part once, at its first occurrence, with factor m * idf(t) (k1 + 1), and the
-// candidate's score is fma(factor, weight, score) over the distinct terms in first-occurrence
-// order: the same fp32 operations in the same order, so a candidate scores exactly what the
-// full BM25 search gives its chunk.  Candidates at or past the sparse corpus's n_docs chunks
+// candidate's score is fma(factor, weight, score) over the distinct terms, the head terms
+// first and then the others, each in first-occurrence order: the same fp32 operations in the
+// same order, so a candidate scores exactly what the full BM25 search gives its chunk.  Candidates at or past the sparse corpus's n_docs chunks
 // hold no postings and score 0.  The candidates with a positive score are ranked by (score
 // desc, id asc); reciprocal rank fusion of that order with the dense order, compared exactly
 // as fractions (as rrf_kernel does), gives the top k.
@@ -617,6 +777,7 @@ constexpr int kRrfExactMax = 100000;  // below this rrf_k the fused quotients or
 constexpr int kDfCand = 128;
 constexpr int kDfLanes = kDfThreads / kDfCand;
 __global__ __launch_bounds__(kDfThreads) void dense_first_kernel(int vocab, long long n_docs,
+                                                                 const int* __restrict__ hidx,
                                                                  const long long* __restrict__ fwd_ptr,
                                                                  const int* __restrict__ fwd_term,
                                                                  const float* __restrict__ idfk,
@@ -628,6 +789,7 @@ __global__ __launch_bounds__(kDfThreads) void dense_first_kernel(int vocab, long
   static_assert(kTerms * 32 == kDfThreads, "32 threads find the multiplicity of each occurrence");
   __shared__ int qt_s[kTerms];    // the pass's distinct-term occurrences (-1: repeat or unknown)
   __shared__ float fw_s[kTerms];  // their factors m * idf(t) (k1 + 1)
+  __shared__ int hd_s[kTerms];    // 1 for a head term
   __shared__ float wq[kDfCand][kTerms + 1];
   __shared__ float lex[kDfCand];
   __shared__ long long cid[kDfCand];
@@ -642,6 +804,11 @@ __global__ __launch_bounds__(kDfThreads) void dense_first_kernel(int vocab, long
   const long long f0 = has_terms ? fwd_ptr[id] : 0, f1 = has_terms ? fwd_ptr[id + 1] : 0;
   float sc = 0.f;  // thread j == 0 of a candidate: its score
   const int tb = qterm_indptr[q], e_end = qterm_indptr[q + 1];
+  // The head terms are summed first, then the others (the order of the full BM25 search).  A
+  // query of at most kTerms occurrences walks the lists once and sums the two kinds from the
+  // stored matches; a longer one walks them once per kind.
+  const bool single = e_end - tb <= kTerms;
+  for (int pass = 0; pass < (single ? 1 : 2); ++pass)
   for (int e0 = tb; e0 < e_end; e0 += kTerms) {
     const int ne = min(kTerms, e_end - e0);
     {
@@ -663,8 +830,12 @@ __global__ __launch_bounds__(kDfThreads) void dense_first_kernel(int vocab, long
         mult += __shfl_xor(mult, o, 32);
       }
       if (sub == 0) {
-        const bool use = u < ne && !earlier && term >= 0 && term < vocab;  // unknown terms match nothing
+        // unknown terms match nothing; a term takes part in the pass of its kind
+        const bool known = u < ne && !earlier && term >= 0 && term < vocab;
+        const bool head = known && hidx[term] >= 0;
+        const bool use = known && (single || head == (pass == 0));
         qt_s[u] = use ? term : -1;
+        hd_s[u] = head ? 1 : 0;
         fw_s[u] = use ? idfk[term] * (float)mult : 0.f;
       }
     }
@@ -693,9 +864,15 @@ __global__ __launch_bounds__(kDfThreads) void dense_first_kernel(int vocab, long
       }
     }
     __syncthreads();
-    if (j == 0 && has_terms) {
-      for (int u = 0; u < ne; ++u)
-        if (qt_s[u] >= 0) sc = __builtin_fmaf(fw_s[u], wq[c][u], sc);  // an unmatched term adds 0 exactly
+    if (j == 0 && has_terms) {  // an unmatched term adds 0 exactly
+      if (single) {
+        for (int kind = 1; kind >= 0; --kind)  // head terms (kind 1) first
+          for (int u = 0; u < ne; ++u)
+            if (qt_s[u] >= 0 && hd_s[u] == kind) sc = __builtin_fmaf(fw_s[u], wq[c][u], sc);
+      } else {  // this pass holds one kind only
+        for (int u = 0; u < ne; ++u)
+          if (qt_s[u] >= 0) sc = __builtin_fmaf(fw_s[u], wq[c][u], sc);
+      }
     }
     __syncthreads();  // qt_s, fw_s and wq are rewritten by the next pass
   }
@@ -826,6 +1003,14 @@ hipError_t sparse_forward(const SparseIndex& sp, int* cnt, hipStream_t s) {
   return hipGetLastError();
 }
 
+hipError_t sparse_head_rows(const SparseIndex& sp, const int* head_terms, hipStream_t s) {
+  hipError_t e = hipMemsetAsync(sp.whead, 0, (size_t)sp.n_head * (size_t)sp.head_ld * sizeof(float), s);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(head_rows_kernel, dim3((unsigned)sp.n_head), dim3(256), 0, s, sp.term_indptr, sp.post_chunk,
+                     sp.wpost, head_terms, sp.head_ld, sp.whead);
+  return hipGetLastError();
+}
+
 hipError_t launch_sparse_dump(const SparseIndex& sp, const int* qterm_indptr, const int* qterms, int nq, float* dump,
                               long long ld, float* dump_mm, long long mm_rows, hipStream_t s) {
   SparseArgs a;
@@ -835,6 +1020,9 @@ hipError_t launch_sparse_dump(const SparseIndex& sp, const int* qterm_indptr, co
   a.chunk = sp.post_chunk;
   a.idfk = sp.idfk;
   a.wpost = sp.wpost;
+  a.hidx = sp.hidx;
+  a.whead = sp.whead;
+  a.head_ld = sp.head_ld;
   a.qterm_indptr = qterm_indptr;
   a.qterms = qterms;
   a.nq = nq;
@@ -866,6 +1054,9 @@ hipError_t launch_sparse(const SparseIndex& sp, const int* qterm_indptr, const i
   a.chunk = sp.post_chunk;
   a.idfk = sp.idfk;
   a.wpost = sp.wpost;
+  a.hidx = sp.hidx;
+  a.whead = sp.whead;
+  a.head_ld = sp.head_ld;
   a.qterm_indptr = qterm_indptr;
   a.qterms = qterms;
   a.nq = nq;
@@ -890,9 +1081,9 @@ hipError_t launch_dense_first(const SparseIndex& sp, const int* qterm_indptr, co
                               const long long* cand, int n_cand, long long nq, int rrf_k, int k, float* out_fused,
                               long long* out_ids, hipStream_t s) {
   if (n_cand < 1 || n_cand > kDfCand) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(dense_first_kernel, dim3((unsigned)nq), dim3(kDfThreads), 0, s, sp.vocab, sp.n_docs, sp.fwd_ptr,
-                     sp.fwd_term, sp.idfk, sp.fwd_w, qterm_indptr, qterms, cand, n_cand, rrf_k, k, out_fused,
-                     out_ids);
+  hipLaunchKernelGGL(dense_first_kernel, dim3((unsigned)nq), dim3(kDfThreads), 0, s, sp.vocab, sp.n_docs, sp.hidx,
+                     sp.fwd_ptr, sp.fwd_term, sp.idfk, sp.fwd_w, qterm_indptr, qterms, cand, n_cand, rrf_k, k,
+                     out_fused, out_ids);
   return hipGetLastError();
 }
 

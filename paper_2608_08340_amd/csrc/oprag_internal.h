@@ -105,11 +105,19 @@ struct SparseIndex {
   long long* fwd_ptr = nullptr;             // [n_docs + 1]
   int* fwd_term = nullptr;                  // [nnz]
   float* fwd_w = nullptr;                   // [nnz]
+  // library-owned dense rows of the head terms (the most frequent ones): row hidx[t] of whead
+  // holds term t's posting weight for every chunk, 0 where t is absent
+  int n_head = 0;
+  long long head_ld = 0;                    // row stride: n_docs rounded up to 4
+  int* hidx = nullptr;                      // [vocab]: row of term t, -1 for the other terms
+  float* whead = nullptr;                   // [n_head x head_ld]
   double avgdl = 0.0;
   float k1 = 0.f, b = 0.f;
 };
 
-constexpr int kSparseRange = 8192;         // chunks scored per workgroup (LDS accumulator)
+constexpr int kSparseRange = 32768;        // chunks scored per workgroup (LDS accumulator, 128 KiB)
+constexpr int kMaxHead = 992;              // head terms at most (the kernel lists a query's in LDS)
+constexpr long long kHeadBytes = 64ll << 20;  // dense head rows at most
 
 // Validates the CSR on the device; returns the number of violations found (synchronous).
 hipError_t sparse_validate(int vocab, long long n_docs, long long nnz, const long long* indptr,
@@ -119,6 +127,9 @@ hipError_t sparse_prepare(SparseIndex& sp, const int* doc_len, unsigned long lon
 // Builds the chunk-major copy (fwd_ptr / fwd_term / fwd_w) from the postings and their
 // weights; cnt is scratch of n_docs ints.
 hipError_t sparse_forward(const SparseIndex& sp, int* cnt, hipStream_t s);
+// Fills the dense head rows (whead, zeroed here) from the postings of the head terms
+// head_terms[0 .. n_head) (device array, row h = term head_terms[h]).
+hipError_t sparse_head_rows(const SparseIndex& sp, const int* head_terms, hipStream_t s);
 size_t sparse_workspace_bytes(long long n_docs, int nq, int k);
 hipError_t launch_sparse(const SparseIndex& sp, const int* qterm_indptr, const int* qterms, int nq, int k,
                          float* out_scores, long long* out_ids, void* ws, hipStream_t s);

@@ -73,10 +73,10 @@ def test_bm25_parameters(k1, b):
     _check_sparse(B, ids, sc, 50, f"k1={k1} b={b}")
 
 
-@pytest.mark.parametrize("n_docs,k", [(70_001, 64), (140_001, 100)])
+@pytest.mark.parametrize("n_docs,k", [(70_001, 64), (360_001, 100)])
 def test_bm25_several_chunk_ranges(n_docs, k):
-    """More chunks than one workgroup's LDS accumulator: per-range lists are merged (9 x 64
-    composites per query fit the LDS ranking merge; 18 x 100 take the queue merge)."""
+    """More chunks than one workgroup's LDS accumulator (32,768): per-range lists are merged
+    (3 x 64 composites per query fit the LDS ranking merge; 11 x 100 take the queue merge)."""
     dev = device()
     ind, toks, csr, qi, qt = _small_corpus(700, n_docs, 2000, 20.0, 30)
     idx = make_index(torch.zeros((n_docs, 128), dtype=torch.bfloat16), "bf16")
@@ -86,6 +86,48 @@ def test_bm25_several_chunk_ranges(n_docs, k):
     qt_oracle = np.where((qt >= 0) & (qt < 2000), qt, 10 ** 6).astype(np.int64)
     B = bm25.scores_batch(ind, toks, qi, qt_oracle, 1.2, 0.75)
     _check_sparse(B, ids, sc, k, f"multi-range n_docs={n_docs}")
+
+
+@pytest.mark.parametrize("kind", ["no_head", "one_head", "all_head"])
+def test_bm25_head_rows_and_postings_mix(kind):
+    """The most frequent terms (df >= N / 8) are scored from dense rows, the rest from their
+    postings.  A flat corpus (uniform tokens, no term that frequent) takes only postings; one
+    term in every chunk gives a single head row next to ordinary terms; a 12-term vocabulary
+    makes every term a head term.  Queries mix kinds, repeat terms and include unknown ones;
+    scores within rtol 1e-5 of the token-scan oracle, and dense-first (same summation order)
+    scores its candidates identically to the full search (one query is longer than the
+    32 occurrences dense-first holds at once)."""
+    dev = device()
+    g = np.random.default_rng({"no_head": 61, "one_head": 62, "all_head": 63}[kind])
+    n, vocab = 3000, 2000 if kind != "all_head" else 12
+    lens = g.integers(5, 40, size=n)
+    docs = [list(g.integers(1 if kind == "one_head" else 0, vocab, size=m)) for m in lens]
+    if kind == "one_head":
+        docs = [d + [0] * int(g.integers(1, 4)) for d in docs]  # term 0 in every chunk
+    ind = np.zeros(n + 1, dtype=np.int64)
+    ind[1:] = np.cumsum([len(d) for d in docs])
+    toks = np.array([t for d in docs for t in d], dtype=np.int32)
+    csr = synth.csr_from_tokens(ind, toks, vocab)
+    nq = 48
+    qs = [list(g.integers(0, vocab, size=g.integers(1, 9))) for _ in range(nq)]
+    qs[0] = [0, 0, 5, -1]
+    qs[1] = [3, 0, 3]
+    qs[2] = list(g.integers(0, vocab, size=45)) + [0, 1, 0]  # longer than one 32-term batch
+    qi = np.zeros(nq + 1, dtype=np.int32)
+    qi[1:] = np.cumsum([len(q) for q in qs])
+    qt = np.array([t for q in qs for t in q], dtype=np.int32)
+    w = synth.mixture_dense(6400 + len(kind), n, 128, 16, nq, 64, "bf16")
+    idx = make_index(w.rows, "bf16")
+    _attach(idx, csr, dev)
+    log("bm25 head rows", kind)
+    sc, ids = idx.search_sparse(_t(qi, dev), _t(qt, dev), 64)
+    fused, fids = idx.search_hybrid_dense_first(w.queries.to(dev), _t(qi, dev), _t(qt, dev), 64, 60, 64)
+    dsc, dids = idx.search_dense(w.queries.to(dev), 64)
+    torch.cuda.synchronize()
+    qt_oracle = np.where((qt >= 0) & (qt < vocab), qt, 10 ** 6).astype(np.int64)
+    B = bm25.scores_batch(ind, toks, qi, qt_oracle, 1.2, 0.75)
+    _check_sparse(B, ids, sc, 64, kind)
+    _check_dense_first(fused, fids, dids, B, qi, qt_oracle, ind, toks, 60, 64, f"dense-first {kind}")
 
 
 def test_attach_rejects_malformed_csr():
