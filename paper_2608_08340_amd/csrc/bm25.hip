@@ -34,8 +34,9 @@ using namespace dev;
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kNT = 256;         // threads per scoring workgroup (one per radix bin)
-constexpr int kTermBatch = kNT / 32;  // query terms whose posting bounds are found together
+constexpr int kBT = 1024;        // threads per scoring workgroup (sixteen waves on one CU)
+constexpr int kNT = 256;         // threads per list-merge workgroup
+constexpr int kTermBatch = kBT / 32;  // query terms whose posting bounds are found together
 
 // Structural checks of the CSR, one thread per term, then one thread per posting (a posting
 // finds its term by binary search over the offsets, so long lists are checked in parallel).
@@ -177,17 +178,16 @@ __device__ __forceinline__ void range_bounds32(const int* chunk, long long lo, l
 // a query of the 32K-chunk corpus takes one workgroup, one selection and no list merge.
 constexpr int kCandCap = 992;
 
-__global__ __launch_bounds__(kNT) void bm25_kernel(SparseArgs a) {
+__global__ __launch_bounds__(kBT) void bm25_kernel(SparseArgs a) {
   __shared__ __attribute__((aligned(16))) float acc[kSparseRange];
-  // One area, used in turn: the thread maxima (threshold step), the candidates (ranking),
-  // or the radix histogram and the winners (fallback path).
-  __shared__ u64 cand[kCandCap];
-  uint32_t* tmax = reinterpret_cast<uint32_t*>(cand);         // [kNT]
+  // One area, used in turn: the head-term list, the group maxima (threshold step), the
+  // candidates (ranking), or the radix histogram and the winners (fallback path).
+  __shared__ __attribute__((aligned(16))) u64 cand[kCandCap];
   unsigned int* hist = reinterpret_cast<unsigned int*>(cand);  // [256]
   u64* selbuf = cand + 128;                                    // [kMaxK]
   __shared__ int s_nc;
   __shared__ uint32_t s_tau;
-  __shared__ int wave_tot[kNT / 64];
+  __shared__ int wave_tot[kBT / 64];
   __shared__ unsigned int s_prefix, s_need, s_take_all, s_ngt;
   __shared__ long long s_lo[kTermBatch], s_hi[kTermBatch];
   __shared__ float s_wt[kTermBatch];
@@ -197,21 +197,25 @@ __global__ __launch_bounds__(kNT) void bm25_kernel(SparseArgs a) {
   const int range = blockIdx.x % a.n_ranges;
   const long long d0 = (long long)range * kSparseRange;
   const int len = (int)std::min<long long>(kSparseRange, a.n_docs - d0);
+  // Thread tid owns the chunks 4 tid + kLayer g + e (g < 8 layers, e < 4) of the range: one
+  // 16-byte column of each layer, so its head-row loads and key reads are whole 16-byte words.
+  constexpr int kLayer = 4 * kBT;
+  static_assert(kSparseRange == 8 * kLayer, "eight layers of four chunks per thread");
+  auto own = [&](int j) { return 4 * tid + kLayer * (j >> 2) + (j & 3); };  // j < 32
 
   const int tb = a.qterm_indptr[q], te = a.qterm_indptr[q + 1];
   // 1. head terms, from their dense rows.  The query's distinct head terms are listed in
   // first-occurrence order (in the candidate area, unused until the selection), each with
   // factor m * idf(t) (k1 + 1) for its m occurrences; then every thread sums, term after term,
-  // the rows over its own chunks (16 bytes = 4 consecutive chunks from each of 8 column groups)
-  // in registers.  A row holds 0 where the term is absent and fma(f, 0, s) = s, so these are
-  // exactly the fp32 operations of walking the terms' postings, without searches, scattered
-  // LDS updates or barriers.
+  // the rows over its own chunks in registers.  A row holds 0 where the term is absent and
+  // fma(f, 0, s) = s, so these are exactly the fp32 operations of walking the terms' postings,
+  // without searches, scattered LDS updates or barriers.
   {
     int* hl_row = reinterpret_cast<int*>(cand);               // [kMaxHead]
     float* hl_wt = reinterpret_cast<float*>(cand) + kMaxHead;  // [kMaxHead]
     static_assert(2 * kMaxHead * 4 <= kCandCap * 8, "the head list fits the candidate area");
     int nh = 0;
-    for (int j0 = tb; j0 < te; j0 += kNT) {
+    for (int j0 = tb; j0 < te; j0 += kBT) {
       const int j = j0 + tid;
       int row = -1;
       float wt = 0.f;
@@ -237,119 +241,107 @@ __global__ __launch_bounds__(kNT) void bm25_kernel(SparseArgs a) {
         hl_row[pos] = row;
         hl_wt[pos] = wt;
       }
-      if (tid == kNT - 1) s_nc = pos + f;  // the count so far, shared
+      if (tid == kBT - 1) s_nc = pos + f;  // the count so far, shared
       __syncthreads();
       nh = s_nc;
       __syncthreads();
     }
-    // Thread tid owns chunks 4 tid + 1024 g + (0 .. 3) of each sub-range of kSub chunks; the
-    // rows of two terms over the whole range (up to 4 sub-ranges) are in flight at once.
-    constexpr int kSub = 8 * 4 * kNT;
-    constexpr int kNS = kSparseRange / kSub;
-    static_assert(kSparseRange % kSub == 0, "whole sub-ranges");
-    f32x4 hs[kNS][8];
+    f32x4 hs[8];
 #pragma unroll
-    for (int r = 0; r < kNS; ++r)
-#pragma unroll
-      for (int g = 0; g < 8; ++g) hs[r][g] = f32x4{0.f, 0.f, 0.f, 0.f};
-    auto load_row = [&](int i, f32x4 (&v)[kNS][8]) __attribute__((always_inline)) {
+    for (int g = 0; g < 8; ++g) hs[g] = f32x4{0.f, 0.f, 0.f, 0.f};
+    auto load_row = [&](int i, f32x4 (&v)[8]) __attribute__((always_inline)) {
       const float* row = a.whead + (long long)hl_row[i] * a.head_ld + d0;
 #pragma unroll
-      for (int r = 0; r < kNS; ++r)
-#pragma unroll
-        for (int g = 0; g < 8; ++g) {
-          const int c = r * kSub + 4 * tid + 1024 * g;  // d0 + c < n_docs: c .. c + 3 lie inside the padded row
-          v[r][g] = c < len ? *reinterpret_cast<const f32x4*>(row + c) : f32x4{0.f, 0.f, 0.f, 0.f};
-        }
+      for (int g = 0; g < 8; ++g) {
+        const int c = 4 * tid + kLayer * g;  // d0 + c < n_docs: c .. c + 3 lie inside the padded row
+        v[g] = c < len ? *reinterpret_cast<const f32x4*>(row + c) : f32x4{0.f, 0.f, 0.f, 0.f};
+      }
     };
-    auto add_row = [&](float wt, const f32x4 (&v)[kNS][8]) __attribute__((always_inline)) {
+    auto add_row = [&](float wt, const f32x4 (&v)[8]) __attribute__((always_inline)) {
 #pragma unroll
-      for (int r = 0; r < kNS; ++r)
+      for (int g = 0; g < 8; ++g)
 #pragma unroll
-        for (int g = 0; g < 8; ++g)
-#pragma unroll
-          for (int e = 0; e < 4; ++e) hs[r][g][e] = __builtin_fmaf(wt, v[r][g][e], hs[r][g][e]);
+        for (int e = 0; e < 4; ++e) hs[g][e] = __builtin_fmaf(wt, v[g][e], hs[g][e]);
     };
+    // the rows of two terms in flight at once
     int i = 0;
     for (; i + 1 < nh; i += 2) {
-      f32x4 v0[kNS][8], v1[kNS][8];
+      f32x4 v0[8], v1[8];
       load_row(i, v0);
       load_row(i + 1, v1);
       add_row(hl_wt[i], v0);
       add_row(hl_wt[i + 1], v1);
     }
     if (i < nh) {
-      f32x4 v0[kNS][8];
+      f32x4 v0[8];
       load_row(i, v0);
       add_row(hl_wt[i], v0);
     }
+    // every position of the accumulator is written, so chunks past len hold 0
 #pragma unroll
-    for (int r = 0; r < kNS; ++r)
-#pragma unroll
-      for (int g = 0; g < 8; ++g) *reinterpret_cast<f32x4*>(acc + r * kSub + 4 * tid + 1024 * g) = hs[r][g];
+    for (int g = 0; g < 8; ++g) *reinterpret_cast<f32x4*>(acc + 4 * tid + kLayer * g) = hs[g];
     __syncthreads();  // the accumulator is complete; the head list area is free again
   }
 
   // 2. the other (tail) terms, from their postings
   for (int j0 = tb; j0 < te; j0 += kTermBatch) {
-    // 1. posting bounds of up to kTermBatch terms at once, 32 threads per term.  A term that
+    // posting bounds of up to kTermBatch terms at once, 32 threads per term.  A term that
     // occurs m times in the query is walked once, at its first occurrence, with weight
     // m * idf(t) * (k1 + 1); its later occurrences walk nothing.
     {
       const int g = tid >> 5, sub = tid & 31;
       const int j = j0 + g;
-      if (g < kTermBatch) {
-        long long lo = 0, hi = 0;
-        float wt = 0.f;
-        if (j < te) {  // uniform over the group's 32 threads
-          const int t = a.qterms[j];
-          if (t >= 0 && t < a.vocab) {  // unknown terms match nothing
-            int earlier = 0, mult = 0;
-            for (int jj = tb + sub; jj < te; jj += 32)
-              if (a.qterms[jj] == t) {
-                if (jj < j) earlier = 1;
-                else mult += 1;
-              }
+      static_assert(kTermBatch * 32 == kBT, "32 threads per term");
+      long long lo = 0, hi = 0;
+      float wt = 0.f;
+      if (j < te) {  // uniform over the group's 32 threads
+        const int t = a.qterms[j];
+        if (t >= 0 && t < a.vocab) {  // unknown terms match nothing
+          int earlier = 0, mult = 0;
+          for (int jj = tb + sub; jj < te; jj += 32)
+            if (a.qterms[jj] == t) {
+              if (jj < j) earlier = 1;
+              else mult += 1;
+            }
 #pragma unroll
-            for (int o = 16; o > 0; o >>= 1) {
-              earlier |= __shfl_xor(earlier, o, 32);
-              mult += __shfl_xor(mult, o, 32);
-            }
-            if (!earlier && a.hidx[t] < 0) {  // head terms were summed from their rows
-              lo = a.indptr[t];
-              hi = a.indptr[t + 1];
-              wt = a.idfk[t] * (float)mult;
-              if (a.n_ranges > 1) range_bounds32(a.chunk, lo, hi, d0, d0 + len, sub, &lo, &hi);
-            }
+          for (int o = 16; o > 0; o >>= 1) {
+            earlier |= __shfl_xor(earlier, o, 32);
+            mult += __shfl_xor(mult, o, 32);
+          }
+          if (!earlier && a.hidx[t] < 0) {  // head terms were summed from their rows
+            lo = a.indptr[t];
+            hi = a.indptr[t + 1];
+            wt = a.idfk[t] * (float)mult;
+            if (a.n_ranges > 1) range_bounds32(a.chunk, lo, hi, d0, d0 + len, sub, &lo, &hi);
           }
         }
-        if (sub == 0) {
-          s_lo[g] = lo;
-          s_hi[g] = hi;
-          s_wt[g] = wt;
-        }
+      }
+      if (sub == 0) {
+        s_lo[g] = lo;
+        s_hi[g] = hi;
+        s_wt[g] = wt;
       }
     }
     __syncthreads();
-    // one term after another (a term's postings name distinct chunks: no atomics)
+    // one term after another (a term's postings name distinct chunks: no atomics); four
+    // postings per thread per step, all loads issued before the first update
     for (int g = 0; g < kTermBatch && j0 + g < te; ++g) {
       const long long lo = s_lo[g], hi = s_hi[g];
       if (lo < hi) {  // workgroup-uniform
         const float wt = s_wt[g];
-        // eight postings per thread per step, all loads issued before the first use
-        long long p = lo + tid;
-        for (; p + 7 * kNT < hi; p += 8 * kNT) {
-          int c[8];
-          float wp[8];
+        for (long long p = lo + tid; p < hi; p += 4 * kBT) {
+          int c[4];
+          float wp[4];
 #pragma unroll
-          for (int u = 0; u < 8; ++u) {
-            c[u] = a.chunk[p + u * kNT];
-            wp[u] = a.wpost[p + u * kNT];
+          for (int u = 0; u < 4; ++u) {
+            const long long pu = p + (long long)u * kBT;
+            c[u] = pu < hi ? a.chunk[pu] - (int)d0 : -1;
+            wp[u] = pu < hi ? a.wpost[pu] : 0.f;
           }
 #pragma unroll
-          for (int u = 0; u < 8; ++u) acc[c[u] - d0] = __builtin_fmaf(wt, wp[u], acc[c[u] - d0]);
+          for (int u = 0; u < 4; ++u)
+            if (c[u] >= 0) acc[c[u]] = __builtin_fmaf(wt, wp[u], acc[c[u]]);
         }
-        for (; p < hi; p += kNT) acc[a.chunk[p] - d0] = __builtin_fmaf(wt, a.wpost[p], acc[a.chunk[p] - d0]);
         __syncthreads();
       }
     }
@@ -359,7 +351,7 @@ __global__ __launch_bounds__(kNT) void bm25_kernel(SparseArgs a) {
     float* dst = a.dump + (long long)q * a.dump_ld + d0;
     const int mm_len = (int)std::max<long long>(0, std::min<long long>(len, a.mm_rows - d0));
     float mn = __builtin_inff(), mx = -__builtin_inff();
-    for (int i = tid; i < len; i += kNT) {
+    for (int i = tid; i < len; i += kBT) {
       const float v = acc[i];
       dst[i] = v;
       if (i < mm_len) {
@@ -372,14 +364,14 @@ __global__ __launch_bounds__(kNT) void bm25_kernel(SparseArgs a) {
         mn = fminf(mn, __shfl_xor(mn, o));
         mx = fmaxf(mx, __shfl_xor(mx, o));
       }
-      float* red = reinterpret_cast<float*>(cand);  // [kNT / 64][2], the candidate area is unused here
+      float* red = reinterpret_cast<float*>(cand);  // [kBT / 64][2], the candidate area is unused here
       if (lane == 0) {
         red[2 * w] = mn;
         red[2 * w + 1] = mx;
       }
       __syncthreads();
       if (tid == 0) {
-        for (int u = 1; u < kNT / 64; ++u) {
+        for (int u = 1; u < kBT / 64; ++u) {
           mn = fminf(mn, red[2 * u]);
           mx = fmaxf(mx, red[2 * u + 1]);
         }
@@ -393,45 +385,51 @@ __global__ __launch_bounds__(kNT) void bm25_kernel(SparseArgs a) {
 
   // ---- exact top-k of the range's positive scores (positive fp32 bits order as uints)
   const uint32_t* keys = reinterpret_cast<const uint32_t*>(acc);
-  // Threshold selection: tau = the k-th largest of the 256 thread maxima (slices i*256 + tid)
-  // is at most the k-th largest score, so only scores >= tau are candidates; when they fit
-  // in kCandCap, each one's rank is the number of larger composites (score, ~chunk), which
-  // are unique.  Otherwise (or with fewer than k positive maxima) the radix path below runs.
-  // The passes over the keys read 8 of a thread's slice per step, all before the first use, so
-  // a step waits for one LDS round trip instead of eight.
-  auto slice8 = [&](int i0, uint32_t (&v)[8]) __attribute__((always_inline)) {
+  uint32_t kv[32];  // this thread's keys, kv[j] = key of chunk own(j)
 #pragma unroll
-    for (int u = 0; u < 8; ++u) v[u] = i0 + u * kNT < len ? keys[i0 + u * kNT] : 0u;
-  };
+  for (int g = 0; g < 8; ++g) {
+    const uint4 x = reinterpret_cast<const uint4*>(acc)[tid + kBT * g];
+    kv[4 * g] = x.x;
+    kv[4 * g + 1] = x.y;
+    kv[4 * g + 2] = x.z;
+    kv[4 * g + 3] = x.w;
+  }
+  // Threshold: the 256 groups of four adjacent threads (128 chunks each) take their largest
+  // key, and tau = the k-th largest of these maxima.  Every maximum is the key of its own
+  // chunk, so at least k chunks score >= tau and the top k lie among them.  Each of a group's
+  // threads counts the maxima above and equal to its group's in a quarter of the list.
   {
     uint32_t m = 0u;
-    for (int i0 = tid; i0 < len; i0 += 8 * kNT) {
-      uint32_t v[8];
-      slice8(i0, v);
 #pragma unroll
-      for (int u = 0; u < 8; ++u) m = max(m, v[u]);
-    }
-    tmax[tid] = m;
+    for (int j = 0; j < 32; ++j) m = max(m, kv[j]);
+    m = max(m, (uint32_t)__shfl_xor((int)m, 1));
+    m = max(m, (uint32_t)__shfl_xor((int)m, 2));
+    const int grp = tid >> 2, sub = tid & 3;
+    // four blocks of 64 maxima, 68 words apart, so the blocks the four threads read start in
+    // different LDS banks
+    uint32_t* gmax = reinterpret_cast<uint32_t*>(cand);
+    if (sub == 0) gmax[(grp >> 6) * 68 + (grp & 63)] = m;
     if (tid == 0) {
       s_tau = 0u;
       s_nc = 0;
     }
     __syncthreads();
     int gt = 0, eq = 0;
-#pragma unroll 8
-    for (int u = 0; u < kNT; ++u) {
-      const uint32_t v = tmax[u];
-      gt += v > m ? 1 : 0;
-      eq += v == m ? 1 : 0;
+    const uint4* blk = reinterpret_cast<const uint4*>(gmax + sub * 68);
+#pragma unroll
+    for (int u = 0; u < 16; ++u) {
+      const uint4 x = blk[u];
+      gt += (x.x > m ? 1 : 0) + (x.y > m ? 1 : 0) + (x.z > m ? 1 : 0) + (x.w > m ? 1 : 0);
+      eq += (x.x == m ? 1 : 0) + (x.y == m ? 1 : 0) + (x.z == m ? 1 : 0) + (x.w == m ? 1 : 0);
     }
-    if (m != 0u && gt <= a.k - 1 && a.k - 1 < gt + eq) s_tau = m;  // the k-th largest maximum
+    gt += __shfl_xor(gt, 1);
+    gt += __shfl_xor(gt, 2);
+    eq += __shfl_xor(eq, 1);
+    eq += __shfl_xor(eq, 2);
+    if (sub == 0 && m != 0u && gt <= a.k - 1 && a.k - 1 < gt + eq) s_tau = m;  // the k-th largest maximum
     __syncthreads();
   }
   const uint32_t tau = s_tau;  // 0: fewer than k positive maxima
-  // At least k scores reach tau (the k largest maxima), so the top k are the G scores above tau
-  // (ranked exactly, as unique composites) and, when G < k, the k - G chunks of smallest id
-  // among the E scores equal to tau (equal scores order by id).  Many chunks can share tau
-  // exactly (equal term frequencies and lengths), which is why the two are taken apart.
   auto emit = [&](int r, u64 key) __attribute__((always_inline)) {
     if (a.n_ranges == 1) {
       a.out_ids[(long long)q * a.k + r] = (long long)comp_row(key);
@@ -440,79 +438,73 @@ __global__ __launch_bounds__(kNT) void bm25_kernel(SparseArgs a) {
       a.partial[((long long)q * a.n_ranges + range) * a.k + r] = key;
     }
   };
+  auto composite = [&](int i) __attribute__((always_inline)) {
+    return ((u64)keys[i] << 32) | (uint32_t)(~(uint32_t)(d0 + i));
+  };
   if (tau != 0u) {
-    // a thread's keys above tau: a mask bit per slice position (at most 128 per thread)
-    static_assert(kSparseRange <= 128 * kNT, "a slice fits the mask");
-    uint32_t mk[4] = {0u, 0u, 0u, 0u};
-    int c = 0;
-    for (int i0 = tid, j0 = 0; i0 < len; i0 += 8 * kNT, j0 += 8) {
-      uint32_t v[8];
-      slice8(i0, v);
+    // G scores above tau and E equal to it.  When G + E fit the candidate area all of them
+    // are ranked as unique composites (score, ~chunk), which orders equal scores by chunk.
+    // Otherwise the G above tau are ranked and, when G < k, ranks G .. k - 1 go to the chunks
+    // equal to tau in chunk order (many chunks can share a score exactly: equal term
+    // frequencies and lengths).  G + E >= k always.
+    uint32_t mgt = 0u, meq = 0u;
 #pragma unroll
-      for (int u = 0; u < 8; ++u)
-        if (v[u] > tau) {
-          ++c;
-          const int j = j0 + u;
-#pragma unroll
-          for (int e = 0; e < 4; ++e) mk[e] |= (j >> 5) == e ? 1u << (j & 31) : 0u;
-        }
+    for (int j = 0; j < 32; ++j) {
+      mgt |= (kv[j] > tau ? 1u : 0u) << j;
+      meq |= (kv[j] == tau ? 1u : 0u) << j;
     }
-    const int before = block_excl_scan(c, wave_tot);
-    if (tid == kNT - 1) s_nc = before + c;
-    int pos = before;
-    if (before + c <= kCandCap) {
-#pragma unroll
-      for (int e = 0; e < 4; ++e)
-        for (uint32_t m = mk[e]; m != 0u; m &= m - 1u) {
-          const int i = tid + (32 * e + __builtin_ctz(m)) * kNT;
-          cand[pos++] = ((u64)keys[i] << 32) | (uint32_t)(~(uint32_t)(d0 + i));
-        }
-    }
+    // both counts in one scan: G and E are at most 32,768, so the low field never carries
+    const int packed = __popc(mgt) | (__popc(meq) << 16);
+    const int before = block_excl_scan(packed, wave_tot);
+    if (tid == kBT - 1) s_nc = before + packed;
     __syncthreads();
-  }
-  const int nc = s_nc;  // G
-  if (tau != 0u && nc <= kCandCap) {  // workgroup-uniform
-    for (int j = tid; j < nc; j += kNT) {
-      const u64 me = cand[j];
+    const int G = s_nc & 0xffff, E = s_nc >> 16;
+    const bool all = G + E <= kCandCap;  // workgroup-uniform
+    if (G <= kCandCap) {
+      int pos = all ? (before & 0xffff) + (before >> 16) : (before & 0xffff);
+      for (uint32_t msk = all ? (mgt | meq) : mgt; msk != 0u; msk &= msk - 1u)
+        cand[pos++] = composite(own(__builtin_ctz(msk)));
+      __syncthreads();
+      // rank = number of larger composites; L adjacent lanes share a candidate, each
+      // comparing every L-th entry
+      const int nc = all ? G + E : G;
+      int lg = 0;
+      while (lg < 4 && (nc << (lg + 1)) <= kBT) ++lg;
+      const int L = 1 << lg, jc = tid >> lg, p = tid & (L - 1);
       int r = 0;
-      for (int o = 0; o < nc; o += 8) {
-        u64 v[8];
+      u64 me = 0ull;
+      if (jc < nc) {
+        me = cand[jc];
+        for (int o = p; o < nc; o += 8 * L) {
+          u64 v[8];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) v[u] = cand[min(o + u, nc - 1)];
+          for (int u = 0; u < 8; ++u) v[u] = cand[min(o + u * L, nc - 1)];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) r += (o + u < nc && v[u] > me) ? 1 : 0;
-      }
-      if (r < a.k) emit(r, me);
-    }
-    if (nc < a.k) {
-      // ranks nc .. k - 1: the scores equal to tau in chunk order.  Each thread owns a
-      // contiguous block of at most 128 chunks; it reads the block starting at a rotated offset
-      // (lanes then hit different LDS banks instead of one) and marks the equal scores in a
-      // 128-bit mask, whose set bits it then emits in order after a scan of the counts.
-      static_assert(kSparseRange <= 128 * kNT, "a block fits the mask");
-      const int per = (len + kNT - 1) / kNT;
-      const int b0 = min(len, tid * per), nb = min(len, b0 + per) - b0;
-      uint32_t mk[4] = {0u, 0u, 0u, 0u};
-      int ce = 0;
-      for (int i = 0; i < nb; ++i) {
-        int o = i + tid;
-        o = o >= nb ? o % nb : o;
-        if (keys[b0 + o] == tau) {
-          ++ce;
-#pragma unroll
-          for (int u = 0; u < 4; ++u) mk[u] |= (o >> 5) == u ? 1u << (o & 31) : 0u;
+          for (int u = 0; u < 8; ++u) r += (o + u * L < nc && v[u] > me) ? 1 : 0;
         }
       }
-      int r = nc + block_excl_scan(ce, wave_tot);
-#pragma unroll
-      for (int u = 0; u < 4; ++u)
-        for (uint32_t m = mk[u]; m != 0u && r < a.k; m &= m - 1u)
-          emit(r++, ((u64)tau << 32) | (uint32_t)(~(uint32_t)(d0 + b0 + 32 * u + __builtin_ctz(m))));
+      for (int s = 1; s < L; s <<= 1) r += __shfl_xor(r, s);
+      if (jc < nc && p == 0 && r < a.k) emit(r, me);
+      if (!all && G < a.k) {
+        // ranks G .. k - 1: each thread marks the scores equal to tau in a contiguous block of
+        // 32 chunks, read from a rotated start (lanes then hit different LDS banks), and emits
+        // them in order after a scan of the counts
+        const int b0 = min(len, 32 * tid), nb = min(len, b0 + 32) - b0;
+        uint32_t mk = 0u;
+        for (int i = 0; i < nb; ++i) {
+          const int o = (i + tid) % nb;
+          mk |= (keys[b0 + o] == tau ? 1u : 0u) << o;
+        }
+        int rr = G + block_excl_scan(__popc(mk), wave_tot);
+        for (uint32_t m2 = mk; m2 != 0u && rr < a.k; m2 &= m2 - 1u) emit(rr++, composite(b0 + __builtin_ctz(m2)));
+      }
+      return;
     }
-    return;
+    __syncthreads();  // the candidate area becomes the histogram
   }
 
-  // ---- radix select of the k-th largest positive score
+  // ---- radix select of the k-th largest positive score (few positive maxima or many
+  // candidates), over the keys held in registers
   if (tid == 0) {
     s_prefix = 0u;
     s_need = (unsigned)a.k;
@@ -525,30 +517,37 @@ __global__ __launch_bounds__(kNT) void bm25_kernel(SparseArgs a) {
     const uint32_t hmask = pass == 0 ? 0u : (0xffffffffu << (shift + 8));
     const uint32_t prefix = s_prefix;
     const unsigned int need = s_need;
-    hist[tid] = 0u;  // kNT == 256 bins
+    if (tid < 256) hist[tid] = 0u;
     __syncthreads();
-    for (int i = tid; i < len; i += kNT) {
-      const uint32_t u = keys[i];
+#pragma unroll
+    for (int j = 0; j < 32; ++j) {
+      const uint32_t u = kv[j];
       if (u != 0u && (u & hmask) == prefix) atomicAdd(&hist[(u >> shift) & 255u], 1u);
     }
     __syncthreads();
-    // thread t holds bin 255 - t; inclusive scan = keys in bins >= 255 - t
-    const int hd = (int)hist[255 - tid];
-    int x = hd;
+    // threads 0 .. 255 (waves 0 .. 3): thread t holds bin 255 - t; its inclusive scan is the
+    // number of keys in bins >= 255 - t
+    int hd = 0, x = 0;
+    if (tid < 256) {
+      hd = (int)hist[255 - tid];
+      x = hd;
 #pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      const int y = __shfl_up(x, o, 64);
-      if (lane >= o) x += y;
+      for (int o = 1; o < 64; o <<= 1) {
+        const int y = __shfl_up(x, o, 64);
+        if (lane >= o) x += y;
+      }
+      if (lane == 63) wave_tot[w] = x;
     }
-    if (lane == 63) wave_tot[w] = x;
     __syncthreads();
-    int before = 0;
-    for (int i = 0; i < w; ++i) before += wave_tot[i];
-    const int incl = before + x, above = incl - hd;
-    if (tid == kNT - 1 && incl < (int)need) s_take_all = 1u;  // fewer than k positive scores (pass 0)
-    if (above < (int)need && incl >= (int)need) {
-      s_prefix = prefix | ((uint32_t)(255 - tid) << shift);
-      s_need = need - (unsigned)above;
+    if (tid < 256) {
+      int before = 0;
+      for (int i = 0; i < w; ++i) before += wave_tot[i];
+      const int incl = before + x, above = incl - hd;
+      if (tid == 255 && incl < (int)need) s_take_all = 1u;  // fewer than k positive scores (pass 0)
+      if (above < (int)need && incl >= (int)need) {
+        s_prefix = prefix | ((uint32_t)(255 - tid) << shift);
+        s_need = need - (unsigned)above;
+      }
     }
     __syncthreads();
   }
@@ -556,18 +555,18 @@ __global__ __launch_bounds__(kNT) void bm25_kernel(SparseArgs a) {
   const uint32_t T = s_prefix;
   const unsigned int need_eq = take_all ? 0u : s_need;
 
-  // ---- collect: every key > T, then the need_eq smallest chunk ids with key == T
+  // ---- collect: every key > T, then the need_eq smallest chunk ids with key == T (contiguous
+  // blocks of 32 chunks per thread, so a scan of the counts orders the equal keys by chunk)
   if (tid == 0) s_ngt = 0u;
   __syncthreads();
-  const int per = (len + kNT - 1) / kNT;
-  const int b0 = tid * per, b1 = std::min(len, b0 + per);
+  const int b0 = min(len, 32 * tid), b1 = min(len, b0 + 32);
   int n_eq = 0;
   for (int i = b0; i < b1; ++i) {
     const uint32_t u = keys[i];
     if (u == 0u) continue;
     if (take_all ? true : u > T) {
       const unsigned int slot = atomicAdd(&s_ngt, 1u);
-      selbuf[slot] = ((u64)u << 32) | (uint32_t)(~(uint32_t)(d0 + i));
+      selbuf[slot] = composite(i);
     } else if (u == T) {
       ++n_eq;
     }
@@ -578,7 +577,7 @@ __global__ __launch_bounds__(kNT) void bm25_kernel(SparseArgs a) {
     int r = before;
     for (int i = b0; i < b1 && r < (int)need_eq; ++i) {
       if (keys[i] == T) {
-        selbuf[ngt + r] = ((u64)T << 32) | (uint32_t)(~(uint32_t)(d0 + i));
+        selbuf[ngt + r] = composite(i);
         ++r;
       }
     }
@@ -1035,7 +1034,7 @@ hipError_t launch_sparse_dump(const SparseIndex& sp, const int* qterm_indptr, co
   a.out_scores = nullptr;
   a.out_ids = nullptr;
   a.partial = nullptr;
-  hipLaunchKernelGGL(bm25_kernel, dim3((unsigned)(nq * a.n_ranges)), dim3(kNT), 0, s, a);
+  hipLaunchKernelGGL(bm25_kernel, dim3((unsigned)(nq * a.n_ranges)), dim3(kBT), 0, s, a);
   return hipGetLastError();
 }
 
@@ -1065,7 +1064,7 @@ hipError_t launch_sparse(const SparseIndex& sp, const int* qterm_indptr, const i
   a.out_scores = out_scores;
   a.out_ids = out_ids;
   a.partial = static_cast<unsigned long long*>(ws);
-  hipLaunchKernelGGL(bm25_kernel, dim3((unsigned)(nq * a.n_ranges)), dim3(kNT), 0, s, a);
+  hipLaunchKernelGGL(bm25_kernel, dim3((unsigned)(nq * a.n_ranges)), dim3(kBT), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.n_ranges == 1) return e;
   if ((long long)a.n_ranges * k <= kMergeCap)
