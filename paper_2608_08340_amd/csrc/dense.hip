@@ -399,12 +399,24 @@ struct SelOf<BN, KS, 1, NT> {
 // Filtered mode (k > 16).  Every row whose score reaches the query's threshold becomes a
 // candidate key in the query's global buffer; an exact selection over the buffer follows in
 // select_topk_kernel.  Candidates of a query are staged in LDS (SCAP keys) and written out
-// with one device-scope reservation per flush.  LDS: stage [BN][SCAP] | staged count [BN].
+// with one device-scope reservation per flush.  A staged entry holds the raw score bits and
+// the row; the flush turns it into the key.  LDS: stage [BN][SCAP] | one discard slot per
+// thread | flush bases [BN] | staged counts [BN] | flush flag.
 // ------------------------------------------------------------------------------------
 template <int BN>
 struct SelFilter {
   static constexpr int SCAP = 32;
-  static constexpr int kBytes = BN * SCAP * 8 + BN * 4;
+  static constexpr int kTrash = 256;  // threads of the kernels that use it
+  static constexpr int kBytes = BN * SCAP * 8 + kTrash * 8 + BN * 8 + BN * 4 + 16;
+  static __device__ __forceinline__ u64* stage(unsigned char* area) { return reinterpret_cast<u64*>(area); }
+  static __device__ __forceinline__ u64* trash(unsigned char* area) { return reinterpret_cast<u64*>(area) + BN * SCAP; }
+  static __device__ __forceinline__ long long* base(unsigned char* area) {
+    return reinterpret_cast<long long*>(area + BN * SCAP * 8 + kTrash * 8);
+  }
+  // the BN staged counts, then the flag
+  static __device__ __forceinline__ int* staged(unsigned char* area) {
+    return reinterpret_cast<int*>(area + BN * SCAP * 8 + kTrash * 8 + BN * 8);
+  }
   __device__ __forceinline__ void init() {}
   __device__ __forceinline__ void pass(const float*, int, int, const PassRows&, int, int, unsigned char*) {}
   __device__ __forceinline__ void write(const DenseArgs&, int, long long) const {}
@@ -465,70 +477,107 @@ __device__ __forceinline__ void dump_tile(const f32x4 (&acc)[MW][BN / 16], long 
   }
 }
 
-// Owner thread of query slot n: append its staged keys (the stage's first SCAP slots; a count
-// beyond SCAP means the rest already went out directly) to the global buffer.
-template <int BN>
-__device__ __forceinline__ void filt_flush(int n, int q, unsigned char* area, const DenseArgs& a) {
+// Flush of the staged keys of every query slot whose count reaches `from` (a count beyond SCAP
+// means the rest already went out directly): the owner threads reserve their slots in the
+// global buffers with one device-scope atomic each, all at once; after a barrier every thread
+// copies staged keys, consecutive threads taking consecutive keys of a query.  The flushed
+// counts and the flag are reset; the stage is next written after a later barrier.
+template <int BN, int NT>
+__device__ __forceinline__ void filt_flush(unsigned char* area, int q0, int q_lim, int from, const DenseArgs& a) {
   constexpr int SCAP = SelFilter<BN>::SCAP;
-  u64* stage = reinterpret_cast<u64*>(area);
-  int* staged = reinterpret_cast<int*>(area + BN * SCAP * 8);
-  const int c = min(staged[n], SCAP);
-  if (c == 0) return;
-  const long long g = atomicAdd(a.ccnt + q, c);
-  u64* dst = a.cbuf + (long long)q * a.cap;
-  for (int j = 0; j < c; ++j)
-    if (g + j < a.cap) dst[g + j] = stage[n * SCAP + j];
-  staged[n] = 0;
+  const u64* stage = SelFilter<BN>::stage(area);
+  long long* base = SelFilter<BN>::base(area);
+  int* staged = SelFilter<BN>::staged(area);
+  const int tid = threadIdx.x;
+  if (tid < BN) {
+    const int c = min(staged[tid], SCAP);
+    base[tid] = tid < q_lim && c > 0 && c >= from ? (long long)atomicAdd(a.ccnt + q0 + tid, c) : -1ll;
+  }
+  lds_barrier();
+#pragma unroll 4
+  for (int i = tid; i < BN * SCAP; i += NT) {
+    const int n = i / SCAP, j = i % SCAP;
+    const long long g = base[n] + j;
+    if (base[n] >= 0 && j < min(staged[n], SCAP) && g < a.cap) {
+      const u64 e = stage[i];
+      a.cbuf[(long long)(q0 + n) * a.cap + g] = composite(__uint_as_float((uint32_t)(e >> 32)), (uint32_t)e);
+    }
+  }
+  lds_barrier();
+  if (tid < BN && base[tid] >= 0) staged[tid] = 0;
+  if (tid == 0) staged[BN] = 0;
 }
 
-// Hits of one tile: a lane compares the maximum of its MW*4 scores of a query with the
-// threshold and, on a hit, counts them, reserves that many stage slots with one LDS atomic
-// and writes them; hits past the stage's end go straight to the global buffer under one
-// device-scope reservation.  FULL: the tile lies inside the chunk (no row-limit test).
+// Hits of one tile.  Each lane first forms, for every query slot, the mask of its MW*4 scores
+// that reach the threshold, then reserves that many stage slots per slot with hits (one LDS
+// atomic each, all issued before the first result is used).  Every score is then stored
+// without a branch: a hit to its stage slot, any other score to the thread's discard slot.
+// Hits past the stage's end (rare) go straight to the global buffer under one device-scope
+// reservation.  A stage at least half full raises the flush flag.  FULL: the tile lies
+// inside the chunk (no row-limit test).
 template <bool FULL, int BN, int MW>
 __device__ __forceinline__ void filt_collect(const f32x4 (&acc)[MW][BN / 16], const float (&th)[BN / 16],
-                                             u64* stage, int* staged, long long tile0, int row0, int lim, int q0,
+                                             unsigned char* area, long long tile0, int row0, int lim, int q0,
                                              const DenseArgs& a) {
   constexpr int NW = BN / 16;
   constexpr int SCAP = SelFilter<BN>::SCAP;
+  static_assert(MW * 4 <= 32, "a lane's scores of a query slot fit one mask");
+  u64* stage = SelFilter<BN>::stage(area);
+  int* staged = SelFilter<BN>::staged(area);
+  u64* trash = SelFilter<BN>::trash(area) + threadIdx.x;
   const int lane = threadIdx.x & 63;
   auto ok = [&](int mi, int r) { return FULL || mi * 16 + r < lim; };
+  uint32_t bits[NW];
 #pragma unroll
   for (int ni = 0; ni < NW; ++ni) {
-    float m = kNegInf;
+    uint32_t b = 0u;
 #pragma unroll
     for (int mi = 0; mi < MW; ++mi)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) m = __builtin_fmaxf(m, ok(mi, r) ? acc[mi][ni][r] : kNegInf);
-    if (!(m >= th[ni])) continue;
-    int c = 0;
+      for (int r = 0; r < 4; ++r) b |= (ok(mi, r) && acc[mi][ni][r] >= th[ni] ? 1u : 0u) << (mi * 4 + r);
+    bits[ni] = b;
+  }
+  int pos[NW];
 #pragma unroll
-    for (int mi = 0; mi < MW; ++mi)
+  for (int ni = 0; ni < NW; ++ni) {
+    const int c = __popc(bits[ni]);
+    pos[ni] = c ? atomicAdd(&staged[ni * 16 + (lane & 15)], c) : 0;
+  }
+  const uint32_t row_l = (uint32_t)(tile0 + row0);
+  bool half = false;
 #pragma unroll
-      for (int r = 0; r < 4; ++r) c += (ok(mi, r) && acc[mi][ni][r] >= th[ni]) ? 1 : 0;
-    const int n = ni * 16 + (lane & 15);
-    const int pos = atomicAdd(&staged[n], c);
-    const int in_stage = max(0, min(c, SCAP - pos));
-    const long long g = in_stage < c ? atomicAdd(a.ccnt + q0 + n, c - in_stage) : 0ll;
-    u64* dst_g = a.cbuf + (long long)(q0 + n) * a.cap;
+  for (int ni = 0; ni < NW; ++ni) {
+    const uint32_t b = bits[ni];
+    const int c = __popc(b), n = ni * 16 + (lane & 15);
+    const int in_stage = max(0, min(c, SCAP - pos[ni]));
+    half = half || (c > 0 && pos[ni] + c >= SCAP / 2);
+    u64* st = stage + n * SCAP + pos[ni];
     int h = 0;
 #pragma unroll
     for (int mi = 0; mi < MW; ++mi)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const float x = acc[mi][ni][r];
-        if (ok(mi, r) && x >= th[ni]) {
-          const u64 key = composite(x, (uint32_t)(tile0 + row0 + mi * 16 + r));
-          if (h < in_stage) {
-            stage[n * SCAP + pos + h] = key;
-          } else {
-            const long long j = g + (h - in_stage);
-            if (j < a.cap) dst_g[j] = key;
-          }
-          ++h;
-        }
+        const int hit = (int)((b >> (mi * 4 + r)) & 1u);
+        u64* dst = hit && h < in_stage ? st + h : trash;
+        *dst = ((u64)__float_as_uint(acc[mi][ni][r]) << 32) | (u64)(row_l + (uint32_t)(mi * 16 + r));
+        h += hit;
       }
+    if (in_stage < c) {  // the lane's hits past the stage
+      const long long g = atomicAdd(a.ccnt + q0 + n, c - in_stage);
+      u64* dst_g = a.cbuf + (long long)(q0 + n) * a.cap;
+      int hh = 0;
+#pragma unroll
+      for (int mi = 0; mi < MW; ++mi)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if ((b >> (mi * 4 + r)) & 1u) {
+            const long long jg = g + (hh - in_stage);
+            if (hh >= in_stage && jg < a.cap) dst_g[jg] = composite(acc[mi][ni][r], row_l + (uint32_t)(mi * 16 + r));
+            ++hh;
+          }
+    }
   }
+  if (half) staged[BN] = 1;
 }
 
 // First level (no threshold): every row of [0, n_rows) is a candidate, so each score goes to
@@ -557,24 +606,24 @@ __device__ __forceinline__ void filt_all_tile(const f32x4 (&acc)[MW][BN / 16], l
 
 // acc[mi][ni][r] = score of row tile0 + 16*MW*wave + 16*mi + 4*(lane/16) + r against query
 // slot 16*ni + lane%16; th[ni] its threshold (+inf for slots past the batch).  One barrier;
-// then the owner of a stage at least half full flushes it.  The stage is next written in the
-// following tile's selection, after a barrier inside that tile's main loop.
+// then the chunk's last tile flushes every stage, and an earlier tile the stages at least half
+// full (when any is).  The stage is next written in the following tile's selection, after a
+// barrier inside that tile's main loop.
 template <int BN, int MW, int WV>
 __device__ __forceinline__ void filt_tile(const f32x4 (&acc)[MW][BN / 16], const float (&th)[BN / 16],
-                                          unsigned char* area, long long tile0, long long row_end, int q0,
-                                          const DenseArgs& a) {
+                                          unsigned char* area, long long tile0, long long row_end, int q0, int q_lim,
+                                          bool last, const DenseArgs& a) {
   constexpr int SCAP = SelFilter<BN>::SCAP;
   constexpr int TR = WV * MW * 16;
-  u64* stage = reinterpret_cast<u64*>(area);
-  int* staged = reinterpret_cast<int*>(area + BN * SCAP * 8);
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int row0 = w * MW * 16 + (lane >> 4) * 4;
   if (tile0 + TR <= row_end)  // workgroup-uniform
-    filt_collect<true, BN, MW>(acc, th, stage, staged, tile0, row0, 0, q0, a);
+    filt_collect<true, BN, MW>(acc, th, area, tile0, row0, 0, q0, a);
   else
-    filt_collect<false, BN, MW>(acc, th, stage, staged, tile0, row0, (int)(row_end - tile0) - row0, q0, a);
+    filt_collect<false, BN, MW>(acc, th, area, tile0, row0, (int)(row_end - tile0) - row0, q0, a);
   lds_barrier();
-  if (tid < BN && staged[tid] >= SCAP / 2) filt_flush<BN>(tid, q0 + tid, area, a);
+  if (last || SelFilter<BN>::staged(area)[BN] != 0)  // workgroup-uniform
+    filt_flush<BN, WV * 64>(area, q0, q_lim, last ? 1 : SCAP / 2, a);
 }
 
 // ------------------------------------------------------------------------------------
@@ -1107,7 +1156,7 @@ __global__ __launch_bounds__(WV * 64) void dense_mfma_kernel(DenseArgs a) {
   Sel sel;
   sel.init();
   if constexpr (SEL == 2) {
-    if (tid < BN) reinterpret_cast<int*>(scratch + BN * SelFilter<BN>::SCAP * 8)[tid] = 0;
+    if (tid <= BN) SelFilter<BN>::staged(scratch)[tid] = 0;  // counts and flag
     // no barrier needed here: the first tile's epilogue follows several barriers
   }
   float dmn[NW], dmx[NW];  // score dump: this lane's minimum and maximum per query slot
@@ -1277,7 +1326,7 @@ __global__ __launch_bounds__(WV * 64) void dense_mfma_kernel(DenseArgs a) {
         if (a.th == nullptr)  // launch-uniform
           filt_all_tile<BN, MW, WV>(acc, tile0, row_end, q0, q_lim, a);
         else
-          filt_tile<BN, MW, WV>(acc, th, scratch, tile0, row_end, q0, a);
+          filt_tile<BN, MW, WV>(acc, th, scratch, tile0, row_end, q0, q_lim, t == n_tiles - 1, a);
         done = true;
       } else if constexpr (SEL == 0) {
         // A chunk's first tile fills the lists through the group path; the tiles after it
@@ -1336,9 +1385,7 @@ __global__ __launch_bounds__(WV * 64) void dense_mfma_kernel(DenseArgs a) {
   if constexpr (SEL == 2) {
     if (a.th == nullptr) {
       if (chunk == 0 && tid < q_lim) a.ccnt[q0 + tid] = (int)a.n_rows;  // every row is a candidate
-    } else if (tid < q_lim) {
-      filt_flush<BN>(tid, q0 + tid, scratch, a);
-    }
+    }  // else the chunk's last tile flushed its stages
   } else if constexpr (SEL == 3) {
     if (a.dump_mm != nullptr) {  // launch-uniform
       // the four lanes of a query slot in a wave, then the waves through LDS
@@ -1467,21 +1514,28 @@ __global__ __launch_bounds__(kThreads) void dense_f32_kernel(DenseArgs a) {
 
 // ------------------------------------------------------------------------------------
 // Filtered mode, selection: exact top-k (sorted) of a query's candidate keys.  One workgroup
-// per query finds the k-th largest 64-bit key by most-significant-digit radix selection
-// (8-bit digits; it stops as soon as a whole bucket is needed), gathers the keys at or above
-// it, and ranks them.  Keys are distinct (row ids are), so exactly min(k, n) keys qualify.
+// of 1,024 threads per query.  Keys are unique composites (row ids are), so exactly
+// min(k, n) keys qualify.  Buffers of up to 4,096 keys are read once (four keys per thread,
+// all loads in flight) and kept in registers.  The 256 groups of four adjacent threads take
+// their largest key, and tau = the need-th largest of these maxima bounds the need-th best key
+// from below (every maximum is a key of its own); the keys >= tau are ranked exactly.  Too
+// many of them, or larger buffers, take a most-significant-digit radix select (8-bit digits,
+// stopping as soon as a whole bucket is needed).
 // ------------------------------------------------------------------------------------
-__global__ __launch_bounds__(kThreads) void select_topk_kernel(const unsigned long long* __restrict__ cbuf,
-                                                               int* __restrict__ ccnt, long long cap, int k,
-                                                               float* out_scores, long long* out_ids, int* overflow,
-                                                               const int* gate, int threshold_only) {
+constexpr int kSelThreads = 1024;
+__global__ __launch_bounds__(kSelThreads) void select_topk_kernel(const unsigned long long* __restrict__ cbuf,
+                                                                  int* __restrict__ ccnt, long long cap, int k,
+                                                                  float* out_scores, long long* out_ids, int* overflow,
+                                                                  const int* gate, int threshold_only) {
+  constexpr int NT = kSelThreads;
   constexpr int kCand = 1024;  // candidates the threshold path ranks directly
+  constexpr int kRegKeys = 4;
   __shared__ u64 cand[kCand];
-  __shared__ u64 tmax[kThreads];
+  __shared__ __attribute__((aligned(16))) u64 gmax[4 * 66];  // four blocks of 64 group maxima, 66 apart
   __shared__ u64 s_tau;
   __shared__ int s_nc;
   __shared__ unsigned int hist[256];
-  __shared__ int wtot[kWaves];
+  __shared__ int wtot[NT / 64];
   __shared__ u64 sel[kMaxK];
   __shared__ u64 s_prefix, s_mask;
   __shared__ int s_need, s_done, s_ns;
@@ -1498,43 +1552,56 @@ __global__ __launch_bounds__(kThreads) void select_topk_kernel(const unsigned lo
     s_need = min(k, n);
     s_done = s_need == 0;
     s_ns = 0;
+    s_tau = 0ull;
   }
   __syncthreads();
   if (t == 0) ccnt[q] = 0;  // every thread has read it: the next pass starts from zero
-  // Threshold path: the keys are unique composites.  tau = the need-th largest of the thread
-  // maxima (lane-strided slices) bounds the need-th best key from below, and the keys >= tau
-  // (about 1-2 need) are ranked exactly.  Too many of them: the radix select below.
   const int need = min(k, n);
-  // Up to kRegKeys keys per thread are read once, all loads in flight together, and kept in
-  // registers for the three passes below; larger buffers are read again in each pass.
-  constexpr int kRegKeys = 16;
-  const bool in_reg = n <= kRegKeys * kThreads;  // workgroup-uniform
+  const bool in_reg = n <= kRegKeys * NT;  // workgroup-uniform
+  // Register keys: thread t holds keys ib + 1,024 u, where ib puts the first 256 keys in 256
+  // different groups, so at least min(n, 256) >= need groups are nonempty.
+  const int ib = (t >> 2) + 256 * (t & 3);
   u64 kv[kRegKeys];
   if (in_reg) {
 #pragma unroll
     for (int u = 0; u < kRegKeys; ++u) {
-      const int i = t + u * kThreads;
+      const int i = ib + u * NT;
       kv[u] = i < n ? src[i] : 0ull;
     }
   }
+  // keys of this thread beyond the registers, eight loads in flight per step
+  auto scan_global = [&](auto&& f) __attribute__((always_inline)) {
+    for (int i0 = t; i0 < n; i0 += 8 * NT) {
+      u64 v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = i0 + u * NT < n ? src[i0 + u * NT] : 0ull;
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (i0 + u * NT < n) f(v[u]);
+    }
+  };
   if (need > 0) {
     u64 m = 0ull;
     if (in_reg) {
 #pragma unroll
       for (int u = 0; u < kRegKeys; ++u) m = umax64(m, kv[u]);
     } else {
-      for (int i = t; i < n; i += kThreads) m = umax64(m, src[i]);
+      scan_global([&](u64 x) { m = umax64(m, x); });
     }
-    tmax[t] = m;
-    if (t == 0) {
-      s_tau = 0ull;
-      s_nc = 0;
-    }
+    m = umax64(m, shfl_xor64(m, 1));
+    m = umax64(m, shfl_xor64(m, 2));
+    const int grp = t >> 2, sub = t & 3;
+    if (sub == 0) gmax[(grp >> 6) * 66 + (grp & 63)] = m;
     __syncthreads();
+    // each of the group's four threads counts the larger maxima in a quarter of the list
     int gt = 0;
-#pragma unroll 8
-    for (int u = 0; u < kThreads; ++u) gt += tmax[u] > m ? 1 : 0;
-    if (m != 0ull && gt == need - 1) s_tau = m;  // nonzero maxima are unique; n >= need of them
+    const u64* blk = gmax + sub * 66;
+#pragma unroll 16
+    for (int u = 0; u < 64; ++u) gt += blk[u] > m ? 1 : 0;
+    gt += __shfl_xor(gt, 1);
+    gt += __shfl_xor(gt, 2);
+    // nonzero maxima are unique, and at least need groups hold keys
+    if (sub == 0 && m != 0ull && gt == need - 1) s_tau = m;
     __syncthreads();
     const u64 tau = s_tau;
     if (threshold_only) {
@@ -1546,9 +1613,9 @@ __global__ __launch_bounds__(kThreads) void select_topk_kernel(const unsigned lo
     int c = 0;
     if (in_reg) {
 #pragma unroll
-      for (int u = 0; u < kRegKeys; ++u) c += (t + u * kThreads < n && kv[u] >= tau) ? 1 : 0;
+      for (int u = 0; u < kRegKeys; ++u) c += (ib + u * NT < n && kv[u] >= tau) ? 1 : 0;
     } else {
-      for (int i = t; i < n; i += kThreads) c += src[i] >= tau ? 1 : 0;
+      scan_global([&](u64 x) { c += x >= tau ? 1 : 0; });
     }
     // exclusive scan of c over the workgroup
     int x = c;
@@ -1561,40 +1628,45 @@ __global__ __launch_bounds__(kThreads) void select_topk_kernel(const unsigned lo
     __syncthreads();
     int pos = x - c;
     for (int i = 0; i < w; ++i) pos += wtot[i];
-    if (t == kThreads - 1) s_nc = pos + c;
-    if (pos + c <= kCand) {
-      if (in_reg) {
-#pragma unroll
-        for (int u = 0; u < kRegKeys; ++u)
-          if (t + u * kThreads < n && kv[u] >= tau) cand[pos++] = kv[u];
-      } else {
-        for (int i = t; i < n; i += kThreads) {
-          const u64 key = src[i];
-          if (key >= tau) cand[pos++] = key;
-        }
-      }
-    }
+    if (t == NT - 1) s_nc = pos + c;
     __syncthreads();
     const int nc = s_nc;
     if (nc <= kCand) {  // workgroup-uniform
-      for (int j = t; j < nc; j += kThreads) {
-        const u64 me = cand[j];
-        int r = 0;
-        for (int b = 0; b < nc; b += 8) {
+      if (in_reg) {
+#pragma unroll
+        for (int u = 0; u < kRegKeys; ++u)
+          if (ib + u * NT < n && kv[u] >= tau) cand[pos++] = kv[u];
+      } else {
+        scan_global([&](u64 x) {
+          if (x >= tau) cand[pos++] = x;
+        });
+      }
+      __syncthreads();
+      // rank = number of larger keys; L adjacent lanes share a candidate, each comparing
+      // every L-th entry
+      int lg = 0;
+      while (lg < 4 && (nc << (lg + 1)) <= NT) ++lg;
+      const int L = 1 << lg, jc = t >> lg, p = t & (L - 1);
+      int r = 0;
+      u64 me = 0ull;
+      if (jc < nc) {
+        me = cand[jc];
+        for (int o = p; o < nc; o += 8 * L) {
           u64 v[8];
 #pragma unroll
-          for (int u = 0; u < 8; ++u) v[u] = cand[min(b + u, nc - 1)];
+          for (int u = 0; u < 8; ++u) v[u] = cand[min(o + u * L, nc - 1)];
 #pragma unroll
-          for (int u = 0; u < 8; ++u) r += (b + u < nc && v[u] > me) ? 1 : 0;
-        }
-        if (r < need) {
-          out_ids[(long long)q * k + r] = (long long)comp_row(me);
-          out_scores[(long long)q * k + r] = comp_score(me);
+          for (int u = 0; u < 8; ++u) r += (o + u * L < nc && v[u] > me) ? 1 : 0;
         }
       }
-      for (int r = need + t; r < k; r += kThreads) {
-        out_ids[(long long)q * k + r] = -1ll;
-        out_scores[(long long)q * k + r] = kNegInf;
+      for (int s = 1; s < L; s <<= 1) r += __shfl_xor(r, s);
+      if (jc < nc && p == 0 && r < need) {
+        out_ids[(long long)q * k + r] = (long long)comp_row(me);
+        out_scores[(long long)q * k + r] = comp_score(me);
+      }
+      for (int r2 = need + t; r2 < k; r2 += NT) {
+        out_ids[(long long)q * k + r2] = -1ll;
+        out_scores[(long long)q * k + r2] = kNegInf;
       }
       return;
     }
@@ -1602,45 +1674,62 @@ __global__ __launch_bounds__(kThreads) void select_topk_kernel(const unsigned lo
   for (int shift = 56; shift >= 0; shift -= 8) {
     if (s_done) break;  // block-uniform
     const u64 prefix = s_prefix, mask = s_mask;
-    const int need = s_need;
-    hist[t] = 0u;
+    const int need_d = s_need;
+    if (t < 256) hist[t] = 0u;
     __syncthreads();
-    for (int i = t; i < n; i += kThreads) {
-      const u64 key = src[i];
+    auto count = [&](u64 key) __attribute__((always_inline)) {
       if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
-    }
-    __syncthreads();
-    // thread t holds digit 255 - t; an inclusive scan over t counts the keys whose digit
-    // is >= 255 - t within the prefix bucket
-    const int hd = (int)hist[255 - t];
-    int x = hd;
+    };
+    if (in_reg) {
 #pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      const int y = __shfl_up(x, o, 64);
-      if (lane >= o) x += y;
+      for (int u = 0; u < kRegKeys; ++u)
+        if (ib + u * NT < n) count(kv[u]);
+    } else {
+      scan_global(count);
     }
-    if (lane == 63) wtot[w] = x;
     __syncthreads();
-    int before = 0;
-    for (int i = 0; i < w; ++i) before += wtot[i];
-    const int incl = before + x;        // keys with digit >= 255 - t
-    const int above = incl - hd;        // keys with digit > 255 - t
-    if (above < need && incl >= need) {  // exactly one thread: the digit of the k-th key
-      const int dgt = 255 - t;
-      s_prefix = prefix | ((u64)dgt << shift);
-      s_mask = mask | (255ull << shift);
-      s_need = need - above;
-      s_done = (hd == need - above) ? 1 : 0;  // the whole bucket is needed: stop here
+    // threads 0 .. 255 (waves 0 .. 3): thread t holds digit 255 - t; an inclusive scan over t
+    // counts the keys whose digit is >= 255 - t within the prefix bucket
+    int hd = 0, x = 0;
+    if (t < 256) {
+      hd = (int)hist[255 - t];
+      x = hd;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const int y = __shfl_up(x, o, 64);
+        if (lane >= o) x += y;
+      }
+      if (lane == 63) wtot[w] = x;
+    }
+    __syncthreads();
+    if (t < 256) {
+      int before = 0;
+      for (int i = 0; i < w; ++i) before += wtot[i];
+      const int incl = before + x;          // keys with digit >= 255 - t
+      const int above = incl - hd;          // keys with digit > 255 - t
+      if (above < need_d && incl >= need_d) {  // exactly one thread: the digit of the k-th key
+        const int dgt = 255 - t;
+        s_prefix = prefix | ((u64)dgt << shift);
+        s_mask = mask | (255ull << shift);
+        s_need = need_d - above;
+        s_done = (hd == need_d - above) ? 1 : 0;  // the whole bucket is needed: stop here
+      }
     }
     __syncthreads();
   }
   const u64 prefix = s_prefix, mask = s_mask;
-  for (int i = t; i < n; i += kThreads) {
-    const u64 key = src[i];
+  auto gather = [&](u64 key) __attribute__((always_inline)) {
     if ((key & mask) >= prefix) {
       const int slot = atomicAdd(&s_ns, 1);
       if (slot < kMaxK) sel[slot] = key;
     }
+  };
+  if (in_reg) {
+#pragma unroll
+    for (int u = 0; u < kRegKeys; ++u)
+      if (ib + u * NT < n) gather(kv[u]);
+  } else {
+    scan_global(gather);
   }
   __syncthreads();
   const int ns = min(s_ns, k);  // == min(k, n)
@@ -1651,7 +1740,7 @@ __global__ __launch_bounds__(kThreads) void select_topk_kernel(const unsigned lo
     out_ids[(long long)q * k + rank] = (long long)comp_row(key);
     out_scores[(long long)q * k + rank] = comp_score(key);
   }
-  for (int r = ns + t; r < k; r += kThreads) {
+  for (int r = ns + t; r < k; r += NT) {
     out_ids[(long long)q * k + r] = -1ll;
     out_scores[(long long)q * k + r] = kNegInf;
   }
@@ -2188,7 +2277,7 @@ hipError_t filter_pass(const DensePlan& p, const DenseArgs& a, long long rows, c
   arg.gate = gate;
   hipError_t e = launch_kernel(ki, lp.grid, arg, s, ev0, ev1);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(select_topk_kernel, dim3((unsigned)a.nq), dim3(kThreads), 0, s, cbuf, ccnt, p.fcap, a.k,
+  hipLaunchKernelGGL(select_topk_kernel, dim3((unsigned)a.nq), dim3(kSelThreads), 0, s, cbuf, ccnt, p.fcap, a.k,
                      a.out_scores, a.out_ids, ovf, gate, threshold_only ? 1 : 0);
   return hipGetLastError();
 }
@@ -2277,7 +2366,7 @@ hipError_t launch_weighted_fuse(const float* D, const float* B, long long ld, lo
                                 hipStream_t s) {
   hipLaunchKernelGGL(weighted_fuse_kernel, dim3((unsigned)nq), dim3(kFuseThreads), 0, s, D, B, ld, n, n_lex, mm_d, pd,
                      mm_l, pl, wd, wl, k, cbuf, ccnt);
-  hipLaunchKernelGGL(select_topk_kernel, dim3((unsigned)nq), dim3(kThreads), 0, s, cbuf, ccnt, n, k, out_scores, out_ids,
+  hipLaunchKernelGGL(select_topk_kernel, dim3((unsigned)nq), dim3(kSelThreads), 0, s, cbuf, ccnt, n, k, out_scores, out_ids,
                      nullptr, nullptr, 0);
   return hipGetLastError();
 }
