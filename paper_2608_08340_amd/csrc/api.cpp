@@ -698,7 +698,7 @@ oprag_status oprag_search_hybrid_weighted(const oprag_index* idx, const void* q_
   if (e == hipSuccess)
     e = oprag::launch_sparse_dump(idx->sp, qterm_indptr_dev, qterms_dev, (int)nq, B, ld, mm_l, idx->n_rows, s);
   if (e == hipSuccess)
-    e = oprag::launch_weighted_fuse(D, B, ld, idx->n_rows, std::min<long long>(idx->sp.n_docs, idx->n_rows), (int)nq,
+    e = oprag::launch_weighted_fuse(idx->n_cus, D, B, ld, idx->n_rows, std::min<long long>(idx->sp.n_docs, idx->n_rows), (int)nq,
                                     mm_d, p.n_chunks, mm_l, pl, (double)w_dense, (double)w_lex, k, cbuf, ccnt,
                                     scores_dev, reinterpret_cast<long long*>(ids_dev), s);
   if (e != hipSuccess) return hip_fail(e, "weighted fusion launch");

@@ -401,19 +401,18 @@ struct SelOf<BN, KS, 1, NT> {
 // select_topk_kernel.  Candidates of a query are staged in LDS (SCAP keys) and written out
 // with one device-scope reservation per flush.  A staged entry holds the raw score bits and
 // the row; the flush turns it into the key.  LDS: stage [BN][SCAP] | one discard slot per
-// thread | flush bases [BN] | staged counts [BN] | flush flag.
+// thread | flush bases [BN] | staged counts [BN].
 // ------------------------------------------------------------------------------------
 template <int BN>
 struct SelFilter {
   static constexpr int SCAP = 32;
   static constexpr int kTrash = 256;  // threads of the kernels that use it
-  static constexpr int kBytes = BN * SCAP * 8 + kTrash * 8 + BN * 8 + BN * 4 + 16;
+  static constexpr int kBytes = BN * SCAP * 8 + kTrash * 8 + BN * 8 + BN * 4;
   static __device__ __forceinline__ u64* stage(unsigned char* area) { return reinterpret_cast<u64*>(area); }
   static __device__ __forceinline__ u64* trash(unsigned char* area) { return reinterpret_cast<u64*>(area) + BN * SCAP; }
   static __device__ __forceinline__ long long* base(unsigned char* area) {
     return reinterpret_cast<long long*>(area + BN * SCAP * 8 + kTrash * 8);
   }
-  // the BN staged counts, then the flag
   static __device__ __forceinline__ int* staged(unsigned char* area) {
     return reinterpret_cast<int*>(area + BN * SCAP * 8 + kTrash * 8 + BN * 8);
   }
@@ -423,6 +422,10 @@ struct SelFilter {
 };
 template <int BN, int KS, int NT>
 struct SelOf<BN, KS, 2, NT> {
+  typedef SelFilter<BN> type;
+};
+template <int BN, int KS, int NT>
+struct SelOf<BN, KS, 4, NT> {  // filtered, many hits per tile
   typedef SelFilter<BN> type;
 };
 
@@ -477,13 +480,30 @@ __device__ __forceinline__ void dump_tile(const f32x4 (&acc)[MW][BN / 16], long 
   }
 }
 
-// Flush of the staged keys of every query slot whose count reaches `from` (a count beyond SCAP
-// means the rest already went out directly): the owner threads reserve their slots in the
-// global buffers with one device-scope atomic each, all at once; after a barrier every thread
-// copies staged keys, consecutive threads taking consecutive keys of a query.  The flushed
-// counts and the flag are reset; the stage is next written after a later barrier.
+// Staged entry -> key.
+__device__ __forceinline__ u64 staged_key(u64 e) { return composite(__uint_as_float((uint32_t)(e >> 32)), (uint32_t)e); }
+
+// Owner thread of query slot n: append its staged keys (a count beyond SCAP means the rest
+// already went out directly) to the global buffer, with no barrier (a mid-chunk flush).
+template <int BN>
+__device__ __forceinline__ void filt_flush_owner(int n, int q, unsigned char* area, const DenseArgs& a) {
+  constexpr int SCAP = SelFilter<BN>::SCAP;
+  const u64* stage = SelFilter<BN>::stage(area);
+  int* staged = SelFilter<BN>::staged(area);
+  const int c = min(staged[n], SCAP);
+  if (c == 0) return;
+  const long long g = atomicAdd(a.ccnt + q, c);
+  u64* dst = a.cbuf + (long long)q * a.cap;
+  for (int j = 0; j < c; ++j)
+    if (g + j < a.cap) dst[g + j] = staged_key(stage[n * SCAP + j]);
+  staged[n] = 0;
+}
+
+// Flush of every staged key at the end of a chunk: the owner threads reserve their slots in
+// the global buffers with one device-scope atomic each, all at once; after a barrier every
+// thread copies staged keys, consecutive threads taking consecutive keys of a query.
 template <int BN, int NT>
-__device__ __forceinline__ void filt_flush(unsigned char* area, int q0, int q_lim, int from, const DenseArgs& a) {
+__device__ __forceinline__ void filt_flush(unsigned char* area, int q0, int q_lim, const DenseArgs& a) {
   constexpr int SCAP = SelFilter<BN>::SCAP;
   const u64* stage = SelFilter<BN>::stage(area);
   long long* base = SelFilter<BN>::base(area);
@@ -491,32 +511,80 @@ __device__ __forceinline__ void filt_flush(unsigned char* area, int q0, int q_li
   const int tid = threadIdx.x;
   if (tid < BN) {
     const int c = min(staged[tid], SCAP);
-    base[tid] = tid < q_lim && c > 0 && c >= from ? (long long)atomicAdd(a.ccnt + q0 + tid, c) : -1ll;
+    base[tid] = tid < q_lim && c > 0 ? (long long)atomicAdd(a.ccnt + q0 + tid, c) : -1ll;
   }
   lds_barrier();
 #pragma unroll 4
   for (int i = tid; i < BN * SCAP; i += NT) {
     const int n = i / SCAP, j = i % SCAP;
     const long long g = base[n] + j;
-    if (base[n] >= 0 && j < min(staged[n], SCAP) && g < a.cap) {
-      const u64 e = stage[i];
-      a.cbuf[(long long)(q0 + n) * a.cap + g] = composite(__uint_as_float((uint32_t)(e >> 32)), (uint32_t)e);
-    }
+    if (base[n] >= 0 && j < min(staged[n], SCAP) && g < a.cap) a.cbuf[(long long)(q0 + n) * a.cap + g] = staged_key(stage[i]);
   }
-  lds_barrier();
-  if (tid < BN && base[tid] >= 0) staged[tid] = 0;
-  if (tid == 0) staged[BN] = 0;
 }
 
-// Hits of one tile.  Each lane first forms, for every query slot, the mask of its MW*4 scores
-// that reach the threshold, then reserves that many stage slots per slot with hits (one LDS
-// atomic each, all issued before the first result is used).  Every score is then stored
-// without a branch: a hit to its stage slot, any other score to the thread's discard slot.
-// Hits past the stage's end (rare) go straight to the global buffer under one device-scope
-// reservation.  A stage at least half full raises the flush flag.  FULL: the tile lies
-// inside the chunk (no row-limit test).
+// Hits of one tile, few of them (most tiles of a long chunk have none): a lane compares the
+// maximum of its MW*4 scores of a query with the threshold and, on a hit, counts them,
+// reserves that many stage slots with one LDS atomic and writes them; hits past the stage's
+// end go straight to the global buffer under one device-scope reservation.  FULL: the tile
+// lies inside the chunk (no row-limit test).
 template <bool FULL, int BN, int MW>
-__device__ __forceinline__ void filt_collect(const f32x4 (&acc)[MW][BN / 16], const float (&th)[BN / 16],
+__device__ __forceinline__ void filt_collect_sparse(const f32x4 (&acc)[MW][BN / 16], const float (&th)[BN / 16],
+                                                    unsigned char* area, long long tile0, int row0, int lim, int q0,
+                                                    const DenseArgs& a) {
+  constexpr int NW = BN / 16;
+  constexpr int SCAP = SelFilter<BN>::SCAP;
+  u64* stage = SelFilter<BN>::stage(area);
+  int* staged = SelFilter<BN>::staged(area);
+  const int lane = threadIdx.x & 63;
+  const uint32_t row_l = (uint32_t)(tile0 + row0);
+  auto ok = [&](int mi, int r) { return FULL || mi * 16 + r < lim; };
+#pragma unroll
+  for (int ni = 0; ni < NW; ++ni) {
+    float m = kNegInf;
+#pragma unroll
+    for (int mi = 0; mi < MW; ++mi)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) m = __builtin_fmaxf(m, ok(mi, r) ? acc[mi][ni][r] : kNegInf);
+    if (!(m >= th[ni])) continue;
+    int c = 0;
+#pragma unroll
+    for (int mi = 0; mi < MW; ++mi)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) c += (ok(mi, r) && acc[mi][ni][r] >= th[ni]) ? 1 : 0;
+    const int n = ni * 16 + (lane & 15);
+    const int pos = atomicAdd(&staged[n], c);
+    const int in_stage = max(0, min(c, SCAP - pos));
+    const long long g = in_stage < c ? atomicAdd(a.ccnt + q0 + n, c - in_stage) : 0ll;
+    u64* dst_g = a.cbuf + (long long)(q0 + n) * a.cap;
+    int h = 0;
+#pragma unroll
+    for (int mi = 0; mi < MW; ++mi)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float x = acc[mi][ni][r];
+        if (ok(mi, r) && x >= th[ni]) {
+          const uint32_t row = row_l + (uint32_t)(mi * 16 + r);
+          if (h < in_stage) {
+            stage[n * SCAP + pos + h] = ((u64)__float_as_uint(x) << 32) | (u64)row;
+          } else {
+            const long long j = g + (h - in_stage);
+            if (j < a.cap) dst_g[j] = composite(x, row);
+          }
+          ++h;
+        }
+      }
+  }
+}
+
+// Hits of one tile, many of them.  Each lane first forms, for every query slot, the mask of
+// its MW*4 scores that reach the threshold, then reserves that many stage slots per slot with
+// hits (one LDS atomic each, all issued before the first result is used), then stores every
+// score of a slot with hits without a branch: a hit to its stage slot, any other score to the
+// thread's discard slot.  Hits past the stage's end (rare) go straight to the global buffer
+// under one device-scope reservation.  FULL: the tile lies inside the chunk (no row-limit
+// test).
+template <bool FULL, int BN, int MW>
+__device__ __forceinline__ void filt_collect_dense(const f32x4 (&acc)[MW][BN / 16], const float (&th)[BN / 16],
                                              unsigned char* area, long long tile0, int row0, int lim, int q0,
                                              const DenseArgs& a) {
   constexpr int NW = BN / 16;
@@ -527,14 +595,23 @@ __device__ __forceinline__ void filt_collect(const f32x4 (&acc)[MW][BN / 16], co
   u64* trash = SelFilter<BN>::trash(area) + threadIdx.x;
   const int lane = threadIdx.x & 63;
   auto ok = [&](int mi, int r) { return FULL || mi * 16 + r < lim; };
+  // a slot's mask is formed only when the maximum of its scores reaches the threshold (after
+  // the first tiles of a long chunk hits are rare, and a wave then skips whole slots)
   uint32_t bits[NW];
 #pragma unroll
   for (int ni = 0; ni < NW; ++ni) {
-    uint32_t b = 0u;
+    float m = kNegInf;
 #pragma unroll
     for (int mi = 0; mi < MW; ++mi)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) b |= (ok(mi, r) && acc[mi][ni][r] >= th[ni] ? 1u : 0u) << (mi * 4 + r);
+      for (int r = 0; r < 4; ++r) m = __builtin_fmaxf(m, ok(mi, r) ? acc[mi][ni][r] : kNegInf);
+    uint32_t b = 0u;
+    if (m >= th[ni]) {
+#pragma unroll
+      for (int mi = 0; mi < MW; ++mi)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) b |= (ok(mi, r) && acc[mi][ni][r] >= th[ni] ? 1u : 0u) << (mi * 4 + r);
+    }
     bits[ni] = b;
   }
   int pos[NW];
@@ -544,13 +621,12 @@ __device__ __forceinline__ void filt_collect(const f32x4 (&acc)[MW][BN / 16], co
     pos[ni] = c ? atomicAdd(&staged[ni * 16 + (lane & 15)], c) : 0;
   }
   const uint32_t row_l = (uint32_t)(tile0 + row0);
-  bool half = false;
 #pragma unroll
   for (int ni = 0; ni < NW; ++ni) {
     const uint32_t b = bits[ni];
+    if (b == 0u) continue;  // a slot no lane of the wave hits is skipped by the whole wave
     const int c = __popc(b), n = ni * 16 + (lane & 15);
     const int in_stage = max(0, min(c, SCAP - pos[ni]));
-    half = half || (c > 0 && pos[ni] + c >= SCAP / 2);
     u64* st = stage + n * SCAP + pos[ni];
     int h = 0;
 #pragma unroll
@@ -577,7 +653,6 @@ __device__ __forceinline__ void filt_collect(const f32x4 (&acc)[MW][BN / 16], co
           }
     }
   }
-  if (half) staged[BN] = 1;
 }
 
 // First level (no threshold): every row of [0, n_rows) is a candidate, so each score goes to
@@ -606,10 +681,10 @@ __device__ __forceinline__ void filt_all_tile(const f32x4 (&acc)[MW][BN / 16], l
 
 // acc[mi][ni][r] = score of row tile0 + 16*MW*wave + 16*mi + 4*(lane/16) + r against query
 // slot 16*ni + lane%16; th[ni] its threshold (+inf for slots past the batch).  One barrier;
-// then the chunk's last tile flushes every stage, and an earlier tile the stages at least half
-// full (when any is).  The stage is next written in the following tile's selection, after a
-// barrier inside that tile's main loop.
-template <int BN, int MW, int WV>
+// then the chunk's last tile flushes every stage together, and after an earlier tile the
+// owners of stages at least half full flush theirs.  The stage is next written in the
+// following tile's selection, after a barrier inside that tile's main loop.
+template <bool DH, int BN, int MW, int WV>
 __device__ __forceinline__ void filt_tile(const f32x4 (&acc)[MW][BN / 16], const float (&th)[BN / 16],
                                           unsigned char* area, long long tile0, long long row_end, int q0, int q_lim,
                                           bool last, const DenseArgs& a) {
@@ -617,13 +692,23 @@ __device__ __forceinline__ void filt_tile(const f32x4 (&acc)[MW][BN / 16], const
   constexpr int TR = WV * MW * 16;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int row0 = w * MW * 16 + (lane >> 4) * 4;
-  if (tile0 + TR <= row_end)  // workgroup-uniform
-    filt_collect<true, BN, MW>(acc, th, area, tile0, row0, 0, q0, a);
-  else
-    filt_collect<false, BN, MW>(acc, th, area, tile0, row0, (int)(row_end - tile0) - row0, q0, a);
+  const int lim = (int)(row_end - tile0) - row0;
+  if constexpr (DH) {
+    if (tile0 + TR <= row_end)  // workgroup-uniform
+      filt_collect_dense<true, BN, MW>(acc, th, area, tile0, row0, 0, q0, a);
+    else
+      filt_collect_dense<false, BN, MW>(acc, th, area, tile0, row0, lim, q0, a);
+  } else {
+    if (tile0 + TR <= row_end)
+      filt_collect_sparse<true, BN, MW>(acc, th, area, tile0, row0, 0, q0, a);
+    else
+      filt_collect_sparse<false, BN, MW>(acc, th, area, tile0, row0, lim, q0, a);
+  }
   lds_barrier();
-  if (last || SelFilter<BN>::staged(area)[BN] != 0)  // workgroup-uniform
-    filt_flush<BN, WV * 64>(area, q0, q_lim, last ? 1 : SCAP / 2, a);
+  if (last)  // workgroup-uniform
+    filt_flush<BN, WV * 64>(area, q0, q_lim, a);
+  else if (tid < BN && SelFilter<BN>::staged(area)[tid] >= SCAP / 2)
+    filt_flush_owner<BN>(tid, q0 + tid, area, a);
 }
 
 // ------------------------------------------------------------------------------------
@@ -1117,7 +1202,8 @@ __global__ __launch_bounds__(WV * 64) void dense_mfma_kernel(DenseArgs a) {
   // once), so the main loop has no query staging and no barrier.  Otherwise two slots
   // alternate, one super-step ahead.
   constexpr int QBYTES = (QR > 0 ? QR : 2) * QSLOT;
-  static_assert(QR == 0 || SEL == 2, "resident queries: filtered selection only");
+  static_assert(QR == 0 || SEL == 2 || SEL == 4, "resident queries: filtered selection only");
+  constexpr bool kFilt = SEL == 2 || SEL == 4;  // filtered: 4 is the variant for many hits per tile
   // k <= 5: the small-tile kernels take the one-pass rank epilogue (and the running-threshold
   // test for later tiles); the 128-query kernel keeps the block epilogue on every tile, which
   // leaves its main loop the register budget it is scheduled for.
@@ -1155,8 +1241,8 @@ __global__ __launch_bounds__(WV * 64) void dense_mfma_kernel(DenseArgs a) {
 
   Sel sel;
   sel.init();
-  if constexpr (SEL == 2) {
-    if (tid <= BN) SelFilter<BN>::staged(scratch)[tid] = 0;  // counts and flag
+  if constexpr (kFilt) {
+    if (tid < BN) SelFilter<BN>::staged(scratch)[tid] = 0;
     // no barrier needed here: the first tile's epilogue follows several barriers
   }
   float dmn[NW], dmx[NW];  // score dump: this lane's minimum and maximum per query slot
@@ -1322,11 +1408,11 @@ __global__ __launch_bounds__(WV * 64) void dense_mfma_kernel(DenseArgs a) {
       if constexpr (SEL == 3) {
         dump_tile<BN, MW, WV>(acc, tile0, row_end, q0, q_lim, a, dmn, dmx);
         done = true;
-      } else if constexpr (SEL == 2) {
+      } else if constexpr (kFilt) {
         if (a.th == nullptr)  // launch-uniform
           filt_all_tile<BN, MW, WV>(acc, tile0, row_end, q0, q_lim, a);
         else
-          filt_tile<BN, MW, WV>(acc, th, scratch, tile0, row_end, q0, q_lim, t == n_tiles - 1, a);
+          filt_tile<SEL == 4, BN, MW, WV>(acc, th, scratch, tile0, row_end, q0, q_lim, t == n_tiles - 1, a);
         done = true;
       } else if constexpr (SEL == 0) {
         // A chunk's first tile fills the lists through the group path; the tiles after it
@@ -1382,7 +1468,7 @@ __global__ __launch_bounds__(WV * 64) void dense_mfma_kernel(DenseArgs a) {
 #undef OPRAG_QUERIES
 #undef OPRAG_ROWS
   }
-  if constexpr (SEL == 2) {
+  if constexpr (kFilt) {
     if (a.th == nullptr) {
       if (chunk == 0 && tid < q_lim) a.ccnt[q0 + tid] = (int)a.n_rows;  // every row is a candidate
     }  // else the chunk's last tile flushed its stages
@@ -1514,24 +1600,28 @@ __global__ __launch_bounds__(kThreads) void dense_f32_kernel(DenseArgs a) {
 
 // ------------------------------------------------------------------------------------
 // Filtered mode, selection: exact top-k (sorted) of a query's candidate keys.  One workgroup
-// of 1,024 threads per query.  Keys are unique composites (row ids are), so exactly
-// min(k, n) keys qualify.  Buffers of up to 4,096 keys are read once (four keys per thread,
-// all loads in flight) and kept in registers.  The 256 groups of four adjacent threads take
-// their largest key, and tau = the need-th largest of these maxima bounds the need-th best key
-// from below (every maximum is a key of its own); the keys >= tau are ranked exactly.  Too
-// many of them, or larger buffers, take a most-significant-digit radix select (8-bit digits,
-// stopping as soon as a whole bucket is needed).
+// of NT threads per query: 1,024 when one round of workgroups covers the batch (the query's
+// latency counts), 256 for larger batches (more queries per CU at once).  Keys are unique
+// composites (row ids are), so exactly min(k, n) keys qualify.  Buffers of up to 4,096 keys
+// are read once (all loads in flight) and kept in registers.  The 256 groups of NT / 256
+// adjacent threads take their largest key, and tau = the need-th largest of these maxima
+// bounds the need-th best key from below (every maximum is a key of its own); the keys >= tau
+// are ranked exactly.  Too many of them, or larger buffers, take a most-significant-digit
+// radix select (8-bit digits, stopping as soon as a whole bucket is needed).
 // ------------------------------------------------------------------------------------
-constexpr int kSelThreads = 1024;
-__global__ __launch_bounds__(kSelThreads) void select_topk_kernel(const unsigned long long* __restrict__ cbuf,
-                                                                  int* __restrict__ ccnt, long long cap, int k,
-                                                                  float* out_scores, long long* out_ids, int* overflow,
-                                                                  const int* gate, int threshold_only) {
-  constexpr int NT = kSelThreads;
+template <int NT>
+__global__ __launch_bounds__(NT) void select_topk_kernel(const unsigned long long* __restrict__ cbuf,
+                                                         int* __restrict__ ccnt, long long cap, int k,
+                                                         float* out_scores, long long* out_ids, int* overflow,
+                                                         const int* gate, int threshold_only) {
   constexpr int kCand = 1024;  // candidates the threshold path ranks directly
-  constexpr int kRegKeys = 4;
+  constexpr int kRegKeys = 4096 / NT;
+  constexpr int GS = NT / 256;        // threads per group
+  constexpr int GB = 256 / GS;        // group maxima each thread of a group counts over
+  constexpr int GST = GB + 2;         // block stride: the GS blocks start in different banks
+  static_assert(NT == 256 || NT == 1024, "workgroup size");
   __shared__ u64 cand[kCand];
-  __shared__ __attribute__((aligned(16))) u64 gmax[4 * 66];  // four blocks of 64 group maxima, 66 apart
+  __shared__ __attribute__((aligned(16))) u64 gmax[GS * GST];
   __shared__ u64 s_tau;
   __shared__ int s_nc;
   __shared__ unsigned int hist[256];
@@ -1558,9 +1648,9 @@ __global__ __launch_bounds__(kSelThreads) void select_topk_kernel(const unsigned
   if (t == 0) ccnt[q] = 0;  // every thread has read it: the next pass starts from zero
   const int need = min(k, n);
   const bool in_reg = n <= kRegKeys * NT;  // workgroup-uniform
-  // Register keys: thread t holds keys ib + 1,024 u, where ib puts the first 256 keys in 256
+  // Register keys: thread t holds keys ib + NT u, where ib puts the first 256 keys in 256
   // different groups, so at least min(n, 256) >= need groups are nonempty.
-  const int ib = (t >> 2) + 256 * (t & 3);
+  const int ib = t / GS + 256 * (t % GS);
   u64 kv[kRegKeys];
   if (in_reg) {
 #pragma unroll
@@ -1588,18 +1678,18 @@ __global__ __launch_bounds__(kSelThreads) void select_topk_kernel(const unsigned
     } else {
       scan_global([&](u64 x) { m = umax64(m, x); });
     }
-    m = umax64(m, shfl_xor64(m, 1));
-    m = umax64(m, shfl_xor64(m, 2));
-    const int grp = t >> 2, sub = t & 3;
-    if (sub == 0) gmax[(grp >> 6) * 66 + (grp & 63)] = m;
+#pragma unroll
+    for (int o = 1; o < GS; o <<= 1) m = umax64(m, shfl_xor64(m, o));
+    const int grp = t / GS, sub = t % GS;
+    if (sub == 0) gmax[(grp / GB) * GST + grp % GB] = m;
     __syncthreads();
-    // each of the group's four threads counts the larger maxima in a quarter of the list
+    // each of the group's threads counts the larger maxima in its share of the list
     int gt = 0;
-    const u64* blk = gmax + sub * 66;
+    const u64* blk = gmax + sub * GST;
 #pragma unroll 16
-    for (int u = 0; u < 64; ++u) gt += blk[u] > m ? 1 : 0;
-    gt += __shfl_xor(gt, 1);
-    gt += __shfl_xor(gt, 2);
+    for (int u = 0; u < GB; ++u) gt += blk[u] > m ? 1 : 0;
+#pragma unroll
+    for (int o = 1; o < GS; o <<= 1) gt += __shfl_xor(gt, o);
     // nonzero maxima are unique, and at least need groups hold keys
     if (sub == 0 && m != 0ull && gt == need - 1) s_tau = m;
     __syncthreads();
@@ -2063,7 +2153,12 @@ struct KernelInfo {
       MFK(DT, 1, 1, 16, 1, 5, 2, 8, 1, 16), MFK(DT, 1, 1, 4, 1, 5, 2, 8, 1, 16),                     \
       MFK(DT, 4, 2, 8, 1, 5, 2, 4, 17, 64), MFK(DT, 4, 2, 4, 1, 5, 2, 4, 17, 64),                    \
       MFKQ(DT, 8, 4, 4, 1, 5, 2, 2, 65, 1 << 30, kWaves, 3), MFK(DT, 8, 4, 4, 1, 5, 2, 2, 65, 1 << 30), \
-      MFK(DT, 8, 4, 4, 1, 5, 3, 2, 1, 1 << 30)
+      MFK(DT, 8, 4, 4, 1, 5, 3, 2, 1, 1 << 30), MF_DH(DT)
+// Filtered kernels for levels with many hits per tile (SEL 4), one per SEL 2 shape.
+#define MF_DH(DT)                                                                                          \
+  MFK(DT, 1, 1, 16, 1, 5, 4, 8, 1, 16), MFK(DT, 1, 1, 4, 1, 5, 4, 8, 1, 16), MFK(DT, 4, 2, 8, 1, 5, 4, 4, 17, 64), \
+      MFK(DT, 4, 2, 4, 1, 5, 4, 4, 17, 64), MFKQ(DT, 8, 4, 4, 1, 5, 4, 2, 65, 1 << 30, kWaves, 3),               \
+      MFK(DT, 8, 4, 4, 1, 5, 4, 2, 65, 1 << 30)
 
 const KernelInfo kKernels[] = {
     {dense_f32_kernel<5, 0>, kDtypeF32, 32, 64, 5, 0, 4, 1, 1 << 30, 0, kThreads, 0},
@@ -2247,16 +2342,40 @@ hipError_t launch_kernel(const KernelInfo& ki, long long grid, DenseArgs& arg, h
                                s);
 }
 
-// One filtered level: clear the counts, collect candidates, select.
+// The many-hits variant (SEL 4) of filtered kernel i: the same shape, or i itself.
+int dense_hits_twin(int i) {
+  const KernelInfo& a = kKernels[i];
+  for (int j = 0; j < kNumKernels; ++j) {
+    const KernelInfo& b = kKernels[j];
+    if (b.sel == 4 && b.dtype == a.dtype && b.bn == a.bn && b.tile_rows == a.tile_rows && b.ring == a.ring &&
+        b.threads == a.threads && b.qres == a.qres && b.min_nq == a.min_nq && b.max_nq == a.max_nq)
+      return j;
+  }
+  return i;
+}
+
+// Exact top-k of each query's candidate buffer (threshold_only: just a valid k-th score).
+void launch_select(int n_cus, const unsigned long long* cbuf, int* ccnt, long long cap, int nq, int k, float* out_scores,
+                   long long* out_ids, int* ovf, const int* gate, bool threshold_only, hipStream_t s) {
+  if (nq <= 2 * n_cus)
+    hipLaunchKernelGGL(select_topk_kernel<1024>, dim3((unsigned)nq), dim3(1024), 0, s, cbuf, ccnt, cap, k, out_scores,
+                       out_ids, ovf, gate, threshold_only ? 1 : 0);
+  else
+    hipLaunchKernelGGL(select_topk_kernel<256>, dim3((unsigned)nq), dim3(256), 0, s, cbuf, ccnt, cap, k, out_scores,
+                       out_ids, ovf, gate, threshold_only ? 1 : 0);
+}
+
 // One filter pass over rows [0, rows): candidates >= th (every row when th is null) into the
 // buffers, then the exact top-k of each buffer (threshold_only: just a valid k-th score for
-// the next level).  The first pass (th null) sets the counts;
-// each selection zeroes its query's count for the next pass.  With a gate, nothing runs
-// unless *gate != 0.
-hipError_t filter_pass(const DensePlan& p, const DenseArgs& a, long long rows, const float* th, int* ovf,
-                       const int* gate, bool threshold_only, bool first, hipStream_t s, hipEvent_t ev0,
+// the next level).  The first pass (th null) sets the counts; each selection zeroes its
+// query's count for the next pass.  prev_rows: the rows of the prefix th comes from (about
+// k / prev_rows of the rows are hits).  With a gate, nothing runs unless *gate != 0.
+hipError_t filter_pass(const DensePlan& p, const DenseArgs& a, long long rows, const float* th, long long prev_rows,
+                       int* ovf, const int* gate, bool threshold_only, bool first, hipStream_t s, hipEvent_t ev0,
                        hipEvent_t ev1) {
-  const KernelInfo& ki = kKernels[first ? p.kernel0 : p.kernel];
+  // about k / prev_rows of the rows are hits: from 1 in 64 on, the many-hits variant
+  const int kidx = first ? p.kernel0 : p.kernel;
+  const KernelInfo& ki = kKernels[th != nullptr && 64ll * a.k >= prev_rows ? dense_hits_twin(kidx) : kidx];
   unsigned long long* cbuf = a.partial;  // the workspace
   int* ccnt = reinterpret_cast<int*>(reinterpret_cast<unsigned char*>(cbuf) +
                                      align_up256((size_t)a.nq * (size_t)p.fcap * 8));
@@ -2277,8 +2396,7 @@ hipError_t filter_pass(const DensePlan& p, const DenseArgs& a, long long rows, c
   arg.gate = gate;
   hipError_t e = launch_kernel(ki, lp.grid, arg, s, ev0, ev1);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(select_topk_kernel, dim3((unsigned)a.nq), dim3(kSelThreads), 0, s, cbuf, ccnt, p.fcap, a.k,
-                     a.out_scores, a.out_ids, ovf, gate, threshold_only ? 1 : 0);
+  launch_select(p.n_cus, cbuf, ccnt, p.fcap, a.nq, a.k, a.out_scores, a.out_ids, ovf, gate, threshold_only, s);
   return hipGetLastError();
 }
 
@@ -2296,7 +2414,7 @@ hipError_t launch_dense(const DensePlan& p, int dtype, const DenseArgs& a, hipSt
       const bool last = l == p.n_levels - 1;
       // level l's threshold: a lower bound of the k-th score over level l - 1's rows
       hipError_t e = filter_pass(p, a, p.level_rows[l], l == 0 ? nullptr : a.out_scores + (a.k - 1),
-                                 fl ? fl + (last ? 0 : 1) : nullptr,
+                                 l == 0 ? 0 : p.level_rows[l - 1], fl ? fl + (last ? 0 : 1) : nullptr,
                                  nullptr, !last, l == 0, s, last ? ev0 : nullptr, last ? ev1 : nullptr);
       if (e != hipSuccess) return e;
     }
@@ -2307,7 +2425,7 @@ hipError_t launch_dense(const DensePlan& p, int dtype, const DenseArgs& a, hipSt
     // their k-th scores are valid thresholds and no lower), and if that overflows too, the
     // per-chunk-list plan runs.  Each repair launch returns at once when its flag is clear.
     hipError_t e =
-        filter_pass(p, a, a.n_rows, a.out_scores + (a.k - 1), fl + 2, fl, false, false, s, nullptr, nullptr);
+        filter_pass(p, a, a.n_rows, a.out_scores + (a.k - 1), a.n_rows, fl + 2, fl, false, false, s, nullptr, nullptr);
     if (e != hipSuccess) return e;
     const DensePlan lp = plan_dense_lists(dtype, a.d, a.n_rows, a.nq, a.k, p.n_cus);
     DenseArgs la = a;
@@ -2360,14 +2478,13 @@ hipError_t launch_dense_dump(const DensePlan& p, const DenseArgs& a, hipStream_t
   return launch_kernel(kKernels[p.kernel], p.grid, arg, s, nullptr, nullptr);
 }
 
-hipError_t launch_weighted_fuse(const float* D, const float* B, long long ld, long long n, long long n_lex, int nq,
+hipError_t launch_weighted_fuse(int n_cus, const float* D, const float* B, long long ld, long long n, long long n_lex, int nq,
                                 const float* mm_d, int pd, const float* mm_l, int pl, double wd, double wl, int k,
                                 unsigned long long* cbuf, int* ccnt, float* out_scores, long long* out_ids,
                                 hipStream_t s) {
   hipLaunchKernelGGL(weighted_fuse_kernel, dim3((unsigned)nq), dim3(kFuseThreads), 0, s, D, B, ld, n, n_lex, mm_d, pd,
                      mm_l, pl, wd, wl, k, cbuf, ccnt);
-  hipLaunchKernelGGL(select_topk_kernel, dim3((unsigned)nq), dim3(kSelThreads), 0, s, cbuf, ccnt, n, k, out_scores, out_ids,
-                     nullptr, nullptr, 0);
+  launch_select(n_cus, cbuf, ccnt, n, nq, k, out_scores, out_ids, nullptr, nullptr, false, s);
   return hipGetLastError();
 }
 

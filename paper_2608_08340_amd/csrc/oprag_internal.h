@@ -78,7 +78,7 @@ hipError_t launch_dense_dump(const DensePlan& p, const DenseArgs& a, hipStream_t
 // Weighted fusion of dense scores D and lexical scores B ([nq x ld], lexical 0 past n_lex),
 // min-max normalised per query over n chunks, then the exact top k (cbuf [nq x n], ccnt [nq]).
 // The minima and maxima come from the dumps' partials mm_d [nq x pd x 2] and mm_l [nq x pl x 2].
-hipError_t launch_weighted_fuse(const float* D, const float* B, long long ld, long long n, long long n_lex, int nq,
+hipError_t launch_weighted_fuse(int n_cus, const float* D, const float* B, long long ld, long long n, long long n_lex, int nq,
                                 const float* mm_d, int pd, const float* mm_l, int pl, double wd, double wl, int k,
                                 unsigned long long* cbuf, int* ccnt, float* out_scores, long long* out_ids,
                                 hipStream_t s);
