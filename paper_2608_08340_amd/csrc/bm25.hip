@@ -204,24 +204,32 @@ __global__ __launch_bounds__(kBT) void bm25_kernel(SparseArgs a) {
   auto own = [&](int j) { return 4 * tid + kLayer * (j >> 2) + (j & 3); };  // j < 32
 
   const int tb = a.qterm_indptr[q], te = a.qterm_indptr[q + 1];
+  // With one range (a term's whole posting list is the range's) the parse pass also finds the
+  // posting bounds of the tail terms among the first kTermBatch occurrences, so the first of
+  // them is loading while the head rows are summed.
+  const bool early = a.n_ranges == 1;
+  // A term that occurs m times in the query takes part once, at its first occurrence, with
+  // factor m * idf(t) (k1 + 1); unknown terms match nothing.
   // 1. head terms, from their dense rows.  The query's distinct head terms are listed in
-  // first-occurrence order (in the candidate area, unused until the selection), each with
-  // factor m * idf(t) (k1 + 1) for its m occurrences; then every thread sums, term after term,
-  // the rows over its own chunks in registers.  A row holds 0 where the term is absent and
-  // fma(f, 0, s) = s, so these are exactly the fp32 operations of walking the terms' postings,
-  // without searches, scattered LDS updates or barriers.
-  {
-    int* hl_row = reinterpret_cast<int*>(cand);               // [kMaxHead]
-    float* hl_wt = reinterpret_cast<float*>(cand) + kMaxHead;  // [kMaxHead]
-    static_assert(2 * kMaxHead * 4 <= kCandCap * 8, "the head list fits the candidate area");
-    int nh = 0;
-    for (int j0 = tb; j0 < te; j0 += kBT) {
-      const int j = j0 + tid;
-      int row = -1;
-      float wt = 0.f;
-      if (j < te) {
-        const int t = a.qterms[j];
-        if (t >= 0 && t < a.vocab && a.hidx[t] >= 0) {
+  // first-occurrence order (in the candidate area, unused until the selection); then every
+  // thread sums, term after term, the rows over its own chunks in registers.  A row holds 0
+  // where the term is absent and fma(f, 0, s) = s, so these are exactly the fp32 operations of
+  // walking the terms' postings, without searches, scattered LDS updates or barriers.
+  int* hl_row = reinterpret_cast<int*>(cand);               // [kMaxHead]
+  float* hl_wt = reinterpret_cast<float*>(cand) + kMaxHead;  // [kMaxHead]
+  static_assert(2 * kMaxHead * 4 <= kCandCap * 8, "the head list fits the candidate area");
+  int nh = 0;
+  for (int j0 = tb; j0 < te; j0 += kBT) {
+    const int j = j0 + tid;
+    int row = -1;
+    float wt = 0.f;
+    long long tlo = 0, thi = 0;
+    float twt = 0.f;
+    if (j < te) {
+      const int t = a.qterms[j];
+      if (t >= 0 && t < a.vocab) {
+        const int h = a.hidx[t];
+        if (h >= 0 || (early && j < tb + kTermBatch)) {
           bool earlier = false;
           int mult = 0;
           for (int jj = tb; jj < te; ++jj)
@@ -230,22 +238,62 @@ __global__ __launch_bounds__(kBT) void bm25_kernel(SparseArgs a) {
               else ++mult;
             }
           if (!earlier) {
-            row = a.hidx[t];
-            wt = a.idfk[t] * (float)mult;
+            if (h >= 0) {
+              row = h;
+              wt = a.idfk[t] * (float)mult;
+            } else {
+              tlo = a.indptr[t];
+              thi = a.indptr[t + 1];
+              twt = a.idfk[t] * (float)mult;
+            }
           }
         }
       }
-      const int f = row >= 0 ? 1 : 0;
-      const int pos = nh + block_excl_scan(f, wave_tot);
-      if (f) {  // distinct head terms <= kMaxHead
-        hl_row[pos] = row;
-        hl_wt[pos] = wt;
-      }
-      if (tid == kBT - 1) s_nc = pos + f;  // the count so far, shared
-      __syncthreads();
-      nh = s_nc;
-      __syncthreads();
     }
+    if (early && j0 == tb && tid < kTermBatch) {
+      s_lo[tid] = tlo;
+      s_hi[tid] = thi;
+      s_wt[tid] = twt;
+    }
+    const int f = row >= 0 ? 1 : 0;
+    const int pos = nh + block_excl_scan(f, wave_tot);
+    if (f) {  // distinct head terms <= kMaxHead
+      hl_row[pos] = row;
+      hl_wt[pos] = wt;
+    }
+    if (tid == kBT - 1) s_nc = pos + f;  // the count so far, shared
+    __syncthreads();
+    nh = s_nc;
+    __syncthreads();
+  }
+
+  // Tail postings, four per thread per step with every load issued before the first update.
+  auto load_step = [&](long long p, long long hi, int (&c)[4], float (&wp)[4]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const long long pu = p + (long long)u * kBT;
+      c[u] = pu < hi ? a.chunk[pu] - (int)d0 : -1;
+      wp[u] = pu < hi ? a.wpost[pu] : 0.f;
+    }
+  };
+  auto apply_step = [&](float wt, const int (&c)[4], const float (&wp)[4]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (c[u] >= 0) acc[c[u]] = __builtin_fmaf(wt, wp[u], acc[c[u]]);
+  };
+  auto next_term = [&](int g, int ng) {  // the first term from g on with postings (uniform)
+    while (g < ng && !(s_lo[g] < s_hi[g])) ++g;
+    return g;
+  };
+  int pc[4] = {-1, -1, -1, -1};  // the first step of the next tail term, in flight
+  float pw[4] = {0.f, 0.f, 0.f, 0.f};
+  int g_first = 0;
+  if (early) {
+    g_first = next_term(0, min(kTermBatch, te - tb));
+    if (g_first < min(kTermBatch, te - tb)) load_step(s_lo[g_first] + tid, s_hi[g_first], pc, pw);
+  }
+
+  {
     f32x4 hs[8];
 #pragma unroll
     for (int g = 0; g < 8; ++g) hs[g] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -283,20 +331,23 @@ __global__ __launch_bounds__(kBT) void bm25_kernel(SparseArgs a) {
     __syncthreads();  // the accumulator is complete; the head list area is free again
   }
 
-  // 2. the other (tail) terms, from their postings
+  // 2. the other (tail) terms, from their postings, one term after another (a term's postings
+  // name distinct chunks: no atomics); the first step of the next term is loading while the
+  // current one is added.
   for (int j0 = tb; j0 < te; j0 += kTermBatch) {
-    // posting bounds of up to kTermBatch terms at once, 32 threads per term.  A term that
-    // occurs m times in the query is walked once, at its first occurrence, with weight
-    // m * idf(t) * (k1 + 1); its later occurrences walk nothing.
-    {
-      const int g = tid >> 5, sub = tid & 31;
-      const int j = j0 + g;
+    const int ng = min(kTermBatch, te - j0);
+    int g = g_first;
+    if (!(early && j0 == tb)) {
+      // posting bounds of up to kTermBatch terms at once, 32 threads per term
+      __syncthreads();  // every thread is done with the previous batch's bounds
+      const int gg = tid >> 5, sub = tid & 31;
+      const int j = j0 + gg;
       static_assert(kTermBatch * 32 == kBT, "32 threads per term");
       long long lo = 0, hi = 0;
       float wt = 0.f;
       if (j < te) {  // uniform over the group's 32 threads
         const int t = a.qterms[j];
-        if (t >= 0 && t < a.vocab) {  // unknown terms match nothing
+        if (t >= 0 && t < a.vocab) {
           int earlier = 0, mult = 0;
           for (int jj = tb + sub; jj < te; jj += 32)
             if (a.qterms[jj] == t) {
@@ -317,33 +368,35 @@ __global__ __launch_bounds__(kBT) void bm25_kernel(SparseArgs a) {
         }
       }
       if (sub == 0) {
-        s_lo[g] = lo;
-        s_hi[g] = hi;
-        s_wt[g] = wt;
+        s_lo[gg] = lo;
+        s_hi[gg] = hi;
+        s_wt[gg] = wt;
       }
+      __syncthreads();
+      g = next_term(0, ng);
+      if (g < ng) load_step(s_lo[g] + tid, s_hi[g], pc, pw);
     }
-    __syncthreads();
-    // one term after another (a term's postings name distinct chunks: no atomics); four
-    // postings per thread per step, all loads issued before the first update
-    for (int g = 0; g < kTermBatch && j0 + g < te; ++g) {
+    while (g < ng) {  // workgroup-uniform
       const long long lo = s_lo[g], hi = s_hi[g];
-      if (lo < hi) {  // workgroup-uniform
-        const float wt = s_wt[g];
-        for (long long p = lo + tid; p < hi; p += 4 * kBT) {
-          int c[4];
-          float wp[4];
-#pragma unroll
-          for (int u = 0; u < 4; ++u) {
-            const long long pu = p + (long long)u * kBT;
-            c[u] = pu < hi ? a.chunk[pu] - (int)d0 : -1;
-            wp[u] = pu < hi ? a.wpost[pu] : 0.f;
-          }
-#pragma unroll
-          for (int u = 0; u < 4; ++u)
-            if (c[u] >= 0) acc[c[u]] = __builtin_fmaf(wt, wp[u], acc[c[u]]);
-        }
-        __syncthreads();
+      const float wt = s_wt[g];
+      const int gn = next_term(g + 1, ng);
+      int nc[4] = {-1, -1, -1, -1};
+      float nw[4] = {0.f, 0.f, 0.f, 0.f};
+      if (gn < ng) load_step(s_lo[gn] + tid, s_hi[gn], nc, nw);
+      apply_step(wt, pc, pw);
+      for (long long p = lo + tid + 4 * kBT; p < hi; p += 4 * kBT) {
+        int c[4];
+        float wp[4];
+        load_step(p, hi, c, wp);
+        apply_step(wt, c, wp);
       }
+      __syncthreads();
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        pc[u] = nc[u];
+        pw[u] = nw[u];
+      }
+      g = gn;
     }
   }
   __syncthreads();
