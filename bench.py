@@ -62,8 +62,8 @@ def cpu_model() -> str:
     return platform.processor() or "unknown"
 
 
-def kernel_source_sha() -> str:
-    return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
+def kernel_source_sha(name: str = "dense.hip") -> str:
+    return hashlib.sha256(open(os.path.join(os.path.dirname(KERNEL_SRC), name), "rb").read()).hexdigest()[:16]
 
 
 def algorithmic_bytes(n_rows: int, dim: int, batch: int, k: int, elem: int = 2) -> int:
@@ -189,16 +189,30 @@ PMC_WORKLOADS = {
     "b1024": {"title": "32,768 x 1,024 bf16, batch 1,024, top-5 (8 cold slabs)", "n": N_ROWS, "d": DIM,
               "batch": 1024, "k": 5},
     "c4": {"title": "1,048,576 x 768 bf16, batch 1,024, top-10", "n": 1 << 20, "d": 768, "batch": 1024, "k": 10},
+    "bm25": {"title": "BM25 top-100 over the 32,768-chunk Zipf corpus (head rows and tail postings), batch 256, "
+                      "8 searches on one index", "kernel": "bm25_kernel", "groups": ("fetch", "write", "l2"),
+             "file": "bm25_32k_zipf_b256_counters.txt", "batch": 256, "k": 100},
 }
 
 
 def pmc_file(name: str) -> str:
-    return os.path.join(ROOT, "profiles", f"dense_scoring_{name}_counters.txt")
+    return os.path.join(ROOT, "profiles", PMC_WORKLOADS[name].get("file", f"dense_scoring_{name}_counters.txt"))
+
+
+def pmc_groups(name: str) -> dict:
+    return {g: PMC_GROUPS[g] for g in PMC_WORKLOADS[name].get("groups", PMC_GROUPS)}
+
+
+def bm25_algorithmic_bytes(hw) -> int:
+    """Distinct postings of the batch's terms (chunk id + weight, 8 bytes each), one 4-byte
+    statistic per chunk and per term offset: each read once."""
+    postings = int(sum(int(hw.csr.term_indptr[u + 1] - hw.csr.term_indptr[u]) for u in set(hw.qterms.tolist())))
+    return postings * 8 + 4 * N_ROWS + 4 * hw.csr.term_indptr.size
 
 
 def pmc_command(name: str) -> str:
     parts = [f"timeout -s KILL 120 rocprofv3 --pmc {c} --output-format csv -d $GRAFT_REPO_ROOT/gpurun_out/pmc_{name}/{g} "
-             f"-- python3 $GRAFT_REPO_ROOT/bench.py --pmc-workload {name}" for g, c in PMC_GROUPS.items()]
+             f"-- python3 $GRAFT_REPO_ROOT/bench.py --pmc-workload {name}" for g, c in pmc_groups(name).items()]
     return ("cd /tmp && export TMPDIR=/tmp && " + " && ".join(parts) +
             f" && python3 $GRAFT_REPO_ROOT/bench.py --pmc-workload {name} --pmc-summarize $GRAFT_REPO_ROOT/gpurun_out/pmc_{name}")
 
@@ -215,6 +229,20 @@ def pmc_workload_run(name: str) -> int:
     ref = Index(DIM, COPY_ROWS, torch.bfloat16)
     ref.upsert(torch.zeros((COPY_ROWS, DIM), dtype=torch.bfloat16, device=dev))
     torch.cuda.synchronize()
+    if name == "bm25":
+        import numpy as np
+        hw = synth.hybrid_32k()
+        t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+        ix = Index(DIM, N_ROWS, torch.bfloat16)
+        ix.upsert(hw.dense.rows.to(dev))
+        ix.attach_sparse(t(hw.csr.term_indptr), t(hw.csr.post_chunk), t(hw.csr.post_tf), t(hw.csr.doc_len))
+        qi, qt = t(hw.qterm_indptr), t(hw.qterms)
+        torch.cuda.synchronize()
+        for _ in range(8):
+            ix.search_sparse(qi, qt, wl["k"])
+        torch.cuda.synchronize()
+        print("pmc workload done", flush=True)
+        return 0
     if name == "c4":
         w = synth.mixture_dense(4, wl["n"], wl["d"], 4096, wl["batch"], wl["k"], "bf16")
         idxs = [Index(wl["d"], wl["n"], torch.bfloat16)]
@@ -235,9 +263,10 @@ def pmc_workload_run(name: str) -> int:
 
 
 def pmc_workload_summarize(name: str, out_dir: str) -> int:
-    """Per-dispatch counter values of the scoring kernel (median over its dispatches) and the
+    """Per-dispatch counter values of the workload's kernel (median over its dispatches) and the
     derived HBM bytes, L2 hit rate and MFMA utilisation, written under profiles/."""
     wl = PMC_WORKLOADS[name]
+    kernel = wl.get("kernel", "dense_mfma_kernel")
     vals, copy, durs = {}, {}, []
     agent = {}
     for f in glob.glob(os.path.join(out_dir, "**", "*agent_info.csv"), recursive=True):
@@ -247,7 +276,7 @@ def pmc_workload_summarize(name: str, out_dir: str) -> int:
         break
     n_xcc = int(agent.get("Num_Xcc", 8) or 8)
     n_simd = int(agent.get("Cu_Count", 256) or 256) * int(agent.get("Simd_Per_Cu", 4) or 4)
-    for g in PMC_GROUPS:
+    for g in pmc_groups(name):
         files = glob.glob(os.path.join(out_dir, g, "**", "*counter_collection.csv"), recursive=True)
         if len(files) != 1:
             print(f"{g}: expected one counter file under {out_dir}/{g}, found {len(files)}", file=sys.stderr)
@@ -260,23 +289,29 @@ def pmc_workload_summarize(name: str, out_dir: str) -> int:
             agg = max(v) if cname == "GRBM_GUI_ACTIVE" else sum(v)
             if "copy16_kernel" in kname:
                 copy.setdefault(cname, []).append((disp, agg))
-            elif "dense_mfma_kernel" in kname:
+            elif kernel in kname:
                 vals.setdefault(cname, []).append(agg)
         if g == "mfma":
             for r in csv.DictReader(open(files[0])):
-                if "dense_mfma_kernel" in r["Kernel_Name"] and r["Counter_Name"] == "GRBM_GUI_ACTIVE":
+                if kernel in r["Kernel_Name"] and r["Counter_Name"] == "GRBM_GUI_ACTIVE":
                     durs.append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
     med = {c: float(np.median(v)) for c, v in vals.items()}
     n_disp = {c: len(v) for c, v in vals.items()}
     ref = {c: min(v)[1] for c, v in copy.items()}  # the pass's first copy is the reference
-    lines = [f"rocprofv3 counters of the dense scoring kernel (dense_mfma_kernel), {wl['title']}",
+    src = "bm25.hip" if kernel == "bm25_kernel" else "dense.hip"
+    lines = [f"rocprofv3 counters of {kernel}, {wl['title']}",
              f"command: {pmc_command(name)}",
-             f"kernel source sha256[:16] of dense.hip: {kernel_source_sha()}", "",
+             f"kernel source sha256[:16] of {src}: {kernel_source_sha(src)}", "",
              "median per dispatch (dispatches counted):"]
     for c in sorted(med):
         lines.append(f"  {c:32s} {med[c]:16.1f}   ({n_disp[c]})")
-    abytes = algorithmic_bytes(wl["n"], wl["d"], wl["batch"], wl["k"])
-    flops = 2.0 * wl["batch"] * wl["n"] * wl["d"]
+    if kernel == "bm25_kernel":
+        import synth
+        abytes = bm25_algorithmic_bytes(synth.hybrid_32k())
+        flops = 0.0
+    else:
+        abytes = algorithmic_bytes(wl["n"], wl["d"], wl["batch"], wl["k"])
+        flops = 2.0 * wl["batch"] * wl["n"] * wl["d"]
     lines.append("derived:")
     copy_kib = COPY_ROWS * DIM * 2 / 1024.0
     if "FETCH_SIZE" in med and "WRITE_SIZE" in med and "FETCH_SIZE" in ref and "WRITE_SIZE" in ref:
@@ -297,7 +332,7 @@ def pmc_workload_summarize(name: str, out_dir: str) -> int:
                          f"active cycles / duration = {gui / d_us / 1e3:.3f} GHz")
         lines.append(f"  MFMA utilisation SQ_VALU_MFMA_BUSY_CYCLES / (cycles per XCD x {n_simd} SIMDs): "
                      f"{med['SQ_VALU_MFMA_BUSY_CYCLES'] / (gui * n_simd):.4f}")
-    if "SQ_INSTS_VALU_MFMA_MOPS_BF16" in med:
+    if "SQ_INSTS_VALU_MFMA_MOPS_BF16" in med and flops:
         lines.append(f"  MFMA flops SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512: {med['SQ_INSTS_VALU_MFMA_MOPS_BF16'] * 512:.4g} "
                      f"(algorithmic 2 B N d = {flops:.4g})")
     out = pmc_file(name)

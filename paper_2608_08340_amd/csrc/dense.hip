@@ -1362,12 +1362,21 @@ __global__ __launch_bounds__(WV * 64) void dense_mfma_kernel(DenseArgs a) {
 
     int qsi = 0;  // resident queries: slot of the current super-step
     if constexpr (QR > 0) {
-      // prologue: every super-step of the queries into its own slot, then rows of k-steps
-      // 0 .. PX-1
-      for (int u = 0; u < nq4; ++u) {
-        OPRAG_QUERIES()
+      // prologue: every super-step of the queries into its own slot (QB super-steps' loads in
+      // flight at once), then rows of k-steps 0 .. PX-1
+      constexpr int QB = QPT >= 8 ? 1 : 8 / QPT;
+      for (int u0 = 0; u0 < nq4; u0 += QB) {
+        u32x4 qb[QB][QPT];
 #pragma unroll
-        for (int j = 0; j < QPT; ++j) *reinterpret_cast<u32x4*>(qslots + u * QSLOT + qdst[j]) = qr[j];
+        for (int u = 0; u < QB; ++u)
+#pragma unroll
+          for (int j = 0; j < QPT; ++j)
+            if (QB == 1 || u0 + u < nq4) qb[u][j] = buffer_load16(r_q, qoff[j] + (u0 + u) * (SK * 2));
+#pragma unroll
+        for (int u = 0; u < QB; ++u)
+#pragma unroll
+          for (int j = 0; j < QPT; ++j)
+            if (QB == 1 || u0 + u < nq4) *reinterpret_cast<u32x4*>(qslots + (u0 + u) * QSLOT + qdst[j]) = qb[u][j];
       }
 #pragma unroll
       for (int u = 0; u < PX; ++u) OPRAG_ROWS(u)
@@ -2004,9 +2013,11 @@ __device__ __forceinline__ u64 wave_max64(u64 x) {
   return x;
 }
 
+// PB: composites per lane per batch, all loaded before any is used; a query whose lists fit one
+// batch (64 PB composites) is read once and kept in registers for both passes.
+template <int PB>
 __global__ __launch_bounds__(kThreads) void merge_lists_kernel(const u64* __restrict__ partial, int n_chunks, int nq,
                                                                int k, float* out_scores, long long* out_ids) {
-  constexpr int PB = 16;  // composites per lane per batch, loaded before any is used
   __shared__ u64 cand[kWaves][64];
   __shared__ u64 s_tau[kWaves];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -2150,7 +2161,8 @@ struct KernelInfo {
       MF_KS(DT, 4, 2, 4, 1, 4, 17, 64), MFK(DT, 8, 4, 4, 2, 5, 0, 2, 65, 1 << 30),                \
       MFK(DT, 8, 4, 4, 4, 8, 0, 2, 65, 1 << 30), MFK(DT, 8, 4, 4, 4, 16, 0, 2, 65, 1 << 30),         \
       MFK(DT, 2, 4, 8, 1, 8, 1, 4, 1, 1 << 30), MFK(DT, 2, 4, 4, 1, 8, 1, 4, 1, 1 << 30),            \
-      MFK(DT, 1, 1, 16, 1, 5, 2, 8, 1, 16), MFK(DT, 1, 1, 4, 1, 5, 2, 8, 1, 16),                     \
+      MFKQ(DT, 1, 1, 16, 1, 5, 2, 8, 1, 16, kWaves, 8), MFK(DT, 1, 1, 16, 1, 5, 2, 8, 1, 16),          \
+      MFK(DT, 1, 1, 4, 1, 5, 2, 8, 1, 16),                                                          \
       MFK(DT, 4, 2, 8, 1, 5, 2, 4, 17, 64), MFK(DT, 4, 2, 4, 1, 5, 2, 4, 17, 64),                    \
       MFKQ(DT, 8, 4, 4, 1, 5, 2, 2, 65, 1 << 30, kWaves, 3), MFK(DT, 8, 4, 4, 1, 5, 2, 2, 65, 1 << 30), \
       MFK(DT, 8, 4, 4, 1, 5, 3, 2, 1, 1 << 30), MF_DH(DT)
@@ -2445,8 +2457,14 @@ hipError_t launch_dense(const DensePlan& p, int dtype, const DenseArgs& a, hipSt
   hipError_t e = launch_kernel(ki, p.grid, arg, s, ev0, ev1);
   if (e != hipSuccess || p.n_chunks == 1) return e;
   if (ki.sel == 0) {
-    hipLaunchKernelGGL(merge_lists_kernel, dim3((unsigned)((a.nq + kWaves - 1) / kWaves)), dim3(kThreads), 0, s,
-                       a.partial, p.n_chunks, a.nq, a.k, a.out_scores, a.out_ids);
+    // one batch of 16 composites per lane where the lists fit it, else 32 (the 256 five-entry
+    // lists of a small batch then still fit one)
+    if ((long long)p.n_chunks * a.k <= 64 * 16)
+      hipLaunchKernelGGL(merge_lists_kernel<16>, dim3((unsigned)((a.nq + kWaves - 1) / kWaves)), dim3(kThreads), 0, s,
+                         a.partial, p.n_chunks, a.nq, a.k, a.out_scores, a.out_ids);
+    else
+      hipLaunchKernelGGL(merge_lists_kernel<32>, dim3((unsigned)((a.nq + kWaves - 1) / kWaves)), dim3(kThreads), 0, s,
+                         a.partial, p.n_chunks, a.nq, a.k, a.out_scores, a.out_ids);
   } else {
     hipLaunchKernelGGL(merge_large_kernel, dim3((unsigned)((a.nq + kWaves - 1) / kWaves)), dim3(kThreads), 0, s,
                        a.partial, p.n_chunks, a.nq, a.k, a.out_scores, a.out_ids, nullptr);
