@@ -1,6 +1,7 @@
 """Build liboprag.so (HIP kernels + C ABI) in-tree for gfx950 with hipcc.
 
     python -m paper_2608_08340_amd.build        # or build() from Python
+    python -m paper_2608_08340_amd.build --sanitized   # host code with ASan + UBSan (CPU tests)
 
 Every call recompiles all sources (in parallel) and relinks.
 """
@@ -47,20 +48,63 @@ def _compile(src: str) -> str:
     return obj
 
 
+def _link(objs: list, out: str, extra: tuple = ()) -> None:
+    tmp = out + ".tmp"
+    cmd = [hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, *extra, "-o", tmp]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"link failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
+    os.replace(tmp, out)
+
+
 def build(verbose: bool = False) -> str:
     os.makedirs(BUILD, exist_ok=True)
     with cf.ThreadPoolExecutor(len(SOURCES)) as ex:
         objs = list(ex.map(_compile, SOURCES))
-    tmp = LIB + ".tmp"
-    cmd = [hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp]
-    r = subprocess.run(cmd, capture_output=True, text=True)
-    if r.returncode != 0:
-        raise RuntimeError(f"link failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
-    os.replace(tmp, LIB)
+    _link(objs, LIB)
     if verbose:
         print(f"built {LIB}")
     return LIB
 
 
+# Host-only sanitizers: every -fsanitize applies to the host pass alone (-Xarch_host right
+# before it); the GPU code is the ordinary build's.
+SAN_FLAGS = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+             "-Xarch_host", "-fno-sanitize-recover=undefined", "-Xarch_host", "-fno-omit-frame-pointer", "-g"]
+SAN_LIB = os.path.join(BUILD, "liboprag_san.so")
+
+
+def asan_runtime() -> str:
+    """The clang AddressSanitizer runtime (it also carries the UndefinedBehaviorSanitizer
+    handlers) that a process loading SAN_LIB must preload."""
+    r = subprocess.run([hipcc(), "-print-file-name=libclang_rt.asan-x86_64.so"], capture_output=True, text=True)
+    path = r.stdout.strip()
+    if r.returncode != 0 or not os.path.isabs(path) or not os.path.exists(path):
+        raise RuntimeError("libclang_rt.asan-x86_64.so not found")
+    return path
+
+
+def build_sanitized(verbose: bool = False) -> str:
+    """SAN_LIB: the host runtime (api.cpp: argument checks, planning, the C ABI) built with
+    AddressSanitizer and UndefinedBehaviorSanitizer, linked with the ordinary kernel objects,
+    for CPU-only runs of the validation tests (start the process with asan_runtime() in
+    LD_PRELOAD)."""
+    kernels = [os.path.join(BUILD, os.path.splitext(s)[0] + ".o") for s in SOURCES if s != "api.cpp"]
+    if not all(os.path.exists(o) for o in kernels):
+        build()
+    obj = os.path.join(BUILD, "api_san.o")
+    cmd = [hipcc(), *FLAGS, *SAN_FLAGS, "-c", os.path.join(CSRC, "api.cpp"), "-o", obj]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"compile failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
+    _link([obj, *kernels], SAN_LIB, tuple(SAN_FLAGS))
+    if verbose:
+        print(f"built {SAN_LIB}")
+    return SAN_LIB
+
+
 if __name__ == "__main__":
-    build(verbose=True)
+    if "--sanitized" in sys.argv[1:]:
+        build_sanitized(verbose=True)
+    else:
+        build(verbose=True)
