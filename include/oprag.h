@@ -274,6 +274,18 @@ oprag_status oprag_search_hybrid_weighted(const oprag_index *idx, const void *q_
  */
 oprag_status oprag_time_next_dense_kernel(void *start_event, void *stop_event);
 
+/*
+ * Read-bandwidth probe (diagnostics: the HBM read rate a plain stream reaches, the ceiling a
+ * search's cold pass over the index is compared with).  Reads `bytes` (a positive multiple of
+ * 16) from `src_dev` (16-byte aligned, device memory of at least `bytes`) with 16-byte loads,
+ * eight in flight per thread, in `blocks` workgroups of 256 threads (1 .. 4,096), grid-
+ * strided, and writes one 32-bit fold of the data per workgroup to `sink_dev[0 .. blocks)`
+ * (device memory, 16-byte aligned, caller-owned).  Asynchronous on `stream`; E_INVALID for a
+ * bad argument.
+ */
+#define OPRAG_PROBE_MAX_BLOCKS 4096
+oprag_status oprag_probe_read(const void *src_dev, size_t bytes, int32_t blocks, uint32_t *sink_dev, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

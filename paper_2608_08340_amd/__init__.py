@@ -61,6 +61,7 @@ _SIGS = {
     "oprag_search_hybrid_weighted": ([_P, _P, _I64, _P, _P, ctypes.c_float, ctypes.c_float, _I32, _P, _P, _P, _SZ, _P],
                                      _I32),
     "oprag_time_next_dense_kernel": ([_P, _P], _I32),
+    "oprag_probe_read": ([_P, _SZ, _I32, _P, _P], _I32),
 }
 _lib = None
 _lock = threading.Lock()
@@ -306,6 +307,18 @@ def rrf_fuse(dense_ids: torch.Tensor, sparse_ids: torch.Tensor, rrf_k: int = 60,
     _check(library().oprag_rrf_fuse(_ptr(dense_ids), dense_ids.shape[1], _ptr(sparse_ids), sparse_ids.shape[1], nq,
                                     rrf_k, k, _ptr(fused), _ptr(ids), _stream(dev)))
     return fused, ids
+
+
+def probe_read(src: torch.Tensor, blocks: int, sink: torch.Tensor) -> None:
+    """A plain streaming read of all of `src` (contiguous device memory, a multiple of 16
+    bytes) in `blocks` workgroups; `sink` (int32, at least `blocks` entries) receives one fold
+    per workgroup (oprag_probe_read)."""
+    if not (src.is_cuda and src.is_contiguous() and sink.is_cuda and sink.dtype == torch.int32):
+        raise OpragError(-1, "src must be contiguous device memory, sink a device int32 tensor")
+    if sink.numel() < blocks:
+        raise OpragError(-1, "sink holds fewer than blocks entries")
+    _check(library().oprag_probe_read(_ptr(src), src.numel() * src.element_size(), blocks, _ptr(sink),
+                                      _stream(src.device)))
 
 
 def time_next_dense_kernel(start: torch.cuda.Event | None, stop: torch.cuda.Event | None) -> None:

@@ -216,6 +216,17 @@ oprag_status oprag_time_next_dense_kernel(void* start_event, void* stop_event) {
   return OPRAG_OK;
 }
 
+oprag_status oprag_probe_read(const void* src_dev, size_t bytes, int32_t blocks, uint32_t* sink_dev, void* stream) {
+  if (oprag_status st = check_buf(src_dev, "src_dev")) return st;
+  if (oprag_status st = check_buf(sink_dev, "sink_dev")) return st;
+  if (bytes == 0 || bytes % 16) return fail(OPRAG_E_INVALID, "bytes %zu is not a positive multiple of 16", bytes);
+  if (blocks < 1 || blocks > OPRAG_PROBE_MAX_BLOCKS)
+    return fail(OPRAG_E_INVALID, "blocks %d outside [1, %d]", blocks, OPRAG_PROBE_MAX_BLOCKS);
+  const hipError_t e = oprag::launch_probe_read(src_dev, (long long)bytes, sink_dev, blocks, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "probe launch");
+  return ok();
+}
+
 const char* oprag_last_error(void) { return g_err.c_str(); }
 
 oprag_status oprag_index_create(const oprag_index_desc* desc, void* slab_dev, size_t slab_bytes, oprag_index** out) {

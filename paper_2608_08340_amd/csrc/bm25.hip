@@ -9,19 +9,20 @@
 // avgdl)) are computed once in fp64 at attach time and stored as fp32, so a posting's
 // contribution is one product; scores accumulate in fp32.
 //
-// One workgroup scores one query over a range of up to 32,768 chunks.  A query's distinct terms
-// each contribute once, with m times their factor for m occurrences, in a fixed order: first
-// the head terms (the most frequent ones, df >= N / 8, whose weights the attach keeps as dense
-// per-chunk rows), then the others, each group in the query's first-occurrence order.  The
-// head terms are summed from their rows in registers, each thread over its own chunks (about
-// nine in ten postings a batch touches belong to them, and walking them made every query read
-// the same long lists again).  The remaining terms add their postings in the range, found by a
-// 32-ary search, to an fp32 accumulator in LDS (128 KiB), one term after another with a barrier
-// in between; a term's postings name distinct chunks, so there are no atomics and the result
-// is deterministic.  The range's top-k then comes from a threshold (the k-th largest of the
-// 256 thread maxima) and exact ranks of the few scores above it; many equal scores at the
-// threshold fall back to a 4 x 8-bit radix select and a wave-wide bitonic sort (score desc,
-// chunk asc).
+// One workgroup of 1,024 threads scores one query over a range of up to 32,768 chunks.  A
+// query's distinct terms each contribute once, with m times their factor for m occurrences, in
+// a fixed order: first the head terms (the most frequent ones, df >= N / 8, whose weights the
+// attach keeps as dense per-chunk rows), then the others, each group in the query's
+// first-occurrence order.  The head terms are summed from their rows in registers, each thread
+// over its own 32 chunks (about nine in ten postings a batch touches belong to them, and walking
+// them made every query read the same long lists again).  The remaining terms add their
+// postings in the range to an fp32 accumulator in LDS (128 KiB), one term after another with a
+// barrier in between, the next term's postings loading while the current one is added; a
+// term's postings name distinct chunks, so there are no atomics and the result is
+// deterministic.  The range's top-k then comes from a threshold (the k-th largest of the 256
+// maxima of groups of four threads) and exact ranks of the few scores at or above it, with the
+// keys held in registers; many scores above the threshold, or few positive ones, fall back to a
+// 4 x 8-bit radix select and a wave-wide bitonic sort (score desc, chunk asc).
 #include <algorithm>
 
 #include "oprag_internal.h"

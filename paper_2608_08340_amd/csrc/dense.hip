@@ -27,7 +27,9 @@
 // passes over an LDS score tile: the top-KS values of each slice (a v_med3 insertion
 // network), then the rows above the exact k-th value and the smallest-id rows equal to it.
 // Filtered mode (bf16 / fp16, 16 < k <= 128): threshold levels over growing row prefixes
-// collect candidate keys per query and select_topk_kernel ranks them.  fp32 with k > 16: one
+// collect candidate keys per query (a kernel instance with branch-free stores for levels with
+// many hits per tile, SEL 4, and one with per-hit stores for the others, SEL 2) and
+// select_topk_kernel ranks them.  fp32 with k > 16: one
 // wave per query keeps a 128-entry sorted queue and merges batches of 64 candidates above
 // its k-th entry with a bitonic network.
 #include <algorithm>

@@ -168,6 +168,28 @@ __device__ __forceinline__ unsigned short f32_to_bf16_rne(float x) {
 }
 
 // Same-dtype copy, 16 bytes per thread per step.
+// Read-bandwidth probe (diagnostics): a plain streaming read of n16 16-byte words, eight
+// loads in flight per thread, grid-strided; each workgroup folds what it read into one word
+// (so the loads cannot be dropped) and writes it to sink[blockIdx.x].
+__global__ __launch_bounds__(256) void probe_read_kernel(const uint4* __restrict__ src, long long n16,
+                                                        unsigned int* __restrict__ sink) {
+  __shared__ unsigned int part[4];
+  const long long stride = (long long)gridDim.x * 256 * 8;
+  unsigned int x = 0u;
+  for (long long i0 = (long long)blockIdx.x * 256 * 8 + threadIdx.x; i0 < n16; i0 += stride) {
+    uint4 v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = i0 + u * 256 < n16 ? src[i0 + u * 256] : make_uint4(0u, 0u, 0u, 0u);
+#pragma unroll
+    for (int u = 0; u < 8; ++u) x ^= v[u].x ^ v[u].y ^ v[u].z ^ v[u].w;
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) x ^= (unsigned int)__shfl_xor((int)x, o);
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = x;
+  __syncthreads();
+  if (threadIdx.x == 0) sink[blockIdx.x] = part[0] ^ part[1] ^ part[2] ^ part[3];
+}
+
 __global__ void copy16_kernel(const uint4* __restrict__ src, uint4* __restrict__ dst, long long n16) {
   const long long stride = (long long)gridDim.x * blockDim.x;
   for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += stride) dst[i] = src[i];
@@ -360,6 +382,12 @@ hipError_t launch_upsert(void* slab, int slab_dtype, int d, long long first_row,
       hipLaunchKernelGGL(convert8_kernel<kDtypeF16>, dim3(std::max(1, blocks)), dim3(256), 0, s,
                          static_cast<const float4*>(rows), reinterpret_cast<uint4*>(dst), n8);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_probe_read(const void* src, long long bytes, unsigned int* sink, int blocks, hipStream_t s) {
+  hipLaunchKernelGGL(probe_read_kernel, dim3((unsigned)blocks), dim3(256), 0, s, static_cast<const uint4*>(src),
+                     bytes / 16, sink);
   return hipGetLastError();
 }
 

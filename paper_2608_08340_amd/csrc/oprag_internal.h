@@ -152,6 +152,7 @@ hipError_t launch_rrf(const long long* dense_ids, int k_dense, const long long* 
 // [first_row, first_row + m).
 hipError_t launch_pool_upsert(void* slab, int slab_dtype, int d, long long first_row, const void* hidden,
                               int hidden_dtype, const int* lengths, long long m, int T, hipStream_t s);
+hipError_t launch_probe_read(const void* src, long long bytes, unsigned int* sink, int blocks, hipStream_t s);
 hipError_t launch_upsert(void* slab, int slab_dtype, int d, long long first_row, const void* rows,
                          int rows_dtype, long long m, hipStream_t s);
 

@@ -117,6 +117,20 @@ def test_time_hook_arms_and_disarms(lib):
     assert lib.oprag_time_next_dense_kernel(None, None) == 0  # disarm: nothing is recorded
 
 
+@pytest.mark.parametrize("src,nbytes,blocks,sink,why", [
+    (None, 4096, 4, 4096, "null src"),
+    (4096, 4096, 4, None, "null sink"),
+    (4096, 0, 4, 4096, "zero bytes"),
+    (4096, 4100, 4, 4096, "bytes not a multiple of 16"),
+    (4096, 4096, 0, 4096, "no workgroups"),
+    (4096, 4096, 4097, 4096, "too many workgroups"),
+    (4104, 4096, 4, 4096, "misaligned src"),
+])
+def test_probe_read_rejects(lib, src, nbytes, blocks, sink, why):
+    p = lambda v: None if v is None else ctypes.c_void_p(v)
+    assert lib.oprag_probe_read(p(src), nbytes, blocks, p(sink), None) == E_INVALID, why
+
+
 def test_rrf_empty_batch_is_noop(lib):
     assert lib.oprag_rrf_fuse(None, 5, None, 5, 0, 60, 5, None, None, None) == 0
 

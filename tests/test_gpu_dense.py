@@ -20,6 +20,20 @@ def _run(rows, queries, k, dtype, capacity=None):
     return idx, sc.cpu(), ids.cpu()
 
 
+def test_read_probe_folds_every_word():
+    """The read probe (diagnostics) reads every 16-byte word exactly once: the XOR of the
+    workgroups' folds equals the XOR of the data (three workgroups, a ragged last stride)."""
+    import paper_2608_08340_amd as P
+    dev = device()
+    g = torch.Generator().manual_seed(7)
+    data = torch.randint(-2 ** 31, 2 ** 31 - 1, (1 << 16,), dtype=torch.int32, generator=g)
+    sink = torch.zeros(3, dtype=torch.int32, device=dev)
+    P.probe_read(data.to(dev), 3, sink)
+    torch.cuda.synchronize()
+    got = np.bitwise_xor.reduce(sink.cpu().numpy().view(np.uint32))
+    assert got == np.bitwise_xor.reduce(data.numpy().view(np.uint32))
+
+
 def test_tiny_f32_1k_x_384():
     """1,024 x 384 fp32 rows, 16 perturbed queries, exact cosine top-5 (rtol 1e-5)."""
     device()
