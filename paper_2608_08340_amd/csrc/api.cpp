@@ -706,6 +706,15 @@ oprag_status oprag_search_hybrid_weighted(const oprag_index* idx, const void* q_
   a.dump_ld = ld;
   a.dump_mm = mm_d;
   hipError_t e = oprag::launch_dense_dump(p, a, s);
+  if (idx->n_rows <= oprag::kSparseRange && idx->sp.n_docs <= oprag::kSparseRange) {
+    // one range: the BM25 kernel fuses its scores with the dense dump and selects the top k
+    if (e == hipSuccess)
+      e = oprag::launch_sparse_weighted(idx->sp, qterm_indptr_dev, qterms_dev, (int)nq, k, D, ld, mm_d, p.n_chunks,
+                                        idx->n_rows, (double)w_dense, (double)w_lex, scores_dev,
+                                        reinterpret_cast<long long*>(ids_dev), s);
+    if (e != hipSuccess) return hip_fail(e, "weighted fusion launch");
+    return ok();
+  }
   if (e == hipSuccess)
     e = oprag::launch_sparse_dump(idx->sp, qterm_indptr_dev, qterms_dev, (int)nq, B, ld, mm_l, idx->n_rows, s);
   if (e == hipSuccess)

@@ -132,6 +132,15 @@ struct SparseArgs {
   long long dump_ld = 0;
   float* dump_mm = nullptr;      // with dump: (min, max) over chunks < mm_rows per (query, range)
   long long mm_rows = 0;
+  // Weighted fusion in the kernel (one range): the top k of w_d minmax(dense) + w_l minmax(BM25)
+  // over chunks [0, wn), the dense scores from wdense[q * wld + chunk] and their (min, max)
+  // partials from wmm[(q * wpd + i) * 2 + {0, 1}], i < wpd.
+  const float* wdense = nullptr;
+  long long wld = 0;
+  const float* wmm = nullptr;
+  int wpd = 0;
+  long long wn = 0;
+  double wd = 0.0, wl = 0.0;
   float* out_scores;            // final output when n_ranges == 1
   long long* out_ids;
   unsigned long long* partial;  // [nq x n_ranges x k] when n_ranges > 1
@@ -448,6 +457,65 @@ __global__ __launch_bounds__(kBT) void bm25_kernel(SparseArgs a) {
     kv[4 * g + 2] = x.z;
     kv[4 * g + 3] = x.w;
   }
+  const bool weighted = a.wdense != nullptr;  // launch-uniform
+  if (weighted) {
+    // Weighted fusion: the lexical row is this range's scores (0 past the corpus) over chunks
+    // [0, wn); both rows are min-max normalised over those chunks, the dense minimum and
+    // maximum from the dump's partials.  Keys become score_key(fused), nonzero for every
+    // chunk below wn (all are candidates), 0 past it; they replace the scores in LDS for the
+    // selection below.
+    float mnd = __builtin_inff(), mxd = -__builtin_inff(), mnl = __builtin_inff(), mxl = -__builtin_inff();
+    for (int i = tid; i < a.wpd; i += kBT) {
+      mnd = fminf(mnd, a.wmm[((long long)q * a.wpd + i) * 2]);
+      mxd = fmaxf(mxd, a.wmm[((long long)q * a.wpd + i) * 2 + 1]);
+    }
+#pragma unroll
+    for (int j = 0; j < 32; ++j)
+      if (own(j) < a.wn) {
+        mnl = fminf(mnl, __uint_as_float(kv[j]));
+        mxl = fmaxf(mxl, __uint_as_float(kv[j]));
+      }
+    for (int o = 32; o > 0; o >>= 1) {
+      mnd = fminf(mnd, __shfl_xor(mnd, o));
+      mxd = fmaxf(mxd, __shfl_xor(mxd, o));
+      mnl = fminf(mnl, __shfl_xor(mnl, o));
+      mxl = fmaxf(mxl, __shfl_xor(mxl, o));
+    }
+    float* red = reinterpret_cast<float*>(cand);  // [4][kBT / 64]; the candidate area is free
+    if (lane == 0) {
+      red[w] = mnd;
+      red[kBT / 64 + w] = mxd;
+      red[2 * (kBT / 64) + w] = mnl;
+      red[3 * (kBT / 64) + w] = mxl;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < kBT / 64; ++u) {
+      mnd = fminf(mnd, red[u]);
+      mxd = fmaxf(mxd, red[kBT / 64 + u]);
+      mnl = fminf(mnl, red[2 * (kBT / 64) + u]);
+      mxl = fmaxf(mxl, red[3 * (kBT / 64) + u]);
+    }
+    const double sd = mxd > mnd ? a.wd / ((double)mxd - (double)mnd) : 0.0;
+    const double sl = mxl > mnl ? a.wl / ((double)mxl - (double)mnl) : 0.0;
+    const float* drow = a.wdense + (long long)q * a.wld;
+#pragma unroll
+    for (int g = 0; g < 8; ++g) {
+      const int c0 = 4 * tid + kLayer * g;  // 16-byte aligned: wld is a multiple of 4
+      const f32x4 x = c0 < a.wn ? *reinterpret_cast<const f32x4*>(drow + c0) : f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int j = 4 * g + e;
+        kv[j] = c0 + e < a.wn ? score_key(fused_value(sd, sl, mnd, mnl, x[e], __uint_as_float(kv[j]))) : 0u;
+      }
+      reinterpret_cast<uint4*>(acc)[tid + kBT * g] = make_uint4(kv[4 * g], kv[4 * g + 1], kv[4 * g + 2], kv[4 * g + 3]);
+    }
+    __syncthreads();  // the keys in LDS are complete; the reduction area is free again
+  }
+  // the score a key stands for
+  auto key_value = [&](uint32_t k32) { return weighted ? key_score(k32) : __uint_as_float(k32); };
+  // chunks that hold keys: the range's, or in weighted mode every chunk below wn
+  const int slen = weighted ? (int)a.wn : len;
   // Threshold: the 256 groups of four adjacent threads (128 chunks each) take their largest
   // key, and tau = the k-th largest of these maxima.  Every maximum is the key of its own
   // chunk, so at least k chunks score >= tau and the top k lie among them.  Each of a group's
@@ -487,7 +555,7 @@ __global__ __launch_bounds__(kBT) void bm25_kernel(SparseArgs a) {
   auto emit = [&](int r, u64 key) __attribute__((always_inline)) {
     if (a.n_ranges == 1) {
       a.out_ids[(long long)q * a.k + r] = (long long)comp_row(key);
-      a.out_scores[(long long)q * a.k + r] = __uint_as_float((uint32_t)(key >> 32));
+      a.out_scores[(long long)q * a.k + r] = key_value((uint32_t)(key >> 32));
     } else {
       a.partial[((long long)q * a.n_ranges + range) * a.k + r] = key;
     }
@@ -543,7 +611,7 @@ __global__ __launch_bounds__(kBT) void bm25_kernel(SparseArgs a) {
         // ranks G .. k - 1: each thread marks the scores equal to tau in a contiguous block of
         // 32 chunks, read from a rotated start (lanes then hit different LDS banks), and emits
         // them in order after a scan of the counts
-        const int b0 = min(len, 32 * tid), nb = min(len, b0 + 32) - b0;
+        const int b0 = min(slen, 32 * tid), nb = min(slen, b0 + 32) - b0;
         uint32_t mk = 0u;
         for (int i = 0; i < nb; ++i) {
           const int o = (i + tid) % nb;
@@ -613,7 +681,7 @@ __global__ __launch_bounds__(kBT) void bm25_kernel(SparseArgs a) {
   // blocks of 32 chunks per thread, so a scan of the counts orders the equal keys by chunk)
   if (tid == 0) s_ngt = 0u;
   __syncthreads();
-  const int b0 = min(len, 32 * tid), b1 = min(len, b0 + 32);
+  const int b0 = min(slen, 32 * tid), b1 = min(slen, b0 + 32);
   int n_eq = 0;
   for (int i = b0; i < b1; ++i) {
     const uint32_t u = keys[i];
@@ -647,16 +715,17 @@ __global__ __launch_bounds__(kBT) void bm25_kernel(SparseArgs a) {
     x1 = wave_sort64_desc(x1, lane);
     u64 q1 = 0ull;
     wave_merge128(x0, q1, x1, lane);
-    // The stored key is the raw fp32 bit pattern of a positive score.
+    // The stored key is the raw fp32 bit pattern of a positive score (score_key of the fused
+    // value in weighted mode).
     if (a.n_ranges == 1) {
       const long long o = (long long)q * a.k;
       if (lane < a.k) {
         a.out_ids[o + lane] = x0 ? (long long)comp_row(x0) : -1ll;
-        a.out_scores[o + lane] = x0 ? __uint_as_float((uint32_t)(x0 >> 32)) : -__builtin_inff();
+        a.out_scores[o + lane] = x0 ? key_value((uint32_t)(x0 >> 32)) : -__builtin_inff();
       }
       if (lane + 64 < a.k) {
         a.out_ids[o + lane + 64] = q1 ? (long long)comp_row(q1) : -1ll;
-        a.out_scores[o + lane + 64] = q1 ? __uint_as_float((uint32_t)(q1 >> 32)) : -__builtin_inff();
+        a.out_scores[o + lane + 64] = q1 ? key_value((uint32_t)(q1 >> 32)) : -__builtin_inff();
       }
     } else {
       unsigned long long* dst = a.partial + ((long long)q * a.n_ranges + range) * a.k;
@@ -1089,6 +1158,39 @@ hipError_t launch_sparse_dump(const SparseIndex& sp, const int* qterm_indptr, co
   a.out_ids = nullptr;
   a.partial = nullptr;
   hipLaunchKernelGGL(bm25_kernel, dim3((unsigned)(nq * a.n_ranges)), dim3(kBT), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_sparse_weighted(const SparseIndex& sp, const int* qterm_indptr, const int* qterms, int nq, int k,
+                                  const float* dense, long long ld, const float* dense_mm, int pd, long long n,
+                                  double wd, double wl, float* out_scores, long long* out_ids, hipStream_t s) {
+  if (sp.n_docs > kSparseRange || n > kSparseRange || ld % 4) return hipErrorInvalidValue;
+  SparseArgs a;
+  a.vocab = sp.vocab;
+  a.n_docs = sp.n_docs;
+  a.indptr = sp.term_indptr;
+  a.chunk = sp.post_chunk;
+  a.idfk = sp.idfk;
+  a.wpost = sp.wpost;
+  a.hidx = sp.hidx;
+  a.whead = sp.whead;
+  a.head_ld = sp.head_ld;
+  a.qterm_indptr = qterm_indptr;
+  a.qterms = qterms;
+  a.nq = nq;
+  a.k = k;
+  a.n_ranges = 1;
+  a.wdense = dense;
+  a.wld = ld;
+  a.wmm = dense_mm;
+  a.wpd = pd;
+  a.wn = n;
+  a.wd = wd;
+  a.wl = wl;
+  a.out_scores = out_scores;
+  a.out_ids = out_ids;
+  a.partial = nullptr;
+  hipLaunchKernelGGL(bm25_kernel, dim3((unsigned)nq), dim3(kBT), 0, s, a);
   return hipGetLastError();
 }
 

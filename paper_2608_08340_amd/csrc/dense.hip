@@ -1865,8 +1865,7 @@ static_assert(kFuseLds % (8 * kFuseThreads) == 0, "whole steps come from LDS");
 static_assert(kMaxK <= kFuseGroups, "tau needs k group maxima");
 __device__ __forceinline__ u64 fused_composite(double sd, double sl, double mnd, double mnl, float x, float y,
                                                long long i) {
-  const double v = __dadd_rn(__dmul_rn(sd, __dsub_rn((double)x, mnd)), __dmul_rn(sl, __dsub_rn((double)y, mnl)));
-  return composite(__double2float_rn(v), (uint32_t)i);
+  return composite(fused_value(sd, sl, mnd, mnl, x, y), (uint32_t)i);
 }
 __global__ __launch_bounds__(kFuseThreads) void weighted_fuse_kernel(const float* __restrict__ D,
                                                                  const float* __restrict__ B, long long ld,

@@ -140,6 +140,11 @@ hipError_t launch_sparse(const SparseIndex& sp, const int* qterm_indptr, const i
 // BM25 scores of every chunk [0, n_docs) for nq queries into dump [nq x ld], and the minimum
 // and maximum over chunks [0, mm_rows) of each (query, range of kSparseRange chunks) into
 // dump_mm [nq x ranges x 2] (+inf / -inf for a range with none of them).
+// Weighted fusion inside the BM25 kernel when the corpus and the n scored chunks fit one
+// range: the top k of w_d minmax(dense) + w_l minmax(BM25) over chunks [0, n).
+hipError_t launch_sparse_weighted(const SparseIndex& sp, const int* qterm_indptr, const int* qterms, int nq, int k,
+                                  const float* dense, long long ld, const float* dense_mm, int pd, long long n,
+                                  double wd, double wl, float* out_scores, long long* out_ids, hipStream_t s);
 hipError_t launch_sparse_dump(const SparseIndex& sp, const int* qterm_indptr, const int* qterms, int nq, float* dump,
                               long long ld, float* dump_mm, long long mm_rows, hipStream_t s);
 hipError_t launch_dense_first(const SparseIndex& sp, const int* qterm_indptr, const int* qterms,

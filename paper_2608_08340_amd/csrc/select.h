@@ -118,5 +118,13 @@ __device__ __forceinline__ void wave_offer(u64& q0, u64& q1, u64 c, u64 kth, int
   }
 }
 
+// Weighted fusion of one chunk: sd (x - mnd) + sl (y - mnl) in fp64 with every operation
+// rounded explicitly, then rounded to fp32 (sd = w_d / (max_d - min_d), 0 for a constant row;
+// likewise sl), so every kernel that fuses gives the same value.
+__device__ __forceinline__ float fused_value(double sd, double sl, double mnd, double mnl, float x, float y) {
+  const double v = __dadd_rn(__dmul_rn(sd, __dsub_rn((double)x, mnd)), __dmul_rn(sl, __dsub_rn((double)y, mnl)));
+  return __double2float_rn(v);
+}
+
 }  // namespace dev
 }  // namespace oprag

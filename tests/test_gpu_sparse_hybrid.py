@@ -441,6 +441,27 @@ def test_weighted_fusion_small_corpus(w_d, w_l, k, n, n_docs, vocab):
     _check_weighted(weighted.fused(S, B, w_d, w_l), sc, ids, k, f"w=({w_d},{w_l}) k={k}")
 
 
+def test_weighted_fusion_index_smaller_than_its_corpus():
+    """An index of 2,000 rows (capacity 3,000) over a 3,000-chunk sparse corpus, both inside
+    one 32,768-chunk range: the fusion covers the chunks with a dense row only, so the lexical
+    minimum and maximum come from those 2,000 chunks (the corpus's statistics from all)."""
+    from oracle import weighted
+    dev = device()
+    n, n_docs, nq = 2000, 3000, 40
+    ind, toks, csr, qi, qt = _small_corpus(6001, n_docs, 300, 30.0, nq)
+    w = synth.mixture_dense(6002, n, 128, 16, nq, 10, "bf16")
+    idx = make_index(w.rows, "bf16", capacity=n_docs)
+    _attach(idx, csr, dev)
+    S, X, Q = oracle_scores(w.rows, w.queries, "bf16")
+    qt_oracle = np.where((qt >= 0) & (qt < 300), qt, 10 ** 6).astype(np.int64)
+    B = bm25.scores_batch(ind, toks, qi, qt_oracle, 1.2, 0.75)
+    for k in (5, 100):
+        log("weighted index smaller than its corpus", n, n_docs, k)
+        sc, ids = idx.search_hybrid_weighted(w.queries.to(dev), _t(qi, dev), _t(qt, dev), 0.7, 0.3, k)
+        torch.cuda.synchronize()
+        _check_weighted(weighted.fused(S, B[:, :n], 0.7, 0.3), sc, ids, k, f"n={n} n_docs={n_docs} k={k}")
+
+
 def test_weighted_fusion_past_the_lds_key_cache():
     """45,001 chunks, more than the 32,768 score keys the fusion kernel keeps in LDS: the
     steps past them compute the composites again from the score rows, and both halves must
