@@ -610,6 +610,13 @@ oprag_status oprag_search_hybrid(const oprag_index* idx, const void* q_dev, int6
   w += align_up((size_t)nq * k_sparse * 4);
   const size_t inner = workspace_bytes - (size_t)(w - static_cast<unsigned char*>(workspace_dev));
   if (oprag_status st = do_dense(idx, q_dev, nq, k_dense, d_sc, d_ids, w, inner, s)) return st;
+  if (idx->sp.n_docs <= oprag::kSparseRange) {  // one range: BM25 and the fusion in one launch
+    const hipError_t e = oprag::launch_sparse_rrf(idx->sp, qterm_indptr_dev, qterms_dev, (int)nq, k_sparse,
+                                                  reinterpret_cast<const long long*>(d_ids), k_dense, rrf_k, k,
+                                                  fused_dev, reinterpret_cast<long long*>(ids_dev), s);
+    if (e != hipSuccess) return hip_fail(e, "sparse search and fusion launch");
+    return ok();
+  }
   hipError_t e = oprag::launch_sparse(idx->sp, qterm_indptr_dev, qterms_dev, (int)nq, k_sparse, s_sc,
                                       reinterpret_cast<long long*>(s_ids), w, s);
   if (e != hipSuccess) return hip_fail(e, "sparse search launch");

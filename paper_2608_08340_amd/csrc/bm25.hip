@@ -26,6 +26,7 @@
 #include <algorithm>
 
 #include "oprag_internal.h"
+#include "rrf.h"
 #include "select.h"
 
 namespace oprag {
@@ -141,6 +142,15 @@ struct SparseArgs {
   int wpd = 0;
   long long wn = 0;
   double wd = 0.0, wl = 0.0;
+  // Hybrid fusion in the kernel (one range): the range's top k (the sparse list) stays in LDS
+  // and is fused by reciprocal rank fusion with the dense list rrf_dense[q * rrf_kd ..] into
+  // the top rrf_kout of rrf_fused / rrf_ids (rows of rrf_kout per query).
+  const long long* rrf_dense = nullptr;
+  int rrf_kd = 0;
+  int rrf_k = 0;
+  int rrf_kout = 0;
+  float* rrf_fused = nullptr;
+  long long* rrf_ids = nullptr;
   float* out_scores;            // final output when n_ranges == 1
   long long* out_ids;
   unsigned long long* partial;  // [nq x n_ranges x k] when n_ranges > 1
@@ -201,6 +211,8 @@ __global__ __launch_bounds__(kBT) void bm25_kernel(SparseArgs a) {
   __shared__ unsigned int s_prefix, s_need, s_take_all, s_ngt;
   __shared__ long long s_lo[kTermBatch], s_hi[kTermBatch];
   __shared__ float s_wt[kTermBatch];
+  __shared__ long long s_sids[kMaxK];  // hybrid fusion: the sparse list by rank (-1 padded)
+  static_assert(RrfScratch::kBytes <= kSparseRange * 4, "the fusion's scratch fits the accumulator");
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int q = blockIdx.x / a.n_ranges;
@@ -514,6 +526,17 @@ __global__ __launch_bounds__(kBT) void bm25_kernel(SparseArgs a) {
   }
   // the score a key stands for
   auto key_value = [&](uint32_t k32) { return weighted ? key_score(k32) : __uint_as_float(k32); };
+  // hybrid fusion: the ranks go to LDS (filled after the barriers of the selection below), then
+  // every thread fuses them with the dense list, the accumulator serving as scratch
+  const bool rrf = a.rrf_dense != nullptr;  // launch-uniform
+  if (rrf)
+    for (int i = tid; i < a.k; i += kBT) s_sids[i] = -1;
+  auto rrf_tail = [&]() {
+    __syncthreads();  // every rank is in LDS and every read of the keys is done
+    rrf_query<kBT>(a.rrf_dense + (long long)q * a.rrf_kd, a.rrf_kd, s_sids, a.k, a.rrf_k, a.rrf_kout,
+                   a.rrf_fused + (long long)q * a.rrf_kout, a.rrf_ids + (long long)q * a.rrf_kout,
+                   RrfScratch(reinterpret_cast<unsigned char*>(acc)));
+  };
   // chunks that hold keys: the range's, or in weighted mode every chunk below wn
   const int slen = weighted ? (int)a.wn : len;
   // Threshold: the 256 groups of four adjacent threads (128 chunks each) take their largest
@@ -553,7 +576,9 @@ __global__ __launch_bounds__(kBT) void bm25_kernel(SparseArgs a) {
   }
   const uint32_t tau = s_tau;  // 0: fewer than k positive maxima
   auto emit = [&](int r, u64 key) __attribute__((always_inline)) {
-    if (a.n_ranges == 1) {
+    if (rrf) {
+      s_sids[r] = (long long)comp_row(key);
+    } else if (a.n_ranges == 1) {
       a.out_ids[(long long)q * a.k + r] = (long long)comp_row(key);
       a.out_scores[(long long)q * a.k + r] = key_value((uint32_t)(key >> 32));
     } else {
@@ -620,6 +645,7 @@ __global__ __launch_bounds__(kBT) void bm25_kernel(SparseArgs a) {
         int rr = G + block_excl_scan(__popc(mk), wave_tot);
         for (uint32_t m2 = mk; m2 != 0u && rr < a.k; m2 &= m2 - 1u) emit(rr++, composite(b0 + __builtin_ctz(m2)));
       }
+      if (rrf) rrf_tail();
       return;
     }
     __syncthreads();  // the candidate area becomes the histogram
@@ -717,7 +743,10 @@ __global__ __launch_bounds__(kBT) void bm25_kernel(SparseArgs a) {
     wave_merge128(x0, q1, x1, lane);
     // The stored key is the raw fp32 bit pattern of a positive score (score_key of the fused
     // value in weighted mode).
-    if (a.n_ranges == 1) {
+    if (rrf) {
+      if (lane < a.k) s_sids[lane] = x0 ? (long long)comp_row(x0) : -1ll;
+      if (lane + 64 < a.k) s_sids[lane + 64] = q1 ? (long long)comp_row(q1) : -1ll;
+    } else if (a.n_ranges == 1) {
       const long long o = (long long)q * a.k;
       if (lane < a.k) {
         a.out_ids[o + lane] = x0 ? (long long)comp_row(x0) : -1ll;
@@ -733,6 +762,7 @@ __global__ __launch_bounds__(kBT) void bm25_kernel(SparseArgs a) {
       if (lane + 64 < a.k) dst[lane + 64] = q1;
     }
   }
+  if (rrf) rrf_tail();
 }
 
 // Merge of the per-range lists when they hold at most kMergeCap composites per query.  Each
@@ -1189,6 +1219,38 @@ hipError_t launch_sparse_weighted(const SparseIndex& sp, const int* qterm_indptr
   a.wl = wl;
   a.out_scores = out_scores;
   a.out_ids = out_ids;
+  a.partial = nullptr;
+  hipLaunchKernelGGL(bm25_kernel, dim3((unsigned)nq), dim3(kBT), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_sparse_rrf(const SparseIndex& sp, const int* qterm_indptr, const int* qterms, int nq, int k_sparse,
+                             const long long* dense_ids, int k_dense, int rrf_k, int k, float* out_fused,
+                             long long* out_ids, hipStream_t s) {
+  if (sp.n_docs > kSparseRange) return hipErrorInvalidValue;
+  SparseArgs a;
+  a.vocab = sp.vocab;
+  a.n_docs = sp.n_docs;
+  a.indptr = sp.term_indptr;
+  a.chunk = sp.post_chunk;
+  a.idfk = sp.idfk;
+  a.wpost = sp.wpost;
+  a.hidx = sp.hidx;
+  a.whead = sp.whead;
+  a.head_ld = sp.head_ld;
+  a.qterm_indptr = qterm_indptr;
+  a.qterms = qterms;
+  a.nq = nq;
+  a.k = k_sparse;
+  a.n_ranges = 1;
+  a.rrf_dense = dense_ids;
+  a.rrf_kd = k_dense;
+  a.rrf_k = rrf_k;
+  a.rrf_kout = k;
+  a.rrf_fused = out_fused;
+  a.rrf_ids = out_ids;
+  a.out_scores = nullptr;
+  a.out_ids = nullptr;
   a.partial = nullptr;
   hipLaunchKernelGGL(bm25_kernel, dim3((unsigned)nq), dim3(kBT), 0, s, a);
   return hipGetLastError();

@@ -14,6 +14,7 @@
 #include <algorithm>
 
 #include "oprag_internal.h"
+#include "rrf.h"
 #include "select.h"
 
 namespace oprag {
@@ -21,142 +22,15 @@ namespace {
 
 using namespace dev;
 
-constexpr int kMaxCand = 2 * kMaxK;
-
-// One workgroup of 256 threads per query.  Thread t < kd inserts dense entry t (rank t + 1)
-// and thread kd + j sparse entry j (rank j + 1) into an LDS hash table keyed by id (open
-// addressing, 64-bit compare-and-swap on the key), so an id present in both lists ends in one
-// slot holding both ranks; the expected probe count is about one.  An occupied slot whose
-// fused value reaches 1 / (rrf_k + k) is a candidate; its rank is the number of candidates
-// that beat it in the exact rational order (fused desc, id asc), counted with LDS reads
-// issued ahead of use.
+// One workgroup of 256 threads per query (rrf_query in rrf.h).
 constexpr int kRrfThreads = 256;
-constexpr int kRrfSlots = 512;  // power of two, at least twice the 256 possible ids
-constexpr int kRrfFastMax = 100000;  // below this rrf_k the fused quotients order exactly
 __global__ __launch_bounds__(kRrfThreads) void rrf_kernel(const long long* dense_ids, int kd,
                                                           const long long* sparse_ids, int ks, long long nq, int rrf_k,
                                                           int k, float* out_fused, long long* out_ids) {
-  __shared__ unsigned long long key[kRrfSlots];  // id, or ~0 when empty
-  __shared__ int rank_d[kRrfSlots];
-  __shared__ int rank_s[kRrfSlots];
-  __shared__ long long cid[kMaxCand];
-  __shared__ long long cnum[kMaxCand];
-  __shared__ long long cden[kMaxCand];
-  __shared__ double cval[kMaxCand];
-  __shared__ int s_nc;
-  constexpr unsigned long long kEmpty = ~0ull;
+  __shared__ __attribute__((aligned(16))) unsigned char area[RrfScratch::kBytes];
   const long long q = blockIdx.x;
-  const int t = threadIdx.x;
-  for (int h = t; h < kRrfSlots; h += kRrfThreads) {
-    key[h] = kEmpty;
-    rank_d[h] = 0;
-    rank_s[h] = 0;
-  }
-  if (t == 0) s_nc = 0;
-  long long id = -1;
-  int rank = 0;
-  bool dense = false;
-  if (t < kd) {
-    id = dense_ids[q * kd + t];
-    rank = t + 1;
-    dense = true;
-  } else if (t - kd < ks) {
-    id = sparse_ids[q * ks + (t - kd)];
-    rank = t - kd + 1;
-  }
-  __syncthreads();
-  if (id >= 0) {
-    unsigned h = ((unsigned)id * 2654435761u) >> 23;  // top 9 bits
-    for (;;) {  // at most 256 ids in 512 slots: a free or matching slot is always found
-      const unsigned long long old = atomicCAS(&key[h], kEmpty, (unsigned long long)id);
-      if (old == kEmpty || old == (unsigned long long)id) break;
-      h = (h + 1) & (kRrfSlots - 1);
-    }
-    if (dense)
-      rank_d[h] = rank;
-    else
-      rank_s[h] = rank;
-  }
-  __syncthreads();
-  // compaction: slots t and t + 256; fused = 1/(rrf_k + a) + 1/(rrf_k + b) = num / den exactly
-#pragma unroll
-  for (int part = 0; part < kRrfSlots / kRrfThreads; ++part) {
-    const int h = t + part * kRrfThreads;
-    if (key[h] != kEmpty) {
-      const long long a = rank_d[h] ? (long long)rrf_k + rank_d[h] : 0, b = rank_s[h] ? (long long)rrf_k + rank_s[h] : 0;
-      long long num, den;
-      if (a && b) {
-        num = a + b;
-        den = a * b;
-      } else {
-        num = 1;
-        den = a ? a : b;
-      }
-      // The entries of rank <= k of either list all fuse to >= 1 / (rrf_k + k), and there
-      // are at least min(k, candidates) of them, so a candidate below that never ranks < k.
-      if (num * ((long long)rrf_k + k) >= den) {
-        const int slot = atomicAdd(&s_nc, 1);
-        cid[slot] = (long long)key[h];
-        cnum[slot] = num;
-        cden[slot] = den;
-        cval[slot] = (double)num / (double)den;
-      }
-    }
-  }
-  __syncthreads();
-  const int nc = s_nc;
-  if (t < nc) {
-    // Rank = candidates that beat this one.
-    const long long n0 = cnum[t], d0 = cden[t], id0 = cid[t];
-    const double v0 = cval[t];
-    int r = 0;
-    if (rrf_k < kRrfFastMax) {
-      // Distinct fused values differ by at least 1 / (den1 den2) >= (rrf_k + 128)^-4, more
-      // than twice the rounding error of the correctly rounded quotients (about
-      // 2 / (rrf_k + 1) * 2^-53) while rrf_k stays below ~1.6e5; equal values round alike.
-      // So the quotients order the candidates exactly, and their bit patterns (positive
-      // doubles) order like unsigned integers.  Eight candidates per step, read before use.
-      const unsigned long long b0 = (unsigned long long)__double_as_longlong(v0);
-      for (int o = 0; o < nc; o += 8) {
-        unsigned long long vb[8];
-        long long ii[8];
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          const int c = min(o + u, nc - 1);
-          vb[u] = (unsigned long long)__double_as_longlong(cval[c]);
-          ii[u] = cid[c];
-        }
-#pragma unroll
-        for (int u = 0; u < 8; ++u) r += (o + u < nc && (vb[u] > b0 || (vb[u] == b0 && ii[u] < id0))) ? 1 : 0;
-      }
-    } else {
-      // Large rrf_k: the quotients order pairs that differ by more than a few ulps; closer
-      // pairs are compared exactly as int64 cross products.
-      const double hi = v0 * (1.0 + 1e-14), lo = v0 * (1.0 - 1e-14);
-      for (int o = 0; o < nc; o += 8) {
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          if (o + u < nc) {
-            const double v = cval[o + u];
-            bool beats = v > hi;
-            if (!beats && v >= lo) {
-              const long long lhs = cnum[o + u] * d0, rhs = n0 * cden[o + u];
-              beats = lhs > rhs || (lhs == rhs && cid[o + u] < id0);
-            }
-            r += beats ? 1 : 0;
-          }
-        }
-      }
-    }
-    if (r < k) {
-      out_ids[q * k + r] = id0;
-      out_fused[q * k + r] = (float)((double)n0 / (double)d0);
-    }
-  }
-  for (int r = nc + t; r < k; r += kRrfThreads) {
-    out_ids[q * k + r] = -1;
-    out_fused[q * k + r] = -__builtin_inff();
-  }
+  rrf_query<kRrfThreads>(dense_ids + q * kd, kd, sparse_ids + q * ks, ks, rrf_k, k, out_fused + q * k, out_ids + q * k,
+                         RrfScratch(area));
 }
 
 constexpr int kMaxPoolDim = 8192;  // OPRAG_MAX_DIM
@@ -167,7 +41,6 @@ __device__ __forceinline__ unsigned short f32_to_bf16_rne(float x) {
   return (unsigned short)((u + 0x7fffu + ((u >> 16) & 1u)) >> 16);
 }
 
-// Same-dtype copy, 16 bytes per thread per step.
 // Read-bandwidth probe (diagnostics): a plain streaming read of n16 16-byte words, eight
 // loads in flight per thread, grid-strided; each workgroup folds what it read into one word
 // (so the loads cannot be dropped) and writes it to sink[blockIdx.x].
@@ -190,6 +63,7 @@ __global__ __launch_bounds__(256) void probe_read_kernel(const uint4* __restrict
   if (threadIdx.x == 0) sink[blockIdx.x] = part[0] ^ part[1] ^ part[2] ^ part[3];
 }
 
+// Same-dtype copy, 16 bytes per thread per step.
 __global__ void copy16_kernel(const uint4* __restrict__ src, uint4* __restrict__ dst, long long n16) {
   const long long stride = (long long)gridDim.x * blockDim.x;
   for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += stride) dst[i] = src[i];

@@ -145,6 +145,11 @@ hipError_t launch_sparse(const SparseIndex& sp, const int* qterm_indptr, const i
 hipError_t launch_sparse_weighted(const SparseIndex& sp, const int* qterm_indptr, const int* qterms, int nq, int k,
                                   const float* dense, long long ld, const float* dense_mm, int pd, long long n,
                                   double wd, double wl, float* out_scores, long long* out_ids, hipStream_t s);
+// The hybrid's BM25 list and its reciprocal rank fusion with the dense list in one launch, when
+// the corpus fits one range: the fused top k of each query.
+hipError_t launch_sparse_rrf(const SparseIndex& sp, const int* qterm_indptr, const int* qterms, int nq, int k_sparse,
+                             const long long* dense_ids, int k_dense, int rrf_k, int k, float* out_fused,
+                             long long* out_ids, hipStream_t s);
 hipError_t launch_sparse_dump(const SparseIndex& sp, const int* qterm_indptr, const int* qterms, int nq, float* dump,
                               long long ld, float* dump_mm, long long mm_rows, hipStream_t s);
 hipError_t launch_dense_first(const SparseIndex& sp, const int* qterm_indptr, const int* qterms,
