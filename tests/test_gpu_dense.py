@@ -278,7 +278,8 @@ def test_1m_x_768_bf16_top10_sampled():
     """1,048,576 x 768 bf16 rows (4,096-cluster mixture), 1,024 queries, exact top-10.
     Every query: fp64 scores of every row, the returned scores within the fp32 bound, list
     order, and no unreturned row above the k-th returned score beyond both bounds; 64 sampled
-    queries: the full acceptance rules against a full sort."""
+    queries: the full acceptance rules against a sort of every row within 0.05 of the oracle's
+    own 10th best score (found by a partition of all rows)."""
     dev = device()
     log("generating 1M x 768")
     n = 1 << 20
@@ -293,5 +294,8 @@ def test_1m_x_768_bf16_top10_sampled():
     samp = np.random.default_rng(4).choice(1024, 64, replace=False)
     S, n_close = certify_all(Xb, "bf16", Q, ids, sc, 10, n, samp=samp)
     log(f"unreturned rows within the bounds of a k-th score: {n_close}")
-    reps = accept.check_batch(S, ids[samp], sc[samp], 10, rtol=2e-3)
+    # rows within 0.05 of the oracle's own 10th best take part in the full check (every other
+    # row is far below the top 10: it may be neither returned nor missed)
+    kth = -np.partition(-S, 9, axis=1)[:, 9]
+    reps = accept.check_batch(S, ids[samp], sc[samp], 10, rtol=2e-3, ranked=S >= (kth - 0.05)[:, None])
     assert all(r.ok for r in reps), [r.problems for r in reps if not r.ok][:2]
