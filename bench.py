@@ -94,7 +94,7 @@ def cpu_baseline(rows, queries, budget_s: float) -> dict:
             list(pool.map(lambda i: od.topk_from_scores(S[i:i + per], K), range(0, S.shape[0], per)))
             done += q.shape[0]
             el = time.perf_counter() - t0
-            if el >= budget_s or done >= 4 * Qall.shape[0]:
+            if el >= budget_s or done >= 256 * Qall.shape[0]:  # the queries repeat cyclically
                 break
     blas = [i for i in threadpool_info() if i.get("user_api") == "blas"]
     threads = max([i.get("num_threads", 1) for i in blas] or [1])
