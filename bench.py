@@ -184,8 +184,12 @@ def pmc_summarize(out_dir: str) -> int:
 # Counter passes for the MFMA-bound workloads: one rocprofv3 --pmc run per group (each within
 # the per-block counter limits), each over a short run of `bench.py --pmc-workload NAME`.
 PMC_GROUPS = {"fetch": "FETCH_SIZE", "write": "WRITE_SIZE", "l2": "TCC_HIT_sum TCC_MISS_sum",
-              "mfma": "SQ_VALU_MFMA_BUSY_CYCLES SQ_INSTS_VALU_MFMA_MOPS_BF16 SQ_BUSY_CYCLES GRBM_GUI_ACTIVE"}
+              "mfma": "SQ_VALU_MFMA_BUSY_CYCLES SQ_INSTS_VALU_MFMA_MOPS_BF16 SQ_BUSY_CYCLES GRBM_GUI_ACTIVE",
+              "lat": "TCP_TCC_READ_REQ_LATENCY_sum TCP_TCC_READ_REQ_sum TCC_EA0_RDREQ_LEVEL_sum TCC_EA0_RDREQ_sum",
+              "wait": "SQ_WAIT_INST_ANY SQ_WAVE_CYCLES SQ_INSTS_LDS SQ_LDS_BANK_CONFLICT SQ_INSTS_VMEM_RD TA_BUSY_avr"}
 PMC_WORKLOADS = {
+    "b256": {"title": "32,768 x 1,024 bf16, batch 256, top-5 (8 cold slabs)", "n": N_ROWS, "d": DIM,
+             "batch": 256, "k": 5},
     "b1024": {"title": "32,768 x 1,024 bf16, batch 1,024, top-5 (8 cold slabs)", "n": N_ROWS, "d": DIM,
               "batch": 1024, "k": 5},
     "c4": {"title": "1,048,576 x 768 bf16, batch 1,024, top-10", "n": 1 << 20, "d": 768, "batch": 1024, "k": 10},
@@ -332,6 +336,17 @@ def pmc_workload_summarize(name: str, out_dir: str) -> int:
                          f"active cycles / duration = {gui / d_us / 1e3:.3f} GHz")
         lines.append(f"  MFMA utilisation SQ_VALU_MFMA_BUSY_CYCLES / (cycles per XCD x {n_simd} SIMDs): "
                      f"{med['SQ_VALU_MFMA_BUSY_CYCLES'] / (gui * n_simd):.4f}")
+    if "TCP_TCC_READ_REQ_LATENCY_sum" in med and med.get("TCP_TCC_READ_REQ_sum"):
+        lines.append(f"  L1 -> L2 read latency (TCP_TCC_READ_REQ_LATENCY / TCP_TCC_READ_REQ): "
+                     f"{med['TCP_TCC_READ_REQ_LATENCY_sum'] / med['TCP_TCC_READ_REQ_sum']:.0f} cycles per request")
+    if "TCC_EA0_RDREQ_LEVEL_sum" in med and med.get("TCC_EA0_RDREQ_sum"):
+        lines.append(f"  L2 -> memory read latency (TCC_EA0_RDREQ_LEVEL / TCC_EA0_RDREQ): "
+                     f"{med['TCC_EA0_RDREQ_LEVEL_sum'] / med['TCC_EA0_RDREQ_sum']:.0f} cycles per request")
+    if "SQ_WAIT_INST_ANY" in med and med.get("SQ_WAVE_CYCLES"):
+        lines.append(f"  wave time waiting on a dependency (SQ_WAIT_INST_ANY / SQ_WAVE_CYCLES): "
+                     f"{med['SQ_WAIT_INST_ANY'] / med['SQ_WAVE_CYCLES']:.3f}")
+    if "SQ_LDS_BANK_CONFLICT" in med and med.get("SQ_INSTS_LDS"):
+        lines.append(f"  LDS bank-conflict cycles per LDS instruction: {med['SQ_LDS_BANK_CONFLICT'] / med['SQ_INSTS_LDS']:.3f}")
     if "SQ_INSTS_VALU_MFMA_MOPS_BF16" in med and flops:
         lines.append(f"  MFMA flops SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512: {med['SQ_INSTS_VALU_MFMA_MOPS_BF16'] * 512:.4g} "
                      f"(algorithmic 2 B N d = {flops:.4g})")
