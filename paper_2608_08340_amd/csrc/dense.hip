@@ -2157,10 +2157,13 @@ struct KernelInfo {
       MFK(DT, NW, MW, RS, G, 16, 0, OCC, LO, HI)
 // The single-query-block kernels aim for one workgroup per CU: two 64-row tiles each, so the
 // ring streams across a tile boundary and the second tile takes the running-threshold path.
+// The 128-query list kernels aim for one workgroup per CU as well (their LDS allows no
+// second): one round of workgroups, each streaming all of its chunk's tiles with the ring
+// running on through the selections, instead of two rounds of half-length chunks.
 #define MF_SET(DT)                                                                              \
   MF_KS(DT, 1, 1, 16, 1, 1, 1, 16), MF_KS(DT, 1, 1, 4, 1, 1, 1, 16), MF_KS(DT, 4, 2, 8, 1, 4, 17, 64), \
-      MF_KS(DT, 4, 2, 4, 1, 4, 17, 64), MFK(DT, 8, 4, 4, 2, 5, 0, 2, 65, 1 << 30),                \
-      MFK(DT, 8, 4, 4, 4, 8, 0, 2, 65, 1 << 30), MFK(DT, 8, 4, 4, 4, 16, 0, 2, 65, 1 << 30),         \
+      MF_KS(DT, 4, 2, 4, 1, 4, 17, 64), MFK(DT, 8, 4, 4, 2, 5, 0, 1, 65, 1 << 30),                \
+      MFK(DT, 8, 4, 4, 4, 8, 0, 1, 65, 1 << 30), MFK(DT, 8, 4, 4, 4, 16, 0, 1, 65, 1 << 30),         \
       MFK(DT, 2, 4, 8, 1, 8, 1, 4, 1, 1 << 30), MFK(DT, 2, 4, 4, 1, 8, 1, 4, 1, 1 << 30),            \
       MFKQ(DT, 1, 1, 16, 1, 5, 2, 8, 1, 16, kWaves, 8), MFK(DT, 1, 1, 16, 1, 5, 2, 8, 1, 16),          \
       MFK(DT, 1, 1, 4, 1, 5, 2, 8, 1, 16),                                                          \
@@ -2203,11 +2206,12 @@ constexpr long long kFilterLast = 16;         // row growth into the last level
 constexpr long long kFilterGrow = 64;         // row growth between earlier levels
 constexpr long long kFilterAllRows = 32768;   // up to this many rows a buffer holds every row
 
-// Workgroups per query block that fill the chip twice over (at least enough to keep every
-// chunk of a ring kernel under 2^30 bytes of rows, the reach of its 32-bit offsets).
+// Workgroups per query block such that the grid holds at most the kernel's target number of
+// workgroups per CU (at least enough to keep every chunk of a ring kernel under 2^30 bytes of
+// rows, the reach of its 32-bit offsets).  Rounding down keeps a one-per-CU grid in one round.
 long long chunk_bound(const KernelInfo& ki, int d, long long n_rows, int n_qblocks, int n_cus, long long* min_chunks) {
   const long long target = (long long)n_cus * ki.chunk_target;
-  long long bound = std::max(1ll, (target + n_qblocks - 1) / n_qblocks);
+  long long bound = std::max(1ll, target / n_qblocks);
   long long mc = 1;
   if (ki.ring) {
     const long long n_tiles = (n_rows + ki.tile_rows - 1) / ki.tile_rows;
