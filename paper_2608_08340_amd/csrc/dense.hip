@@ -951,7 +951,7 @@ struct BlockArea {
 template <int BN, int MW, int WV, typename Sel>
 __device__ __forceinline__ bool blk_epilogue(const f32x4 (&acc)[MW][BN / 16], Sel& sel, unsigned char* area,
                                              unsigned char* scratch, long long tile0, long long row_end, int q_lim,
-                                             int k) {
+                                             int k, bool split) {
   constexpr int NW = BN / 16;
   constexpr int KS = 5;
   constexpr int NG = WV * 4;              // groups (lanes) per query
@@ -1026,16 +1026,21 @@ __device__ __forceinline__ bool blk_epilogue(const f32x4 (&acc)[MW][BN / 16], Se
     }
   }
   lds_barrier();
-  // 4. the owner takes the scores >= tau of its query's blocks: a mask of the hits of a block
-  // (one per active group, so usually a single bit), then one insertion per set bit with the
-  // score re-read at its offset
-  if (tid < q_lim) {
-    const float tau = thr[tid];
+  // 4. the query's two threads (sub 0, its owner, and sub 1) take the scores >= tau of its
+  // blocks, alternate blocks each: a mask of the hits of a block (one per active group, so
+  // usually a single bit), then one insertion per set bit with the score re-read at its offset.
+  // Sub 1 collects into its own (otherwise empty) list and hands it to the owner through LDS.
+  constexpr int SP = WV * 64 / BN >= 2 ? 2 : 1;  // threads sharing a query's blocks
+  const int qq = tid % BN, sub = tid / BN;
+  const int sp = split ? SP : 1;
+  if (qq < q_lim && sub < sp) {
+    const float tau = thr[qq];
     int rank = 0;
-    for (unsigned mm = gmask[tid]; mm; mm &= mm - 1, ++rank) {
+    for (unsigned mm = gmask[qq]; mm; mm &= mm - 1, ++rank) {
+      if (sp == 2 && (rank & 1) != sub) continue;
       const int gg = __builtin_ctz(mm);
       const long long r0 = tile0 + (gg >> 2) * MW * 16 + (gg & 3) * 4;
-      const float* src = blk + tid * QSTR + rank * VALS;
+      const float* src = blk + qq * QSTR + rank * VALS;
       unsigned hm = 0;
 #pragma unroll
       for (int mi = 0; mi < MW; ++mi) {
@@ -1046,6 +1051,22 @@ __device__ __forceinline__ bool blk_epilogue(const f32x4 (&acc)[MW][BN / 16], Se
       for (; hm; hm &= hm - 1) {
         const int pp = __builtin_ctz(hm);
         sel.run.insert(composite(src[pp], (uint32_t)(r0 + (pp >> 2) * 16 + (pp & 3))));
+      }
+    }
+  }
+  if (SP == 2 && split) {
+    u64* hand = Sel::cand_of(scratch);  // [BN][KS]; the group maxima there are consumed
+    if (sub == 1 && qq < q_lim) {
+#pragma unroll
+      for (int i = 0; i < KS; ++i) hand[qq * KS + i] = sel.run.v[i];
+      sel.run.clear();
+    }
+    lds_barrier();
+    if (sub == 0 && qq < q_lim) {
+#pragma unroll
+      for (int i = 0; i < KS; ++i) {
+        const u64 c = hand[qq * KS + i];
+        if (c) sel.run.insert(c);
       }
     }
   }
@@ -1434,7 +1455,7 @@ __global__ __launch_bounds__(WV * 64) void dense_mfma_kernel(DenseArgs a) {
         if (!done) {
           if constexpr (kBlk)
             done = blk_epilogue<BN, MW, WV>(acc, sel, reinterpret_cast<unsigned char*>(S), scratch, tile0, row_end,
-                                            q_lim, a.k);
+                                            q_lim, a.k, t == 0);
           else if constexpr (kRank)
             done = rank_epilogue<BN, MW, KS, WV>(acc, sel, reinterpret_cast<unsigned char*>(S), scratch, tile0,
                                                  row_end, q_lim, a.k);
