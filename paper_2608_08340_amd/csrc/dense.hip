@@ -2226,7 +2226,7 @@ int pick_kernel(int dtype, int d, int nq, int k, int sel) {
 constexpr long long kFilterMin = 2048;        // fewest rows of a level that has a successor
 constexpr long long kFilterFirstMax = 4096;   // most rows of the first level
 constexpr long long kFilterLast = 16;         // row growth into the last level
-constexpr long long kFilterGrow = 64;         // row growth between earlier levels
+constexpr long long kFilterGrow = 8;          // row growth between earlier levels
 constexpr long long kFilterAllRows = 32768;   // up to this many rows a buffer holds every row
 
 // Workgroups per query block such that the grid holds at most the kernel's target number of
@@ -2296,8 +2296,8 @@ DensePlan plan_dense(int dtype, int d, long long n_rows, int nq, int k, int n_cu
   // the last holds n_rows / kFilterLast rows (the last level, the one that streams the whole
   // index, then admits about k * kFilterLast rows per query), earlier ones shrink
   // kFilterGrow-fold (to no fewer than kFilterMin rows) until the first has at most
-  // kFilterFirstMax.  A level expects at most about k * kFilterGrow candidates per query; fcap
-  // allows four times that, and the whole first level.  Up to kFilterAllRows rows a buffer
+  // kFilterFirstMax.  A level expects at most about k * max(kFilterGrow, kFilterLast)
+  // candidates per query; fcap allows four times that, and the whole first level.  Up to kFilterAllRows rows a buffer
   // holds every row (at most 256 KB per query), so no level can overflow and the repair
   // launches are left out.
   long long back[8];
@@ -2317,7 +2317,8 @@ DensePlan plan_dense(int dtype, int d, long long n_rows, int nq, int k, int n_cu
   for (int l = 0; l < nb; ++l) p.level_rows[l] = back[nb - 1 - l];
   p.fcap = n_rows <= kFilterAllRows
                ? std::max(1ll, n_rows)
-               : std::max(1ll, std::min(n_rows, std::max(p.level_rows[0], 4 * kFilterGrow * (long long)k)));
+               : std::max(1ll, std::min(n_rows, std::max(p.level_rows[0],
+                                                         4 * std::max(kFilterGrow, kFilterLast) * (long long)k)));
   p.repair = p.fcap < n_rows;
   p.chunk_bound = chunk_bound(ki, d, n_rows, p.n_qblocks, n_cus, nullptr);
   p.kernel0 = p.kernel;
