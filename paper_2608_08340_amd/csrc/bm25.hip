@@ -960,6 +960,22 @@ __global__ __launch_bounds__(kDfThreads) void dense_first_kernel(int vocab, long
   // query of at most kTerms occurrences walks the lists once and sums the two kinds from the
   // stored matches; a longer one walks them once per kind.
   const bool single = e_end - tb <= kTerms;
+  // The first step of the candidate's list is loaded here, before the query-term setup and
+  // its barrier, so its latency overlaps them; every later step (and every later walk of the
+  // list) loads its own entries.
+  constexpr int kStep = 16;
+  int tm[kStep];
+  float wt[kStep];
+  auto load_step = [&](long long f) {
+#pragma unroll
+    for (int v = 0; v < kStep; ++v) {
+      const long long g = f + v * kDfLanes;
+      tm[v] = g < f1 ? fwd_term[g] : -1;
+      wt[v] = g < f1 ? fwd_w[g] : 0.f;
+    }
+  };
+  load_step(f0 + j);
+  bool pre = true;  // tm / wt hold the first step of the list
   for (int pass = 0; pass < (single ? 1 : 2); ++pass)
   for (int e0 = tb; e0 < e_end; e0 += kTerms) {
     const int ne = min(kTerms, e_end - e0);
@@ -996,16 +1012,9 @@ __global__ __launch_bounds__(kDfThreads) void dense_first_kernel(int vocab, long
     // sixteen entries per thread and step, all loads issued before any comparison; per query
     // term the weights of matching entries are summed (a list holds a term once, so the sum
     // is that weight or 0) and a match is stored
-    constexpr int kStep = 16;
     for (long long f = f0 + j; f < f1; f += kStep * kDfLanes) {
-      int tm[kStep];
-      float wt[kStep];
-#pragma unroll
-      for (int v = 0; v < kStep; ++v) {
-        const long long g = f + v * kDfLanes;
-        tm[v] = g < f1 ? fwd_term[g] : -1;
-        wt[v] = g < f1 ? fwd_w[g] : 0.f;
-      }
+      if (!pre) load_step(f);
+      pre = false;
       for (int u = 0; u < ne; ++u) {
         const int tu = qt_s[u];
         if (tu < 0) continue;  // uniform: the term takes part at an earlier occurrence, or never
