@@ -1026,10 +1026,11 @@ __device__ __forceinline__ bool blk_epilogue(const f32x4 (&acc)[MW][BN / 16], Se
     }
   }
   lds_barrier();
-  // 4. the query's two threads (sub 0, its owner, and sub 1) take the scores >= tau of its
-  // blocks, alternate blocks each: a mask of the hits of a block (one per active group, so
-  // usually a single bit), then one insertion per set bit with the score re-read at its offset.
-  // Sub 1 collects into its own (otherwise empty) list and hands it to the owner through LDS.
+  // 4. the scores >= tau of the query's blocks go into its list: a mask of the hits of a block
+  // (one per active group, so usually a single bit), then one insertion per set bit with the
+  // score re-read at its offset.  The owner (sub 0) does this alone, except with split (a
+  // chunk's first tile, where most hits fall): then the query's two threads take alternate
+  // blocks, sub 1 into its own (otherwise empty) list, which it hands to the owner through LDS.
   constexpr int SP = WV * 64 / BN >= 2 ? 2 : 1;  // threads sharing a query's blocks
   const int qq = tid % BN, sub = tid / BN;
   const int sp = split ? SP : 1;
@@ -2297,9 +2298,9 @@ DensePlan plan_dense(int dtype, int d, long long n_rows, int nq, int k, int n_cu
   // index, then admits about k * kFilterLast rows per query), earlier ones shrink
   // kFilterGrow-fold (to no fewer than kFilterMin rows) until the first has at most
   // kFilterFirstMax.  A level expects at most about k * max(kFilterGrow, kFilterLast)
-  // candidates per query; fcap allows four times that, and the whole first level.  Up to kFilterAllRows rows a buffer
-  // holds every row (at most 256 KB per query), so no level can overflow and the repair
-  // launches are left out.
+  // candidates per query; fcap allows four times that, and the whole first level.  Up to
+  // kFilterAllRows rows a buffer holds every row (at most 256 KB per query), so no level can
+  // overflow and the repair launches are left out.
   long long back[8];
   int nb = 0;
   back[nb++] = n_rows;
