@@ -52,9 +52,11 @@ def c2():
     return synth.dense_32k()
 
 
-@pytest.mark.parametrize("nq", [1, 16, 256, 1024])
+@pytest.mark.parametrize("nq", [1, 16, 256, 384, 768, 1024])
 def test_32k_x_1024_bf16_top5(c2, nq):
-    """32,768 x 1,024 bf16 mixture rows; query batches 1, 16, 256, 1,024; exact top-5."""
+    """32,768 x 1,024 bf16 mixture rows; query batches 1, 16, 256, 384, 768, 1,024; exact
+    top-5.  384 and 768 queries (three and six query blocks) get grids of fewer workgroups
+    than CUs, with two and four tiles per chunk."""
     log("32k bf16 nq", nq)
     q = c2.queries[:nq].contiguous()
     _, sc, ids = _run(c2.rows, q, 5, "bf16")
