@@ -65,6 +65,19 @@ def test_32k_x_1024_bf16_top5(c2, nq):
     assert all(r.recall == 1.0 for r in reps)
 
 
+@pytest.mark.parametrize("nq", [100, 256])
+def test_32k_x_1024_bf16_top100(c2, nq):
+    """The hybrid's dense list shape: 32,768 x 1,024 bf16, top-100 (filtered levels 2,048 ->
+    32,768), at 100 queries (two 64-query blocks over 128-row tiles) and 256 (two 128-query
+    blocks)."""
+    log("32k bf16 top-100 nq", nq)
+    q = c2.queries[:nq].contiguous()
+    _, sc, ids = _run(c2.rows, q, 100, "bf16")
+    S, X, Q = oracle_scores(c2.rows, q, "bf16")
+    reps = check_dense(S, X, Q, ids, sc, 100, "bf16")
+    assert all(r.recall == 1.0 for r in reps)
+
+
 @pytest.mark.parametrize("dtype", ["bf16", "f16", "f32"])
 @pytest.mark.parametrize("k", [1, 5, 16, 100])
 def test_exact_integer_scores_and_ties(dtype, k):
