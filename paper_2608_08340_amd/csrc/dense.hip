@@ -1226,7 +1226,7 @@ __global__ __launch_bounds__(WV * 64) void dense_mfma_kernel(DenseArgs a) {
   // once), so the main loop has no query staging and no barrier.  Otherwise two slots
   // alternate, one super-step ahead.
   constexpr int QBYTES = (QR > 0 ? QR : 2) * QSLOT;
-  static_assert(QR == 0 || SEL == 2 || SEL == 4, "resident queries: filtered selection only");
+  static_assert(QR == 0 || SEL == 0 || SEL == 2 || SEL == 4, "resident queries: lists or filtered selection");
   constexpr bool kFilt = SEL == 2 || SEL == 4;  // filtered: 4 is the variant for many hits per tile
   // k <= 5: the small-tile kernels take the one-pass rank epilogue (and the running-threshold
   // test for later tiles); the 128-query kernel keeps the block epilogue on every tile, which
@@ -1389,21 +1389,41 @@ __global__ __launch_bounds__(WV * 64) void dense_mfma_kernel(DenseArgs a) {
       // prologue: every super-step of the queries into its own slot (QB super-steps' loads in
       // flight at once), then rows of k-steps 0 .. PX-1
       constexpr int QB = QPT >= 8 ? 1 : 8 / QPT;
-      for (int u0 = 0; u0 < nq4; u0 += QB) {
+      if (SEL == 0 && QB > 1 && nq4 <= QB) {
+        // one batch (the small-batch lists kernel): every super-step's queries, then the rows
+        // of k-steps 0 .. PX-1, then the queries to their slots, so the wait for the queries
+        // leaves the rows in flight
         u32x4 qb[QB][QPT];
 #pragma unroll
         for (int u = 0; u < QB; ++u)
 #pragma unroll
-          for (int j = 0; j < QPT; ++j)
-            if (QB == 1 || u0 + u < nq4) qb[u][j] = buffer_load16(r_q, qoff[j] + (u0 + u) * (SK * 2));
+          for (int j = 0; j < QPT; ++j) qb[u][j] = buffer_load16(r_q, qoff[j] + min(u, nq4 - 1) * (SK * 2));
+        __builtin_amdgcn_sched_barrier(0);  // keep the queries ahead of the rows in the load order
+#pragma unroll
+        for (int u = 0; u < PX; ++u) OPRAG_ROWS(u)
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int u = 0; u < QB; ++u)
 #pragma unroll
           for (int j = 0; j < QPT; ++j)
-            if (QB == 1 || u0 + u < nq4) *reinterpret_cast<u32x4*>(qslots + (u0 + u) * QSLOT + qdst[j]) = qb[u][j];
-      }
+            if (u < nq4) *reinterpret_cast<u32x4*>(qslots + u * QSLOT + qdst[j]) = qb[u][j];
+      } else {
+        for (int u0 = 0; u0 < nq4; u0 += QB) {
+          u32x4 qb[QB][QPT];
 #pragma unroll
-      for (int u = 0; u < PX; ++u) OPRAG_ROWS(u)
+          for (int u = 0; u < QB; ++u)
+#pragma unroll
+            for (int j = 0; j < QPT; ++j)
+              if (QB == 1 || u0 + u < nq4) qb[u][j] = buffer_load16(r_q, qoff[j] + (u0 + u) * (SK * 2));
+#pragma unroll
+          for (int u = 0; u < QB; ++u)
+#pragma unroll
+            for (int j = 0; j < QPT; ++j)
+              if (QB == 1 || u0 + u < nq4) *reinterpret_cast<u32x4*>(qslots + (u0 + u) * QSLOT + qdst[j]) = qb[u][j];
+        }
+#pragma unroll
+        for (int u = 0; u < PX; ++u) OPRAG_ROWS(u)
+      }
     } else {
       // prologue: queries of super-step 0 first (their wait then leaves the row loads in
       // flight), rows of k-steps 0 .. PX-1, queries of super-step 0 to slot 0, queries of
@@ -2179,12 +2199,15 @@ struct KernelInfo {
       MFK(DT, NW, MW, RS, G, 16, 0, OCC, LO, HI)
 // The single-query-block kernels aim for one workgroup per CU: two 64-row tiles each, so the
 // ring streams across a tile boundary and the second tile takes the running-threshold path.
+// Their top-5 instance keeps the block's queries resident in LDS (d <= 1,024): no query loads
+// join the ring's in-order load counter, and one barrier per tile.
 // The 128-query list kernels aim for one workgroup per CU as well (their LDS allows no
 // second): one round of workgroups, each streaming all of its chunk's tiles with the ring
 // running on through the selections, instead of two rounds of half-length chunks.
 #define MF_SET(DT)                                                                              \
-  MF_KS(DT, 1, 1, 16, 1, 1, 1, 16), MF_KS(DT, 1, 1, 4, 1, 1, 1, 16), MF_KS(DT, 4, 2, 8, 1, 4, 17, 64), \
-      MF_KS(DT, 4, 2, 4, 1, 4, 17, 64), MFK(DT, 8, 4, 4, 2, 5, 0, 1, 65, 1 << 30),                \
+  MFKQ(DT, 1, 1, 16, 1, 5, 0, 1, 1, 16, kWaves, 8), MF_KS(DT, 1, 1, 16, 1, 1, 1, 16),                \
+      MF_KS(DT, 1, 1, 4, 1, 1, 1, 16), MF_KS(DT, 4, 2, 8, 1, 4, 17, 64), MF_KS(DT, 4, 2, 4, 1, 4, 17, 64), \
+      MFK(DT, 8, 4, 4, 2, 5, 0, 1, 65, 1 << 30),                                                    \
       MFK(DT, 8, 4, 4, 4, 8, 0, 1, 65, 1 << 30), MFK(DT, 8, 4, 4, 4, 16, 0, 1, 65, 1 << 30),         \
       MFK(DT, 2, 4, 8, 1, 8, 1, 4, 1, 1 << 30), MFK(DT, 2, 4, 4, 1, 8, 1, 4, 1, 1 << 30),            \
       MFKQ(DT, 1, 1, 16, 1, 5, 2, 8, 1, 16, kWaves, 8), MFK(DT, 1, 1, 16, 1, 5, 2, 8, 1, 16),          \
