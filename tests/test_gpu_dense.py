@@ -110,6 +110,18 @@ def test_ragged_sizes_and_k(dtype, n, nq, k):
     check_dense(S, X, Q, ids, sc, k, dtype, label=f"n={n} nq={nq} k={k}")
 
 
+@pytest.mark.parametrize("d", [512, 1536])
+@pytest.mark.parametrize("nq", [1, 16])
+def test_small_batch_resident_and_streamed_queries(d, nq):
+    """The batch-1 to 16 top-5 kernel keeps its query block resident in LDS up to 1,024
+    dimensions: d = 512 fills four of its eight slices; d = 1,536 takes the streamed kernel."""
+    device()
+    w = synth.mixture_dense(300 + d // 128, 5000, d, 16, nq, 5, "bf16")
+    _, sc, ids = _run(w.rows, w.queries, 5, "bf16")
+    S, X, Q = oracle_scores(w.rows, w.queries, "bf16")
+    check_dense(S, X, Q, ids, sc, 5, "bf16", label=f"d={d} nq={nq}")
+
+
 @pytest.mark.parametrize("kind", ["ints", "four_rows"])
 @pytest.mark.parametrize("dtype", ["bf16", "f16"])
 @pytest.mark.parametrize("nq,k", [(1, 7), (16, 5), (40, 16), (130, 5), (130, 10)])
