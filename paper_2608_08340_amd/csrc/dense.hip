@@ -689,7 +689,7 @@ __device__ __forceinline__ void filt_all_tile(const f32x4 (&acc)[MW][BN / 16], l
 template <bool DH, int BN, int MW, int WV>
 __device__ __forceinline__ void filt_tile(const f32x4 (&acc)[MW][BN / 16], const float (&th)[BN / 16],
                                           unsigned char* area, long long tile0, long long row_end, int q0, int q_lim,
-                                          bool last, const DenseArgs& a) {
+                                          bool last, bool check, const DenseArgs& a) {
   constexpr int SCAP = SelFilter<BN>::SCAP;
   constexpr int TR = WV * MW * 16;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -706,6 +706,9 @@ __device__ __forceinline__ void filt_tile(const f32x4 (&acc)[MW][BN / 16], const
     else
       filt_collect_sparse<false, BN, MW>(acc, th, area, tile0, row0, lim, q0, a);
   }
+  // The stage is looked at (and flushed) only on check tiles; in between it fills, and hits
+  // past its capacity go straight to the global buffer (filt_collect_*), so no barrier is needed.
+  if (!check && !last) return;  // workgroup-uniform
   lds_barrier();
   if (last)  // workgroup-uniform
     filt_flush<BN, WV * 64>(area, q0, q_lim, a);
@@ -1228,6 +1231,7 @@ __global__ __launch_bounds__(WV * 64) void dense_mfma_kernel(DenseArgs a) {
   constexpr int QBYTES = (QR > 0 ? QR : 2) * QSLOT;
   static_assert(QR == 0 || SEL == 0 || SEL == 2 || SEL == 4, "resident queries: lists or filtered selection");
   constexpr bool kFilt = SEL == 2 || SEL == 4;  // filtered: 4 is the variant for many hits per tile
+  constexpr int kFiltCheck = 32;  // SEL 2: tiles between looks at the stage (a power of two)
   // k <= 5: the small-tile kernels take the one-pass rank epilogue (and the running-threshold
   // test for later tiles); the 128-query kernel keeps the block epilogue on every tile, which
   // leaves its main loop the register budget it is scheduled for.
@@ -1366,7 +1370,11 @@ __global__ __launch_bounds__(WV * 64) void dense_mfma_kernel(DenseArgs a) {
       OPRAG_KSTEP(4 * (H) + 1, 1, qs)                                                    \
       OPRAG_KSTEP(4 * (H) + 2, 2, qs)                                                    \
       OPRAG_KSTEP(4 * (H) + 3, 3, qs)                                                    \
-      if ((H) == 0 && s0 == t * nk) lds_barrier(); /* previous tile's stage flushes done */ \
+      /* the previous tile's stage flushes are done (filtered mode: if it looked at the  \
+         stage) */                                                                       \
+      if ((H) == 0 && s0 == t * nk &&                                                    \
+          (!kFilt || SEL == 4 || (t > 0 && ((t - 1) & (kFiltCheck - 1)) == kFiltCheck - 1))) \
+        lds_barrier();                                                                   \
       OPRAG_BFRAG(qn, 0)                                                                 \
     } else {                                                                             \
       const int sup = s0 / 4 + (H);                                                      \
@@ -1465,7 +1473,8 @@ __global__ __launch_bounds__(WV * 64) void dense_mfma_kernel(DenseArgs a) {
         if (a.th == nullptr)  // launch-uniform
           filt_all_tile<BN, MW, WV>(acc, tile0, row_end, q0, q_lim, a);
         else
-          filt_tile<SEL == 4, BN, MW, WV>(acc, th, scratch, tile0, row_end, q0, q_lim, t == n_tiles - 1, a);
+          filt_tile<SEL == 4, BN, MW, WV>(acc, th, scratch, tile0, row_end, q0, q_lim, t == n_tiles - 1,
+                                          SEL == 4 || (t & (kFiltCheck - 1)) == kFiltCheck - 1, a);
         done = true;
       } else if constexpr (SEL == 0) {
         // A chunk's first tile fills the lists through the group path; the tiles after it
