@@ -2221,14 +2221,15 @@ struct KernelInfo {
       MFK(DT, 2, 4, 8, 1, 8, 1, 4, 1, 1 << 30), MFK(DT, 2, 4, 4, 1, 8, 1, 4, 1, 1 << 30),            \
       MFKQ(DT, 1, 1, 16, 1, 5, 2, 1, 1, 16, kWaves, 8), MFK(DT, 1, 1, 16, 1, 5, 2, 8, 1, 16),          \
       MFK(DT, 1, 1, 4, 1, 5, 2, 8, 1, 16),                                                          \
-      MFK(DT, 4, 2, 8, 1, 5, 2, 4, 17, 128), MFK(DT, 4, 2, 4, 1, 5, 2, 4, 17, 128),                    \
+      MFK(DT, 4, 2, 8, 1, 5, 2, 1, 17, 128), MFK(DT, 4, 2, 4, 1, 5, 2, 1, 17, 128),                    \
       MFKQ(DT, 8, 4, 4, 1, 5, 2, 2, 65, 1 << 30, kWaves, 3), MFK(DT, 8, 4, 4, 1, 5, 2, 2, 65, 1 << 30), \
       MFK(DT, 8, 4, 4, 1, 5, 3, 2, 1, 1 << 30), MF_DH(DT)
 // The resident-query small filtered kernel (batches up to 16, and every first level) aims
 // for one workgroup per CU too: 2,048 first-level rows are 16 query blocks x 16 chunks of two
 // 64-row tiles, one round, instead of 512 one-tile workgroups that each load their queries.
 // The 64-query filtered kernels also serve 65-128 queries (two query blocks over 128-row
-// tiles keep every CU busy, where one 128-query block over 256-row tiles fills half of them).
+// tiles keep every CU busy, where one 128-query block over 256-row tiles fills half of them),
+// and aim for one workgroup per CU as well.
 // Filtered kernels for levels with many hits per tile (SEL 4), one per SEL 2 shape.
 #define MF_DH(DT)                                                                                          \
   MFK(DT, 1, 1, 16, 1, 5, 4, 8, 1, 16), MFK(DT, 1, 1, 4, 1, 5, 4, 8, 1, 16), MFK(DT, 4, 2, 8, 1, 5, 4, 4, 17, 128), \
