@@ -841,21 +841,32 @@ __device__ __forceinline__ void thr_collect(const f32x4 (&acc)[MW][BN / 16], con
   constexpr int NW = BN / 16;
   const int lane = threadIdx.x & 63;
   auto ok = [&](int mi, int r) { return FULL || mi * 16 + r < lim; };
-  int c[NW];
+  // the thresholds of this lane's query slots, read together (one wait), and the maxima
+  float th[NW], mx[NW];
+#pragma unroll
+  for (int ni = 0; ni < NW; ++ni) th[ni] = thr[ni * 16 + (lane & 15)];
 #pragma unroll
   for (int ni = 0; ni < NW; ++ni) {
-    const float th = thr[ni * 16 + (lane & 15)];
     float m = kNegInf;
 #pragma unroll
     for (int mi = 0; mi < MW; ++mi)
 #pragma unroll
       for (int r = 0; r < 4; ++r) m = __builtin_fmaxf(m, ok(mi, r) ? acc[mi][ni][r] : kNegInf);
+    mx[ni] = m;
+  }
+  bool any = false;
+#pragma unroll
+  for (int ni = 0; ni < NW; ++ni) any |= mx[ni] >= th[ni];
+  if (__ballot(any) == 0ull) return;  // wave-uniform: no score of this wave reaches its threshold
+  int c[NW];
+#pragma unroll
+  for (int ni = 0; ni < NW; ++ni) {
     int cc = 0;
-    if (m >= th) {
+    if (mx[ni] >= th[ni]) {
 #pragma unroll
       for (int mi = 0; mi < MW; ++mi)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) cc += (ok(mi, r) && acc[mi][ni][r] >= th) ? 1 : 0;
+        for (int r = 0; r < 4; ++r) cc += (ok(mi, r) && acc[mi][ni][r] >= th[ni]) ? 1 : 0;
     }
     c[ni] = cc;
   }
@@ -870,7 +881,6 @@ __device__ __forceinline__ void thr_collect(const f32x4 (&acc)[MW][BN / 16], con
       continue;
     }
     const int n = ni * 16 + (lane & 15);
-    const float th = thr[n];
     uint2* dst = cand + n * CAP;
     int j = base[ni];
 #pragma unroll
@@ -878,7 +888,7 @@ __device__ __forceinline__ void thr_collect(const f32x4 (&acc)[MW][BN / 16], con
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const float x = acc[mi][ni][r];
-        if (ok(mi, r) && x >= th) {
+        if (ok(mi, r) && x >= th[ni]) {
           dst[j] = make_uint2(__float_as_uint(x), (unsigned)(row0 + mi * 16 + r));
           ++j;
         }
