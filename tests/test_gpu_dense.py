@@ -65,6 +65,18 @@ def test_32k_x_1024_bf16_top5(c2, nq):
     assert all(r.recall == 1.0 for r in reps)
 
 
+@pytest.mark.parametrize("k", [8, 16])
+def test_32k_x_1024_bf16_top8_top16_batch512(c2, k):
+    """32,768 x 1,024 bf16, 512 queries, k = 8 and 16: the 128-query kernels with the running
+    threshold on every tile after a chunk's first (two tiles per chunk at this batch)."""
+    log("32k bf16 nq 512 k", k)
+    q = c2.queries[:512].contiguous()
+    _, sc, ids = _run(c2.rows, q, k, "bf16")
+    S, X, Q = oracle_scores(c2.rows, q, "bf16")
+    reps = check_dense(S, X, Q, ids, sc, k, "bf16")
+    assert all(r.recall == 1.0 for r in reps)
+
+
 @pytest.mark.parametrize("nq", [100, 256])
 def test_32k_x_1024_bf16_top100(c2, nq):
     """The hybrid's dense list shape: 32,768 x 1,024 bf16, top-100 (filtered levels 2,048 ->
