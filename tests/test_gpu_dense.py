@@ -122,6 +122,37 @@ def test_ragged_sizes_and_k(dtype, n, nq, k):
     check_dense(S, X, Q, ids, sc, k, dtype, label=f"n={n} nq={nq} k={k}")
 
 
+def _sweep_cases(n_cases=40, seed=2608):
+    """Seeded (dtype, n, d, nq, k) draws across the kernel table: dimensions whose k-step count
+    admits rings of 4, 8 or 16 (or only 4), query blocks resident or streamed, the largest
+    dimension, every batch class and both selection strategies."""
+    r = np.random.default_rng(seed)
+    dims = [128, 256, 384, 640, 896, 1024, 1152, 2048, 4096, 8192]
+    batches = [1, 2, 5, 16, 17, 40, 64, 65, 100, 128, 129, 200, 256, 300, 513]
+    ks = [1, 2, 5, 6, 8, 9, 16, 17, 33, 100, 128]
+    out = []
+    for i in range(n_cases):
+        d = dims[i % len(dims)]
+        nq = int(r.choice(batches))
+        k = int(r.choice(ks))
+        n = int(r.integers(300, 5000)) if d <= 2048 else int(r.integers(200, 1500))
+        out.append(("bf16" if i % 3 else "f16", n, d, nq, k))
+    return out
+
+
+@pytest.mark.parametrize("dtype,n,d,nq,k", _sweep_cases())
+def test_seeded_shape_sweep(dtype, n, d, nq, k):
+    """Parity over seeded shapes that reach every ring depth, resident and streamed query
+    blocks, d up to the largest supported dimension, ragged rows and batches, k on both sides
+    of the list/threshold boundary."""
+    log("sweep", dtype, n, d, nq, k)
+    device()
+    w = synth.mixture_dense(500 + d // 128 + nq, n, d, 24, nq, k, dtype)
+    _, sc, ids = _run(w.rows, w.queries, k, dtype)
+    S, X, Q = oracle_scores(w.rows, w.queries, dtype)
+    check_dense(S, X, Q, ids, sc, k, dtype, label=f"{dtype} n={n} d={d} nq={nq} k={k}")
+
+
 @pytest.mark.parametrize("d", [512, 1536])
 @pytest.mark.parametrize("nq", [1, 16])
 def test_small_batch_resident_and_streamed_queries(d, nq):
