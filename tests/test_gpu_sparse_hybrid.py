@@ -88,6 +88,43 @@ def test_bm25_several_chunk_ranges(n_docs, k):
     _check_sparse(B, ids, sc, k, f"multi-range n_docs={n_docs}")
 
 
+def _bm25_sweep_cases(n_cases=14, seed=2609):
+    """Seeded (n_docs, vocab, mean_len, nq, k, max_terms) draws: one chunk to several 32,768-chunk
+    ranges, vocabularies from all-head to flat, short to long queries, k below and above the
+    corpus size."""
+    r = np.random.default_rng(seed)
+    sizes = [1, 7, 300, 5000, 32768, 32769, 45000]
+    out = []
+    for i in range(n_cases):
+        n = sizes[i % len(sizes)]
+        out.append((n, int(r.choice([6, 60, 3000])), float(r.choice([3.0, 20.0, 60.0])),
+                    int(r.choice([1, 7, 64, 300])), int(r.choice([1, 7, 100, 128])), int(r.choice([4, 12, 48]))))
+    return out
+
+
+@pytest.mark.parametrize("n_docs,vocab,mean_len,nq,k,max_terms", _bm25_sweep_cases())
+def test_bm25_seeded_sweep(n_docs, vocab, mean_len, nq, k, max_terms):
+    """BM25 top-k over seeded corpora and query batches against the token-scan oracle
+    (rtol 1e-5), including chunks with no positive score, queries without known terms and
+    queries longer than one 32-occurrence parse batch."""
+    log("bm25 sweep", n_docs, vocab, mean_len, nq, k, max_terms)
+    dev = device()
+    g = np.random.default_rng(n_docs + vocab + nq + k)
+    ind, toks = synth.sparse_corpus(synth.rng(900 + n_docs % 97, 3), n_docs, vocab, 1.1, mean_len)
+    csr = synth.csr_from_tokens(ind, toks, vocab)
+    qs = [list(g.integers(-2, vocab + 2, size=g.integers(0, max_terms + 1))) for _ in range(nq)]
+    qi = np.zeros(nq + 1, dtype=np.int32)
+    qi[1:] = np.cumsum([len(q) for q in qs])
+    qt = np.array([t for q in qs for t in q], dtype=np.int32)
+    idx = make_index(torch.zeros((n_docs, 128), dtype=torch.bfloat16), "bf16")
+    _attach(idx, csr, dev)
+    sc, ids = idx.search_sparse(_t(qi, dev), _t(qt, dev), k)
+    torch.cuda.synchronize()
+    qt_oracle = np.where((qt >= 0) & (qt < vocab), qt, 10 ** 6).astype(np.int64)
+    B = bm25.scores_batch(ind, toks, qi, qt_oracle, 1.2, 0.75)
+    _check_sparse(B, ids, sc, k, f"n_docs={n_docs} vocab={vocab} nq={nq} k={k}")
+
+
 @pytest.mark.parametrize("kind", ["no_head", "one_head", "all_head"])
 def test_bm25_head_rows_and_postings_mix(kind):
     """The most frequent terms (df >= N / 8) are scored from dense rows, the rest from their
