@@ -259,6 +259,57 @@ def test_hybrid_32k_bm25_rrf_top5(c3, correlated):
     log("queries whose stage lists equal the oracle's exactly:", int(same.sum()), "of", len(same))
 
 
+OPRAG_MAX_K = 128
+
+
+def _hybrid_sweep_cases(n_cases=10, seed=2610):
+    """Seeded (n, d, nq, k_dense, k_sparse, rrf_k, k) draws for the RRF hybrid: corpora inside one
+    32,768-chunk range (BM25 and RRF in one launch) and past it (separate RRF launch), fused k
+    from 1 to the sum of both list lengths."""
+    r = np.random.default_rng(seed)
+    out = []
+    for i in range(n_cases):
+        n = [900, 5000, 32768, 40000][i % 4]
+        kd, ks = int(r.choice([1, 5, 17, 100, 128])), int(r.choice([1, 5, 17, 100, 128]))
+        k = int(min(kd + ks, OPRAG_MAX_K, r.choice([1, 5, 10, 64, 128])))
+        out.append((n, int(r.choice([128, 384, 1024])), int(r.choice([1, 16, 100, 257])), kd, ks,
+                    int(r.choice([0, 1, 60, 1000])), k))
+    return out
+
+
+@pytest.mark.timeout(300)
+@pytest.mark.parametrize("n,d,nq,k_dense,k_sparse,rrf_k,k", _hybrid_sweep_cases())
+def test_hybrid_seeded_sweep(n, d, nq, k_dense, k_sparse, rrf_k, k):
+    """The one-call RRF hybrid over seeded shapes: its dense and BM25 stages pass the
+    acceptance rules as stand-alone searches, and the fused list equals exact RRF of those two
+    lists bit for bit."""
+    log("hybrid sweep", n, d, nq, k_dense, k_sparse, rrf_k, k)
+    dev = device()
+    w = synth.mixture_dense(7000 + n % 101 + d, n, d, 32, nq, k_dense, "bf16")
+    g = np.random.default_rng(n + nq)
+    ind, toks = synth.sparse_corpus(synth.rng(950 + n % 89, 3), n, 2000, 1.1, 30.0)
+    csr = synth.csr_from_tokens(ind, toks, 2000)
+    qs = [list(g.integers(0, 2000, size=g.integers(0, 12))) for _ in range(nq)]
+    qi = np.zeros(nq + 1, dtype=np.int32)
+    qi[1:] = np.cumsum([len(q) for q in qs])
+    qt = np.array([t for q in qs for t in q], dtype=np.int32)
+    idx = make_index(w.rows, "bf16")
+    _attach(idx, csr, dev)
+    q = w.queries.to(dev)
+    qit, qtt = _t(qi, dev), _t(qt, dev)
+    fused, fids = idx.search_hybrid(q, qit, qtt, k_dense, k_sparse, rrf_k, k)
+    dsc, dids = idx.search_dense(q, k_dense)
+    ssc, sids = idx.search_sparse(qit, qtt, k_sparse)
+    torch.cuda.synchronize()
+    S, X, Q = oracle_scores(w.rows, w.queries, "bf16")
+    check_dense(S, X, Q, dids, dsc, k_dense, "bf16", label="dense stage")
+    B = bm25.scores_batch(ind, toks, qi, qt.astype(np.int64), 1.2, 0.75)
+    _check_sparse(B, sids, ssc, k_sparse, "bm25 stage")
+    ref_ids, ref_f32, _ = rrf.fuse(dids.cpu().numpy(), sids.cpu().numpy(), rrf_k, k)
+    assert np.array_equal(fids.cpu().numpy(), ref_ids)
+    assert np.array_equal(fused.cpu().numpy().view(np.uint32), ref_f32.view(np.uint32))
+
+
 @pytest.mark.timeout(300)
 def test_hybrid_other_stream_and_graph_replay(c3):
     """A hybrid search (threshold levels with device-side repair gates, BM25, RRF) issued on a
