@@ -529,6 +529,53 @@ def test_weighted_fusion_small_corpus(w_d, w_l, k, n, n_docs, vocab):
     _check_weighted(weighted.fused(S, B, w_d, w_l), sc, ids, k, f"w=({w_d},{w_l}) k={k}")
 
 
+def _fusion_sweep_cases(n_cases=10, seed=2611):
+    """Seeded (n, n_docs, d, nq, n_cand, k, w_dense, w_lex) draws for dense-first and weighted
+    fusion: sparse corpora covering all or part of the index, one or several chunk ranges."""
+    r = np.random.default_rng(seed)
+    out = []
+    for i in range(n_cases):
+        n = [600, 4000, 32768, 40000][i % 4]
+        n_docs = n if i % 3 else int(n * 0.8)
+        w_d = float(r.choice([0.0, 0.25, 0.5, 1.0]))
+        out.append((n, n_docs, int(r.choice([128, 384, 1024])), int(r.choice([1, 16, 100, 257])),
+                    int(r.choice([1, 8, 64, 128])), int(r.choice([1, 5, 33, 128])), w_d, 1.0 - w_d))
+    return out
+
+
+@pytest.mark.timeout(300)
+@pytest.mark.parametrize("n,n_docs,d,nq,n_cand,k,w_d,w_l", _fusion_sweep_cases())
+def test_dense_first_and_weighted_seeded_sweep(n, n_docs, d, nq, n_cand, k, w_d, w_l):
+    """Dense-first (tie-aware check against the oracle's reranking of the GPU's candidates)
+    and weighted fusion (acceptance rules against the fp64 fused scores) over seeded shapes."""
+    from oracle import weighted
+    log("fusion sweep", n, n_docs, d, nq, n_cand, k, w_d, w_l)
+    dev = device()
+    w = synth.mixture_dense(7100 + n % 103 + d, n, d, 32, nq, n_cand, "bf16")
+    g = np.random.default_rng(n + nq + k)
+    ind, toks = synth.sparse_corpus(synth.rng(970 + n % 83, 3), n_docs, 1500, 1.1, 25.0)
+    csr = synth.csr_from_tokens(ind, toks, 1500)
+    qs = [list(g.integers(-1, 1501, size=g.integers(0, 40))) for _ in range(nq)]
+    qi = np.zeros(nq + 1, dtype=np.int32)
+    qi[1:] = np.cumsum([len(q) for q in qs])
+    qt = np.array([t for q in qs for t in q], dtype=np.int32)
+    idx = make_index(w.rows, "bf16")
+    _attach(idx, csr, dev)
+    q = w.queries.to(dev)
+    qit, qtt = _t(qi, dev), _t(qt, dev)
+    fused, fids = idx.search_hybrid_dense_first(q, qit, qtt, n_cand, 60, k)
+    dsc, dids = idx.search_dense(q, n_cand)
+    wsc, wids = idx.search_hybrid_weighted(q, qit, qtt, w_d, w_l, k)
+    torch.cuda.synchronize()
+    S, X, Q = oracle_scores(w.rows, w.queries, "bf16")
+    check_dense(S, X, Q, dids, dsc, n_cand, "bf16", label="candidates")
+    qt_oracle = np.where((qt >= 0) & (qt < 1500), qt, 10 ** 6).astype(np.int64)
+    B = np.zeros((nq, n))
+    B[:, :n_docs] = bm25.scores_batch(ind, toks, qi, qt_oracle, 1.2, 0.75)
+    _check_dense_first(fused, fids, dids, B, qi, qt_oracle, ind, toks, 60, k, f"dense-first n={n} nq={nq}")
+    _check_weighted(weighted.fused(S, B, w_d, w_l), wsc, wids, k, f"weighted n={n} w=({w_d},{w_l}) k={k}")
+
+
 def test_weighted_fusion_index_smaller_than_its_corpus():
     """An index of 2,000 rows (capacity 3,000) over a 3,000-chunk sparse corpus, both inside
     one 32,768-chunk range: the fusion covers the chunks with a dense row only, so the lexical
