@@ -17,7 +17,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "liboprag.so")
-SOURCES = ["api.cpp", "dense.hip", "bm25.hip", "fuse_upsert.hip"]
+SOURCES = ["api.cpp", "dense.hip", "dense_ilp.hip", "bm25.hip", "fuse_upsert.hip"]
 ARCH = "gfx950"
 FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function",
@@ -29,6 +29,12 @@ FLAGS = [
 ]
 
 
+# Per-source additions: some top-5 list kernels (dense_ilp.hip) under the machine scheduler that
+# favours instruction-level parallelism, which shortens their main loops (measured: batch 256
+# scoring 34.0 -> 33.3 us, batch 16 18.6 -> 18.0 us) but lengthens those of the other kernels.
+SOURCE_FLAGS = {"dense_ilp.hip": ["-mllvm", "--amdgpu-sched-strategy=max-ilp"]}
+
+
 def hipcc() -> str:
     for c in (os.environ.get("HIPCC"), "/opt/rocm/bin/hipcc", shutil.which("hipcc")):
         if c and os.path.exists(c):
@@ -38,7 +44,7 @@ def hipcc() -> str:
 
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
-    cmd = [hipcc(), *FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [hipcc(), *FLAGS, *SOURCE_FLAGS.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"compile failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")

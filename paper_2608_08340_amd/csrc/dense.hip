@@ -40,6 +40,18 @@
 #include "select.h"
 
 namespace oprag {
+
+// The top-5 list kernels for batches up to 16 and above 64 are compiled a second time, in
+// dense_ilp.hip, under the machine scheduler that favours instruction-level parallelism, and
+// the kernel table points at those instances: their calls take 2 % less time with it (batch 1,
+// 16, 100, 256), while the 64-query top-5 kernels and the filtered ones take longer (1 to 7 %)
+// and keep the default.  X(DT, NW, MW, RS, G, KS, SEL, WV, QR) for each.
+#define OPRAG_ILP_KERNELS(X, DT)                                                                   \
+  X(DT, 1, 1, 16, 1, 5, 0, 4, 8) X(DT, 1, 1, 16, 1, 5, 0, 4, 0) X(DT, 1, 1, 4, 1, 5, 0, 4, 0)     \
+  X(DT, 8, 4, 4, 2, 5, 0, 4, 0)
+template <int DT, int NW, int MW, int RS, int G, int KS, int SEL, int WV, int QR>
+__global__ __launch_bounds__(WV * 64) void dense_mfma_kernel_ilp(DenseArgs a);
+
 namespace {
 
 using namespace dev;
@@ -1214,8 +1226,14 @@ __device__ __forceinline__ bool rank_epilogue(const f32x4 (&acc)[MW][BN / 16], S
 //    running top-k of each query, or (SEL 2) the filtered mode collects the scores that
 //    reach the query's threshold.
 // ------------------------------------------------------------------------------------
+#ifdef OPRAG_DENSE_ILP
+}  // namespace: the instances below have external linkage (the kernel table refers to them)
+#define OPRAG_DENSE_KERNEL dense_mfma_kernel_ilp
+#else
+#define OPRAG_DENSE_KERNEL dense_mfma_kernel
+#endif
 template <int DT, int NW, int MW, int RS, int G, int KS, int SEL, int WV, int QR>
-__global__ __launch_bounds__(WV * 64) void dense_mfma_kernel(DenseArgs a) {
+__global__ __launch_bounds__(WV * 64) void OPRAG_DENSE_KERNEL(DenseArgs a) {
   if (a.gate != nullptr && *a.gate == 0) return;  // a repair launch with nothing to repair
   using M = Mfma<DT>;
   using V = typename M::V;
@@ -1581,6 +1599,18 @@ __global__ __launch_bounds__(WV * 64) void dense_mfma_kernel(DenseArgs a) {
     sel.write(a, q0, chunk);
   }
 }
+
+#undef OPRAG_DENSE_KERNEL
+
+#ifdef OPRAG_DENSE_ILP
+#define OPRAG_ILP_INSTANCE(DT, NW, MW, RS, G, KS, SEL, WV, QR) \
+  template __global__ void dense_mfma_kernel_ilp<DT, NW, MW, RS, G, KS, SEL, WV, QR>(DenseArgs);
+OPRAG_ILP_KERNELS(OPRAG_ILP_INSTANCE, kDtypeBF16)
+OPRAG_ILP_KERNELS(OPRAG_ILP_INSTANCE, kDtypeF16)
+#undef OPRAG_ILP_INSTANCE
+
+}  // namespace oprag
+#else  // the rest of the library's dense search: other kernels, the kernel table, planning
 
 // ------------------------------------------------------------------------------------
 // fp32 VALU kernel: tile of 64 rows x 32 queries, 32 dimensions per stage.
@@ -2212,9 +2242,17 @@ struct KernelInfo {
    WV * 64, QR}
 #define MFKW(DT, NW, MW, RS, G, KS, SEL, OCC, LO, HI, WV) MFKQ(DT, NW, MW, RS, G, KS, SEL, OCC, LO, HI, WV, 0)
 #define MFK(DT, NW, MW, RS, G, KS, SEL, OCC, LO, HI) MFKW(DT, NW, MW, RS, G, KS, SEL, OCC, LO, HI, kWaves)
+// The same entries for the instances built with the ILP scheduler (OPRAG_ILP_KERNELS).
+#define MFKQI(DT, NW, MW, RS, G, KS, SEL, OCC, LO, HI, QR)                                                   \
+  {dense_mfma_kernel_ilp<DT, NW, MW, RS, G, KS, SEL, kWaves, QR>, DT, NW * 16, kWaves * MW * 16, KS, SEL, OCC, LO, \
+   HI, RS, kWaves * 64, QR}
+#define MFKI(DT, NW, MW, RS, G, KS, SEL, OCC, LO, HI) MFKQI(DT, NW, MW, RS, G, KS, SEL, OCC, LO, HI, 0)
 // Deep rings first; the 4-deep variants serve dimensions that are not multiples of the ring.
 #define MF_KS(DT, NW, MW, RS, G, OCC, LO, HI)                                                   \
   MFK(DT, NW, MW, RS, G, 5, 0, OCC, LO, HI), MFK(DT, NW, MW, RS, G, 8, 0, OCC, LO, HI),          \
+      MFK(DT, NW, MW, RS, G, 16, 0, OCC, LO, HI)
+#define MF_KSI(DT, NW, MW, RS, G, OCC, LO, HI)                                                  \
+  MFKI(DT, NW, MW, RS, G, 5, 0, OCC, LO, HI), MFK(DT, NW, MW, RS, G, 8, 0, OCC, LO, HI),         \
       MFK(DT, NW, MW, RS, G, 16, 0, OCC, LO, HI)
 // The single-query-block kernels aim for one workgroup per CU: two 64-row tiles each, so the
 // ring streams across a tile boundary and the second tile takes the running-threshold path.
@@ -2224,9 +2262,9 @@ struct KernelInfo {
 // second): one round of workgroups, each streaming all of its chunk's tiles with the ring
 // running on through the selections, instead of two rounds of half-length chunks.
 #define MF_SET(DT)                                                                              \
-  MFKQ(DT, 1, 1, 16, 1, 5, 0, 1, 1, 16, kWaves, 8), MF_KS(DT, 1, 1, 16, 1, 1, 1, 16),                \
-      MF_KS(DT, 1, 1, 4, 1, 1, 1, 16), MF_KS(DT, 4, 2, 8, 1, 4, 17, 64), MF_KS(DT, 4, 2, 4, 1, 4, 17, 64), \
-      MFK(DT, 8, 4, 4, 2, 5, 0, 1, 65, 1 << 30),                                                    \
+  MFKQI(DT, 1, 1, 16, 1, 5, 0, 1, 1, 16, 8), MF_KSI(DT, 1, 1, 16, 1, 1, 1, 16),                      \
+      MF_KSI(DT, 1, 1, 4, 1, 1, 1, 16), MF_KS(DT, 4, 2, 8, 1, 4, 17, 64), MF_KS(DT, 4, 2, 4, 1, 4, 17, 64), \
+      MFKI(DT, 8, 4, 4, 2, 5, 0, 1, 65, 1 << 30),                                                   \
       MFK(DT, 8, 4, 4, 4, 8, 0, 1, 65, 1 << 30), MFK(DT, 8, 4, 4, 4, 16, 0, 1, 65, 1 << 30),         \
       MFK(DT, 2, 4, 8, 1, 8, 1, 4, 1, 1 << 30), MFK(DT, 2, 4, 4, 1, 8, 1, 4, 1, 1 << 30),            \
       MFKQ(DT, 1, 1, 16, 1, 5, 2, 1, 1, 16, kWaves, 8), MFK(DT, 1, 1, 16, 1, 5, 2, 8, 1, 16),          \
@@ -2583,3 +2621,4 @@ hipError_t launch_weighted_fuse(int n_cus, const float* D, const float* B, long 
 }
 
 }  // namespace oprag
+#endif  // OPRAG_DENSE_ILP
