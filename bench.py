@@ -62,8 +62,23 @@ def cpu_model() -> str:
     return platform.processor() or "unknown"
 
 
+KERNEL_UNITS = {"dense.hip": ("dense.hip", "dense_ilp.hip"), "bm25.hip": ("bm25.hip",)}
+
+
 def kernel_source_sha(name: str = "dense.hip") -> str:
-    return hashlib.sha256(open(os.path.join(os.path.dirname(KERNEL_SRC), name), "rb").read()).hexdigest()[:16]
+    """sha256[:16] of what a kernel is built from: its source files (the scoring kernel's
+    second compile unit included) and the compile flags."""
+    from paper_2608_08340_amd import build as B
+    h = hashlib.sha256()
+    for f in KERNEL_UNITS.get(name, (name,)):
+        h.update(open(os.path.join(os.path.dirname(KERNEL_SRC), f), "rb").read())
+    h.update(repr((B.FLAGS, B.SOURCE_FLAGS)).encode())
+    return h.hexdigest()[:16]
+
+
+def kernel_sha_label(name: str = "dense.hip") -> str:
+    return f"kernel build sha256[:16] ({' + '.join(KERNEL_UNITS.get(name, (name,)))} + compile flags): " \
+           f"{kernel_source_sha(name)}"
 
 
 def algorithmic_bytes(n_rows: int, dim: int, batch: int, k: int, elem: int = 2) -> int:
@@ -305,7 +320,7 @@ def pmc_workload_summarize(name: str, out_dir: str) -> int:
     src = "bm25.hip" if kernel == "bm25_kernel" else "dense.hip"
     lines = [f"rocprofv3 counters of {kernel}, {wl['title']}",
              f"command: {pmc_command(name)}",
-             f"kernel source sha256[:16] of {src}: {kernel_source_sha(src)}", "",
+             kernel_sha_label(src), "",
              "median per dispatch (dispatches counted):"]
     for c in sorted(med):
         lines.append(f"  {c:32s} {med[c]:16.1f}   ({n_disp[c]})")
@@ -391,7 +406,7 @@ def trace_summarize(out_dir: str, suite: bool = False) -> int:
         ]
         out_file, n_show = STATS_FILE, 12
     lines = head + [
-        f"kernel source sha256[:16] of dense.hip: {kernel_source_sha()}",
+        kernel_sha_label(),
         "",
         f"{'calls':>7} {'avg_us':>9} {'min_us':>9} {'max_us':>9} {'share%':>7}  kernel",
     ]
