@@ -2120,10 +2120,15 @@ __global__ __launch_bounds__(kThreads) void merge_lists_kernel(const u64* __rest
   float* osc = out_scores + q * k;
   long long* oid = out_ids + q * k;
   u64 kb[PB];
+  // Row r of 64 composites goes to the lanes rotated by r: the lists are sorted and, when 64 is
+  // a multiple of k, an unrotated lane would see the same list position in every row (lanes of
+  // the first positions then hold every large maximum, and with k = 16 hundreds of composites
+  // reached tau); rotated, each lane's maximum mixes positions and about k composites reach it.
   auto load_batch = [&](long long base) {
 #pragma unroll
     for (int u = 0; u < PB; ++u) {
-      const long long j = base + u * 64 + lane;
+      const long long r = (base >> 6) + u;  // base is a multiple of 64
+      const long long j = r * 64 + ((lane - (int)(r & 63)) & 63);
       kb[u] = j < n ? src[j] : 0ull;
     }
   };
@@ -2572,13 +2577,18 @@ hipError_t launch_dense(const DensePlan& p, int dtype, const DenseArgs& a, hipSt
   if (e != hipSuccess || p.n_chunks == 1) return e;
   if (ki.sel == 0) {
     // one batch of 16 composites per lane where the lists fit it, else 32 (the 256 five-entry
-    // lists of a small batch then still fit one)
-    if ((long long)p.n_chunks * a.k <= 64 * 16)
-      hipLaunchKernelGGL(merge_lists_kernel<16>, dim3((unsigned)((a.nq + kWaves - 1) / kWaves)), dim3(kThreads), 0, s,
-                         a.partial, p.n_chunks, a.nq, a.k, a.out_scores, a.out_ids);
+    // lists of a small batch then still fit one), else 64 (256 lists of up to 16 entries)
+    const long long nc = (long long)p.n_chunks * a.k;
+    const dim3 mg((unsigned)((a.nq + kWaves - 1) / kWaves));
+    if (nc <= 64 * 16)
+      hipLaunchKernelGGL(merge_lists_kernel<16>, mg, dim3(kThreads), 0, s, a.partial, p.n_chunks, a.nq, a.k,
+                         a.out_scores, a.out_ids);
+    else if (nc <= 64 * 32)
+      hipLaunchKernelGGL(merge_lists_kernel<32>, mg, dim3(kThreads), 0, s, a.partial, p.n_chunks, a.nq, a.k,
+                         a.out_scores, a.out_ids);
     else
-      hipLaunchKernelGGL(merge_lists_kernel<32>, dim3((unsigned)((a.nq + kWaves - 1) / kWaves)), dim3(kThreads), 0, s,
-                         a.partial, p.n_chunks, a.nq, a.k, a.out_scores, a.out_ids);
+      hipLaunchKernelGGL(merge_lists_kernel<64>, mg, dim3(kThreads), 0, s, a.partial, p.n_chunks, a.nq, a.k,
+                         a.out_scores, a.out_ids);
   } else {
     hipLaunchKernelGGL(merge_large_kernel, dim3((unsigned)((a.nq + kWaves - 1) / kWaves)), dim3(kThreads), 0, s,
                        a.partial, p.n_chunks, a.nq, a.k, a.out_scores, a.out_ids, nullptr);

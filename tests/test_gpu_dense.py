@@ -77,6 +77,19 @@ def test_32k_x_1024_bf16_top8_top16_batch512(c2, k):
     assert all(r.recall == 1.0 for r in reps)
 
 
+@pytest.mark.parametrize("nq,k", [(1, 10), (1, 16), (16, 16), (64, 10), (64, 16), (100, 16)])
+def test_32k_x_1024_bf16_small_batch_top10_top16(c2, nq, k):
+    """32,768 x 1,024 bf16 at small batches with k = 10 and 16: 128 to 256 chunk lists of k
+    entries per query, merged from one load batch of 64 composites per lane (sorted lists whose
+    length divides 64, the case where lanes must not all see the same list position)."""
+    log("32k bf16 nq", nq, "k", k)
+    q = c2.queries[:nq].contiguous()
+    _, sc, ids = _run(c2.rows, q, k, "bf16")
+    S, X, Q = oracle_scores(c2.rows, q, "bf16")
+    reps = check_dense(S, X, Q, ids, sc, k, "bf16")
+    assert all(r.recall == 1.0 for r in reps)
+
+
 @pytest.mark.parametrize("nq", [100, 256])
 def test_32k_x_1024_bf16_top100(c2, nq):
     """The hybrid's dense list shape: 32,768 x 1,024 bf16, top-100 (filtered levels 2,048 ->
