@@ -52,7 +52,7 @@ def c2():
     return synth.dense_32k()
 
 
-@pytest.mark.parametrize("nq", [1, 16, 256, 384, 768, 1024])
+@pytest.mark.parametrize("nq", [1, 16, 65, 128, 256, 384, 768, 1024])
 def test_32k_x_1024_bf16_top5(c2, nq):
     """32,768 x 1,024 bf16 mixture rows; query batches 1, 16, 256, 384, 768, 1,024; exact
     top-5.  384 and 768 queries (three and six query blocks) get grids of fewer workgroups
@@ -77,7 +77,7 @@ def test_32k_x_1024_bf16_top8_top16_batch512(c2, k):
     assert all(r.recall == 1.0 for r in reps)
 
 
-@pytest.mark.parametrize("nq,k", [(1, 10), (1, 16), (16, 16), (64, 10), (64, 16), (100, 16)])
+@pytest.mark.parametrize("nq,k", [(1, 10), (1, 16), (16, 16), (64, 10), (64, 16), (100, 8), (100, 16), (128, 10)])
 def test_32k_x_1024_bf16_small_batch_top10_top16(c2, nq, k):
     """32,768 x 1,024 bf16 at small batches with k = 10 and 16: 128 to 256 chunk lists of k
     entries per query, merged from one load batch of 64 composites per lane (sorted lists whose
