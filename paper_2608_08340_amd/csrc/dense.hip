@@ -1208,6 +1208,59 @@ __device__ __forceinline__ bool rank_epilogue(const f32x4 (&acc)[MW][BN / 16], S
 }
 
 // ------------------------------------------------------------------------------------
+// First tile of a chunk in the 16-query, 64-row-tile kernels with k <= KS = 16: the
+// running lists are still empty, so each query's k best rows of the tile are found by exact
+// ranks instead of insertions.  Every score goes to LDS as its composite (query q's row i at
+// q * 64 + (i ^ 2q), which puts the 16 queries' entries of one row in distinct banks); thread
+// t ranks rows 4s .. 4s + 3 of query q = t % 16 (s = t / 16) against the query's valid rows
+// (composites are unique, so the ranks are a permutation), writes those of rank below k to
+// the query's candidate slots in rank order, and the owner copies them into its list.
+// ------------------------------------------------------------------------------------
+template <int KS, int WV, typename Sel>
+__device__ __forceinline__ void first_tile_rank(const f32x4 (&acc)[1][1], Sel& sel, unsigned char* scratch,
+                                                long long tile0, long long row_end, int q_lim, int k) {
+  constexpr int BN = 16, TR = WV * 16, CAP = Sel::CAP;
+  static_assert(TR == 64 && WV * 64 == BN * TR / 4, "16 threads per query, four rows each");
+  static_assert(Sel::kVals >= BN * TR * 8 && CAP >= KS, "scratch areas");
+  u64* lists = Sel::cand_of(scratch);                                   // [BN][CAP]
+  u64* keys = reinterpret_cast<u64*>(scratch + BN * CAP * 8);           // [BN][TR], swizzled
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int nvalid = (int)min((long long)TR, row_end - tile0);
+  {
+    const int n = lane & 15, row0 = w * 16 + (lane >> 4) * 4;
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+      keys[n * TR + ((row0 + r) ^ (2 * n))] = composite(acc[0][0][r], (uint32_t)(tile0 + row0 + r));
+  }
+  lds_barrier();
+  const int q = tid & 15, s = tid >> 4;
+  const u64* kq = keys + q * TR;
+  u64 mine[4];
+  int rank[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    mine[e] = kq[(4 * s + e) ^ (2 * q)];
+    rank[e] = 0;
+  }
+#pragma unroll 16
+  for (int i = 0; i < TR; ++i) {
+    const u64 x = kq[i ^ (2 * q)];
+    const bool v = i < nvalid;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) rank[e] += (v && x > mine[e]) ? 1 : 0;
+  }
+#pragma unroll
+  for (int e = 0; e < 4; ++e)
+    if (4 * s + e < nvalid && rank[e] < k) lists[q * CAP + rank[e]] = mine[e];
+  lds_barrier();
+  if (tid < q_lim) {
+    const int nv = min(k, nvalid);
+#pragma unroll
+    for (int i = 0; i < KS; ++i) sel.run.v[i] = i < nv ? lists[tid * CAP + i] : 0ull;
+  }
+}
+
+// ------------------------------------------------------------------------------------
 // bf16 / fp16 MFMA kernel.  Four waves split a tile of TR = 4*MW*16 rows (each wave owns
 // MW distinct 16-row subtiles) and share a block of BN = NW*16 queries.  A k-step is one
 // MFMA depth (32 dimensions); four k-steps form a super-step of 128 dimensions.
@@ -1265,6 +1318,10 @@ __global__ __launch_bounds__(WV * 64) void OPRAG_DENSE_KERNEL(DenseArgs a) {
   // leaves its main loop the register budget it is scheduled for.
   constexpr bool kBlk = SEL == 0 && KS == 5 && NW * MW > 2;
   constexpr bool kRank = SEL == 0 && KS == 5 && !kBlk;
+  // 9 <= k <= 16 on 16-query, 64-row tiles: a chunk's first tile by exact ranks (the group path
+  // keeps four values per group for KS 16, and its owners' insertions took longer; with KS 8 the
+  // group path is the faster one)
+  constexpr bool kTileRank = SEL == 0 && KS == 16 && NW == 1 && MW == 1 && WV == 4;
   constexpr int SB0 = SEL >= 2 ? 0 : BN * SR * 4;
   constexpr int SBYTES = kBlk && BlockArea<MW, BN>::kBytes > SB0   ? BlockArea<MW, BN>::kBytes
                          : kRank && RankArea<BN, WV>::kBytes > SB0 ? RankArea<BN, WV>::kBytes
@@ -1517,7 +1574,10 @@ __global__ __launch_bounds__(WV * 64) void OPRAG_DENSE_KERNEL(DenseArgs a) {
           else if constexpr (kRank)
             done = rank_epilogue<BN, MW, KS, WV>(acc, sel, reinterpret_cast<unsigned char*>(S), scratch, tile0,
                                                  row_end, q_lim, a.k);
-          else
+          else if (kTileRank && t == 0) {
+            if constexpr (kTileRank) first_tile_rank<KS, WV>(acc, sel, scratch, tile0, row_end, q_lim, a.k);
+            done = true;
+          } else
             done = reg_epilogue<BN, MW, KS, WV>(acc, sel, S, scratch, tile0, row_end, q_lim, a.k);
           refresh = true;
         }
