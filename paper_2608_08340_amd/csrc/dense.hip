@@ -2321,15 +2321,17 @@ struct KernelInfo {
       MFK(DT, NW, MW, RS, G, 16, 0, OCC, LO, HI)
 // The single-query-block kernels aim for one workgroup per CU: two 64-row tiles each, so the
 // ring streams across a tile boundary and the second tile takes the running-threshold path.
-// Their top-5 instance keeps the block's queries resident in LDS (d <= 1,024): no query loads
-// join the ring's in-order load counter, and one barrier per tile.
+// Their instances for d <= 1,024 keep the block's queries resident in LDS: no query loads
+// join the ring's in-order load counter, and one barrier per tile (1.3 to 2 us per call at
+// batches 1 and 16).
 // The 128-query list kernels aim for one workgroup per CU as well (their LDS allows no
 // second): one round of workgroups, each streaming all of its chunk's tiles with the ring
 // running on through the selections, instead of two rounds of half-length chunks.  Batches of
 // 65 to 128 queries (one query block) take 128-row tiles, so that the chunks of a small index
 // still fill every CU (32,768 rows: 256 workgroups instead of 128).
 #define MF_SET(DT)                                                                              \
-  MFKQI(DT, 1, 1, 16, 1, 5, 0, 1, 1, 16, 8), MF_KSI(DT, 1, 1, 16, 1, 1, 1, 16),                      \
+  MFKQI(DT, 1, 1, 16, 1, 5, 0, 1, 1, 16, 8), MFKQ(DT, 1, 1, 16, 1, 8, 0, 1, 1, 16, kWaves, 8),        \
+      MFKQ(DT, 1, 1, 16, 1, 16, 0, 1, 1, 16, kWaves, 8), MF_KSI(DT, 1, 1, 16, 1, 1, 1, 16),             \
       MF_KSI(DT, 1, 1, 4, 1, 1, 1, 16), MF_KS(DT, 4, 2, 8, 1, 4, 17, 64), MF_KS(DT, 4, 2, 4, 1, 4, 17, 64), \
       MFK(DT, 8, 2, 4, 2, 5, 0, 1, 65, 128), MFK(DT, 8, 2, 4, 2, 8, 0, 1, 65, 128),                   \
       MFK(DT, 8, 2, 4, 2, 16, 0, 1, 65, 128), MFKI(DT, 8, 4, 4, 2, 5, 0, 1, 65, 1 << 30),              \
