@@ -388,7 +388,7 @@ def trace_summarize(out_dir: str, suite: bool = False) -> int:
     rows = list(csv.DictReader(open(files[0])))
     if suite:
         head = [
-            "rocprofv3 kernel statistics of bench.py --suite (every workload: 32K x 1,024 bf16 batches 1 / 16 / 256 / "
+            "rocprofv3 kernel statistics of bench.py --suite (every workload: 32K x 1,024 bf16 batches 1 / 16 / 100 / 256 / "
             "1,024, hybrid dense / BM25 / RRF / full, dense-first, weighted fusion, embedding tail, 1M x 768, "
             "streaming upsert and search); calls include warm-up and the eager timing passes",
             "command: cd /tmp && export TMPDIR=/tmp && timeout -k 10 600 rocprofv3 --kernel-trace --stats "
@@ -485,7 +485,8 @@ def suite() -> int:
            2.0 * 16 * 1024 * 384, _kernel_ms(lambda: ix.search_dense(qt, 5), 100, stream))
     ix.close()
 
-    # 32K x 1,024 bf16, batches 1 / 16 / 256 / 1,024, top-5, HBM-cold (16 slab copies rotated)
+    # 32K x 1,024 bf16, batches 1 / 16 / 100 / 256 / 1,024 top-5 and 1 / 16 top-10, HBM-cold (16 slab
+    # copies rotated)
     w = synth.dense_32k()
     rows = w.rows.to(dev)
     idxs = []
@@ -515,19 +516,20 @@ def suite() -> int:
     out.append(rd)
     print(json.dumps(rd), flush=True)
     sweep = []
-    for b in (1, 16, 256, 1024):
+    for b, kk in ((1, K), (16, K), (100, K), (256, K), (1024, K), (1, 10), (16, 10)):
         q = w.queries[:b].contiguous().to(dev)
-        outs = [(torch.empty((b, K), device=dev), torch.empty((b, K), dtype=torch.int64, device=dev))
+        outs = [(torch.empty((b, kk), device=dev), torch.empty((b, kk), dtype=torch.int64, device=dev))
                 for _ in range(COPIES)]
         it = [0]
 
         def step():
             c = it[0] % COPIES
             it[0] += 1
-            idxs[c].search_dense(q, K, out=outs[c])
+            idxs[c].search_dense(q, kk, out=outs[c])
         ms = _timed(step, 256, stream, COPIES)
-        sweep.append((b, ms))
-        report(f"32,768 x 1,024 bf16, batch {b}, top-5, cold", ms, b, algorithmic_bytes(N_ROWS, DIM, b, K),
+        if kk == K:
+            sweep.append((b, ms))
+        report(f"32,768 x 1,024 bf16, batch {b}, top-{kk}, cold", ms, b, algorithmic_bytes(N_ROWS, DIM, b, kk),
                2.0 * b * N_ROWS * DIM, _kernel_ms(step, 128, stream))
     # cost model t(B) = alpha + beta * B over the batch sweep (least squares)
     bs = np.array([b for b, _ in sweep], dtype=np.float64)
