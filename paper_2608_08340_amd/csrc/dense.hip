@@ -2260,6 +2260,115 @@ __global__ __launch_bounds__(kThreads) void merge_lists_kernel(const u64* __rest
   }
 }
 
+// Long list sets (more than 2,048 composites per query, k <= 16): one workgroup per query.  Wave w
+// takes the query's rows of 64 composites [R w / 4, R (w + 1) / 4) (R rows in all), rotated across
+// lanes as above, finds their k best exactly by the same steps (lane maxima, tau, the composites
+// reaching it ranked in LDS, or k rounds of maxima when more than 64 reach it), and writes them in
+// rank order to its list in LDS; the first wave then ranks the four sorted lists against each
+// other (lane l holds entry l % 16 of list l / 16).
+constexpr int kWgMergeK = 16;
+__global__ __launch_bounds__(kThreads) void merge_lists_wg_kernel(const u64* __restrict__ partial, int n_chunks,
+                                                                  int nq, int k, float* out_scores,
+                                                                  long long* out_ids) {
+  constexpr int PB = 16;
+  __shared__ u64 cand[kWaves][64];
+  __shared__ u64 s_tau[kWaves];
+  __shared__ u64 best[kWaves][kWgMergeK];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const long long q = blockIdx.x;  // one query per workgroup: grid = nq
+  const long long n = (long long)n_chunks * k;
+  const long long rows = (n + 63) / 64;
+  const long long r0 = rows * w / kWaves, r1 = rows * (w + 1) / kWaves;
+  const u64* src = partial + q * n;
+  u64 kb[PB];
+  auto load_batch = [&](long long rb) {  // rows rb .. rb + PB - 1 of this wave's range
+#pragma unroll
+    for (int u = 0; u < PB; ++u) {
+      const long long r = rb + u;
+      const long long j = r * 64 + ((lane - (int)(r & 63)) & 63);
+      kb[u] = (r < r1 && j < n) ? src[j] : 0ull;
+    }
+  };
+  u64 m = 0;
+  for (long long rb = r0; rb < r1; rb += PB) {
+    load_batch(rb);
+#pragma unroll
+    for (int u = 0; u < PB; ++u) m = umax64(m, kb[u]);
+  }
+  cand[w][lane] = m;
+  if (lane == 0) s_tau[w] = 0ull;
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  {
+    int rank = 0;
+#pragma unroll 8
+    for (int u = 0; u < 64; ++u) rank += cand[w][u] > m ? 1 : 0;
+    if (rank == k - 1) s_tau[w] = m;
+  }
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  const u64 tau = s_tau[w];
+  const u64 below = (1ull << lane) - 1ull;
+  const bool one_batch = r1 - r0 <= PB;
+  int c = 0;
+  for (long long rb = r0; rb < r1; rb += PB) {
+    if (!one_batch) load_batch(rb);
+#pragma unroll
+    for (int u = 0; u < PB; ++u) {
+      const bool take = kb[u] != 0ull && kb[u] >= tau;
+      const u64 bal = __ballot(take);
+      if (take) {
+        const int pos = c + __popcll(bal & below);
+        if (pos < 64) cand[w][pos] = kb[u];
+      }
+      c += __popcll(bal);
+    }
+  }
+  if (lane < kWgMergeK) best[w][lane] = 0ull;
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  if (c <= 64) {
+    const u64 me = lane < c ? cand[w][lane] : 0ull;
+    int rank = 0;
+    for (int u = 0; u < c; ++u) rank += cand[w][u] > me ? 1 : 0;
+    if (lane < c && rank < k) best[w][rank] = me;
+  } else {
+    // at least 64 >= k composites reach tau, so every round finds one
+    u64 last = ~0ull;
+    for (int r = 0; r < k; ++r) {
+      u64 mx = 0;
+      for (long long rb = r0; rb < r1; rb += PB) {
+        if (!one_batch) load_batch(rb);
+#pragma unroll
+        for (int u = 0; u < PB; ++u)
+          if (kb[u] >= tau && kb[u] < last) mx = umax64(mx, kb[u]);
+      }
+      last = wave_max64(mx);
+      if (lane == 0) best[w][r] = last;
+    }
+  }
+  __syncthreads();
+  if (w == 0) {
+    const int li = lane >> 4, pos = lane & 15;
+    const u64 x = pos < k ? best[li][pos] : 0ull;
+    int rank = pos;
+#pragma unroll
+    for (int lj = 0; lj < kWaves; ++lj) {
+      if (lj == li) continue;
+#pragma unroll
+      for (int p2 = 0; p2 < kWgMergeK; ++p2) rank += (p2 < k && best[lj][p2] > x) ? 1 : 0;
+    }
+    float* osc = out_scores + q * k;
+    long long* oid = out_ids + q * k;
+    if (x != 0ull && rank < k) {
+      oid[rank] = (long long)comp_row(x);
+      osc[rank] = comp_score(x);
+    }
+    const int tot = __popcll(__ballot(x != 0ull));
+    for (int r = tot + lane; r < k; r += 64) {
+      oid[r] = -1;
+      osc[r] = kNegInf;
+    }
+  }
+}
+
 // k <= 128: one wave per query keeps a 128-entry queue and merges 64 candidates at a time.
 __global__ __launch_bounds__(kThreads) void merge_large_kernel(const unsigned long long* __restrict__ partial,
                                                                int n_chunks, int nq, int k, float* out_scores,
@@ -2642,7 +2751,7 @@ hipError_t launch_dense(const DensePlan& p, int dtype, const DenseArgs& a, hipSt
   if (e != hipSuccess || p.n_chunks == 1) return e;
   if (ki.sel == 0) {
     // one batch of 16 composites per lane where the lists fit it, else 32 (the 256 five-entry
-    // lists of a small batch then still fit one), else 64 (256 lists of up to 16 entries)
+    // lists of a small batch then still fit one), else a workgroup per query
     const long long nc = (long long)p.n_chunks * a.k;
     const dim3 mg((unsigned)((a.nq + kWaves - 1) / kWaves));
     if (nc <= 64 * 16)
@@ -2651,9 +2760,9 @@ hipError_t launch_dense(const DensePlan& p, int dtype, const DenseArgs& a, hipSt
     else if (nc <= 64 * 32)
       hipLaunchKernelGGL(merge_lists_kernel<32>, mg, dim3(kThreads), 0, s, a.partial, p.n_chunks, a.nq, a.k,
                          a.out_scores, a.out_ids);
-    else
-      hipLaunchKernelGGL(merge_lists_kernel<64>, mg, dim3(kThreads), 0, s, a.partial, p.n_chunks, a.nq, a.k,
-                         a.out_scores, a.out_ids);
+    else  // the list kernels have k <= 16 = kWgMergeK
+      hipLaunchKernelGGL(merge_lists_wg_kernel, dim3((unsigned)a.nq), dim3(kThreads), 0, s, a.partial, p.n_chunks,
+                         a.nq, a.k, a.out_scores, a.out_ids);
   } else {
     hipLaunchKernelGGL(merge_large_kernel, dim3((unsigned)((a.nq + kWaves - 1) / kWaves)), dim3(kThreads), 0, s,
                        a.partial, p.n_chunks, a.nq, a.k, a.out_scores, a.out_ids, nullptr);
