@@ -26,6 +26,7 @@ def _noalloc(idx, q, k):
 
 
 @pytest.mark.parametrize("dtype,n,d,k,nq1,nq2", [("bf16", 32768, 1024, 5, 256, 16),
+                                                 ("bf16", 32768, 1024, 16, 64, 1),
                                                  ("f16", 20000, 384, 100, 40, 7),
                                                  ("f32", 3000, 128, 10, 33, 2)])
 def test_noalloc_matches_workspace_search(dtype, n, d, k, nq1, nq2):
