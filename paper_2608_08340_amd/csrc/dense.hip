@@ -41,11 +41,12 @@
 
 namespace oprag {
 
-// The top-5 list kernels for batches up to 16 and above 64 are compiled a second time, in
+// The top-5 list kernels for batches up to 16 and above 128 are compiled a second time, in
 // dense_ilp.hip, under the machine scheduler that favours instruction-level parallelism, and
-// the kernel table points at those instances: their calls take 2 % less time with it (batch 1,
-// 16, 100, 256), while the 64-query top-5 kernels and the filtered ones take longer (1 to 7 %)
-// and keep the default.  X(DT, NW, MW, RS, G, KS, SEL, WV, QR) for each.
+// the kernel table points at those instances: their calls take 2 % less time with it (batches
+// 1, 16 and 256), while the 64-query top-5 kernels and the filtered ones take longer (1 to 7 %)
+// and the 65-128-query one the same, and keep the default.  X(DT, NW, MW, RS, G, KS, SEL, WV,
+// QR) for each.
 #define OPRAG_ILP_KERNELS(X, DT)                                                                   \
   X(DT, 1, 1, 16, 1, 5, 0, 4, 8) X(DT, 1, 1, 16, 1, 5, 0, 4, 0) X(DT, 1, 1, 4, 1, 5, 0, 4, 0)     \
   X(DT, 8, 4, 4, 2, 5, 0, 4, 0)
