@@ -90,6 +90,19 @@ def test_32k_x_1024_bf16_small_batch_top10_top16(c2, nq, k):
     assert all(r.recall == 1.0 for r in reps)
 
 
+@pytest.mark.parametrize("nq,k", [(1, 16), (16, 10), (50, 16)])
+def test_long_list_merge_with_a_short_last_chunk(nq, k):
+    """19,973 rows (156 full 128-row chunks and one of 5 rows, so one list holds fewer than k
+    entries and is padded) at small batches: with k = 16, 2,512 composites per query, the
+    workgroup-per-query merge; with k = 10, the one-wave merge of 1,570."""
+    log("long list merge", nq, k)
+    device()
+    w = synth.mixture_dense(7300 + k + nq, 19973, 256, 48, nq, k, "bf16")
+    _, sc, ids = _run(w.rows, w.queries, k, "bf16")
+    S, X, Q = oracle_scores(w.rows, w.queries, "bf16")
+    check_dense(S, X, Q, ids, sc, k, "bf16", label=f"nq={nq} k={k}")
+
+
 @pytest.mark.parametrize("nq", [100, 256])
 def test_32k_x_1024_bf16_top100(c2, nq):
     """The hybrid's dense list shape: 32,768 x 1,024 bf16, top-100 (filtered levels 2,048 ->
